@@ -1,0 +1,201 @@
+/*
+ * libmurmur -- decode-step GQA attention over a sliding-window-evicted KV cache
+ * (Murmur, "An Efficient Inference System for Long-Form ASR", Section 3.2).
+ *
+ * An LLM-based ASR decoder keeps, per sequence (one audio chunk), a KV cache
+ * laid out as [system prompt][speech tokens][system prompt][output tokens]
+ * (Section 3.2, the sequence structure paragraph).  At every decode step only a
+ * positional subset of that cache is attended: the system prompts, a window of
+ * speech tokens that starts to advance after a delay (Algorithm 2, with the
+ * speech sinks of Equation 2), and StreamingLLM-style sinks plus a recent
+ * window of output tokens (Algorithm 1).  The current token attends over the
+ * kept entries with ordinary softmax attention (Equation 1).
+ *
+ * Two calls form the hot path of one decode step:
+ *   murmur_evict_compact  -- policy -> per-sequence retained-position lists
+ *                            (and an equivalent table of contiguous ranges);
+ *   murmur_decode_attn    -- split-K grouped-query attention over those
+ *                            positions with a log-sum-exp merge of the splits.
+ *
+ * Conventions shared by every call:
+ *   - Pointers named *_dev are device memory (HIP, the current device); all
+ *     other pointers are host memory.  Every buffer is owned by the caller;
+ *     the library keeps no pointer after a call returns and allocates nothing.
+ *   - Hot calls are asynchronous on `stream` (NULL = the null stream), never
+ *     synchronise the host, issue only kernel launches, and may be captured
+ *     into a HIP graph.
+ *   - Return value: MURMUR_OK (0) or a negative MURMUR_E* code.  All argument
+ *     checks run before any HIP call, so a rejected call touches no device
+ *     state.  murmur_last_error() then describes the failure.
+ *   - Conditions only the device can see (a retained count above max_keep, a
+ *     position outside the cache, an invalid per-sequence policy) set bits in
+ *     a per-device error word read by murmur_device_error(); the affected
+ *     sequence's outputs are written as NaN so the failure is never silent.
+ */
+#ifndef MURMUR_H
+#define MURMUR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same object as hipStream_t; declared here so the header needs no HIP headers. */
+typedef struct ihipStream_t *murmur_stream_t;
+
+enum {
+    MURMUR_OK = 0,
+    MURMUR_EINVAL = -1,       /* a pointer, size, stride or policy value is invalid */
+    MURMUR_EUNSUPPORTED = -2, /* valid but not implemented (head_dim != 128, group > 16, dtype) */
+    MURMUR_ENOSPACE = -3,     /* max_keep below a retained count, or workspace too small */
+    MURMUR_EHIP = -4,         /* a HIP runtime call failed; the message has hipGetErrorString */
+};
+
+enum { MURMUR_DTYPE_BF16 = 1, MURMUR_DTYPE_F32 = 2 };
+
+/* Device error word bits (murmur_device_error). */
+enum {
+    MURMUR_DEVERR_OVERFLOW = 1,  /* evict_compact: retained count > max_keep */
+    MURMUR_DEVERR_POLICY = 2,    /* evict_compact: invalid layout or policy for a sequence */
+    MURMUR_DEVERR_POSITION = 4,  /* decode_attn: retained position outside [0, max_len) */
+    MURMUR_DEVERR_COUNT = 8,     /* decode_attn: count outside [1, max_keep] */
+};
+
+/* One sequence (audio chunk) of the batch, Section 3.2's layout
+ * [prompt_pre][speech_len speech tokens][prompt_mid][out_len output tokens].
+ * out_len is the paper's decode-step index j (>= 1): it counts the token being
+ * generated, whose K/V the caller has already appended at output slot j-1.
+ * Global positions are 0-based: speech starts at prompt_pre, output at
+ * prompt_pre + speech_len + prompt_mid. */
+typedef struct murmur_seg {
+    int32_t prompt_pre;
+    int32_t speech_len;
+    int32_t prompt_mid;
+    int32_t out_len;
+} murmur_seg;
+
+/* Eviction policy of one sequence (Section 3.2).
+ *   speech_window  w of Algorithm 2 (>= 1), or -1 to keep every speech token;
+ *   speech_delay   d of Algorithm 2 (>= 0): the window starts at speech token
+ *                  l_j = max(0, j - max(d,1) + 1), i.e. 0 while j < d and one
+ *                  further per step from j = d on, clamped to speech_len - w so
+ *                  the window ends no later than the last speech token;
+ *   speech_sink    n_sink of Equation 2 (>= 0): the first speech tokens, always kept;
+ *   out_window     w of Algorithm 1 (>= 1), or -1 to keep every output token;
+ *   out_sink       n_sink of Algorithm 1 (>= 0), counted from the first output token.
+ * Both system prompts are always kept.  The retained set is a pure function of
+ * (murmur_seg, murmur_policy): no state is carried between steps. */
+typedef struct murmur_policy {
+    int32_t speech_window;
+    int32_t speech_delay;
+    int32_t speech_sink;
+    int32_t out_window;
+    int32_t out_sink;
+} murmur_policy;
+
+/* One layer-stacked KV cache (Section 3.2: K, V in R^{L x d} per layer).
+ * Element (layer, b, kv_head, pos, e) of K lives at
+ *   k + layer*stride_layer + b*stride_b + kv_head*stride_h + pos*stride_pos + e
+ * (strides in bf16 elements; the head_dim stride is 1).  V uses the same
+ * strides.  max_len bounds the positions that may be read: every retained
+ * position must lie in [0, max_len).  Both base pointers must be 16-byte
+ * aligned and stride_layer, stride_b, stride_h, stride_pos multiples of 8. */
+typedef struct murmur_kv {
+    const void *k;
+    const void *v;
+    int32_t n_layers;
+    int32_t max_len;
+    int64_t stride_layer;
+    int64_t stride_b;
+    int64_t stride_h;
+    int64_t stride_pos;
+} murmur_kv;
+
+/* ABI version of this header (bumped on any signature change). */
+#define MURMUR_ABI_VERSION 1
+int murmur_abi_version(void);
+
+/* Text of the last failure on the calling thread; valid until the next call
+ * on that thread.  Empty string after a successful call. */
+const char *murmur_last_error(void);
+
+/* Host-only sizing (no GPU needed).  Computes the retained count of each of
+ * the B sequences -- prompts + |speech sinks U speech window| + |output sinks
+ * U output window| (Algorithms 1 and 2, Equation 2) -- into counts[B] and
+ * their maximum into *max_count.
+ *   seg: host [B]; pol: host [pol_per_seq ? B : 1]; counts: host [B] or NULL.
+ * Errors: MURMUR_EINVAL for a negative length, out_len < 1, speech_window or
+ * out_window outside {-1} U [1, inf), a negative delay or sink count, or
+ * pol_per_seq not 0/1. */
+int murmur_retained_count_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq,
+                               int32_t B, int32_t *counts, int32_t *max_count);
+
+/* Applies the eviction policy on the device (Algorithm 1, Algorithm 2,
+ * Equation 2) and emits, per sequence b:
+ *   idx_dev[b*max_keep + r], r < count: the r-th retained global position,
+ *       ascending and without duplicates; slots r >= count hold -1;
+ *   count_dev[b]: the retained count;
+ *   ranges_dev (nullable) [b][6][2]: the same set as six (start, length)
+ *       pieces in ascending position order -- prompt_pre, speech sinks, speech
+ *       window, prompt_mid, output sinks, output window -- non-overlapping,
+ *       lengths >= 0, summing to count.
+ *   seg_dev: device [B]; pol_dev: device [pol_per_seq ? B : 1].
+ * Host errors: MURMUR_EINVAL (null pointers, B < 1, max_keep < 1,
+ * pol_per_seq not 0/1).  Device errors: MURMUR_DEVERR_POLICY (count 0 and all
+ * slots -1 for that sequence), MURMUR_DEVERR_OVERFLOW (count holds the true
+ * count, idx the first max_keep positions). */
+int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                         int32_t B, int32_t *idx_dev, int32_t max_keep, int32_t *count_dev,
+                         int32_t *ranges_dev, murmur_stream_t stream);
+
+/* Workspace bytes murmur_decode_attn needs for these sizes and split_len
+ * (0 = the automatic choice).  The workspace holds the split partials and a
+ * ticket counter per (layer, sequence, kv-head).  It must be zero-filled once
+ * before its first use (or reset with murmur_decode_attn_workspace_init);
+ * every completed call leaves the tickets at zero again.  Calls that share a
+ * workspace must not run concurrently. */
+int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
+                                 int32_t split_len, size_t *bytes);
+
+/* Zeroes the ticket counters of a workspace with a small kernel (no memset
+ * node, so it may be captured). */
+int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stream_t stream);
+
+/* Decode-step attention (Equation 1) of the current token of every sequence,
+ * in every layer, over the retained positions only:
+ *   out[l,b,h,:] = sum_{i in R_b} softmax_i(scale * q[l,b,h,:] . K[l,b,g,i,:]) V[l,b,g,i,:]
+ *   lse[l,b,h]   = log sum_{i in R_b} exp(scale * q[l,b,h,:] . K[l,b,g,i,:])
+ * with g = h / (Hq/Hkv) (grouped-query attention, contiguous head groups) and
+ * R_b the retained set of sequence b, shared by all layers and heads.
+ *   q_dev:      bf16 [n_layers][B][Hq][D], contiguous, 16-byte aligned;
+ *   kv:         host struct describing the bf16 K/V caches (see murmur_kv);
+ *   ranges_dev: nullable [B][6][2] range table from murmur_evict_compact; when
+ *               given it is used and idx_dev is not read;
+ *   idx_dev:    [B][max_keep] positions (used when ranges_dev is NULL);
+ *   count_dev:  [B] retained counts;
+ *   D:          head_dim, must be 128; Hq/Hkv must be in [1, 16];
+ *   scale:      logit scale (1/sqrt(D) for unscaled queries), finite;
+ *   split_len:  retained positions per split (a multiple of 128), 0 = automatic;
+ *   out_dev:    [n_layers][B][Hq][D] of out_dtype (MURMUR_DTYPE_BF16 rounds to
+ *               nearest even, MURMUR_DTYPE_F32 stores the fp32 accumulation);
+ *   lse_dev:    nullable fp32 [n_layers][B][Hq], natural log;
+ *   ws_dev:     workspace of ws_bytes >= murmur_decode_attn_workspace(...).
+ * Accumulation is fp32 throughout.  Errors: MURMUR_EINVAL, MURMUR_EUNSUPPORTED,
+ * MURMUR_ENOSPACE (workspace), MURMUR_EHIP; device errors
+ * MURMUR_DEVERR_POSITION and MURMUR_DEVERR_COUNT. */
+int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *idx_dev, const int32_t *ranges_dev,
+                       const int32_t *count_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                       float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                       void *ws_dev, size_t ws_bytes, murmur_stream_t stream);
+
+/* Synchronises `stream`, returns the device error word of the current device
+ * in *code (0 = none) and clears it.  Not for use inside a captured graph. */
+int murmur_device_error(murmur_stream_t stream, int32_t *code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MURMUR_H */
