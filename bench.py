@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Decode-attention benchmark on one MI355X: µs per decode step and achieved HBM GB/s.
+
+One step is the whole hot path on one batch: murmur_evict_compact (retained
+lists from the eviction policy) then murmur_decode_attn (split-K GQA attention
+over the retained K/V with the log-sum-exp merge), on synthetic inputs already
+resident in HBM.  Default workload: 12 chunks of 300 s (2250 speech tokens, 32
+prompt tokens, 600-1200 output tokens), speech window 562 with delay 512,
+output window 256, 1 layer, GQA 28/4, head_dim 128, bf16.
+
+Timing:
+  * value / ms_per_step: K steps captured once into a HIP graph and replayed,
+    bracketed by device synchronisation and HIP events on the replay stream;
+  * roofline.achieved: algorithmic bytes of one decode_attn launch divided by
+    its mean duration, from HIP events recorded around each launch on the
+    stream it is launched on;
+  * every step reads a different replica of the KV cache (rotation over more
+    than 2 x 256 MB), so reads come from HBM, not the 256 MB Infinity Cache.
+cpu_baseline: the fp64 oracle timed on this host's cores on a bounded number
+of steps of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "decode-attn µs/step + achieved HBM GB/s (% peak), 12×300s chunks w/ eviction"
+HBM_PEAK_GBPS = 8000.0
+MALL_BYTES = 256 << 20
+
+DESCRIPTIONS = {
+    "c1": "tiny: 1 layer, batch 1, 32 prompt + 450 speech + 64 output tokens, speech window 128, output window 32",
+    "c2": "12 x 300 s chunks, dense: 1 layer, 32 prompt + 2250 speech + U{600..1200} output tokens, no eviction",
+    "c3": "12 x 300 s chunks with eviction: 1 layer, 32 prompt + 2250 speech + U{600..1200} output tokens, "
+          "speech window 562 (delay 512), output window 256, 5% planted keys",
+    "c4_dense": "single-pass hour, dense: 1 layer, batch 1, 32 prompt + 27000 speech + 8000 output tokens",
+    "c4_evict": "single-pass hour with eviction: speech window 2048 (delay 512), output window 512",
+    "c5": "28 layers x 12 chunks: speech U{1800..2250}, output U{300..1200}, speech window L_s/4 (delay 512), "
+          "output window 256, all layers in one launch",
+}
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
+    import oracle
+    oracle.build()
+    t0 = time.perf_counter()
+    n = 0
+    while n < wl.steps:
+        idx, cnt = oracle.retained(wl.seg(n), wl.policy)
+        oracle.attend(wl.q(n), wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=threads)
+        n += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": dt / n * 1e6, "unit": "us/step", "cores": threads, "kind": "oracle",
+            "sample": f"{n} decode step(s) of workload {wl.name} (all {wl.batch} sequences, {wl.n_layers} layer(s), "
+                      f"{wl.hq} heads), retained set + fp64 attention, {threads} threads, {dt:.1f} s wall"}
+
+
+def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, cpu_budget: float,
+        split_len: int, use_ranges: bool) -> dict:
+    import torch
+    from paper_2606_01483_amd import murmur as M
+    from paper_2606_01483_amd import workloads as W
+    from paper_2606_01483_amd.decode import DecodeBatch
+
+    torch.cuda.init()
+    M.lib()
+    lay = W.layout(config)
+    n_steps = max(lay.steps, steps)
+    log(f"workload {config}: drawing inputs ({n_steps} steps)")
+    wl = W.make(config, steps=n_steps)
+    counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[0] for s in range(n_steps)]
+    kv_step = [int(c.sum()) * wl.n_layers * wl.hkv * 2 * wl.head_dim * 2 for c in counts]
+    if replicas is None:
+        replicas = max(1, math.ceil(2.2 * MALL_BYTES / min(kv_step)))
+        cache_bytes = wl.k.nbytes * 2
+        replicas = min(replicas, max(1, (24 << 30) // cache_bytes))
+    log(f"uploading: {replicas} KV replica(s) of {wl.k.nbytes * 2 / 1e6:.1f} MB")
+    db = DecodeBatch(wl, replicas=replicas, out_dtype=M.MURMUR_DTYPE_BF16, split_len=split_len,
+                     use_ranges=use_ranges, steps=list(range(n_steps)))
+    stream = torch.cuda.current_stream()
+
+    order = [i % n_steps for i in range(steps)]
+    rep = [i % replicas for i in range(steps)]
+
+    for i in range(warmup):
+        db.step(i % n_steps, i % replicas)
+    torch.cuda.synchronize()
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during warm-up")
+
+    # Per-launch decode_attn durations (HIP events on the launch stream).
+    log("timing decode_attn launches with HIP events")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i in range(steps):
+        db.evict(order[i])
+        evs[i][0].record(stream)
+        db.attend(order[i], rep[i])
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    attn_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+
+    # Whole steps, captured once into a graph and replayed.
+    log("capturing the timed steps into a HIP graph")
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(stream)
+    with torch.cuda.stream(cap):
+        db.step(order[0], rep[0])  # one eager step on the capture stream before capture
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=cap):
+        for i in range(steps):
+            db.step(order[i], rep[i])
+    torch.cuda.synchronize()
+    graph.replay()  # warm replay
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    graph.replay()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    step_us = t0.elapsed_time(t1) * 1e3 / steps
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during the timed steps")
+
+    io = db.io_bytes()
+    alg_bytes = np.array([kv_step[o] + io for o in order], dtype=np.float64)
+    mean_attn = float(attn_us.mean())
+    achieved = float(alg_bytes.mean() / (mean_attn * 1e-6) / 1e9)
+    res = {
+        "metric": METRIC,
+        "value": round(step_us, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(step_us / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{config}: {DESCRIPTIONS[config]}", "batch": wl.batch, "layers": wl.n_layers,
+                   "q_heads": wl.hq, "kv_heads": wl.hkv, "head_dim": wl.head_dim,
+                   "retained_per_step": int(np.mean([int(counts[o].sum()) for o in order])),
+                   "kv_replicas": replicas, "selection": "ranges" if use_ranges else "index list",
+                   "split_len": db.split_len or "auto"},
+        "decode_attn_us": {"mean": round(mean_attn, 3), "median": round(float(np.median(attn_us)), 3),
+                           "p90": round(float(np.percentile(attn_us, 90)), 3)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "decode_attn_kernel", "alg_bytes_per_launch": int(alg_bytes.mean())},
+    }
+    if cpu:
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+        log(f"timing the fp64 oracle on {threads} host threads")
+        res["cpu_baseline"] = cpu_baseline(wl, cpu_budget, threads)
+    return res
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c3", help="workload: c1, c2, c3, c4_dense, c4_evict, c5")
+    ap.add_argument("--replicas", type=int, default=None, help="KV cache replicas to rotate over (default: auto)")
+    ap.add_argument("--split-len", type=int, default=0)
+    ap.add_argument("--index-list", action="store_true", help="attend from the index list instead of ranges")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this decode path has no multi-GPU mode (got --gpus {args.gpus})",
+              file=sys.stderr)
+        return 2
+    res = run(args.config, args.steps, args.warmup, args.replicas, not args.no_cpu_baseline, args.cpu_budget,
+              args.split_len, not args.index_list)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,221 @@
+// C ABI of libmurmur (include/murmur.h): argument validation, workspace
+// planning, error text, and dispatch to the gfx950 kernels.  Every check runs
+// before the first HIP call, so rejected calls leave the device untouched.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "internal.h"
+#include "murmur.h"
+#include "policy.h"
+
+#define MURMUR_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace murmur {
+namespace {
+
+thread_local char g_last_error[512];
+
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_last_error[0] = '\0';
+    return MURMUR_OK;
+}
+
+bool aligned(const void *p, size_t n) { return ((uintptr_t)p % n) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
+                             int32_t split_len) {
+    WorkspacePlan p{};
+    const int64_t units = ((int64_t)max_keep + kSplitUnit - 1) / kSplitUnit;
+    if (split_len <= 0) {
+        // At most kMaxAutoSplits partials per (layer, sequence, KV head): the
+        // merge reads them all, so very long lists take longer splits.
+        const int64_t per = (units + kMaxAutoSplits - 1) / kMaxAutoSplits;
+        split_len = (int32_t)((per < 1 ? 1 : per) * kSplitUnit);
+    }
+    p.split_len = split_len;
+    p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
+    p.groups = (int64_t)n_layers * B * Hkv;
+    const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
+    p.ticket_bytes = round_up((size_t)p.groups * sizeof(int32_t), 256);
+    if (p.n_split > 1) {
+        p.ml_bytes = round_up((size_t)p.groups * p.n_split * G * 2 * sizeof(float), 256);
+        p.o_bytes = round_up((size_t)p.groups * p.n_split * G * kHeadDim * sizeof(float), 256);
+    }
+    p.total = p.ticket_bytes + p.ml_bytes + p.o_bytes;
+    return p;
+}
+
+namespace {
+
+int check_host_policy(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
+                      int32_t *counts, int32_t *max_count) {
+    int32_t mx = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        const murmur_seg &s = seg[b];
+        const murmur_policy &p = pol[pol_per_seq ? b : 0];
+        Pieces pc;
+        if (retained_pieces(s.prompt_pre, s.speech_len, s.prompt_mid, s.out_len, p.speech_window, p.speech_delay,
+                            p.speech_sink, p.out_window, p.out_sink, &pc) != 0)
+            return fail(MURMUR_EINVAL,
+                        "sequence %d: invalid layout or policy (seg %d/%d/%d/%d, policy %d/%d/%d/%d/%d)", b,
+                        s.prompt_pre, s.speech_len, s.prompt_mid, s.out_len, p.speech_window, p.speech_delay,
+                        p.speech_sink, p.out_window, p.out_sink);
+        if (counts) counts[b] = pc.count;
+        if (pc.count > mx) mx = pc.count;
+    }
+    if (max_count) *max_count = mx;
+    return ok();
+}
+
+}  // namespace
+}  // namespace murmur
+
+using namespace murmur;
+
+MURMUR_EXPORT int murmur_abi_version(void) { return MURMUR_ABI_VERSION; }
+
+MURMUR_EXPORT const char *murmur_last_error(void) { return g_last_error; }
+
+MURMUR_EXPORT int murmur_retained_count_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq,
+                                             int32_t B, int32_t *counts, int32_t *max_count) {
+    if (!seg || !pol) return fail(MURMUR_EINVAL, "seg and pol must not be NULL");
+    if (B < 1) return fail(MURMUR_EINVAL, "B must be >= 1 (got %d)", B);
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    return check_host_policy(seg, pol, pol_per_seq, B, counts, max_count);
+}
+
+MURMUR_EXPORT int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                                       int32_t B, int32_t *idx_dev, int32_t max_keep, int32_t *count_dev,
+                                       int32_t *ranges_dev, murmur_stream_t stream) {
+    if (!seg_dev || !pol_dev || !idx_dev || !count_dev)
+        return fail(MURMUR_EINVAL, "seg_dev, pol_dev, idx_dev and count_dev must not be NULL");
+    if (B < 1) return fail(MURMUR_EINVAL, "B must be >= 1 (got %d)", B);
+    if (max_keep < 1) return fail(MURMUR_EINVAL, "max_keep must be >= 1 (got %d)", max_keep);
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
+        !aligned(ranges_dev, 4))
+        return fail(MURMUR_EINVAL, "device pointers must be 4-byte aligned");
+    if ((int64_t)B * max_keep > ((int64_t)1 << 40)) return fail(MURMUR_EINVAL, "B * max_keep too large");
+    const int e = launch_evict_compact(seg_dev, pol_dev, pol_per_seq, B, idx_dev, max_keep, count_dev, ranges_dev,
+                                       stream);
+    if (e != 0) return fail(MURMUR_EHIP, "evict_compact launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv,
+                                               int32_t max_keep, int32_t split_len, size_t *bytes) {
+    if (!bytes) return fail(MURMUR_EINVAL, "bytes must not be NULL");
+    if (n_layers < 1 || B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1)
+        return fail(MURMUR_EINVAL, "n_layers, B, Hq, Hkv and max_keep must be >= 1");
+    if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+    if (split_len < 0 || split_len % kSplitUnit != 0)
+        return fail(MURMUR_EINVAL, "split_len must be 0 or a positive multiple of %d (got %d)", kSplitUnit,
+                    split_len);
+    *bytes = plan_workspace(n_layers, B, Hq, Hkv, max_keep, split_len).total;
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
+    if (!ws_dev) return fail(MURMUR_EINVAL, "ws_dev must not be NULL");
+    if (!aligned(ws_dev, 256)) return fail(MURMUR_EINVAL, "ws_dev must be 256-byte aligned");
+    const int64_t n = (int64_t)(ws_bytes / sizeof(int32_t));
+    if (n < 1) return ok();
+    const int e = launch_workspace_init((int32_t *)ws_dev, n, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "workspace_init launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *idx_dev,
+                                     const int32_t *ranges_dev, const int32_t *count_dev, int32_t max_keep,
+                                     int32_t B, int32_t Hq, int32_t Hkv, int32_t D, float scale, int32_t split_len,
+                                     void *out_dev, int32_t out_dtype, float *lse_dev, void *ws_dev, size_t ws_bytes,
+                                     murmur_stream_t stream) {
+    if (!q_dev || !kv || !count_dev || !out_dev || !ws_dev)
+        return fail(MURMUR_EINVAL, "q_dev, kv, count_dev, out_dev and ws_dev must not be NULL");
+    if (!kv->k || !kv->v) return fail(MURMUR_EINVAL, "kv->k and kv->v must not be NULL");
+    if (!idx_dev && !ranges_dev) return fail(MURMUR_EINVAL, "one of idx_dev and ranges_dev is required");
+    if (B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1 || kv->n_layers < 1 || kv->max_len < 1)
+        return fail(MURMUR_EINVAL, "B, Hq, Hkv, max_keep, kv->n_layers and kv->max_len must be >= 1");
+    if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+    if (D != kHeadDim) return fail(MURMUR_EUNSUPPORTED, "head_dim %d is not supported (only %d)", D, kHeadDim);
+    if (Hq / Hkv > kMaxGroup)
+        return fail(MURMUR_EUNSUPPORTED, "query heads per KV head %d exceeds %d", Hq / Hkv, kMaxGroup);
+    if (out_dtype != MURMUR_DTYPE_BF16 && out_dtype != MURMUR_DTYPE_F32)
+        return fail(MURMUR_EINVAL, "out_dtype must be MURMUR_DTYPE_BF16 or MURMUR_DTYPE_F32 (got %d)", out_dtype);
+    if (!isfinite(scale)) return fail(MURMUR_EINVAL, "scale must be finite");
+    if (split_len < 0 || split_len % kSplitUnit != 0)
+        return fail(MURMUR_EINVAL, "split_len must be 0 or a positive multiple of %d (got %d)", kSplitUnit,
+                    split_len);
+    const int64_t strides[4] = {kv->stride_layer, kv->stride_b, kv->stride_h, kv->stride_pos};
+    for (int i = 0; i < 4; ++i)
+        if (strides[i] < 0 || strides[i] % 8 != 0)
+            return fail(MURMUR_EINVAL, "KV strides must be non-negative multiples of 8 elements");
+    if (kv->stride_pos < kHeadDim && kv->max_len > 1)
+        return fail(MURMUR_EINVAL, "kv->stride_pos (%lld) must be >= head_dim", (long long)kv->stride_pos);
+    if (!aligned(q_dev, 16) || !aligned(kv->k, 16) || !aligned(kv->v, 16))
+        return fail(MURMUR_EINVAL, "q_dev, kv->k and kv->v must be 16-byte aligned");
+    if (!aligned(out_dev, out_dtype == MURMUR_DTYPE_F32 ? 4 : 2) || !aligned(lse_dev, 4) ||
+        !aligned(count_dev, 4) || !aligned(idx_dev, 4) || !aligned(ranges_dev, 4))
+        return fail(MURMUR_EINVAL, "out/lse/count/idx/ranges pointers are misaligned");
+    if (!aligned(ws_dev, 256)) return fail(MURMUR_EINVAL, "ws_dev must be 256-byte aligned");
+
+    const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
+    if (ws_bytes < plan.total)
+        return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
+    const int64_t grid = plan.groups * plan.n_split;
+    if (grid > 0x7fffffffLL || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
+        return fail(MURMUR_EINVAL, "problem too large for one launch (%lld workgroups)", (long long)grid);
+
+    AttnLaunch a{};
+    a.q = (const uint16_t *)q_dev;
+    a.k = (const uint16_t *)kv->k;
+    a.v = (const uint16_t *)kv->v;
+    a.s_layer = kv->stride_layer;
+    a.s_b = kv->stride_b;
+    a.s_h = kv->stride_h;
+    a.s_pos = kv->stride_pos;
+    a.idx = idx_dev;
+    a.ranges = ranges_dev;
+    a.count = count_dev;
+    a.out = out_dev;
+    a.lse = lse_dev;
+    uint8_t *ws = (uint8_t *)ws_dev;
+    a.ticket = (int32_t *)ws;
+    a.part_ml = plan.n_split > 1 ? (float *)(ws + plan.ticket_bytes) : nullptr;
+    a.part_o = plan.n_split > 1 ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
+    a.max_len = kv->max_len;
+    a.max_keep = max_keep;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = Hq / Hkv;
+    a.NL = kv->n_layers;
+    a.split_len = plan.split_len;
+    a.n_split = plan.n_split;
+    a.out_f32 = out_dtype == MURMUR_DTYPE_F32;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    const int e = launch_decode_attn(a, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "decode_attn launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_device_error(murmur_stream_t stream, int32_t *code) {
+    if (!code) return fail(MURMUR_EINVAL, "code must not be NULL");
+    const int e = read_and_clear_device_error(stream, code);
+    if (e != 0) return fail(MURMUR_EHIP, "reading the device error word failed: %s", hip_error_text(e));
+    return ok();
+}

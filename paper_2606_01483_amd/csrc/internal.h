@@ -1,0 +1,57 @@
+// Internal interface between the C ABI layer (api.cpp) and the gfx950 kernels
+// (kernels.hip).  Not installed; include/murmur.h is the public surface.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "murmur.h"
+
+namespace murmur {
+
+constexpr int kHeadDim = 128;     // head_dim supported by the attention kernel
+constexpr int kMaxGroup = 16;     // query heads per KV head (MFMA tile height)
+constexpr int kWaveTile = 32;     // retained positions one wavefront handles per pass
+constexpr int kWavesPerWg = 4;
+constexpr int kSplitUnit = kWaveTile * kWavesPerWg;  // 128 positions: one pass of a workgroup
+constexpr int kMaxAutoSplits = 64;
+
+// Launch description of one decode_attn call, fully validated by the caller.
+struct AttnLaunch {
+    const uint16_t *q;
+    const uint16_t *k;
+    const uint16_t *v;
+    int64_t s_layer, s_b, s_h, s_pos;
+    const int32_t *idx;
+    const int32_t *ranges;
+    const int32_t *count;
+    void *out;
+    float *lse;
+    int32_t *ticket;   // [groups]
+    float *part_ml;    // [groups][n_split][G][2]  (running max in log2 units, sum)
+    float *part_o;     // [groups][n_split][G][128]
+    int32_t max_len, max_keep, B, Hq, Hkv, G, NL;
+    int32_t split_len, n_split, out_f32;
+    float scale_log2;  // logit scale times log2(e)
+};
+
+struct WorkspacePlan {
+    int32_t split_len;
+    int32_t n_split;
+    int64_t groups;
+    size_t ticket_bytes, ml_bytes, o_bytes, total;
+};
+
+// Split choice and workspace layout; deterministic in its arguments.
+WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
+                             int32_t split_len);
+
+// Kernel launchers (kernels.hip).  They return a hipError_t value as int.
+int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
+                         int32_t *idx, int32_t max_keep, int32_t *count, int32_t *ranges, murmur_stream_t stream);
+int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream);
+int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream);
+int read_and_clear_device_error(murmur_stream_t stream, int32_t *code);
+const char *hip_error_text(int err);
+
+}  // namespace murmur

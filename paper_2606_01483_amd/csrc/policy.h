@@ -1,0 +1,110 @@
+// Closed form of Murmur's retained KV set (Section 3.2), shared by the host
+// sizing call and the device kernels of libmurmur.
+//
+// For one sequence with layout [prompt_pre][speech][prompt_mid][output] at
+// output step j (1-based, counting the current token) the kept positions are:
+//   * both system prompts, always;
+//   * speech (Algorithm 2 with Equation 2's sinks): the first n_sink speech
+//     tokens and a window of w speech tokens starting at
+//     l_j = max(0, j - max(d,1) + 1), clamped to speech_len - w;
+//     the window count is w (Algorithm 2), not w + 1;
+//   * output (Algorithm 1, applied to the output region): 1-based output
+//     tokens 1..n_sink and max(1, j-w+1)..j.
+// A window of -1 (or one at least as long as its region) keeps the region.
+//
+// The set is returned as six non-overlapping pieces in ascending position
+// order: prompt_pre, speech sinks, speech window, prompt_mid, output sinks,
+// output window.  Adjacent or overlapping parts are merged into the earlier
+// piece, so every piece but a merged-away one is maximal and empty pieces
+// start where the previous one ends.
+#pragma once
+
+#include <stdint.h>
+
+#if defined(__HIPCC__)
+#define MURMUR_HD __host__ __device__
+#else
+#define MURMUR_HD
+#endif
+
+namespace murmur {
+
+constexpr int kPieces = 6;
+
+struct Pieces {
+    int32_t start[kPieces];
+    int32_t len[kPieces];
+    int32_t count;
+};
+
+// Returns 0 and fills *out, or -1 if the layout or policy is invalid (negative
+// lengths, j < 1, a window of 0 or below -1, a negative delay or sink count,
+// or a sequence longer than 2^31 - 1 positions).
+MURMUR_HD inline int retained_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s, int32_t d,
+                                     int32_t n_ss, int32_t w_o, int32_t n_so, Pieces *out) {
+    if (p_pre < 0 || l_s < 0 || p_mid < 0 || j < 1) return -1;
+    if (!(w_s == -1 || w_s >= 1) || d < 0 || n_ss < 0) return -1;
+    if (!(w_o == -1 || w_o >= 1) || n_so < 0) return -1;
+    const int64_t total = (int64_t)p_pre + l_s + p_mid + j;
+    if (total > 0x7fffffffLL) return -1;
+    const int32_t speech0 = p_pre, mid0 = p_pre + l_s, out0 = p_pre + l_s + p_mid;
+
+    out->start[0] = 0;
+    out->len[0] = p_pre;
+
+    // Speech: sinks [0, ns) united with the window [l, l + w).
+    if (w_s == -1 || w_s >= l_s) {
+        out->start[1] = speech0;
+        out->len[1] = l_s;
+        out->start[2] = speech0 + l_s;
+        out->len[2] = 0;
+    } else {
+        const int32_t first_move = d > 1 ? d : 1;
+        int32_t l = j >= first_move ? j - first_move + 1 : 0;
+        if (l > l_s - w_s) l = l_s - w_s;
+        const int32_t ns = n_ss < l_s ? n_ss : l_s;
+        if (l <= ns) {  // the window touches or overlaps the sinks: one piece
+            const int32_t end = ns > l + w_s ? ns : l + w_s;
+            out->start[1] = speech0;
+            out->len[1] = end;
+            out->start[2] = speech0 + end;
+            out->len[2] = 0;
+        } else {
+            out->start[1] = speech0;
+            out->len[1] = ns;
+            out->start[2] = speech0 + l;
+            out->len[2] = w_s;
+        }
+    }
+
+    out->start[3] = mid0;
+    out->len[3] = p_mid;
+
+    // Output: 0-based sinks [0, so) united with the window [j - w, j).
+    if (w_o == -1 || w_o >= j) {
+        out->start[4] = out0;
+        out->len[4] = j;
+        out->start[5] = out0 + j;
+        out->len[5] = 0;
+    } else {
+        const int32_t so = n_so < j ? n_so : j;
+        const int32_t w0 = j - w_o;
+        if (w0 <= so) {
+            out->start[4] = out0;
+            out->len[4] = j;
+            out->start[5] = out0 + j;
+            out->len[5] = 0;
+        } else {
+            out->start[4] = out0;
+            out->len[4] = so;
+            out->start[5] = out0 + w0;
+            out->len[5] = w_o;
+        }
+    }
+    int32_t c = 0;
+    for (int k = 0; k < kPieces; ++k) c += out->len[k];
+    out->count = c;
+    return 0;
+}
+
+}  // namespace murmur

@@ -1,0 +1,88 @@
+"""Device-resident decode batch: uploads a workload once and runs the two C-ABI calls per step.
+
+Memory plumbing only (torch allocates, the HIP kernels compute):
+  * K/V caches [R][NL][B][Hkv][max_len][D] bf16, R identical replicas so that
+    consecutive timed steps can read different addresses (cold caches);
+  * per-step layouts [steps][B][4] and queries [steps][NL][B][Hq][D];
+  * retained lists, counts, range tables, outputs and the split workspace.
+A step is murmur_evict_compact followed by murmur_decode_attn, both enqueued on
+the current torch stream with no host synchronisation.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import murmur as M
+from .workloads import Workload
+
+
+class DecodeBatch:
+    def __init__(self, wl: Workload, device: str = "cuda", replicas: int = 1, out_dtype: int = M.MURMUR_DTYPE_BF16,
+                 split_len: int = 0, use_ranges: bool = True, steps: list[int] | None = None,
+                 max_keep: int | None = None):
+        self.wl = wl
+        self.device = torch.device(device)
+        self.steps = list(range(wl.steps)) if steps is None else list(steps)
+        self.out_dtype = out_dtype
+        self.split_len = split_len
+        self.use_ranges = use_ranges
+        B, NL, Hq, Hkv, D = wl.batch, wl.n_layers, wl.hq, wl.hkv, wl.head_dim
+        self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
+
+        # Sizing from the host closed form over every step this batch will run.
+        counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[1] for s in self.steps]
+        self.max_keep = int(max(counts)) if max_keep is None else int(max_keep)
+
+        dev = self.device
+        k = torch.from_numpy(wl.k).view(torch.bfloat16)
+        v = torch.from_numpy(wl.v).view(torch.bfloat16)
+        self.replicas = replicas
+        self.k = torch.empty((replicas,) + tuple(k.shape), dtype=torch.bfloat16, device=dev)
+        self.v = torch.empty_like(self.k)
+        self.k[0].copy_(k)
+        self.v[0].copy_(v)
+        for r in range(1, replicas):
+            self.k[r].copy_(self.k[0])
+            self.v[r].copy_(self.v[0])
+        self.kv = [M.kv_from_tensors(self.k[r], self.v[r]) for r in range(replicas)]
+
+        self.seg = torch.from_numpy(np.stack([wl.seg(s) for s in self.steps]).astype(np.int32)).to(dev)
+        self.pol = torch.from_numpy(np.ascontiguousarray(wl.policy, dtype=np.int32)).to(dev)
+        self.q = torch.from_numpy(np.stack([wl.q(s) for s in self.steps])).view(torch.bfloat16).to(dev)
+
+        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
+        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.ranges = torch.zeros((B, M.N_PIECES, 2), dtype=torch.int32, device=dev)
+        odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
+        self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
+        self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
+        self.ws_bytes = M.murmur_decode_attn_workspace(NL, B, Hq, Hkv, self.max_keep, split_len)
+        self.ws = torch.zeros(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.int32, device=dev)
+
+    def evict(self, i: int, stream=None) -> None:
+        """murmur_evict_compact for the i-th step of this batch."""
+        M.murmur_evict_compact(self.seg[i], self.pol, 1, self.B, self.idx, self.max_keep, self.count, self.ranges,
+                               stream)
+
+    def attend(self, i: int, replica: int = 0, stream=None) -> None:
+        """murmur_decode_attn for the i-th step, reading K/V replica `replica`."""
+        M.murmur_decode_attn(self.q[i], self.kv[replica], self.idx, self.ranges if self.use_ranges else None,
+                             self.count, self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale,
+                             self.split_len, self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes, stream)
+
+    def step(self, i: int, replica: int = 0, stream=None) -> None:
+        self.evict(i, stream)
+        self.attend(i, replica, stream)
+
+    def kv_bytes_read(self, i: int) -> int:
+        """Algorithmic K/V bytes of step i: retained positions x layers x KV heads x (K + V) x D x 2 B."""
+        counts, _ = M.murmur_retained_count_host(self.wl.seg(self.steps[i]), self.wl.policy, 1)
+        return int(counts.sum()) * self.NL * self.Hkv * 2 * self.D * 2
+
+    def io_bytes(self) -> int:
+        """Algorithmic bytes besides K/V: queries, outputs, lse, count and range table (or index list)."""
+        out_b = 4 if self.out_dtype == M.MURMUR_DTYPE_F32 else 2
+        n = self.NL * self.B * self.Hq
+        sel = self.B * M.N_PIECES * 2 * 4 if self.use_ranges else self.B * self.max_keep * 4
+        return n * self.D * 2 + n * self.D * out_b + n * 4 + self.B * 4 + sel

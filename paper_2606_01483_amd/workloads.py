@@ -19,8 +19,10 @@ the caches.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import math
+import os
 
 import numpy as np
 
@@ -37,9 +39,12 @@ BF16_NAN = np.uint16(0x7FC0)
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round fp32 values to bf16 (round to nearest, ties to even); returns uint16 bit patterns."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+    odd = (u >> np.uint32(16)) & np.uint32(1)
+    u += np.uint32(0x7FFF)
+    u += odd
+    u >>= np.uint32(16)
+    return u.astype(np.uint16)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -99,11 +104,19 @@ class Workload:
 
 
 def _draw_cache(seed: int, stream: int, shape: tuple[int, ...]) -> np.ndarray:
-    """N(0,1) bf16 bits, drawn layer by layer to bound peak memory."""
+    """N(0,1) bf16 bits.  Each (layer, sequence) slab has its own stream, so the result does not depend
+    on how many threads draw it (numpy releases the GIL while filling and converting)."""
     out = np.empty(shape, dtype=np.uint16)
-    for layer in range(shape[0]):
-        rng = _rng(seed, stream, layer)
-        out[layer] = f32_to_bf16_bits(rng.standard_normal(shape[1:], dtype=np.float32))
+
+    def fill(lb: tuple[int, int]) -> None:
+        layer, b = lb
+        rng = _rng(seed, stream, layer, b)
+        out[layer, b] = f32_to_bf16_bits(rng.standard_normal(shape[2:], dtype=np.float32))
+
+    jobs = [(layer, b) for layer in range(shape[0]) for b in range(shape[1])]
+    workers = max(1, min(16, len(os.sched_getaffinity(0)), len(jobs)))
+    with concurrent.futures.ThreadPoolExecutor(workers) as pool:
+        list(pool.map(fill, jobs))
     return out
 
 
@@ -147,7 +160,30 @@ def build(name: str, seed: int, n_layers: int, seg0: np.ndarray, policy: np.ndar
 OFF = -1  # window value that disables eviction for a region
 
 
+@dataclasses.dataclass
+class Layout:
+    """Sizes and policy of a workload without its caches (enough for the retained sets)."""
+    name: str
+    seed: int
+    n_layers: int
+    steps: int
+    seg0: np.ndarray
+    policy: np.ndarray
+    planted: bool
+
+    def seg(self, step: int) -> np.ndarray:
+        s = self.seg0.copy()
+        s[:, 3] += step + 1
+        return s
+
+
 def make(config: str, steps: int | None = None) -> Workload:
+    """The five workloads of the evaluation, with caches drawn (see layout())."""
+    lay = layout(config, steps)
+    return build(lay.name, lay.seed, lay.n_layers, lay.seg0, lay.policy, lay.steps, planted=lay.planted)
+
+
+def layout(config: str, steps: int | None = None) -> Layout:
     """The five workloads of the evaluation.
 
     c1        Tiny: 1 layer, batch 1, 32 prompt + 450 speech (60 s) + 64 output tokens,
@@ -165,7 +201,7 @@ def make(config: str, steps: int | None = None) -> Workload:
         seed = 1001
         seg0 = np.array([[32, 450, 0, 64]], dtype=np.int32)
         pol = np.array([128, 72, 0, 32, 0], dtype=np.int32)
-        return build("c1", seed, 1, seg0, pol, steps or 16, planted=False)
+        return _layout("c1", seed, 1, seg0, pol, steps or 16, planted=False)
     if config in ("c2", "c3"):
         seed = 1002 if config == "c2" else 1003
         rng = _rng(seed, _S_LAYOUT)
@@ -173,9 +209,9 @@ def make(config: str, steps: int | None = None) -> Workload:
         seg0 = np.stack([np.full(12, 32), np.full(12, 2250), np.zeros(12), out0], axis=1).astype(np.int32)
         if config == "c2":
             pol = np.array([OFF, 0, 0, OFF, 0], dtype=np.int32)
-            return build("c2", seed, 1, seg0, pol, steps or 64, planted=False)
+            return _layout("c2", seed, 1, seg0, pol, steps or 64, planted=False)
         pol = np.array([2250 // 4, 512, 0, 256, 0], dtype=np.int32)
-        return build("c3", seed, 1, seg0, pol, steps or 64, planted=True)
+        return _layout("c3", seed, 1, seg0, pol, steps or 64, planted=True)
     if config in ("c4_dense", "c4_evict"):
         seed = 1004
         seg0 = np.array([[32, 27000, 0, 8000]], dtype=np.int32)
@@ -183,7 +219,7 @@ def make(config: str, steps: int | None = None) -> Workload:
             pol = np.array([OFF, 0, 0, OFF, 0], dtype=np.int32)
         else:
             pol = np.array([2048, 512, 0, 512, 0], dtype=np.int32)
-        return build(config, seed, 1, seg0, pol, steps or 128, planted=False)
+        return _layout(config, seed, 1, seg0, pol, steps or 128, planted=False)
     if config == "c5":
         seed = 1005
         rng = _rng(seed, _S_LAYOUT)
@@ -192,8 +228,16 @@ def make(config: str, steps: int | None = None) -> Workload:
         seg0 = np.stack([np.full(12, 32), l_s, np.zeros(12), out0], axis=1).astype(np.int32)
         pol = np.stack([l_s // 4, np.full(12, 512), np.zeros(12), np.full(12, 256), np.zeros(12)],
                        axis=1).astype(np.int32)
-        return build("c5", seed, 28, seg0, pol, steps or 256, planted=True)
+        return _layout("c5", seed, 28, seg0, pol, steps or 256, planted=True)
     raise KeyError(f"unknown workload {config!r}")
+
+
+def _layout(name, seed, n_layers, seg0, pol, steps, planted) -> Layout:
+    seg0 = np.ascontiguousarray(seg0, dtype=np.int32)
+    pol = np.ascontiguousarray(pol, dtype=np.int32)
+    if pol.ndim == 1:
+        pol = np.repeat(pol.reshape(1, 5), seg0.shape[0], axis=0)
+    return Layout(name=name, seed=seed, n_layers=n_layers, steps=steps, seg0=seg0, policy=pol, planted=planted)
 
 
 CONFIGS = ("c1", "c2", "c3", "c4_dense", "c4_evict", "c5")

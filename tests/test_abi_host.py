@@ -1,0 +1,159 @@
+"""Host-side checks of the C ABI (no GPU): exported symbols, argument validation, sizing.
+
+Every call here is rejected by the host-side checks, which run before any HIP
+call, so nothing reaches a device.  The module is skipped where a GPU is
+visible, so that no malformed pointer could ever be launched on one.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_01483_amd import _build
+from paper_2606_01483_amd import murmur as M
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OFF = -1
+
+pytestmark = pytest.mark.skipif(torch.cuda.device_count() > 0, reason="host-only checks run where no GPU is visible")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    if not os.path.exists(M.LIB_PATH):
+        _build.build()
+    M.lib()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "murmur.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(murmur_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) == 8
+    lib = ctypes.CDLL(M.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_abi_version():
+    assert M.murmur_abi_version() == 1
+
+
+def test_retained_count_host_matches_oracle():
+    rng = np.random.default_rng(3)
+    B = 300
+    seg = np.stack([rng.integers(0, 40, B), rng.integers(0, 400, B), rng.integers(0, 20, B),
+                    rng.integers(1, 500, B)], axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 300, B)), rng.integers(0, 300, B),
+                    rng.integers(0, 30, B), np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 300, B)),
+                    rng.integers(0, 30, B)], axis=1).astype(np.int32)
+    counts, mx = M.murmur_retained_count_host(seg, pol, 1)
+    _, ref = oracle.retained(seg, pol)
+    assert np.array_equal(counts, ref) and mx == ref.max()
+
+
+@pytest.mark.parametrize("seg,pol", [
+    ([0, 5, 0, 0], [OFF, 0, 0, OFF, 0]),
+    ([0, 5, 0, 3], [0, 0, 0, OFF, 0]),
+    ([0, 5, 0, 3], [OFF, 0, 0, 0, 0]),
+    ([0, 5, 0, 3], [-2, 0, 0, OFF, 0]),
+    ([0, 5, 0, 3], [2, -1, 0, OFF, 0]),
+    ([0, 5, 0, 3], [2, 0, -1, OFF, 0]),
+    ([0, 5, 0, 3], [2, 0, 0, OFF, -3]),
+    ([-1, 5, 0, 3], [OFF, 0, 0, OFF, 0]),
+    ([0x7fffffff, 5, 0, 3], [OFF, 0, 0, OFF, 0]),
+])
+def test_retained_count_host_rejects_invalid(seg, pol):
+    with pytest.raises(M.MurmurError) as e:
+        M.murmur_retained_count_host(np.array([seg]), np.array(pol))
+    assert e.value.code == M.MURMUR_EINVAL
+    assert "invalid layout or policy" in M.murmur_last_error()
+
+
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def attn_args(**over):
+    a = dict(q=FAKE, kv=M.murmur_kv(FAKE, FAKE, 1, 4096, 4096 * 128 * 4, 4096 * 128 * 4, 4096 * 128, 128),
+             idx=FAKE, ranges=None, count=FAKE, max_keep=850, B=12, Hq=28, Hkv=4, D=128, scale=1.0, split_len=0,
+             out=FAKE, out_dtype=M.MURMUR_DTYPE_BF16, lse=None, ws=FAKE, ws_bytes=1 << 30)
+    a.update(over)
+    return a
+
+
+def call_attn(a):
+    return M.lib().murmur_decode_attn(a["q"], ctypes.byref(a["kv"]), a["idx"], a["ranges"], a["count"],
+                                      a["max_keep"], a["B"], a["Hq"], a["Hkv"], a["D"], a["scale"], a["split_len"],
+                                      a["out"], a["out_dtype"], a["lse"], a["ws"], a["ws_bytes"], 0)
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(q=None), M.MURMUR_EINVAL),
+    (dict(out=None), M.MURMUR_EINVAL),
+    (dict(ws=None), M.MURMUR_EINVAL),
+    (dict(count=None), M.MURMUR_EINVAL),
+    (dict(idx=None, ranges=None), M.MURMUR_EINVAL),
+    (dict(B=0), M.MURMUR_EINVAL),
+    (dict(max_keep=0), M.MURMUR_EINVAL),
+    (dict(Hq=30), M.MURMUR_EINVAL),
+    (dict(D=64), M.MURMUR_EUNSUPPORTED),
+    (dict(Hq=68, Hkv=4), M.MURMUR_EUNSUPPORTED),
+    (dict(out_dtype=7), M.MURMUR_EINVAL),
+    (dict(scale=float("nan")), M.MURMUR_EINVAL),
+    (dict(scale=float("inf")), M.MURMUR_EINVAL),
+    (dict(split_len=100), M.MURMUR_EINVAL),
+    (dict(split_len=-128), M.MURMUR_EINVAL),
+    (dict(q=FAKE + 8), M.MURMUR_EINVAL),
+    (dict(ws=FAKE + 64), M.MURMUR_EINVAL),
+    (dict(lse=FAKE + 2), M.MURMUR_EINVAL),
+    (dict(kv=M.murmur_kv(FAKE, FAKE, 1, 4096, 0, 0, 0, 100)), M.MURMUR_EINVAL),   # stride not a multiple of 8
+    (dict(kv=M.murmur_kv(FAKE, FAKE, 1, 4096, 0, 0, 0, 64)), M.MURMUR_EINVAL),    # rows overlap
+    (dict(kv=M.murmur_kv(FAKE, None, 1, 4096, 0, 0, 0, 128)), M.MURMUR_EINVAL),
+    (dict(kv=M.murmur_kv(FAKE, FAKE, 0, 4096, 0, 0, 0, 128)), M.MURMUR_EINVAL),
+    (dict(kv=M.murmur_kv(FAKE + 4, FAKE, 1, 4096, 0, 0, 0, 128)), M.MURMUR_EINVAL),
+    (dict(ws_bytes=1000), M.MURMUR_ENOSPACE),
+])
+def test_decode_attn_rejects(over, code):
+    assert call_attn(attn_args(**over)) == code
+    assert M.murmur_last_error() != ""
+
+
+def test_evict_compact_rejects():
+    lib = M.lib()
+    assert lib.murmur_evict_compact(None, FAKE, 0, 12, FAKE, 10, FAKE, None, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_evict_compact(FAKE, FAKE, 0, 0, FAKE, 10, FAKE, None, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_evict_compact(FAKE, FAKE, 0, 12, FAKE, 0, FAKE, None, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_evict_compact(FAKE, FAKE, 2, 12, FAKE, 10, FAKE, None, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_evict_compact(FAKE, FAKE, 0, 12, FAKE + 2, 10, FAKE, None, 0) == M.MURMUR_EINVAL
+
+
+def test_workspace_sizing():
+    ws = M.murmur_decode_attn_workspace(1, 12, 28, 4, 850)
+    # 48 tickets; 7 splits of 128 positions: 48*7*7 partials of (m, l) and 128 outputs
+    assert ws == 256 + (48 * 7 * 7 * 2 * 4 + 255) // 256 * 256 + (48 * 7 * 7 * 128 * 4 + 255) // 256 * 256
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 100) == 256  # one split: tickets only
+    assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 1024) == 256
+    # long lists are capped at 64 splits
+    big = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160)
+    n_split = -(-35160 // (128 * -(-(-(-35160 // 128)) // 64)))
+    assert n_split <= 64
+    assert big == 256 + (4 * n_split * 7 * 2 * 4 + 255) // 256 * 256 + (4 * n_split * 7 * 128 * 4 + 255) // 256 * 256
+    with pytest.raises(M.MurmurError):
+        M.murmur_decode_attn_workspace(1, 12, 28, 5, 850)
+    with pytest.raises(M.MurmurError):
+        M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 64)
+
+
+def test_workspace_init_and_device_error_reject_null():
+    lib = M.lib()
+    assert lib.murmur_decode_attn_workspace_init(None, 1024, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_decode_attn_workspace_init(FAKE + 4, 1024, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_device_error(0, None) == M.MURMUR_EINVAL

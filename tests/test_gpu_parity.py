@@ -1,0 +1,275 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle (paper Section 3.2).
+
+Retained lists must match bit for bit; attention outputs must meet the
+criteria in _tol.py.  Every case prints its name before it touches the GPU.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_01483_amd import murmur as M
+from paper_2606_01483_amd import workloads as W
+from paper_2606_01483_amd.decode import DecodeBatch
+from _tol import REL_TOL, LSE_TOL, bf16_excess, lse_err, rel_err_fp32
+
+pytestmark = pytest.mark.gpu
+OFF = -1
+THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def announce(msg):
+    print(f"\n[case] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    M.lib()
+    yield
+    torch.cuda.synchronize()
+    assert M.murmur_device_error() == 0
+
+
+def expand(ranges_row):
+    out = []
+    for start, length in ranges_row:
+        out.extend(range(int(start), int(start) + int(length)))
+    return out
+
+
+def gpu_evict(seg, pol, max_keep, per_seq=1):
+    B = seg.shape[0]
+    seg_d = torch.from_numpy(np.ascontiguousarray(seg, dtype=np.int32)).cuda()
+    pol_d = torch.from_numpy(np.ascontiguousarray(pol, dtype=np.int32)).cuda()
+    idx = torch.full((B, max_keep), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    rng = torch.full((B, 6, 2), -7, dtype=torch.int32, device="cuda")
+    M.murmur_evict_compact(seg_d, pol_d, per_seq, B, idx, max_keep, cnt, rng)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), cnt.cpu().numpy(), rng.cpu().numpy()
+
+
+def check_evict(seg, pol):
+    ref_idx, ref_cnt = oracle.retained(seg, pol)
+    max_keep = ref_idx.shape[1]
+    idx, cnt, rng = gpu_evict(seg, pol, max_keep)
+    assert np.array_equal(cnt, ref_cnt)
+    assert np.array_equal(idx, ref_idx)
+    for b in range(seg.shape[0]):
+        assert expand(rng[b]) == ref_idx[b, :ref_cnt[b]].tolist()
+        assert np.all(rng[b, :, 1] >= 0)
+
+
+# ---- evict_compact: bit-exact ---------------------------------------------------------------------
+
+@pytest.mark.parametrize("config", W.CONFIGS)
+def test_evict_workloads_bitexact(config):
+    lay = W.layout(config)
+    for step in sorted({0, lay.steps // 2, lay.steps - 1}):
+        announce(f"evict {config} step {step}")
+        check_evict(lay.seg(step), lay.policy)
+
+
+def test_evict_edge_layouts_bitexact():
+    announce("evict edge layouts")
+    rows = [  # (seg, policy)
+        ([0, 0, 0, 1], [OFF, 0, 0, OFF, 0]),          # a single position
+        ([5, 40, 7, 30], [8, 3, 2, 6, 2]),             # prompt_mid > 0, both sinks
+        ([5, 40, 7, 3], [8, 3, 2, 6, 2]),              # j < output window
+        ([2, 20, 0, 200], [8, 0, 0, 6, 0]),            # window clamped at the end of speech
+        ([2, 20, 0, 9], [4, 0, 10, 6, 0]),             # sinks cover the window
+        ([3, 10, 1, 5], [10, 0, 0, 5, 0]),             # windows exactly the region length
+        ([3, 0, 4, 12], [5, 2, 1, 3, 20]),             # no speech; output sinks beyond j
+        ([0, 64, 0, 64], [1, 1, 0, 1, 0]),             # one-token windows
+        ([32, 2250, 0, 1264], [562, 512, 0, 256, 0]),  # the 300 s eviction workload at its last step
+    ]
+    seg = np.array([r[0] for r in rows], dtype=np.int32)
+    pol = np.array([r[1] for r in rows], dtype=np.int32)
+    check_evict(seg, pol)
+
+
+def test_evict_random_layouts_bitexact():
+    announce("evict 600 random layouts")
+    rng = np.random.default_rng(2024)
+    B = 600
+    seg = np.stack([rng.integers(0, 40, B), rng.integers(0, 400, B), rng.integers(0, 20, B),
+                    rng.integers(1, 500, B)], axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 300, B)), rng.integers(0, 300, B),
+                    rng.integers(0, 30, B), np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 300, B)),
+                    rng.integers(0, 30, B)], axis=1).astype(np.int32)
+    check_evict(seg, pol)
+
+
+def test_evict_overflow_and_policy_errors():
+    announce("evict device errors")
+    seg = np.array([[4, 10, 0, 3], [4, 10, 0, 3]], dtype=np.int32)
+    pol = np.array([[OFF, 0, 0, OFF, 0], [0, 0, 0, OFF, 0]], dtype=np.int32)  # row 1: window 0 is invalid
+    idx, cnt, rng = gpu_evict(seg, pol, max_keep=5)
+    code = M.murmur_device_error()
+    assert code == M.MURMUR_DEVERR_OVERFLOW | M.MURMUR_DEVERR_POLICY
+    assert cnt.tolist() == [17, 0]
+    assert idx[0].tolist() == [0, 1, 2, 3, 4] and idx[1].tolist() == [-1] * 5
+    assert M.murmur_device_error() == 0
+
+
+# ---- decode_attn against the oracle ------------------------------------------------------------------
+
+def oracle_step(wl, step, layers=None, batch=None):
+    seg = wl.seg(step)
+    idx, cnt = oracle.retained(seg, wl.policy)
+    q, k, v = wl.q(step), wl.k, wl.v
+    if layers is not None:
+        q, k, v = q[layers], k[layers], v[layers]
+    if batch is not None:
+        q, k, v, idx, cnt = q[:, batch], k[:, batch], v[:, batch], idx[batch], cnt[batch]
+    return oracle.attend(q, k, v, idx, cnt, scale=wl.scale, n_threads=THREADS)
+
+
+def run_gpu(db, i, replica=0):
+    db.step(i, replica)
+    torch.cuda.synchronize()
+    return db.out.float().cpu().numpy().astype(np.float64), db.lse.cpu().numpy().astype(np.float64)
+
+
+_cache = {}
+
+
+def workload(name):
+    if name not in _cache:
+        _cache[name] = W.make(name)
+    return _cache[name]
+
+
+def test_attn_tiny_all_steps():
+    wl = workload("c1")
+    db32 = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32)
+    db16 = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_BF16)
+    for i in range(wl.steps):
+        announce(f"attn c1 step {i}")
+        ref, ref_lse = oracle_step(wl, i)
+        y32, l32 = run_gpu(db32, i)
+        y16, _ = run_gpu(db16, i)
+        assert rel_err_fp32(y32, ref) <= REL_TOL
+        assert lse_err(l32, ref_lse) <= LSE_TOL
+        assert bf16_excess(y16, ref) <= REL_TOL
+
+
+@pytest.mark.parametrize("config", ["c2", "c3", "c4_dense", "c4_evict"])
+def test_attn_workloads(config):
+    wl = workload(config)
+    steps = sorted({0, wl.steps // 2, wl.steps - 1})
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps)
+    for i, s in enumerate(steps):
+        announce(f"attn {config} step {s}")
+        ref, ref_lse = oracle_step(wl, s)
+        y, l = run_gpu(db, i)
+        e = rel_err_fp32(y, ref)
+        print(f"  max rel err {e:.3e}  lse err {lse_err(l, ref_lse):.3e}", flush=True)
+        assert e <= REL_TOL
+        assert lse_err(l, ref_lse) <= LSE_TOL
+
+
+def test_attn_28_layers_sampled():
+    """The 28-layer workload at full size: every output is computed on the GPU in one launch per step;
+    the oracle checks a sample of (layer, sequence) pairs and the bf16 store path."""
+    wl = workload("c5")
+    steps = [0, wl.steps - 1]
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_BF16, steps=steps)
+    rng = np.random.default_rng(5)
+    for i, s in enumerate(steps):
+        announce(f"attn c5 step {s} (28 layers)")
+        y, l = run_gpu(db, i)
+        assert np.all(np.isfinite(y)) and np.all(np.isfinite(l))
+        for layer, b in zip(rng.choice(28, 4, replace=False), rng.choice(12, 4, replace=False)):
+            ref, ref_lse = oracle_step(wl, s, layers=[layer], batch=[b])
+            assert bf16_excess(y[layer:layer + 1, b:b + 1], ref) <= REL_TOL
+            assert lse_err(l[layer:layer + 1, b:b + 1], ref_lse) <= LSE_TOL
+
+
+def test_split_count_invariance():
+    wl = workload("c3")
+    ref, ref_lse = oracle_step(wl, 0)
+    outs = []
+    for split_len in (0, 128, 256, 512, 1024):
+        announce(f"attn c3 split_len {split_len}")
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, split_len=split_len, steps=[0])
+        y, l = run_gpu(db, 0)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+        outs.append(y)
+    for y in outs[1:]:
+        assert rel_err_fp32(y, outs[0]) <= 1e-4
+
+
+def test_index_mode_matches_range_mode_and_is_deterministic():
+    wl = workload("c3")
+    announce("attn c3 index vs range mode")
+    a = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[5], use_ranges=True)
+    b = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[5], use_ranges=False)
+    ya, la = run_gpu(a, 0)
+    yb, lb = run_gpu(b, 0)
+    assert np.array_equal(ya, yb) and np.array_equal(la, lb)
+    yc, lc = run_gpu(a, 0)
+    assert np.array_equal(ya, yc) and np.array_equal(la, lc)
+    # the workspace tickets are back at zero after every call
+    assert int(a.ws[: a.B * a.Hkv].abs().sum().item()) == 0
+
+
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (4, 4), (16, 1), (12, 3)])
+def test_attn_edge_shapes(hq, hkv):
+    announce(f"attn edge shapes hq={hq} hkv={hkv}")
+    seg0 = np.array([[0, 0, 0, 0], [5, 40, 7, 2], [3, 300, 2, 100], [1, 9, 0, 400]], dtype=np.int32)
+    pol = np.array([[OFF, 0, 0, OFF, 0], [8, 3, 2, 6, 2], [64, 10, 4, 16, 1], [OFF, 0, 0, 128, 3]], dtype=np.int32)
+    wl = W.build("edge", 77, 3, seg0, pol, steps=3, planted=False, hq=hq, hkv=hkv)
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32)
+    for i in range(wl.steps):
+        ref, ref_lse = oracle_step(wl, i)
+        y, l = run_gpu(db, i)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+
+
+def test_attn_strided_cache_layout():
+    """K/V stored [layer][kv head][sequence][pos] with padded rows: only the strides change."""
+    announce("attn strided cache layout")
+    wl = workload("c3")
+    ref, ref_lse = oracle_step(wl, 3)
+    NL, B, Hkv, L, D = wl.k.shape
+    pad = 136
+    def relayout(x):
+        t = torch.zeros((NL, Hkv, B, L, pad), dtype=torch.bfloat16, device="cuda")
+        t[..., :D] = torch.from_numpy(x).view(torch.bfloat16).cuda().permute(0, 2, 1, 3, 4)
+        return t
+    kt, vt = relayout(wl.k), relayout(wl.v)
+    kv = M.make_kv(kt, vt, NL, L, (kt.stride(0), kt.stride(2), kt.stride(1), kt.stride(3)))
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[3])
+    db.evict(0)
+    M.murmur_decode_attn(db.q[0], kv, db.idx, db.ranges, db.count, db.max_keep, B, wl.hq, Hkv, D, wl.scale, 0,
+                         db.out, M.MURMUR_DTYPE_F32, db.lse, db.ws, db.ws_bytes)
+    torch.cuda.synchronize()
+    y = db.out.cpu().numpy().astype(np.float64)
+    assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(db.lse.cpu().numpy(), ref_lse) <= LSE_TOL
+
+
+def test_attn_device_errors_give_nan():
+    """A position outside the cache (index mode) and a count above max_keep are caught by the kernel's
+    own bounds checks: nothing outside the cache is read, the sequence's outputs are NaN and the
+    device error word says why."""
+    announce("attn device errors")
+    wl = workload("c1")
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[0], use_ranges=False)
+    db.evict(0)
+    torch.cuda.synchronize()
+    db.idx[0, 3] = wl.max_len + 5
+    db.attend(0)
+    torch.cuda.synchronize()
+    assert M.murmur_device_error() == M.MURMUR_DEVERR_POSITION
+    assert torch.isnan(db.out).all().item()
+    db.evict(0)
+    db.count.fill_(db.max_keep + 1)
+    db.attend(0)
+    torch.cuda.synchronize()
+    assert M.murmur_device_error() == M.MURMUR_DEVERR_COUNT
+    assert torch.isnan(db.out).all().item()
