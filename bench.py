@@ -53,11 +53,13 @@ def log(msg: str) -> None:
 def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
     import oracle
     oracle.build()
+    qs = [wl.q(s) for s in range(wl.steps)]
     t0 = time.perf_counter()
     n = 0
-    while n < wl.steps:
-        idx, cnt = oracle.retained(wl.seg(n), wl.policy)
-        oracle.attend(wl.q(n), wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=threads)
+    while True:
+        s = n % wl.steps
+        idx, cnt = oracle.retained(wl.seg(s), wl.policy)
+        oracle.attend(qs[s], wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=threads)
         n += 1
         if time.perf_counter() - t0 > budget_s:
             break

@@ -178,8 +178,9 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  *   D:          head_dim, must be 128; Hq/Hkv must be in [1, 16];
  *   scale:      logit scale (1/sqrt(D) for unscaled queries), finite;
  *   split_len:  retained positions per split (a multiple of 128), 0 = automatic;
- *   out_dev:    [n_layers][B][Hq][D] of out_dtype (MURMUR_DTYPE_BF16 rounds to
- *               nearest even, MURMUR_DTYPE_F32 stores the fp32 accumulation);
+ *   out_dev:    [n_layers][B][Hq][D] of out_dtype, 16-byte aligned
+ *               (MURMUR_DTYPE_BF16 rounds to nearest even, MURMUR_DTYPE_F32
+ *               stores the fp32 accumulation);
  *   lse_dev:    nullable fp32 [n_layers][B][Hq], natural log;
  *   ws_dev:     workspace of ws_bytes >= murmur_decode_attn_workspace(...).
  * Accumulation is fp32 throughout.  Errors: MURMUR_EINVAL, MURMUR_EUNSUPPORTED,

@@ -168,7 +168,7 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
         return fail(MURMUR_EINVAL, "kv->stride_pos (%lld) must be >= head_dim", (long long)kv->stride_pos);
     if (!aligned(q_dev, 16) || !aligned(kv->k, 16) || !aligned(kv->v, 16))
         return fail(MURMUR_EINVAL, "q_dev, kv->k and kv->v must be 16-byte aligned");
-    if (!aligned(out_dev, out_dtype == MURMUR_DTYPE_F32 ? 4 : 2) || !aligned(lse_dev, 4) ||
+    if (!aligned(out_dev, 16) || !aligned(lse_dev, 4) ||
         !aligned(count_dev, 4) || !aligned(idx_dev, 4) || !aligned(ranges_dev, 4))
         return fail(MURMUR_EINVAL, "out/lse/count/idx/ranges pointers are misaligned");
     if (!aligned(ws_dev, 256)) return fail(MURMUR_EINVAL, "ws_dev must be 256-byte aligned");
@@ -176,6 +176,9 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
     if (ws_bytes < plan.total)
         return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
+    if (plan.n_split > kMaxMergeSplits)
+        return fail(MURMUR_EINVAL, "split_len %d gives %d splits for max_keep %d; at most %d are supported",
+                    plan.split_len, plan.n_split, max_keep, kMaxMergeSplits);
     const int64_t grid = plan.groups * plan.n_split;
     if (grid > 0x7fffffffLL || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
         return fail(MURMUR_EINVAL, "problem too large for one launch (%lld workgroups)", (long long)grid);

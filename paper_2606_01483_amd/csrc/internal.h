@@ -15,6 +15,10 @@ constexpr int kWaveTile = 32;     // retained positions one wavefront handles pe
 constexpr int kWavesPerWg = 4;
 constexpr int kSplitUnit = kWaveTile * kWavesPerWg;  // 128 positions: one pass of a workgroup
 constexpr int kMaxAutoSplits = 64;
+// Splits one merge can combine: it stages 2 * n_split * G + 2 * G floats in
+// the workgroup's 32 KiB of V-tile LDS.
+constexpr int kMaxMergeSplits = 240;
+constexpr int kMergeBatch = 8;  // splits whose partials one merging thread loads at once
 
 // Launch description of one decode_attn call, fully validated by the caller.
 struct AttnLaunch {

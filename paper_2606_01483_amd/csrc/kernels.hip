@@ -98,6 +98,15 @@ static __device__ __forceinline__ uint32_t bf16_rne(float f) {
 
 static __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __builtin_bit_cast(float, bits16 << 16); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values -> packed bf16 pair (x in the low half), round to nearest
+// even: one v_cvt_pk_bf16_f32 on gfx950.
+static __device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
+    const bf16x2 v = {(__bf16)x, (__bf16)y};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 // Rank r of the retained list -> global position, from the six-piece table.
 static __device__ __forceinline__ int rank_to_pos(const int32_t (&rg)[2 * kPieces], int r) {
 #pragma unroll
@@ -121,9 +130,66 @@ static __device__ __forceinline__ int vt_unit(int d, int q) {
 constexpr int kVtBytesPerWave = 4 * 128 * 16;  // 8 KiB
 constexpr float kNegInf = -__builtin_huge_valf();
 
+// Device-coherent (scope: agent) accesses for the split partials.  On gfx950
+// they compile to sc1 loads and stores, which bypass the per-XCD L2's
+// non-coherent copies, so the partials need no L2 writeback or invalidate --
+// the __threadfence() route costs a full L2 write-back per wavefront.
+static __device__ __forceinline__ void store_coherent(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+static __device__ __forceinline__ float load_coherent(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until every vector-memory access of this wavefront has completed; also a
+// compiler barrier, so no store is moved past it.
+static __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Reductions over the four lanes n16 + 16*c4 (c4 = 0..3) that share a head
+// column, with the gfx950 lane-swap instructions: after
+// v_permlane16_swap(a, b) with a == b on entry, {a, b} holds {x[l], x[l^16]}
+// in every lane l; v_permlane32_swap likewise pairs lane l with l^32.  Pure
+// VALU, no LDS round trip.  Written as inline assembly: the compiler's own
+// builtins for these instructions fold the two results of a swap into one
+// when both feed a commutative operation.  The s_nop pairs cover the wait
+// states these instructions need around VALU writes and reads of their
+// operands.
+static __device__ __forceinline__ void swap16(uint32_t &a, uint32_t &b) {
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+static __device__ __forceinline__ void swap32(uint32_t &a, uint32_t &b) {
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+static __device__ __forceinline__ float max_over_c4(float x) {
+    uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+    swap16(a, b);
+    x = fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+    a = b = __builtin_bit_cast(uint32_t, x);
+    swap32(a, b);
+    return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+static __device__ __forceinline__ float sum_over_c4(float x) {
+    uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+    swap16(a, b);
+    x = __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+    a = b = __builtin_bit_cast(uint32_t, x);
+    swap32(a, b);
+    return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+
+// K and V fragments of one pass of kWaveTile retained positions.
+struct PassRegs {
+    u32x4 kf[2][4];  // MFMA A operands: position 16*blk + n16, head dims kc*32 + 8*c4 .. +8
+    u32x4 vf[8];     // position 8*c4 + t, head dims 8*n16 .. +8
+};
+
 // ---------------------------------------------------------------------------
-// decode_attn: one workgroup per (split, KV head, sequence, layer).
+// decode_attn: one workgroup per (split, KV head, sequence, layer).  Each of
+// its four wavefronts takes passes of 32 retained positions, interleaved over
+// the split.  kMultiPass: splits longer than one workgroup pass keep an online
+// softmax across passes and have the next pass's loads in flight while the
+// current one is computed; otherwise every wavefront makes at most one pass.
 // ---------------------------------------------------------------------------
+template <bool kMultiPass>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
     __shared__ float ml_lds[kWavesPerWg][kMaxGroup][2];
@@ -176,10 +242,10 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
 #pragma unroll
     for (int db = 0; db < 8; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int r0 = r_begin + wave * kWaveTile; r0 < r_end; r0 += kSplitUnit) {
-        // Position of rank r0 + (lane & 31); -1 past the split or if invalid.
+    // Positions of the pass starting at rank r0, then every K and V load of it.
+    auto issue = [&](int r0, PassRegs &R) {
         const int myrank = r0 + (lane & 31);
-        int mypos = -1;
+        int mypos = -1;  // position of rank r0 + (lane & 31); -1 past the split or if invalid
         if (myrank < r_end) {
             const int p = use_ranges ? rank_to_pos(rg, myrank) : idx_row[myrank];
             if (p >= 0 && p < a.max_len)
@@ -187,27 +253,23 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
             else
                 bad_pos = 1;
         }
-        int kpos[2], vpos[8];
-        kpos[0] = __shfl(mypos, n16);
-        kpos[1] = __shfl(mypos, 16 + n16);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) vpos[t] = __shfl(mypos, 8 * c4 + t);
-
-        // Issue every K and V load of the pass before any use.
-        u32x4 kf[2][4], vf[8];
 #pragma unroll
         for (int blk = 0; blk < 2; ++blk) {
-            const uint16_t *row = kbase + (int64_t)(kpos[blk] < 0 ? 0 : kpos[blk]) * a.s_pos;
+            const int pos = __shfl(mypos, 16 * blk + n16);
+            const uint16_t *row = kbase + (int64_t)(pos < 0 ? 0 : pos) * a.s_pos;
 #pragma unroll
             for (int kc = 0; kc < 4; ++kc)
-                kf[blk][kc] = kpos[blk] >= 0 ? load16(row + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
+                R.kf[blk][kc] = pos >= 0 ? load16(row + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
         }
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-            const uint16_t *row = vbase + (int64_t)(vpos[t] < 0 ? 0 : vpos[t]) * a.s_pos;
-            vf[t] = vpos[t] >= 0 ? load16(row + 8 * n16) : u32x4{0, 0, 0, 0};
+            const int pos = __shfl(mypos, 8 * c4 + t);
+            const uint16_t *row = vbase + (int64_t)(pos < 0 ? 0 : pos) * a.s_pos;
+            R.vf[t] = pos >= 0 ? load16(row + 8 * n16) : u32x4{0, 0, 0, 0};
         }
+    };
 
+    auto consume = [&](int r0, const PassRegs &R) {
         // S^T = K Q^T: lane (head n16, c4), register i of block blk holds the
         // logit of rank r0 + 16*blk + 4*c4 + i.
         f32x4 s[2];
@@ -215,69 +277,73 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
         for (int blk = 0; blk < 2; ++blk) {
             s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(kf[blk][kc], qf[kc], s[blk]);
+            for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(R.kf[blk][kc], qf[kc], s[blk]);
         }
 
+        // Logits in log2 units; ranks past the split end are masked (only a
+        // wavefront's last, partial pass has any).
         float x[2][4];
-        float tmax = kNegInf;
+        const bool partial = r_end - r0 < kWaveTile;
 #pragma unroll
         for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int rank = r0 + 16 * blk + 4 * c4 + i;
-                x[blk][i] = rank < r_end ? s[blk][i] * a.scale_log2 : kNegInf;
-                tmax = fmaxf(tmax, x[blk][i]);
+                x[blk][i] = s[blk][i] * a.scale_log2;
+                if (partial && 16 * blk + 4 * c4 + i >= r_end - r0) x[blk][i] = kNegInf;
             }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-        const float m_new = fmaxf(m_run, tmax);  // finite: rank r0 is always valid
-        const float alpha = exp2f(m_run - m_new);
+        float tmax = fmaxf(fmaxf(fmaxf(x[0][0], x[0][1]), fmaxf(x[0][2], x[0][3])),
+                           fmaxf(fmaxf(x[1][0], x[1][1]), fmaxf(x[1][2], x[1][3])));
+        tmax = max_over_c4(tmax);
+        const float m_new = kMultiPass ? fmaxf(m_run, tmax) : tmax;  // finite: rank r0 is always valid
         float psum = 0.f;
         float pr[2][4];
 #pragma unroll
         for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                pr[blk][i] = exp2f(x[blk][i] - m_new);
+                pr[blk][i] = __builtin_amdgcn_exp2f(x[blk][i] - m_new);  // in [0, 1]
                 psum += pr[blk][i];
             }
-        psum += __shfl_xor(psum, 16);
-        psum += __shfl_xor(psum, 32);
-        l_run = l_run * alpha + psum;
+        psum = sum_over_c4(psum);
+        if (kMultiPass) {
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first pass (m_run = -inf)
+            l_run = l_run * alpha + psum;
+            // Rescale O rows: row 4*c4 + i belongs to head 4*c4 + i.
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float ai = __shfl(alpha, 4 * c4 + i);
+#pragma unroll
+                for (int db = 0; db < 8; ++db) acc[db][i] *= ai;
+            }
+        } else {
+            l_run = psum;
+        }
         m_run = m_new;
 
-        // Rescale O rows: row 4*c4 + i belongs to head 4*c4 + i.
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float ai = __shfl(alpha, 4 * c4 + i);
-#pragma unroll
-            for (int db = 0; db < 8; ++db) acc[db][i] *= ai;
-        }
-
-        // P as the A operand of O = P V: k order (4*c4 + 0..3, 16 + 4*c4 + 0..3).
+        // P as the A operand of O = P V, k order (4*c4 + 0..3, 16 + 4*c4 + 0..3),
+        // split into bf16 hi + lo so that hi + lo carries ~16 mantissa bits.
         u32x4 p_hi, p_lo;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const int blk = w >> 1, i0 = (w & 1) * 2;
-            const uint32_t h0 = bf16_rne(pr[blk][i0]), h1 = bf16_rne(pr[blk][i0 + 1]);
-            const uint32_t l0 = bf16_rne(pr[blk][i0] - bf16_to_f32(h0));
-            const uint32_t l1 = bf16_rne(pr[blk][i0 + 1] - bf16_to_f32(h1));
-            p_hi[w] = h0 | (h1 << 16);
-            p_lo[w] = l0 | (l1 << 16);
+            const float e0 = pr[blk][i0], e1 = pr[blk][i0 + 1];
+            const uint32_t hi = pack_bf16(e0, e1);
+            p_hi[w] = hi;
+            p_lo[w] = pack_bf16(e0 - __builtin_bit_cast(float, hi << 16),
+                                e1 - __builtin_bit_cast(float, hi & 0xffff0000u));
         }
 
         // V^T through LDS.  Lane (e = n16, octet c4) holds positions 8*c4 + t
-        // (t = 0..7) of head dims 8e .. 8e+7; transpose to one 16-byte unit per
-        // head dim and store it (halves swapped for odd head dims).
+        // (t = 0..7) of head dims 8e .. 8e+7; one v_perm_b32 per output word
+        // gathers a head dim's values of two positions, then one 16-byte unit
+        // per head dim is stored (halves swapped for odd head dims).
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int w = i >> 1;
+            const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;  // high or low halves of both words
             uint32_t o[4];
 #pragma unroll
-            for (int pp = 0; pp < 4; ++pp) {
-                const uint32_t lo = vf[2 * pp][w], hi = vf[2 * pp + 1][w];
-                o[pp] = (i & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-            }
+            for (int pp = 0; pp < 4; ++pp) o[pp] = __builtin_amdgcn_perm(R.vf[2 * pp + 1][w], R.vf[2 * pp][w], sel);
             const u32x4 unit = (i & 1) ? u32x4{o[2], o[3], o[0], o[1]} : u32x4{o[0], o[1], o[2], o[3]};
             *reinterpret_cast<u32x4 *>(vt + vt_unit(8 * n16 + i, c4) * 16) = unit;
         }
@@ -299,9 +365,27 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
         }
         // The next pass overwrites this wave's tile only after these reads
         // have returned (their results feed the MFMAs above).
+    };
+
+    {
+        int r0 = r_begin + wave * kWaveTile;
+        PassRegs cur;
+        if (r0 < r_end) issue(r0, cur);
+        if (kMultiPass) {
+            for (; r0 < r_end; r0 += kSplitUnit) {
+                PassRegs nxt;
+                const bool more = r0 + kSplitUnit < r_end;
+                if (more) issue(r0 + kSplitUnit, nxt);
+                consume(r0, cur);
+                if (more) cur = nxt;
+            }
+        } else if (r0 < r_end) {
+            consume(r0, cur);
+        }
     }
 
     // ---- combine the four wavefronts of the workgroup -------------------
+    __shared__ float mlf_lds[kMaxGroup][2];  // per head: workgroup max (log2 units), workgroup sum
     if (c4 == 0) {
         ml_lds[wave][n16][0] = m_run;
         ml_lds[wave][n16][1] = l_run;
@@ -313,47 +397,51 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
     for (int i = 0; i < 4; ++i) {
         const int h = 4 * c4 + i;
         if (h < G) {
-            float mx = kNegInf;
-#pragma unroll
-            for (int w = 0; w < kWavesPerWg; ++w) mx = fmaxf(mx, ml_lds[w][h][0]);
+            const float mx = fmaxf(fmaxf(ml_lds[0][h][0], ml_lds[1][h][0]), fmaxf(ml_lds[2][h][0], ml_lds[3][h][0]));
             const float mine = ml_lds[wave][h][0];
-            const float f = mine == kNegInf ? 0.f : exp2f(mine - mx);
+            const float f = mine == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mine - mx);
 #pragma unroll
             for (int db = 0; db < 8; ++db) o_lds[(wave * kMaxGroup + h) * kHeadDim + 16 * db + n16] = acc[db][i] * f;
         }
     }
-    __syncthreads();
-
-    const int64_t row0 = (int64_t)(layer * a.B + b) * a.Hq + g * G;  // first output row of the group
-    const float qnan = __builtin_nanf("");
-    const float ln2 = 0.69314718055994530942f;
-    for (int e = tid; e < G * kHeadDim; e += blockDim.x) {
-        const int h = e >> 7, d = e & 127;
-        float mx = kNegInf;
-#pragma unroll
-        for (int w = 0; w < kWavesPerWg; ++w) mx = fmaxf(mx, ml_lds[w][h][0]);
-        float L = 0.f, O = 0.f;
+    if (tid < G) {
+        const float mx = fmaxf(fmaxf(ml_lds[0][tid][0], ml_lds[1][tid][0]), fmaxf(ml_lds[2][tid][0], ml_lds[3][tid][0]));
+        float L = 0.f;
 #pragma unroll
         for (int w = 0; w < kWavesPerWg; ++w) {
-            const float mw = ml_lds[w][h][0];
-            const float f = mw == kNegInf ? 0.f : exp2f(mw - mx);
-            L += ml_lds[w][h][1] * f;
-            O += o_lds[(w * kMaxGroup + h) * kHeadDim + d];
+            const float mw = ml_lds[w][tid][0];
+            L += ml_lds[w][tid][1] * (mw == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mw - mx));
         }
-        if (bad) L = qnan;
+        mlf_lds[tid][0] = mx;
+        mlf_lds[tid][1] = bad ? __builtin_nanf("") : L;
+    }
+    __syncthreads();
+
+    // Each thread owns four consecutive head dims of one head.
+    const int64_t row0 = (int64_t)(layer * a.B + b) * a.Hq + g * G;  // first output row of the group
+    const float ln2 = 0.69314718055994530942f;
+    for (int c = tid; c < G * (kHeadDim / 4); c += blockDim.x) {
+        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
+        f32x4 O = *reinterpret_cast<const f32x4 *>(&o_lds[h * kHeadDim + d0]);
+#pragma unroll
+        for (int w = 1; w < kWavesPerWg; ++w) O += *reinterpret_cast<const f32x4 *>(&o_lds[(w * kMaxGroup + h) * kHeadDim + d0]);
+        const float mx = mlf_lds[h][0], L = mlf_lds[h][1];
         if (a.n_split == 1) {
-            const float y = O / L;
+            const int64_t orow = (row0 + h) * kHeadDim + d0;
+            const float inv = 1.f / L;
             if (a.out_f32)
-                reinterpret_cast<float *>(a.out)[(row0 + h) * kHeadDim + d] = y;
+                *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(a.out) + orow) = O * inv;
             else
-                reinterpret_cast<uint16_t *>(a.out)[(row0 + h) * kHeadDim + d] = (uint16_t)bf16_rne(y);
-            if (d == 0 && a.lse) a.lse[row0 + h] = (mx + log2f(L)) * ln2;
+                *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(a.out) + orow) =
+                    u32x2{pack_bf16(O[0] * inv, O[1] * inv), pack_bf16(O[2] * inv, O[3] * inv)};
+            if (d0 == 0 && a.lse) a.lse[row0 + h] = (mx + __builtin_log2f(L)) * ln2;
         } else {
             const int64_t prow = ((int64_t)grp * a.n_split + split) * G + h;
-            a.part_o[prow * kHeadDim + d] = O;
-            if (d == 0) {
-                a.part_ml[prow * 2 + 0] = mx;
-                a.part_ml[prow * 2 + 1] = L;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) store_coherent(&a.part_o[prow * kHeadDim + d0 + j], O[j]);
+            if (d0 == 0) {
+                store_coherent(&a.part_ml[prow * 2 + 0], mx);
+                store_coherent(&a.part_ml[prow * 2 + 1], L);
             }
         }
     }
@@ -362,36 +450,61 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
     if (a.n_split == 1) return;
 
     // ---- cross-split log-sum-exp merge by the last workgroup of the group ----
-    __threadfence();
+    // Every partial store has completed before the ticket is taken, so the
+    // workgroup that draws the last ticket sees all partials.
+    wait_vmem();
     __syncthreads();
     if (tid == 0) {
-        const int prev = atomicAdd(&a.ticket[grp], 1);
+        const int prev = __hip_atomic_fetch_add(&a.ticket[grp], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = prev == a.n_split - 1;
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
-    if (tid == 0) atomicExch(&a.ticket[grp], 0);  // ready for the next call
+    if (tid == 0) __hip_atomic_store(&a.ticket[grp], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
+    // Each thread owns four consecutive head dims of one head and folds the
+    // splits in batches whose loads are all in flight together.
     const int64_t pbase = (int64_t)grp * a.n_split;
-    for (int e = tid; e < G * kHeadDim; e += blockDim.x) {
-        const int h = e >> 7, d = e & 127;
-        float mx = kNegInf;
-        for (int sp = 0; sp < a.n_split; ++sp) mx = fmaxf(mx, a.part_ml[((pbase + sp) * G + h) * 2]);
-        float L = 0.f, O = 0.f;
-        for (int sp = 0; sp < a.n_split; ++sp) {
-            const int64_t prow = (pbase + sp) * G + h;
-            const float ms = a.part_ml[prow * 2];
-            const float f = ms == kNegInf ? 0.f : exp2f(ms - mx);
-            L += a.part_ml[prow * 2 + 1] * f;
-            O += a.part_o[prow * kHeadDim + d] * f;
+    for (int c = tid; c < G * (kHeadDim / 4); c += blockDim.x) {
+        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
+        float M = kNegInf, L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int base = 0; base < a.n_split; base += kMergeBatch) {
+            float mm[kMergeBatch], ll[kMergeBatch], oo[kMergeBatch][4];
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const int sp = base + k;
+                const int64_t prow = (pbase + (sp < a.n_split ? sp : 0)) * G + h;
+                mm[k] = sp < a.n_split ? load_coherent(&a.part_ml[prow * 2]) : kNegInf;
+                ll[k] = sp < a.n_split ? load_coherent(&a.part_ml[prow * 2 + 1]) : 0.f;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    oo[k][j] = sp < a.n_split ? load_coherent(&a.part_o[prow * kHeadDim + d0 + j]) : 0.f;
+            }
+            float bm = M;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) bm = fmaxf(bm, mm[k]);
+            const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - bm);
+            L *= sc;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) O[j] *= sc;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const float f = mm[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mm[k] - bm);
+                L += ll[k] * f;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) O[j] += oo[k][j] * f;
+            }
+            M = bm;
         }
-        const float y = O / L;
+        const int64_t orow = (row0 + h) * kHeadDim + d0;
+        const float inv = 1.f / L;
         if (a.out_f32)
-            reinterpret_cast<float *>(a.out)[(row0 + h) * kHeadDim + d] = y;
+            *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(a.out) + orow) =
+                f32x4{O[0] * inv, O[1] * inv, O[2] * inv, O[3] * inv};
         else
-            reinterpret_cast<uint16_t *>(a.out)[(row0 + h) * kHeadDim + d] = (uint16_t)bf16_rne(y);
-        if (d == 0 && a.lse) a.lse[row0 + h] = (mx + log2f(L)) * ln2;
+            *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(a.out) + orow) =
+                u32x2{pack_bf16(O[0] * inv, O[1] * inv), pack_bf16(O[2] * inv, O[3] * inv)};
+        if (d0 == 0 && a.lse) a.lse[row0 + h] = (M + __builtin_log2f(L)) * ln2;
     }
 }
 
@@ -413,7 +526,13 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
     const int64_t groups = (int64_t)a.NL * a.B * a.Hkv;
     const int64_t grid = groups * a.n_split;
-    hipLaunchKernelGGL(decode_attn_kernel, dim3((unsigned)grid), dim3(kWavesPerWg * 64), 0, (hipStream_t)stream, a);
+    // Splits of more than one pass per wavefront double-buffer their loads.
+    if (a.split_len > kSplitUnit)
+        hipLaunchKernelGGL(decode_attn_kernel<true>, dim3((unsigned)grid), dim3(kWavesPerWg * 64), 0,
+                           (hipStream_t)stream, a);
+    else
+        hipLaunchKernelGGL(decode_attn_kernel<false>, dim3((unsigned)grid), dim3(kWavesPerWg * 64), 0,
+                           (hipStream_t)stream, a);
     return (int)hipGetLastError();
 }
 

@@ -114,6 +114,7 @@ def call_attn(a):
     (dict(q=FAKE + 8), M.MURMUR_EINVAL),
     (dict(ws=FAKE + 64), M.MURMUR_EINVAL),
     (dict(lse=FAKE + 2), M.MURMUR_EINVAL),
+    (dict(out=FAKE + 8), M.MURMUR_EINVAL),
     (dict(kv=M.murmur_kv(FAKE, FAKE, 1, 4096, 0, 0, 0, 100)), M.MURMUR_EINVAL),   # stride not a multiple of 8
     (dict(kv=M.murmur_kv(FAKE, FAKE, 1, 4096, 0, 0, 0, 64)), M.MURMUR_EINVAL),    # rows overlap
     (dict(kv=M.murmur_kv(FAKE, None, 1, 4096, 0, 0, 0, 128)), M.MURMUR_EINVAL),
