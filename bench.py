@@ -12,8 +12,10 @@ Timing:
   * value / ms_per_step: K steps captured once into a HIP graph and replayed,
     bracketed by device synchronisation and HIP events on the replay stream;
   * roofline.achieved: algorithmic bytes of one decode_attn launch divided by
-    its mean duration, from HIP events recorded around each launch on the
-    stream it is launched on;
+    its mean duration: K decode_attn launches captured into a graph, replayed
+    between two HIP events on the stream they are launched on, divided by K
+    (per-launch event brackets, which also count each launch's dispatch
+    latency, are reported alongside);
   * every step reads a different replica of the KV cache (rotation over more
     than 2 x 256 MB), so reads come from HBM, not the 256 MB Infinity Cache.
 cpu_baseline: the fp64 oracle timed on this host's cores on a bounded number
@@ -46,8 +48,48 @@ DESCRIPTIONS = {
 }
 
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_01483_amd", "csrc", "kernels.hip")
+
+
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def committed_traffic(config: str) -> float | None:
+    """HBM bytes per decode_attn launch from the committed rocprofv3 counter summary of this workload,
+    or None if there is none or the kernel source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"decode_attn_{config}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.lstrip().startswith("#"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_reference(mbytes: int, reps: int) -> dict:
+    """A plain device copy of known size, the reference for scaling the PMC byte counters."""
+    import torch
+    n = mbytes << 20
+    x = torch.ones(n, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    return {"copy_reference_bytes_read": n, "copy_reference_bytes_written": n, "launches": reps}
 
 
 def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
@@ -102,8 +144,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during warm-up")
 
-    # Per-launch decode_attn durations (HIP events on the launch stream).
-    log("timing decode_attn launches with HIP events")
+    # Per-launch event brackets (diagnostic: they include each launch's dispatch latency).
+    log("timing decode_attn launches with HIP event brackets")
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for i in range(steps):
         db.evict(order[i])
@@ -111,36 +153,48 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         db.attend(order[i], rep[i])
         evs[i][1].record(stream)
     torch.cuda.synchronize()
-    attn_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    bracket_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
 
-    # Whole steps, captured once into a graph and replayed.
-    log("capturing the timed steps into a HIP graph")
-    graph = torch.cuda.CUDAGraph()
-    cap = torch.cuda.Stream()
-    cap.wait_stream(stream)
-    with torch.cuda.stream(cap):
-        db.step(order[0], rep[0])  # one eager step on the capture stream before capture
-    torch.cuda.synchronize()
-    with torch.cuda.graph(graph, stream=cap):
-        for i in range(steps):
-            db.step(order[i], rep[i])
-    torch.cuda.synchronize()
-    graph.replay()  # warm replay
-    torch.cuda.synchronize()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    graph.replay()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    step_us = t0.elapsed_time(t1) * 1e3 / steps
+    def capture(fn):
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            fn()
+        torch.cuda.synchronize()
+        graph.replay()  # warm replay
+        torch.cuda.synchronize()
+        return graph
+
+    def time_graph(graph) -> float:
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        graph.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) * 1e3
+
+    # Whole steps (evict_compact + decode_attn), captured once into a graph and replayed.
+    log("timing the steps as a replayed HIP graph")
+    step_graph = capture(lambda: [db.step(order[i], rep[i]) for i in range(steps)])
+    step_us = time_graph(step_graph) / steps
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during the timed steps")
 
+    # decode_attn alone: the same launches back to back (retained set of the first timed step, each launch
+    # reading the next KV replica), so the mean is the kernel's own duration.
+    log("timing decode_attn launches as a replayed HIP graph")
+    db.evict(order[0])
+    attn_graph = capture(lambda: [db.attend(order[i], rep[i]) for i in range(steps)])
+    attn_us = time_graph(attn_graph) / steps
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during the timed decode_attn launches")
+
     io = db.io_bytes()
-    alg_bytes = np.array([kv_step[o] + io for o in order], dtype=np.float64)
-    mean_attn = float(attn_us.mean())
-    achieved = float(alg_bytes.mean() / (mean_attn * 1e-6) / 1e9)
+    alg_bytes = float(kv_step[order[0]] + io)  # every launch of the decode_attn graph reads this set
+    achieved = float(alg_bytes / (attn_us * 1e-6) / 1e9)
     res = {
         "metric": METRIC,
         "value": round(step_us, 3),
@@ -159,11 +213,13 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
                    "retained_per_step": int(np.mean([int(counts[o].sum()) for o in order])),
                    "kv_replicas": replicas, "selection": "ranges" if use_ranges else "index list",
                    "split_len": db.split_len or "auto"},
-        "decode_attn_us": {"mean": round(mean_attn, 3), "median": round(float(np.median(attn_us)), 3),
-                           "p90": round(float(np.percentile(attn_us, 90)), 3)},
+        "decode_attn_us": round(attn_us, 3),
+        "decode_attn_event_bracket_us": {"mean": round(float(bracket_us.mean()), 3),
+                                         "median": round(float(np.median(bracket_us)), 3),
+                                         "p90": round(float(np.percentile(bracket_us, 90)), 3)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "decode_attn_kernel", "alg_bytes_per_launch": int(alg_bytes.mean())},
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": committed_traffic(config),
+                     "kernel": "decode_attn_kernel", "alg_bytes_per_launch": int(alg_bytes)},
     }
     if cpu:
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
@@ -183,11 +239,23 @@ def main() -> int:
     ap.add_argument("--index-list", action="store_true", help="attend from the index list instead of ranges")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
+    ap.add_argument("--all", action="store_true", help="one JSON line per workload (c1 .. c5), no CPU baseline")
+    ap.add_argument("--copy-reference", type=int, default=0, metavar="MB",
+                    help="only run plain device copies of this many MiB (PMC counter reference)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this decode path has no multi-GPU mode (got --gpus {args.gpus})",
               file=sys.stderr)
         return 2
+    if args.copy_reference:
+        print(json.dumps(copy_reference(args.copy_reference, 8)), flush=True)
+        return 0
+    if args.all:
+        from paper_2606_01483_amd import workloads as W
+        for cfg in W.CONFIGS:
+            res = run(cfg, args.steps, args.warmup, None, False, 0.0, args.split_len, not args.index_list)
+            print(json.dumps(res), flush=True)
+        return 0
     res = run(args.config, args.steps, args.warmup, args.replicas, not args.no_cpu_baseline, args.cpu_budget,
               args.split_len, not args.index_list)
     print(json.dumps(res), flush=True)

@@ -41,10 +41,16 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     WorkspacePlan p{};
     const int64_t units = ((int64_t)max_keep + kSplitUnit - 1) / kSplitUnit;
     if (split_len <= 0) {
-        // At most kMaxAutoSplits partials per (layer, sequence, KV head): the
-        // merge reads them all, so very long lists take longer splits.
-        const int64_t per = (units + kMaxAutoSplits - 1) / kMaxAutoSplits;
-        split_len = (int32_t)((per < 1 ? 1 : per) * kSplitUnit);
+        // Enough workgroups to cover the chip about twice (kTargetWorkgroups),
+        // otherwise as few splits as possible: every split adds a partial that
+        // the merge has to read back.  At most kMaxAutoSplits splits.
+        const int64_t groups = (int64_t)n_layers * B * Hkv;
+        int64_t want = (kTargetWorkgroups + groups - 1) / groups;
+        if (want > kMaxAutoSplits) want = kMaxAutoSplits;
+        if (want > units) want = units;
+        if (want < 1) want = 1;
+        const int64_t per = (units + want - 1) / want;
+        split_len = (int32_t)(per * kSplitUnit);
     }
     p.split_len = split_len;
     p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
@@ -179,6 +185,9 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     if (plan.n_split > kMaxMergeSplits)
         return fail(MURMUR_EINVAL, "split_len %d gives %d splits for max_keep %d; at most %d are supported",
                     plan.split_len, plan.n_split, max_keep, kMaxMergeSplits);
+    if (plan.o_bytes >= ((size_t)1 << 31))
+        return fail(MURMUR_EINVAL, "split partials of %zu bytes exceed the 2 GiB a launch can address; use a longer "
+                    "split_len", plan.o_bytes);
     const int64_t grid = plan.groups * plan.n_split;
     if (grid > 0x7fffffffLL || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
         return fail(MURMUR_EINVAL, "problem too large for one launch (%lld workgroups)", (long long)grid);
@@ -200,6 +209,8 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     a.ticket = (int32_t *)ws;
     a.part_ml = plan.n_split > 1 ? (float *)(ws + plan.ticket_bytes) : nullptr;
     a.part_o = plan.n_split > 1 ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
+    a.part_ml_bytes = (uint32_t)plan.ml_bytes;
+    a.part_o_bytes = (uint32_t)plan.o_bytes;
     a.max_len = kv->max_len;
     a.max_keep = max_keep;
     a.B = B;

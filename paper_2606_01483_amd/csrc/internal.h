@@ -15,6 +15,7 @@ constexpr int kWaveTile = 32;     // retained positions one wavefront handles pe
 constexpr int kWavesPerWg = 4;
 constexpr int kSplitUnit = kWaveTile * kWavesPerWg;  // 128 positions: one pass of a workgroup
 constexpr int kMaxAutoSplits = 64;
+constexpr int kTargetWorkgroups = 512;  // about two workgroups per compute unit of the 256
 // Splits one merge can combine: it stages 2 * n_split * G + 2 * G floats in
 // the workgroup's 32 KiB of V-tile LDS.
 constexpr int kMaxMergeSplits = 240;
@@ -34,6 +35,7 @@ struct AttnLaunch {
     int32_t *ticket;   // [groups]
     float *part_ml;    // [groups][n_split][G][2]  (running max in log2 units, sum)
     float *part_o;     // [groups][n_split][G][128]
+    uint32_t part_ml_bytes, part_o_bytes;  // extents of the two partial arrays (< 2^31)
     int32_t max_len, max_keep, B, Hq, Hkv, G, NL;
     int32_t split_len, n_split, out_f32;
     float scale_log2;  // logit scale times log2(e)

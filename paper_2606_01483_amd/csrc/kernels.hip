@@ -130,15 +130,27 @@ static __device__ __forceinline__ int vt_unit(int d, int q) {
 constexpr int kVtBytesPerWave = 4 * 128 * 16;  // 8 KiB
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// Device-coherent (scope: agent) accesses for the split partials.  On gfx950
-// they compile to sc1 loads and stores, which bypass the per-XCD L2's
-// non-coherent copies, so the partials need no L2 writeback or invalidate --
-// the __threadfence() route costs a full L2 write-back per wavefront.
-static __device__ __forceinline__ void store_coherent(float *p, float v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Device-coherent accesses for the split partials: raw buffer loads and stores
+// with the sc1 cache-policy bit, which bypass the per-XCD L2's non-coherent
+// copies, so the partials need no L2 writeback or invalidate (the
+// __threadfence() route costs a full L2 write-back per wavefront).  The buffer
+// resource's byte count also bounds every access in hardware.
+constexpr int kCoherent = 16;  // sc1
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+static __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_buffer(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
 }
-static __device__ __forceinline__ float load_coherent(const float *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+static __device__ __forceinline__ void store_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, kCoherent);
+}
+static __device__ __forceinline__ void store_coherent1(__amdgpu_buffer_rsrc_t r, uint32_t off, float x) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, kCoherent);
+}
+static __device__ __forceinline__ f32x4 load_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCoherent));
+}
+static __device__ __forceinline__ float load_coherent1(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
 }
 // Wait until every vector-memory access of this wavefront has completed; also a
 // compiler barrier, so no store is moved past it.
@@ -436,12 +448,12 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
                     u32x2{pack_bf16(O[0] * inv, O[1] * inv), pack_bf16(O[2] * inv, O[3] * inv)};
             if (d0 == 0 && a.lse) a.lse[row0 + h] = (mx + __builtin_log2f(L)) * ln2;
         } else {
-            const int64_t prow = ((int64_t)grp * a.n_split + split) * G + h;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) store_coherent(&a.part_o[prow * kHeadDim + d0 + j], O[j]);
+            const uint32_t prow = ((uint32_t)grp * a.n_split + split) * G + h;
+            store_coherent4(raw_buffer(a.part_o, a.part_o_bytes), (prow * kHeadDim + d0) * 4, O);
             if (d0 == 0) {
-                store_coherent(&a.part_ml[prow * 2 + 0], mx);
-                store_coherent(&a.part_ml[prow * 2 + 1], L);
+                const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+                store_coherent1(rml, prow * 8, mx);
+                store_coherent1(rml, prow * 8 + 4, L);
             }
         }
     }
@@ -464,35 +476,35 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
 
     // Each thread owns four consecutive head dims of one head and folds the
     // splits in batches whose loads are all in flight together.
-    const int64_t pbase = (int64_t)grp * a.n_split;
+    const uint32_t pbase = (uint32_t)grp * a.n_split;
+    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
     for (int c = tid; c < G * (kHeadDim / 4); c += blockDim.x) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        float M = kNegInf, L = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
+        float M = kNegInf, L = 0.f;
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
         for (int base = 0; base < a.n_split; base += kMergeBatch) {
-            float mm[kMergeBatch], ll[kMergeBatch], oo[kMergeBatch][4];
+            float mm[kMergeBatch], ll[kMergeBatch];
+            f32x4 oo[kMergeBatch];
 #pragma unroll
             for (int k = 0; k < kMergeBatch; ++k) {
-                const int sp = base + k;
-                const int64_t prow = (pbase + (sp < a.n_split ? sp : 0)) * G + h;
-                mm[k] = sp < a.n_split ? load_coherent(&a.part_ml[prow * 2]) : kNegInf;
-                ll[k] = sp < a.n_split ? load_coherent(&a.part_ml[prow * 2 + 1]) : 0.f;
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    oo[k][j] = sp < a.n_split ? load_coherent(&a.part_o[prow * kHeadDim + d0 + j]) : 0.f;
+                const uint32_t prow = (pbase + (base + k < a.n_split ? base + k : 0)) * G + h;
+                mm[k] = load_coherent1(rml, prow * 8);
+                ll[k] = load_coherent1(rml, prow * 8 + 4);
+                oo[k] = load_coherent4(ro, (prow * kHeadDim + d0) * 4);
             }
             float bm = M;
 #pragma unroll
-            for (int k = 0; k < kMergeBatch; ++k) bm = fmaxf(bm, mm[k]);
+            for (int k = 0; k < kMergeBatch; ++k)
+                if (base + k < a.n_split) bm = fmaxf(bm, mm[k]);
             const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - bm);
             L *= sc;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) O[j] *= sc;
+            O *= sc;
 #pragma unroll
             for (int k = 0; k < kMergeBatch; ++k) {
-                const float f = mm[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mm[k] - bm);
+                const float f = (base + k >= a.n_split || mm[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mm[k] - bm);
                 L += ll[k] * f;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) O[j] += oo[k][j] * f;
+                O += oo[k] * f;
             }
             M = bm;
         }
