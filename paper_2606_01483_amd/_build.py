@@ -3,7 +3,8 @@
 kernels.hip is compiled by hipcc for gfx950 only; api.cpp (host-only C ABI
 layer) by g++.  The shared object lands next to this file, where the ctypes
 binding loads it.  Packed-fp32 instruction selection is disabled for device
-code.  Only the murmur_* entry points are exported.
+code, and the first 16 kernel-argument dwords are preloaded into SGPRs.  Only
+the murmur_* entry points are exported.
 """
 from __future__ import annotations
 
@@ -42,7 +43,7 @@ def build(verbose: bool = False) -> str:
     a_obj = os.path.join(BUILD_DIR, "api.o")
     steps = [
         [hipcc, f"--offload-arch={ARCH}", *common, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-c", os.path.join(CSRC, "kernels.hip"), "-o", k_obj],
+         "-mllvm", "-amdgpu-kernarg-preload-count=16", "-c", os.path.join(CSRC, "kernels.hip"), "-o", k_obj],
         ["g++", *common, "-Wextra", "-c", os.path.join(CSRC, "api.cpp"), "-o", a_obj],
     ]
     for cmd in steps:

@@ -188,9 +188,9 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     if (plan.o_bytes >= ((size_t)1 << 31))
         return fail(MURMUR_EINVAL, "split partials of %zu bytes exceed the 2 GiB a launch can address; use a longer "
                     "split_len", plan.o_bytes);
-    const int64_t grid = plan.groups * plan.n_split;
-    if (grid > 0x7fffffffLL || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
-        return fail(MURMUR_EINVAL, "problem too large for one launch (%lld workgroups)", (long long)grid);
+    if ((int64_t)kv->n_layers * B > 65535 || Hkv > 65535 || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
+        return fail(MURMUR_EINVAL, "problem too large for one launch (n_layers * B = %lld, Hkv = %d)",
+                    (long long)kv->n_layers * B, Hkv);
 
     AttnLaunch a{};
     a.q = (const uint16_t *)q_dev;

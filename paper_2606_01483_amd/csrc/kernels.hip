@@ -202,7 +202,14 @@ struct PassRegs {
 // current one is computed; otherwise every wavefront makes at most one pass.
 // ---------------------------------------------------------------------------
 template <bool kMultiPass>
-__global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
+// The leading scalar arguments are the ones the first memory accesses need;
+// the build preloads them into SGPRs so no kernel-argument load precedes the
+// range-table load.
+__global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ count,
+                                                          const int32_t *__restrict__ ranges,
+                                                          const int32_t *__restrict__ idx,
+                                                          const uint16_t *__restrict__ q, int32_t max_keep,
+                                                          int32_t B, const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
     __shared__ float ml_lds[kWavesPerWg][kMaxGroup][2];
     __shared__ int s_last;
@@ -213,33 +220,34 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
 
-    const int split = blockIdx.x % a.n_split;
-    const int grp = blockIdx.x / a.n_split;  // ((layer * B) + b) * Hkv + g
-    const int g = grp % a.Hkv;
-    const int lb = grp / a.Hkv;
-    const int b = lb % a.B;
-    const int layer = lb / a.B;
+    // Grid: x = split, y = KV head, z = layer * B + sequence.
+    const int split = blockIdx.x;
+    const int g = blockIdx.y;
+    const int lb = blockIdx.z;
+    const int b = lb % B;
+    const int layer = lb / B;
+    const int grp = lb * a.Hkv + g;  // ((layer * B) + b) * Hkv + g
     const int G = a.G;
 
-    int cnt = a.count[b];
-    const bool bad_count = cnt < 1 || cnt > a.max_keep;
-    if (bad_count) cnt = cnt < 0 ? 0 : (cnt > a.max_keep ? a.max_keep : cnt);
+    int cnt = count[b];
+    const bool bad_count = cnt < 1 || cnt > max_keep;
+    if (bad_count) cnt = cnt < 0 ? 0 : (cnt > max_keep ? max_keep : cnt);
     int bad_pos = 0;
     const int r_begin = split * a.split_len;
     const int r_end = min(r_begin + a.split_len, cnt);
 
     int32_t rg[2 * kPieces];
-    const bool use_ranges = a.ranges != nullptr;
+    const bool use_ranges = ranges != nullptr;
 #pragma unroll
-    for (int k = 0; k < 2 * kPieces; ++k) rg[k] = use_ranges ? a.ranges[b * 2 * kPieces + k] : 0;
-    const int32_t *idx_row = a.idx + (int64_t)b * a.max_keep;
+    for (int k = 0; k < 2 * kPieces; ++k) rg[k] = use_ranges ? ranges[b * 2 * kPieces + k] : 0;
+    const int32_t *idx_row = idx + (int64_t)b * max_keep;
 
     // Q^T as the MFMA B operand: lane (head n16, k-group c4) holds head dims
     // kc*32 + 8*c4 .. +8 for kc = 0..3.  Rows past the group are zero.
     u32x4 qf[4];
     {
         const int hq = n16 < G ? n16 : G - 1;  // keep the address inside q for padded rows
-        const uint16_t *qrow = a.q + ((int64_t)(layer * a.B + b) * a.Hq + g * G + hq) * kHeadDim;
+        const uint16_t *qrow = q + ((int64_t)lb * a.Hq + g * G + hq) * kHeadDim;
 #pragma unroll
         for (int kc = 0; kc < 4; ++kc) qf[kc] = n16 < G ? load16(qrow + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
     }
@@ -430,7 +438,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const AttnLaunch a) {
     __syncthreads();
 
     // Each thread owns four consecutive head dims of one head.
-    const int64_t row0 = (int64_t)(layer * a.B + b) * a.Hq + g * G;  // first output row of the group
+    const int64_t row0 = (int64_t)lb * a.Hq + g * G;  // first output row of the group
     const float ln2 = 0.69314718055994530942f;
     for (int c = tid; c < G * (kHeadDim / 4); c += blockDim.x) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
@@ -536,15 +544,14 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 }
 
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
-    const int64_t groups = (int64_t)a.NL * a.B * a.Hkv;
-    const int64_t grid = groups * a.n_split;
+    const dim3 grid((unsigned)a.n_split, (unsigned)a.Hkv, (unsigned)(a.NL * a.B));
     // Splits of more than one pass per wavefront double-buffer their loads.
     if (a.split_len > kSplitUnit)
-        hipLaunchKernelGGL(decode_attn_kernel<true>, dim3((unsigned)grid), dim3(kWavesPerWg * 64), 0,
-                           (hipStream_t)stream, a);
+        hipLaunchKernelGGL(decode_attn_kernel<true>, grid, dim3(kWavesPerWg * 64), 0, (hipStream_t)stream, a.count,
+                           a.ranges, a.idx, a.q, a.max_keep, a.B, a);
     else
-        hipLaunchKernelGGL(decode_attn_kernel<false>, dim3((unsigned)grid), dim3(kWavesPerWg * 64), 0,
-                           (hipStream_t)stream, a);
+        hipLaunchKernelGGL(decode_attn_kernel<false>, grid, dim3(kWavesPerWg * 64), 0, (hipStream_t)stream, a.count,
+                           a.ranges, a.idx, a.q, a.max_keep, a.B, a);
     return (int)hipGetLastError();
 }
 
