@@ -176,7 +176,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) * 1e3
 
-    # Whole steps (evict_compact + decode_attn), captured once into a graph and replayed.
+    # Whole steps (evict_compact then decode_attn on one stream), captured once into a graph and replayed.
     log("timing the steps as a replayed HIP graph")
     step_graph = capture(lambda: [db.step(order[i], rep[i]) for i in range(steps)])
     step_us = time_graph(step_graph) / steps

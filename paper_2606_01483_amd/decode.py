@@ -51,29 +51,61 @@ class DecodeBatch:
         self.pol = torch.from_numpy(np.ascontiguousarray(wl.policy, dtype=np.int32)).to(dev)
         self.q = torch.from_numpy(np.stack([wl.q(s) for s in self.steps])).view(torch.bfloat16).to(dev)
 
-        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
-        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
-        self.ranges = torch.zeros((B, M.N_PIECES, 2), dtype=torch.int32, device=dev)
+        # Two sets of retained-set buffers, so that the eviction of the next step can run while the
+        # attention of the current one still reads its set.
+        self.sets = [(torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev),
+                      torch.zeros(B, dtype=torch.int32, device=dev),
+                      torch.zeros((B, M.N_PIECES, 2), dtype=torch.int32, device=dev)) for _ in range(2)]
+        self.idx, self.count, self.ranges = self.sets[0]
         odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
         self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
         self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
         self.ws_bytes = M.murmur_decode_attn_workspace(NL, B, Hq, Hkv, self.max_keep, split_len)
         self.ws = torch.zeros(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.int32, device=dev)
 
-    def evict(self, i: int, stream=None) -> None:
-        """murmur_evict_compact for the i-th step of this batch."""
-        M.murmur_evict_compact(self.seg[i], self.pol, 1, self.B, self.idx, self.max_keep, self.count, self.ranges,
-                               stream)
+    def evict(self, i: int, stream=None, buf: int = 0) -> None:
+        """murmur_evict_compact for the i-th step of this batch into retained-set buffer `buf`."""
+        idx, count, ranges = self.sets[buf]
+        M.murmur_evict_compact(self.seg[i], self.pol, 1, self.B, idx, self.max_keep, count, ranges, stream)
 
-    def attend(self, i: int, replica: int = 0, stream=None) -> None:
-        """murmur_decode_attn for the i-th step, reading K/V replica `replica`."""
-        M.murmur_decode_attn(self.q[i], self.kv[replica], self.idx, self.ranges if self.use_ranges else None,
-                             self.count, self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale,
-                             self.split_len, self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes, stream)
+    def attend(self, i: int, replica: int = 0, stream=None, buf: int = 0) -> None:
+        """murmur_decode_attn for the i-th step, reading K/V replica `replica` and retained-set buffer `buf`."""
+        idx, count, ranges = self.sets[buf]
+        M.murmur_decode_attn(self.q[i], self.kv[replica], idx, ranges if self.use_ranges else None, count,
+                             self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale, self.split_len,
+                             self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes, stream)
 
     def step(self, i: int, replica: int = 0, stream=None) -> None:
         self.evict(i, stream)
         self.attend(i, replica, stream)
+
+    def pipelined_steps(self, steps: list[int], replicas: list[int], attn_stream, evict_stream) -> None:
+        """Enqueue the given steps with the eviction of step k+1 overlapping the attention of step k.
+
+        The retained set is a function of the layout alone, so the next step's set can be built while
+        the current step attends; the two buffer sets alternate.  attention(k) waits for eviction(k);
+        eviction(k+1) reuses the buffer attention(k-1) read and waits for it.  Both streams keep the
+        default priority.  Ends with attn_stream waiting for evict_stream."""
+        import torch
+        n = len(steps)
+        ev_evict = [torch.cuda.Event() for _ in range(n)]
+        ev_attn = [torch.cuda.Event() for _ in range(n)]
+        evict_stream.wait_stream(attn_stream)
+        with torch.cuda.stream(evict_stream):
+            self.evict(steps[0], buf=0)
+            ev_evict[0].record(evict_stream)
+        for k in range(n):
+            attn_stream.wait_event(ev_evict[k])
+            with torch.cuda.stream(attn_stream):
+                self.attend(steps[k], replicas[k], buf=k % 2)
+                ev_attn[k].record(attn_stream)
+            if k + 1 < n:
+                if k >= 1:
+                    evict_stream.wait_event(ev_attn[k - 1])
+                with torch.cuda.stream(evict_stream):
+                    self.evict(steps[k + 1], buf=(k + 1) % 2)
+                    ev_evict[k + 1].record(evict_stream)
+        attn_stream.wait_stream(evict_stream)
 
     def kv_bytes_read(self, i: int) -> int:
         """Algorithmic K/V bytes of step i: retained positions x layers x KV heads x (K + V) x D x 2 B."""

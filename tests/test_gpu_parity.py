@@ -273,3 +273,48 @@ def test_attn_device_errors_give_nan():
     torch.cuda.synchronize()
     assert M.murmur_device_error() == M.MURMUR_DEVERR_COUNT
     assert torch.isnan(db.out).all().item()
+
+
+def test_graph_replays_match_eager_and_pipelined_schedule():
+    """Steps captured into a HIP graph (serial, and pipelined over two streams) replay to the eager result
+    every time, with eager work and synchronisation between the replays."""
+    announce("attn c3 graph replays (serial and pipelined)")
+    wl = workload("c3")
+    steps = [0, 1, 2, 3]
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps, replicas=2)
+    reps = [0, 1, 0, 1]
+    for i in range(4):
+        db.step(i, reps[i])
+    torch.cuda.synchronize()
+    eager = db.out.clone()
+    eager_lse = db.lse.clone()
+
+    stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    graphs = {}
+    for name, fn in (("serial", lambda: [db.step(i, reps[i]) for i in range(4)]),
+                     ("pipelined", lambda: db.pipelined_steps(list(range(4)), reps, torch.cuda.current_stream(),
+                                                              side))):
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=cap):
+            fn()
+        torch.cuda.synchronize()
+        graphs[name] = g
+    for trial in range(3):
+        for name, g in graphs.items():
+            db.out.zero_()
+            db.lse.zero_()
+            db.step(1, 1)  # unrelated eager work between replays
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(db.out, eager), (name, trial)
+            assert torch.equal(db.lse, eager_lse), (name, trial)
+    # the eagerly pipelined schedule gives the same result too
+    db.out.zero_()
+    db.pipelined_steps(list(range(4)), reps, stream, side)
+    torch.cuda.synchronize()
+    assert torch.equal(db.out, eager)
