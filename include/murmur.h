@@ -55,6 +55,9 @@ enum {
 
 enum { MURMUR_DTYPE_BF16 = 1, MURMUR_DTYPE_F32 = 2 };
 
+/* split_len value selecting the persistent stream schedule of murmur_decode_attn. */
+#define MURMUR_SPLIT_STREAM (-1)
+
 /* Device error word bits (murmur_device_error). */
 enum {
     MURMUR_DEVERR_OVERFLOW = 1,  /* evict_compact: retained count > max_keep */
@@ -151,8 +154,9 @@ int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev
                          int32_t *ranges_dev, murmur_stream_t stream);
 
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
- * (0 = the automatic choice).  The workspace holds the split partials and a
- * ticket counter per (layer, sequence, kv-head).  It must be zero-filled once
+ * (0 = the automatic choice, MURMUR_SPLIT_STREAM, or positions per split).
+ * The workspace holds the split partials and a ticket counter per (layer,
+ * sequence, kv-head).  It must be zero-filled once
  * before its first use (or reset with murmur_decode_attn_workspace_init);
  * every completed call leaves the tickets at zero again.  Calls that share a
  * workspace must not run concurrently. */
@@ -177,7 +181,14 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  *   count_dev:  [B] retained counts;
  *   D:          head_dim, must be 128; Hq/Hkv must be in [1, 16];
  *   scale:      logit scale (1/sqrt(D) for unscaled queries), finite;
- *   split_len:  retained positions per split (a multiple of 128), 0 = automatic;
+ *   split_len:  the work schedule.  A positive multiple of 128: each (layer,
+ *               sequence, KV head) is cut into splits of that many retained
+ *               positions, one workgroup each, merged by log-sum-exp.
+ *               MURMUR_SPLIT_STREAM: persistent workgroups, one per compute
+ *               unit, stream balanced runs of 128-position units across all
+ *               groups; only groups cut by a run boundary are merged (at most
+ *               256 sequences).  0: automatic split length (about two
+ *               workgroups per compute unit, at most 64 splits);
  *   out_dev:    [n_layers][B][Hq][D] of out_dtype, 16-byte aligned
  *               (MURMUR_DTYPE_BF16 rounds to nearest even, MURMUR_DTYPE_F32
  *               stores the fp32 accumulation);

@@ -40,11 +40,26 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
                              int32_t split_len) {
     WorkspacePlan p{};
     const int64_t units = ((int64_t)max_keep + kSplitUnit - 1) / kSplitUnit;
+    const int64_t groups = (int64_t)n_layers * B * Hkv;
+    const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
+    p.groups = groups;
+    p.ticket_bytes = round_up((size_t)groups * sizeof(int32_t), 256);
+    const bool stream = split_len == MURMUR_SPLIT_STREAM;
+    if (stream) {
+        // Persistent workgroups, each leaving at most two partial segments.
+        const int64_t wg = groups * units < kStreamWorkgroups ? groups * units : kStreamWorkgroups;
+        p.stream_wg = (int32_t)(wg < 1 ? 1 : wg);
+        p.split_len = 0;
+        p.n_split = 0;
+        p.ml_bytes = round_up((size_t)2 * p.stream_wg * G * 2 * sizeof(float), 256);
+        p.o_bytes = round_up((size_t)2 * p.stream_wg * G * kHeadDim * sizeof(float), 256);
+        p.total = p.ticket_bytes + p.ml_bytes + p.o_bytes;
+        return p;
+    }
     if (split_len <= 0) {
         // Enough workgroups to cover the chip about twice (kTargetWorkgroups),
         // otherwise as few splits as possible: every split adds a partial that
         // the merge has to read back.  At most kMaxAutoSplits splits.
-        const int64_t groups = (int64_t)n_layers * B * Hkv;
         int64_t want = (kTargetWorkgroups + groups - 1) / groups;
         if (want > kMaxAutoSplits) want = kMaxAutoSplits;
         if (want > units) want = units;
@@ -54,12 +69,9 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     }
     p.split_len = split_len;
     p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
-    p.groups = (int64_t)n_layers * B * Hkv;
-    const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
-    p.ticket_bytes = round_up((size_t)p.groups * sizeof(int32_t), 256);
     if (p.n_split > 1) {
-        p.ml_bytes = round_up((size_t)p.groups * p.n_split * G * 2 * sizeof(float), 256);
-        p.o_bytes = round_up((size_t)p.groups * p.n_split * G * kHeadDim * sizeof(float), 256);
+        p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
+        p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
     }
     p.total = p.ticket_bytes + p.ml_bytes + p.o_bytes;
     return p;
@@ -128,9 +140,11 @@ MURMUR_EXPORT int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int3
     if (n_layers < 1 || B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1)
         return fail(MURMUR_EINVAL, "n_layers, B, Hq, Hkv and max_keep must be >= 1");
     if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
-    if (split_len < 0 || split_len % kSplitUnit != 0)
-        return fail(MURMUR_EINVAL, "split_len must be 0 or a positive multiple of %d (got %d)", kSplitUnit,
-                    split_len);
+    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kSplitUnit != 0))
+        return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
+                    kSplitUnit, split_len);
+    if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
+        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
     *bytes = plan_workspace(n_layers, B, Hq, Hkv, max_keep, split_len).total;
     return ok();
 }
@@ -163,9 +177,11 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     if (out_dtype != MURMUR_DTYPE_BF16 && out_dtype != MURMUR_DTYPE_F32)
         return fail(MURMUR_EINVAL, "out_dtype must be MURMUR_DTYPE_BF16 or MURMUR_DTYPE_F32 (got %d)", out_dtype);
     if (!isfinite(scale)) return fail(MURMUR_EINVAL, "scale must be finite");
-    if (split_len < 0 || split_len % kSplitUnit != 0)
-        return fail(MURMUR_EINVAL, "split_len must be 0 or a positive multiple of %d (got %d)", kSplitUnit,
-                    split_len);
+    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kSplitUnit != 0))
+        return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
+                    kSplitUnit, split_len);
+    if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
+        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
     const int64_t strides[4] = {kv->stride_layer, kv->stride_b, kv->stride_h, kv->stride_pos};
     for (int i = 0; i < 4; ++i)
         if (strides[i] < 0 || strides[i] % 8 != 0)
@@ -182,7 +198,7 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
     if (ws_bytes < plan.total)
         return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
-    if (plan.n_split > kMaxMergeSplits)
+    if (!plan.stream_wg && plan.n_split > kMaxMergeSplits)
         return fail(MURMUR_EINVAL, "split_len %d gives %d splits for max_keep %d; at most %d are supported",
                     plan.split_len, plan.n_split, max_keep, kMaxMergeSplits);
     if (plan.o_bytes >= ((size_t)1 << 31))
@@ -207,8 +223,12 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     a.lse = lse_dev;
     uint8_t *ws = (uint8_t *)ws_dev;
     a.ticket = (int32_t *)ws;
-    a.part_ml = plan.n_split > 1 ? (float *)(ws + plan.ticket_bytes) : nullptr;
-    a.part_o = plan.n_split > 1 ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
+    // Partials exist for split schedules of more than one split and for the stream schedule.
+    const bool partials = plan.ml_bytes > 0;
+    if (partials != (plan.stream_wg > 0 || plan.n_split > 1))
+        return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
+    a.part_ml = partials ? (float *)(ws + plan.ticket_bytes) : nullptr;
+    a.part_o = partials ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
     a.part_ml_bytes = (uint32_t)plan.ml_bytes;
     a.part_o_bytes = (uint32_t)plan.o_bytes;
     a.max_len = kv->max_len;
@@ -220,6 +240,7 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     a.NL = kv->n_layers;
     a.split_len = plan.split_len;
     a.n_split = plan.n_split;
+    a.stream_wg = plan.stream_wg;
     a.out_f32 = out_dtype == MURMUR_DTYPE_F32;
     a.scale_log2 = scale * 1.4426950408889634f;
     const int e = launch_decode_attn(a, stream);

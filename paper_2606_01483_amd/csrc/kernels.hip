@@ -194,24 +194,324 @@ struct PassRegs {
     u32x4 vf[8];     // position 8*c4 + t, head dims 8*n16 .. +8
 };
 
+// Running softmax state of one wavefront for one (layer, sequence, KV head):
+// lane (head n16, c4) holds the max (log2 units) and sum of head n16; acc holds
+// O rows 4*c4 + i (heads) at head dims 16*db + n16.
+struct WaveAcc {
+    float m_run, l_run;
+    f32x4 acc[8];
+    int bad_pos;
+};
+
+static __device__ __forceinline__ void wave_acc_reset(WaveAcc &w) {
+    w.m_run = kNegInf;
+    w.l_run = 0.f;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) w.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    w.bad_pos = 0;
+}
+
+// Q^T as the MFMA B operand: lane (head n16, k-group c4) holds head dims
+// kc*32 + 8*c4 .. +8 for kc = 0..3.  Rows past the group are zero (their
+// address is clamped into the group so that nothing outside q is touched).
+static __device__ __forceinline__ void load_q(u32x4 (&qf)[4], const uint16_t *q, int64_t row_of_head0, int G,
+                                              int n16, int c4) {
+    const int hq = n16 < G ? n16 : G - 1;
+    const uint16_t *qrow = q + (row_of_head0 + hq) * kHeadDim;
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) qf[kc] = n16 < G ? load16(qrow + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
+}
+
+// Where the ranks of a pass live: the six-piece range table (rg, in
+// registers) or the index list (idx_row).  Returns the position of rank
+// `rank`, -1 if rank >= r_end; sets bad_pos for positions outside the cache.
+static __device__ __forceinline__ int resolve_rank(int rank, int r_end, bool use_ranges, const int32_t (&rg)[2 * kPieces],
+                                                   const int32_t *idx_row, int max_len, int &bad_pos) {
+    if (rank >= r_end) return -1;
+    const int p = use_ranges ? rank_to_pos(rg, rank) : idx_row[rank];
+    if (p >= 0 && p < max_len) return p;
+    bad_pos = 1;
+    return -1;
+}
+
+// Issues every K and V load of a pass.  mypos: position of rank r0 + (lane & 31)
+// (or -1); positions reach the loading lanes by __shfl.
+static __device__ __forceinline__ void load_pass(PassRegs &R, const uint16_t *kbase, const uint16_t *vbase,
+                                                 int64_t s_pos, int mypos, int n16, int c4) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+        const int pos = __shfl(mypos, 16 * blk + n16);
+        const uint16_t *row = kbase + (int64_t)(pos < 0 ? 0 : pos) * s_pos;
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) R.kf[blk][kc] = pos >= 0 ? load16(row + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int pos = __shfl(mypos, 8 * c4 + t);
+        const uint16_t *row = vbase + (int64_t)(pos < 0 ? 0 : pos) * s_pos;
+        R.vf[t] = pos >= 0 ? load16(row + 8 * n16) : u32x4{0, 0, 0, 0};
+    }
+}
+
+// One pass: S^T = K Q^T, softmax update, O += P V.  `valid` = number of valid
+// ranks of the pass (1..32).  kOnline: fold into a running state (rescaling
+// what is there); otherwise the state is known to be empty.
+template <bool kOnline>
+static __device__ __forceinline__ void compute_pass(const PassRegs &R, const u32x4 (&qf)[4], int valid,
+                                                    float scale_log2, uint8_t *vt, WaveAcc &w, int n16, int c4) {
+    // S^T: lane (head n16, c4), register i of block blk holds the logit of rank
+    // r0 + 16*blk + 4*c4 + i.
+    f32x4 s[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+        s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(R.kf[blk][kc], qf[kc], s[blk]);
+    }
+    // Logits in log2 units; ranks past `valid` are masked (a partial pass).
+    float x[2][4];
+    const bool partial = valid < kWaveTile;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[blk][i] = s[blk][i] * scale_log2;
+            if (partial && 16 * blk + 4 * c4 + i >= valid) x[blk][i] = kNegInf;
+        }
+    float tmax = fmaxf(fmaxf(fmaxf(x[0][0], x[0][1]), fmaxf(x[0][2], x[0][3])),
+                       fmaxf(fmaxf(x[1][0], x[1][1]), fmaxf(x[1][2], x[1][3])));
+    tmax = max_over_c4(tmax);
+    const float m_new = kOnline ? fmaxf(w.m_run, tmax) : tmax;  // finite: rank 0 of the pass is valid
+    float psum = 0.f;
+    float pr[2][4];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            pr[blk][i] = __builtin_amdgcn_exp2f(x[blk][i] - m_new);  // in [0, 1]
+            psum += pr[blk][i];
+        }
+    psum = sum_over_c4(psum);
+    if (kOnline) {
+        const float alpha = __builtin_amdgcn_exp2f(w.m_run - m_new);  // 0 while the state is empty
+        w.l_run = w.l_run * alpha + psum;
+        // Rescale O rows: row 4*c4 + i belongs to head 4*c4 + i.
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float ai = __shfl(alpha, 4 * c4 + i);
+#pragma unroll
+            for (int db = 0; db < 8; ++db) w.acc[db][i] *= ai;
+        }
+    } else {
+        w.l_run = psum;
+    }
+    w.m_run = m_new;
+
+    // P as the A operand of O = P V, k order (4*c4 + 0..3, 16 + 4*c4 + 0..3),
+    // split into bf16 hi + lo so that hi + lo carries ~16 mantissa bits.
+    u32x4 p_hi, p_lo;
+#pragma unroll
+    for (int wd = 0; wd < 4; ++wd) {
+        const int blk = wd >> 1, i0 = (wd & 1) * 2;
+        const float e0 = pr[blk][i0], e1 = pr[blk][i0 + 1];
+        const uint32_t hi = pack_bf16(e0, e1);
+        p_hi[wd] = hi;
+        p_lo[wd] = pack_bf16(e0 - __builtin_bit_cast(float, hi << 16), e1 - __builtin_bit_cast(float, hi & 0xffff0000u));
+    }
+
+    // V^T through LDS.  Lane (e = n16, octet c4) holds positions 8*c4 + t
+    // (t = 0..7) of head dims 8e .. 8e+7; one v_perm_b32 per output word
+    // gathers a head dim's values of two positions, then one 16-byte unit per
+    // head dim is stored (halves swapped for odd head dims).
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int wd = i >> 1;
+        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;  // high or low halves of both words
+        uint32_t o[4];
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) o[pp] = __builtin_amdgcn_perm(R.vf[2 * pp + 1][wd], R.vf[2 * pp][wd], sel);
+        const u32x4 unit = (i & 1) ? u32x4{o[2], o[3], o[0], o[1]} : u32x4{o[0], o[1], o[2], o[3]};
+        *reinterpret_cast<u32x4 *>(vt + vt_unit(8 * n16 + i, c4) * 16) = unit;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // O += P V for each block of 16 head dims.  B operand lane (dim n16, c4)
+    // needs positions 4*c4 .. +3 and 16 + 4*c4 .. +3 of head dim d.
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+        const int d = 16 * db + n16;
+        const int hsw = ((c4 & 1) ^ (d & 1)) * 8;
+        const u32x2 lo = *reinterpret_cast<const u32x2 *>(vt + vt_unit(d, c4 >> 1) * 16 + hsw);
+        const u32x2 hi = *reinterpret_cast<const u32x2 *>(vt + vt_unit(d, 2 + (c4 >> 1)) * 16 + hsw);
+        const u32x4 bv = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        w.acc[db] = mfma16x16x32(p_hi, bv, w.acc[db]);
+        w.acc[db] = mfma16x16x32(p_lo, bv, w.acc[db]);
+    }
+    // The next pass overwrites this wave's tile only after these reads have
+    // returned (their results feed the MFMAs above).
+}
+
+// LDS shared by the combine step of both schedules.
+struct CombineLds {
+    float ml[kWavesPerWg][kMaxGroup][2];  // per wave and head: max (log2 units), sum
+    float mlf[kMaxGroup][2];              // per head: workgroup max, workgroup sum (NaN when bad)
+};
+
+// Merges the four wavefronts' states of one (layer, sequence, KV head) in LDS.
+// Afterwards o_lds[w][h][d] holds wave w's O rescaled to the workgroup max,
+// whose sum over w is the workgroup's unnormalised O; cl.mlf holds (max, sum).
+// Block-wide: every thread calls it.
+static __device__ __forceinline__ void combine_waves(const WaveAcc &w, bool bad, float *o_lds, CombineLds &cl,
+                                                     int G, int tid, int wave, int n16, int c4) {
+    if (c4 == 0) {
+        cl.ml[wave][n16][0] = w.m_run;
+        cl.ml[wave][n16][1] = w.l_run;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int h = 4 * c4 + i;
+        if (h < G) {
+            const float mx = fmaxf(fmaxf(cl.ml[0][h][0], cl.ml[1][h][0]), fmaxf(cl.ml[2][h][0], cl.ml[3][h][0]));
+            const float mine = cl.ml[wave][h][0];
+            const float f = mine == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mine - mx);
+#pragma unroll
+            for (int db = 0; db < 8; ++db) o_lds[(wave * kMaxGroup + h) * kHeadDim + 16 * db + n16] = w.acc[db][i] * f;
+        }
+    }
+    if (tid < G) {
+        const float mx = fmaxf(fmaxf(cl.ml[0][tid][0], cl.ml[1][tid][0]), fmaxf(cl.ml[2][tid][0], cl.ml[3][tid][0]));
+        float L = 0.f;
+#pragma unroll
+        for (int wv = 0; wv < kWavesPerWg; ++wv) {
+            const float mw = cl.ml[wv][tid][0];
+            L += cl.ml[wv][tid][1] * (mw == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mw - mx));
+        }
+        cl.mlf[tid][0] = mx;
+        cl.mlf[tid][1] = bad ? __builtin_nanf("") : L;
+    }
+    __syncthreads();
+}
+
+static __device__ __forceinline__ f32x4 combined_o(const float *o_lds, int h, int d0) {
+    f32x4 O = *reinterpret_cast<const f32x4 *>(&o_lds[h * kHeadDim + d0]);
+#pragma unroll
+    for (int wv = 1; wv < kWavesPerWg; ++wv) O += *reinterpret_cast<const f32x4 *>(&o_lds[(wv * kMaxGroup + h) * kHeadDim + d0]);
+    return O;
+}
+
+// Normalised output of four head dims and, from the thread owning d0 == 0, the lse.
+static __device__ __forceinline__ void store_output(const AttnLaunch &a, int64_t row, int d0, f32x4 O, float M, float L) {
+    const int64_t orow = row * kHeadDim + d0;
+    const float inv = 1.f / L;
+    if (a.out_f32)
+        *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(a.out) + orow) = O * inv;
+    else
+        *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(a.out) + orow) =
+            u32x2{pack_bf16(O[0] * inv, O[1] * inv), pack_bf16(O[2] * inv, O[3] * inv)};
+    if (d0 == 0 && a.lse) a.lse[row] = (M + __builtin_log2f(L)) * 0.69314718055994530942f;
+}
+
+// Writes the workgroup's combined result: the output itself when it covered
+// the whole (layer, sequence, KV head), else a partial in slot `slot`.
+static __device__ __forceinline__ void write_result(const AttnLaunch &a, const float *o_lds, const CombineLds &cl,
+                                                    int G, int tid, int64_t row0, bool whole, uint32_t slot) {
+    for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
+        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
+        const f32x4 O = combined_o(o_lds, h, d0);
+        const float mx = cl.mlf[h][0], L = cl.mlf[h][1];
+        if (whole) {
+            store_output(a, row0 + h, d0, O, mx, L);
+        } else {
+            const uint32_t prow = slot * G + h;
+            store_coherent4(raw_buffer(a.part_o, a.part_o_bytes), (prow * kHeadDim + d0) * 4, O);
+            if (d0 == 0) {
+                const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+                store_coherent1(rml, prow * 8, mx);
+                store_coherent1(rml, prow * 8 + 4, L);
+            }
+        }
+    }
+}
+
+// Takes a ticket for group `grp` after this workgroup's partial stores have
+// completed; true in the workgroup that draws the last of `n` tickets (which
+// also resets the counter for the next call).  Block-wide.
+static __device__ __forceinline__ bool take_ticket(const AttnLaunch &a, int grp, int n, int tid, int &s_last) {
+    wait_vmem();
+    __syncthreads();
+    if (tid == 0) {
+        const int prev = __hip_atomic_fetch_add(&a.ticket[grp], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = prev == n - 1;
+        if (s_last) __hip_atomic_store(&a.ticket[grp], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    return s_last != 0;
+}
+
+// Cross-split log-sum-exp merge of the n partials of one group; slot_of(i)
+// gives the slot of the i-th.  Each thread owns four consecutive head dims of
+// one head and folds the partials in batches whose loads are all in flight
+// together.  Block-wide.
+template <typename SlotOf>
+static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
+                                                      int64_t row0) {
+    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+    for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
+        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
+        float M = kNegInf, L = 0.f;
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
+        for (int base = 0; base < n; base += kMergeBatch) {
+            float mm[kMergeBatch], ll[kMergeBatch];
+            f32x4 oo[kMergeBatch];
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const uint32_t prow = slot_of(base + k < n ? base + k : 0) * G + h;
+                mm[k] = load_coherent1(rml, prow * 8);
+                ll[k] = load_coherent1(rml, prow * 8 + 4);
+                oo[k] = load_coherent4(ro, (prow * kHeadDim + d0) * 4);
+            }
+            float bm = M;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k)
+                if (base + k < n) bm = fmaxf(bm, mm[k]);
+            const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - bm);
+            L *= sc;
+            O *= sc;
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const float f = (base + k >= n || mm[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mm[k] - bm);
+                L += ll[k] * f;
+                O += oo[k] * f;
+            }
+            M = bm;
+        }
+        store_output(a, row0 + h, d0, O, M, L);
+    }
+}
+
 // ---------------------------------------------------------------------------
-// decode_attn: one workgroup per (split, KV head, sequence, layer).  Each of
-// its four wavefronts takes passes of 32 retained positions, interleaved over
-// the split.  kMultiPass: splits longer than one workgroup pass keep an online
-// softmax across passes and have the next pass's loads in flight while the
-// current one is computed; otherwise every wavefront makes at most one pass.
-// ---------------------------------------------------------------------------
-template <bool kMultiPass>
+// decode_attn, split schedule: one workgroup per (split, KV head, sequence,
+// layer).  Each of its four wavefronts takes passes of 32 retained positions,
+// interleaved over the split.  kMultiPass: splits longer than one workgroup
+// pass keep an online softmax across passes and have the next pass's loads in
+// flight while the current one is computed; otherwise every wavefront makes at
+// most one pass.  The last workgroup of each group merges the splits.
 // The leading scalar arguments are the ones the first memory accesses need;
 // the build preloads them into SGPRs so no kernel-argument load precedes the
 // range-table load.
+// ---------------------------------------------------------------------------
+template <bool kMultiPass>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ count,
                                                           const int32_t *__restrict__ ranges,
                                                           const int32_t *__restrict__ idx,
                                                           const uint16_t *__restrict__ q, int32_t max_keep,
                                                           int32_t B, const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
-    __shared__ float ml_lds[kWavesPerWg][kMaxGroup][2];
+    __shared__ CombineLds cl;
     __shared__ int s_last;
 
     const int tid = threadIdx.x;
@@ -232,7 +532,6 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     int cnt = count[b];
     const bool bad_count = cnt < 1 || cnt > max_keep;
     if (bad_count) cnt = cnt < 0 ? 0 : (cnt > max_keep ? max_keep : cnt);
-    int bad_pos = 0;
     const int r_begin = split * a.split_len;
     const int r_end = min(r_begin + a.split_len, cnt);
 
@@ -242,289 +541,245 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     for (int k = 0; k < 2 * kPieces; ++k) rg[k] = use_ranges ? ranges[b * 2 * kPieces + k] : 0;
     const int32_t *idx_row = idx + (int64_t)b * max_keep;
 
-    // Q^T as the MFMA B operand: lane (head n16, k-group c4) holds head dims
-    // kc*32 + 8*c4 .. +8 for kc = 0..3.  Rows past the group are zero.
+    const int64_t row0 = (int64_t)lb * a.Hq + g * G;  // first output row of the group
     u32x4 qf[4];
-    {
-        const int hq = n16 < G ? n16 : G - 1;  // keep the address inside q for padded rows
-        const uint16_t *qrow = q + ((int64_t)lb * a.Hq + g * G + hq) * kHeadDim;
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) qf[kc] = n16 < G ? load16(qrow + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
-    }
+    load_q(qf, q, row0, G, n16, c4);
     const uint16_t *kbase = a.k + layer * a.s_layer + b * a.s_b + g * a.s_h;
     const uint16_t *vbase = a.v + layer * a.s_layer + b * a.s_b + g * a.s_h;
-
     uint8_t *vt = smem + wave * kVtBytesPerWave;
 
-    float m_run = kNegInf;  // running max of head n16, log2 units
-    float l_run = 0.f;      // running sum of exp2(s - m_run) of head n16
-    f32x4 acc[8];           // O rows 4*c4 + i (heads), column 16*db + n16 (head dim)
-#pragma unroll
-    for (int db = 0; db < 8; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // Positions of the pass starting at rank r0, then every K and V load of it.
-    auto issue = [&](int r0, PassRegs &R) {
-        const int myrank = r0 + (lane & 31);
-        int mypos = -1;  // position of rank r0 + (lane & 31); -1 past the split or if invalid
-        if (myrank < r_end) {
-            const int p = use_ranges ? rank_to_pos(rg, myrank) : idx_row[myrank];
-            if (p >= 0 && p < a.max_len)
-                mypos = p;
-            else
-                bad_pos = 1;
-        }
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk) {
-            const int pos = __shfl(mypos, 16 * blk + n16);
-            const uint16_t *row = kbase + (int64_t)(pos < 0 ? 0 : pos) * a.s_pos;
-#pragma unroll
-            for (int kc = 0; kc < 4; ++kc)
-                R.kf[blk][kc] = pos >= 0 ? load16(row + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
-        }
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const int pos = __shfl(mypos, 8 * c4 + t);
-            const uint16_t *row = vbase + (int64_t)(pos < 0 ? 0 : pos) * a.s_pos;
-            R.vf[t] = pos >= 0 ? load16(row + 8 * n16) : u32x4{0, 0, 0, 0};
-        }
-    };
-
-    auto consume = [&](int r0, const PassRegs &R) {
-        // S^T = K Q^T: lane (head n16, c4), register i of block blk holds the
-        // logit of rank r0 + 16*blk + 4*c4 + i.
-        f32x4 s[2];
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk) {
-            s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(R.kf[blk][kc], qf[kc], s[blk]);
-        }
-
-        // Logits in log2 units; ranks past the split end are masked (only a
-        // wavefront's last, partial pass has any).
-        float x[2][4];
-        const bool partial = r_end - r0 < kWaveTile;
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                x[blk][i] = s[blk][i] * a.scale_log2;
-                if (partial && 16 * blk + 4 * c4 + i >= r_end - r0) x[blk][i] = kNegInf;
-            }
-        float tmax = fmaxf(fmaxf(fmaxf(x[0][0], x[0][1]), fmaxf(x[0][2], x[0][3])),
-                           fmaxf(fmaxf(x[1][0], x[1][1]), fmaxf(x[1][2], x[1][3])));
-        tmax = max_over_c4(tmax);
-        const float m_new = kMultiPass ? fmaxf(m_run, tmax) : tmax;  // finite: rank r0 is always valid
-        float psum = 0.f;
-        float pr[2][4];
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                pr[blk][i] = __builtin_amdgcn_exp2f(x[blk][i] - m_new);  // in [0, 1]
-                psum += pr[blk][i];
-            }
-        psum = sum_over_c4(psum);
-        if (kMultiPass) {
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first pass (m_run = -inf)
-            l_run = l_run * alpha + psum;
-            // Rescale O rows: row 4*c4 + i belongs to head 4*c4 + i.
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float ai = __shfl(alpha, 4 * c4 + i);
-#pragma unroll
-                for (int db = 0; db < 8; ++db) acc[db][i] *= ai;
-            }
-        } else {
-            l_run = psum;
-        }
-        m_run = m_new;
-
-        // P as the A operand of O = P V, k order (4*c4 + 0..3, 16 + 4*c4 + 0..3),
-        // split into bf16 hi + lo so that hi + lo carries ~16 mantissa bits.
-        u32x4 p_hi, p_lo;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const int blk = w >> 1, i0 = (w & 1) * 2;
-            const float e0 = pr[blk][i0], e1 = pr[blk][i0 + 1];
-            const uint32_t hi = pack_bf16(e0, e1);
-            p_hi[w] = hi;
-            p_lo[w] = pack_bf16(e0 - __builtin_bit_cast(float, hi << 16),
-                                e1 - __builtin_bit_cast(float, hi & 0xffff0000u));
-        }
-
-        // V^T through LDS.  Lane (e = n16, octet c4) holds positions 8*c4 + t
-        // (t = 0..7) of head dims 8e .. 8e+7; one v_perm_b32 per output word
-        // gathers a head dim's values of two positions, then one 16-byte unit
-        // per head dim is stored (halves swapped for odd head dims).
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int w = i >> 1;
-            const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;  // high or low halves of both words
-            uint32_t o[4];
-#pragma unroll
-            for (int pp = 0; pp < 4; ++pp) o[pp] = __builtin_amdgcn_perm(R.vf[2 * pp + 1][w], R.vf[2 * pp][w], sel);
-            const u32x4 unit = (i & 1) ? u32x4{o[2], o[3], o[0], o[1]} : u32x4{o[0], o[1], o[2], o[3]};
-            *reinterpret_cast<u32x4 *>(vt + vt_unit(8 * n16 + i, c4) * 16) = unit;
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        // O += P V for each block of 16 head dims.  B operand lane (dim n16,
-        // c4) needs positions 4*c4 .. +3 and 16 + 4*c4 .. +3 of head dim d.
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-            const int d = 16 * db + n16;
-            const int hsw = ((c4 & 1) ^ (d & 1)) * 8;
-            const u32x2 lo = *reinterpret_cast<const u32x2 *>(vt + vt_unit(d, c4 >> 1) * 16 + hsw);
-            const u32x2 hi = *reinterpret_cast<const u32x2 *>(vt + vt_unit(d, 2 + (c4 >> 1)) * 16 + hsw);
-            const u32x4 bv = u32x4{lo[0], lo[1], hi[0], hi[1]};
-            acc[db] = mfma16x16x32(p_hi, bv, acc[db]);
-            acc[db] = mfma16x16x32(p_lo, bv, acc[db]);
-        }
-        // The next pass overwrites this wave's tile only after these reads
-        // have returned (their results feed the MFMAs above).
-    };
-
+    WaveAcc w;
+    wave_acc_reset(w);
     {
         int r0 = r_begin + wave * kWaveTile;
         PassRegs cur;
-        if (r0 < r_end) issue(r0, cur);
+        if (r0 < r_end)
+            load_pass(cur, kbase, vbase, a.s_pos,
+                      resolve_rank(r0 + (lane & 31), r_end, use_ranges, rg, idx_row, a.max_len, w.bad_pos), n16, c4);
         if (kMultiPass) {
             for (; r0 < r_end; r0 += kSplitUnit) {
                 PassRegs nxt;
-                const bool more = r0 + kSplitUnit < r_end;
-                if (more) issue(r0 + kSplitUnit, nxt);
-                consume(r0, cur);
+                const int rn = r0 + kSplitUnit;
+                const bool more = rn < r_end;
+                if (more)
+                    load_pass(nxt, kbase, vbase, a.s_pos,
+                              resolve_rank(rn + (lane & 31), r_end, use_ranges, rg, idx_row, a.max_len, w.bad_pos), n16,
+                              c4);
+                compute_pass<true>(cur, qf, min(kWaveTile, r_end - r0), a.scale_log2, vt, w, n16, c4);
                 if (more) cur = nxt;
             }
         } else if (r0 < r_end) {
-            consume(r0, cur);
+            compute_pass<false>(cur, qf, min(kWaveTile, r_end - r0), a.scale_log2, vt, w, n16, c4);
         }
     }
 
-    // ---- combine the four wavefronts of the workgroup -------------------
-    __shared__ float mlf_lds[kMaxGroup][2];  // per head: workgroup max (log2 units), workgroup sum
-    if (c4 == 0) {
-        ml_lds[wave][n16][0] = m_run;
-        ml_lds[wave][n16][1] = l_run;
-    }
-    const int wg_bad_pos = __syncthreads_or(bad_pos);
+    const int wg_bad_pos = __syncthreads_or(w.bad_pos);
     const bool bad = wg_bad_pos || bad_count;
     float *o_lds = reinterpret_cast<float *>(smem);  // [wave][16][128], reuses the V tiles
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int h = 4 * c4 + i;
-        if (h < G) {
-            const float mx = fmaxf(fmaxf(ml_lds[0][h][0], ml_lds[1][h][0]), fmaxf(ml_lds[2][h][0], ml_lds[3][h][0]));
-            const float mine = ml_lds[wave][h][0];
-            const float f = mine == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mine - mx);
-#pragma unroll
-            for (int db = 0; db < 8; ++db) o_lds[(wave * kMaxGroup + h) * kHeadDim + 16 * db + n16] = acc[db][i] * f;
-        }
-    }
-    if (tid < G) {
-        const float mx = fmaxf(fmaxf(ml_lds[0][tid][0], ml_lds[1][tid][0]), fmaxf(ml_lds[2][tid][0], ml_lds[3][tid][0]));
-        float L = 0.f;
-#pragma unroll
-        for (int w = 0; w < kWavesPerWg; ++w) {
-            const float mw = ml_lds[w][tid][0];
-            L += ml_lds[w][tid][1] * (mw == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mw - mx));
-        }
-        mlf_lds[tid][0] = mx;
-        mlf_lds[tid][1] = bad ? __builtin_nanf("") : L;
-    }
-    __syncthreads();
-
-    // Each thread owns four consecutive head dims of one head.
-    const int64_t row0 = (int64_t)lb * a.Hq + g * G;  // first output row of the group
-    const float ln2 = 0.69314718055994530942f;
-    for (int c = tid; c < G * (kHeadDim / 4); c += blockDim.x) {
-        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        f32x4 O = *reinterpret_cast<const f32x4 *>(&o_lds[h * kHeadDim + d0]);
-#pragma unroll
-        for (int w = 1; w < kWavesPerWg; ++w) O += *reinterpret_cast<const f32x4 *>(&o_lds[(w * kMaxGroup + h) * kHeadDim + d0]);
-        const float mx = mlf_lds[h][0], L = mlf_lds[h][1];
-        if (a.n_split == 1) {
-            const int64_t orow = (row0 + h) * kHeadDim + d0;
-            const float inv = 1.f / L;
-            if (a.out_f32)
-                *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(a.out) + orow) = O * inv;
-            else
-                *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(a.out) + orow) =
-                    u32x2{pack_bf16(O[0] * inv, O[1] * inv), pack_bf16(O[2] * inv, O[3] * inv)};
-            if (d0 == 0 && a.lse) a.lse[row0 + h] = (mx + __builtin_log2f(L)) * ln2;
-        } else {
-            const uint32_t prow = ((uint32_t)grp * a.n_split + split) * G + h;
-            store_coherent4(raw_buffer(a.part_o, a.part_o_bytes), (prow * kHeadDim + d0) * 4, O);
-            if (d0 == 0) {
-                const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-                store_coherent1(rml, prow * 8, mx);
-                store_coherent1(rml, prow * 8 + 4, L);
-            }
-        }
-    }
+    combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
+    write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
+    if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
+    const uint32_t pbase = (uint32_t)grp * a.n_split;
+    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0);
+}
 
-    // ---- cross-split log-sum-exp merge by the last workgroup of the group ----
-    // Every partial store has completed before the ticket is taken, so the
-    // workgroup that draws the last ticket sees all partials.
-    wait_vmem();
+// ---------------------------------------------------------------------------
+// decode_attn, stream schedule: a persistent grid of P workgroups.  The work
+// is the sequence of 128-position units of every (layer, sequence, KV head)
+// group in (layer, sequence, KV head) order; workgroup p takes the contiguous
+// units [p*U/P, (p+1)*U/P) and streams through them with the next unit's
+// loads in flight, across group boundaries.  A group it covers whole is
+// written directly; a group cut by a range boundary leaves a partial in slot
+// 2p (its first segment) or 2p+1 (its last), and the last contributor merges.
+// Per-sequence counts, range tables and unit offsets are staged in LDS.
+// ---------------------------------------------------------------------------
+struct UnitPos {
+    int layer, b, g, k;  // k: unit index within the group
+};
+
+__global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *__restrict__ count,
+                                                                 const int32_t *__restrict__ ranges,
+                                                                 const int32_t *__restrict__ idx,
+                                                                 const uint16_t *__restrict__ q, int32_t max_keep,
+                                                                 int32_t B, const AttnLaunch a) {
+    __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
+    __shared__ CombineLds cl;
+    __shared__ int s_last;
+    __shared__ int32_t s_cnt[kStreamMaxB];      // counts clamped to [0, max_keep]
+    __shared__ int32_t s_pre[kStreamMaxB + 1];  // Hkv * (units of the sequences before b), b = 0..B
+    __shared__ int32_t s_rg[kStreamMaxB][2 * kPieces];
+    __shared__ uint32_t s_bad[kStreamMaxB / 32];  // sequences with an invalid count
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int n16 = lane & 15;
+    const int c4 = lane >> 4;
+    const int Hkv = a.Hkv, G = a.G;
+    const bool use_ranges = ranges != nullptr;
+
+    // ---- per-sequence tables -------------------------------------------------
+    if (tid < kStreamMaxB / 32) s_bad[tid] = 0;
     __syncthreads();
-    if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&a.ticket[grp], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = prev == a.n_split - 1;
+    for (int t = tid; t < B; t += blockDim.x) {
+        const int c = count[t];
+        const bool badc = c < 1 || c > max_keep;
+        const int cc = c < 0 ? 0 : (c > max_keep ? max_keep : c);
+        s_cnt[t] = cc;
+        s_pre[t + 1] = cc > kSplitUnit ? (cc + kSplitUnit - 1) / kSplitUnit : 1;  // units, at least one
+        if (badc) atomicOr(&s_bad[t >> 5], 1u << (t & 31));
+        if (use_ranges) {
+#pragma unroll
+            for (int k = 0; k < 2 * kPieces; ++k) s_rg[t][k] = ranges[t * 2 * kPieces + k];
+        }
     }
     __syncthreads();
-    if (!s_last) return;
-    if (tid == 0) __hip_atomic_store(&a.ticket[grp], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-
-    // Each thread owns four consecutive head dims of one head and folds the
-    // splits in batches whose loads are all in flight together.
-    const uint32_t pbase = (uint32_t)grp * a.n_split;
-    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
-    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-    for (int c = tid; c < G * (kHeadDim / 4); c += blockDim.x) {
-        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        float M = kNegInf, L = 0.f;
-        f32x4 O = {0.f, 0.f, 0.f, 0.f};
-        for (int base = 0; base < a.n_split; base += kMergeBatch) {
-            float mm[kMergeBatch], ll[kMergeBatch];
-            f32x4 oo[kMergeBatch];
+    if (wave == 0) {  // exclusive prefix sum of the unit counts by one wavefront, a chunk per lane
+        constexpr int kPer = kStreamMaxB / 64;
+        const int per = (B + 63) / 64;
+        int units[kPer];
+        int local = 0;
 #pragma unroll
-            for (int k = 0; k < kMergeBatch; ++k) {
-                const uint32_t prow = (pbase + (base + k < a.n_split ? base + k : 0)) * G + h;
-                mm[k] = load_coherent1(rml, prow * 8);
-                ll[k] = load_coherent1(rml, prow * 8 + 4);
-                oo[k] = load_coherent4(ro, (prow * kHeadDim + d0) * 4);
-            }
-            float bm = M;
-#pragma unroll
-            for (int k = 0; k < kMergeBatch; ++k)
-                if (base + k < a.n_split) bm = fmaxf(bm, mm[k]);
-            const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - bm);
-            L *= sc;
-            O *= sc;
-#pragma unroll
-            for (int k = 0; k < kMergeBatch; ++k) {
-                const float f = (base + k >= a.n_split || mm[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mm[k] - bm);
-                L += ll[k] * f;
-                O += oo[k] * f;
-            }
-            M = bm;
+        for (int i = 0; i < kPer; ++i) {  // read every count before any prefix overwrites it
+            const int t = lane * per + i;
+            units[i] = (i < per && t < B) ? s_pre[t + 1] : 0;
+            local += units[i];
         }
-        const int64_t orow = (row0 + h) * kHeadDim + d0;
-        const float inv = 1.f / L;
-        if (a.out_f32)
-            *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(a.out) + orow) =
-                f32x4{O[0] * inv, O[1] * inv, O[2] * inv, O[3] * inv};
-        else
-            *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(a.out) + orow) =
-                u32x2{pack_bf16(O[0] * inv, O[1] * inv), pack_bf16(O[2] * inv, O[3] * inv)};
-        if (d0 == 0 && a.lse) a.lse[row0 + h] = (M + __builtin_log2f(L)) * ln2;
+        int incl = local;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(incl, off);
+            if (lane >= off) incl += v;
+        }
+        int run = incl - local;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const int t = lane * per + i;
+            if (i < per && t < B) s_pre[t] = run * Hkv;
+            run += units[i];
+        }
+        if (lane == 63) s_pre[B] = incl * Hkv;
+    }
+    __syncthreads();
+
+    const int64_t U_layer = s_pre[B];
+    const int64_t U = (int64_t)a.NL * U_layer;
+    // Counts below max_keep can leave fewer units than workgroups: only the
+    // first P = min(grid, U) take part, so that every one of them has work and
+    // the contributor count of a group is the number of its owners.
+    const int64_t P = U < (int64_t)gridDim.x ? U : (int64_t)gridDim.x, p = blockIdx.x;
+    if (p >= P) return;
+    int64_t u = p * U / P;
+    const int64_t u_end = (p + 1) * U / P;
+    const int64_t u_begin = u;
+    auto owner = [&](int64_t unit) { return ((unit + 1) * P - 1) / U; };
+    auto units_of = [&](int b) { return (s_pre[b + 1] - s_pre[b]) / Hkv; };
+
+    UnitPos cur;
+    {
+        cur.layer = (int)(u / U_layer);
+        const int r = (int)(u - cur.layer * U_layer);
+        int lo = 0, hi = B - 1;  // last b with s_pre[b] <= r
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_pre[mid] <= r) lo = mid; else hi = mid - 1;
+        }
+        cur.b = lo;
+        const int off = r - s_pre[lo], ub = units_of(lo);
+        cur.g = off / ub;
+        cur.k = off - cur.g * ub;
+    }
+    auto advance = [&](UnitPos x) {
+        if (++x.k == units_of(x.b)) {
+            x.k = 0;
+            if (++x.g == Hkv) {
+                x.g = 0;
+                if (++x.b == B) {
+                    x.b = 0;
+                    ++x.layer;
+                }
+            }
+        }
+        return x;
+    };
+    auto issue_unit = [&](const UnitPos &x, PassRegs &R, int &bad_pos) {
+        const int cnt = s_cnt[x.b];
+        const int r0 = x.k * kSplitUnit + wave * kWaveTile;
+        if (r0 >= cnt) return;
+        int32_t rg[2 * kPieces];
+#pragma unroll
+        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = use_ranges ? s_rg[x.b][k] : 0;
+        const int32_t *idx_row = idx + (int64_t)x.b * max_keep;
+        const int64_t off = x.layer * a.s_layer + x.b * a.s_b + x.g * a.s_h;
+        load_pass(R, a.k + off, a.v + off, a.s_pos,
+                  resolve_rank(r0 + (lane & 31), cnt, use_ranges, rg, idx_row, a.max_len, bad_pos), n16, c4);
+    };
+    auto row_of = [&](const UnitPos &x) { return ((int64_t)x.layer * B + x.b) * a.Hq + x.g * G; };
+
+    uint8_t *vt = smem + wave * kVtBytesPerWave;
+    float *o_lds = reinterpret_cast<float *>(smem);
+    WaveAcc w;
+    wave_acc_reset(w);
+    u32x4 qf[4], qn[4];
+    load_q(qf, q, row_of(cur), G, n16, c4);
+    PassRegs R, Rn;
+    issue_unit(cur, R, w.bad_pos);
+    int seg_k0 = cur.k;  // first unit of the current segment within its group
+
+    for (; u < u_end; ++u) {
+        const bool has_next = u + 1 < u_end;
+        const UnitPos nxt = advance(cur);
+        const bool next_new_group = !(nxt.layer == cur.layer && nxt.b == cur.b && nxt.g == cur.g);
+        int next_bad = 0;  // invalid positions met while resolving the next unit
+        if (has_next) {
+            issue_unit(nxt, Rn, next_bad);
+            if (next_new_group) load_q(qn, q, row_of(nxt), G, n16, c4);
+        }
+        {
+            const int valid = s_cnt[cur.b] - (cur.k * kSplitUnit + wave * kWaveTile);
+            if (valid > 0) compute_pass<true>(R, qf, min(kWaveTile, valid), a.scale_log2, vt, w, n16, c4);
+        }
+        if (!has_next || next_new_group) {
+            // The segment of group `cur` in this workgroup ends here.
+            const bool bad_count = (s_bad[cur.b >> 5] >> (cur.b & 31)) & 1u;
+            const int wg_bad_pos = __syncthreads_or(w.bad_pos);
+            const bool bad = wg_bad_pos || bad_count;
+            combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
+            const int ub = units_of(cur.b);
+            const bool whole = seg_k0 == 0 && cur.k == ub - 1;
+            const int64_t s_g = cur.layer * U_layer + s_pre[cur.b] + (int64_t)cur.g * ub;  // group's first unit
+            const uint32_t slot = (uint32_t)(2 * p + (u_begin < s_g ? 1 : 0));
+            const int64_t row0 = row_of(cur);
+            write_result(a, o_lds, cl, G, tid, row0, whole, slot);
+            if (bad && tid == 0)
+                raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
+            if (!whole) {
+                const int64_t first = owner(s_g), last = owner(s_g + ub - 1);
+                const int grp = (int)(((int64_t)cur.layer * B + cur.b) * Hkv + cur.g);
+                if (take_ticket(a, grp, (int)(last - first + 1), tid, s_last)) {
+                    merge_partials(
+                        a, (int)(last - first + 1),
+                        [&](int i) {
+                            const int64_t pp = first + i;
+                            return (uint32_t)(2 * pp + ((pp * U / P) < s_g ? 1 : 0));
+                        },
+                        G, tid, row0);
+                }
+            }
+            __syncthreads();  // the next pass reuses the LDS tiles
+            wave_acc_reset(w);
+            seg_k0 = 0;
+            if (has_next && next_new_group) {
+#pragma unroll
+                for (int kc = 0; kc < 4; ++kc) qf[kc] = qn[kc];
+            }
+        }
+        w.bad_pos |= next_bad;
+        cur = nxt;
+        R = Rn;
     }
 }
 
@@ -544,6 +799,11 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 }
 
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
+    if (a.stream_wg > 0) {
+        hipLaunchKernelGGL(decode_attn_stream_kernel, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
+                           (hipStream_t)stream, a.count, a.ranges, a.idx, a.q, a.max_keep, a.B, a);
+        return (int)hipGetLastError();
+    }
     const dim3 grid((unsigned)a.n_split, (unsigned)a.Hkv, (unsigned)(a.NL * a.B));
     // Splits of more than one pass per wavefront double-buffer their loads.
     if (a.split_len > kSplitUnit)

@@ -20,6 +20,7 @@ MURMUR_DTYPE_BF16, MURMUR_DTYPE_F32 = 1, 2
 MURMUR_DEVERR_OVERFLOW, MURMUR_DEVERR_POLICY, MURMUR_DEVERR_POSITION, MURMUR_DEVERR_COUNT = 1, 2, 4, 8
 N_PIECES = 6
 SPLIT_UNIT = 128
+MURMUR_SPLIT_STREAM = -1
 
 _ERROR_NAMES = {MURMUR_EINVAL: "EINVAL", MURMUR_EUNSUPPORTED: "EUNSUPPORTED", MURMUR_ENOSPACE: "ENOSPACE",
                 MURMUR_EHIP: "EHIP"}

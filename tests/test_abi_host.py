@@ -111,6 +111,8 @@ def call_attn(a):
     (dict(scale=float("inf")), M.MURMUR_EINVAL),
     (dict(split_len=100), M.MURMUR_EINVAL),
     (dict(split_len=-128), M.MURMUR_EINVAL),
+    (dict(split_len=-2), M.MURMUR_EINVAL),
+    (dict(split_len=M.MURMUR_SPLIT_STREAM, B=300), M.MURMUR_EUNSUPPORTED),
     (dict(q=FAKE + 8), M.MURMUR_EINVAL),
     (dict(ws=FAKE + 64), M.MURMUR_EINVAL),
     (dict(lse=FAKE + 2), M.MURMUR_EINVAL),
@@ -137,20 +139,34 @@ def test_evict_compact_rejects():
 
 
 def test_workspace_sizing():
+    def rnd(x):
+        return (x + 255) // 256 * 256
     ws = M.murmur_decode_attn_workspace(1, 12, 28, 4, 850)
-    # 48 tickets; 7 splits of 128 positions: 48*7*7 partials of (m, l) and 128 outputs
-    assert ws == 256 + (48 * 7 * 7 * 2 * 4 + 255) // 256 * 256 + (48 * 7 * 7 * 128 * 4 + 255) // 256 * 256
+    # 336 units of 128 positions: split schedule, 48 tickets, 7 splits of 128 positions:
+    # 48*7*7 partials of (m, l) and of 128 outputs
+    assert ws == 256 + rnd(48 * 7 * 7 * 2 * 4) + rnd(48 * 7 * 7 * 128 * 4)
     assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 100) == 256  # one split: tickets only
     assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 1024) == 256
-    # long lists are capped at 64 splits
-    big = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160)
-    n_split = -(-35160 // (128 * -(-(-(-35160 // 128)) // 64)))
-    assert n_split <= 64
-    assert big == 256 + (4 * n_split * 7 * 2 * 4 + 255) // 256 * 256 + (4 * n_split * 7 * 128 * 4 + 255) // 256 * 256
+    # an explicit split length on a long list
+    n_split = -(-35160 // 640)
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, 640) == \
+        256 + rnd(4 * n_split * 7 * 2 * 4) + rnd(4 * n_split * 7 * 128 * 4)
+    # automatic split of 1100 units over 4 groups: 64 splits of 5 units
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160) == \
+        256 + rnd(4 * 55 * 7 * 2 * 4) + rnd(4 * 55 * 7 * 128 * 4)
+    # the stream schedule: 256 workgroups with two partial slots each
+    stream = 256 + rnd(2 * 256 * 7 * 2 * 4) + rnd(2 * 256 * 7 * 128 * 4)
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, M.MURMUR_SPLIT_STREAM) == stream
+    # forced stream on a tiny problem: as many workgroups as units (4 groups x 2 units)
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 192, M.MURMUR_SPLIT_STREAM) == \
+        256 + rnd(2 * 8 * 7 * 2 * 4) + rnd(2 * 8 * 7 * 128 * 4)
     with pytest.raises(M.MurmurError):
         M.murmur_decode_attn_workspace(1, 12, 28, 5, 850)
     with pytest.raises(M.MurmurError):
         M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 64)
+    with pytest.raises(M.MurmurError) as e:
+        M.murmur_decode_attn_workspace(1, 300, 28, 4, 850, M.MURMUR_SPLIT_STREAM)
+    assert e.value.code == M.MURMUR_EUNSUPPORTED
 
 
 def test_workspace_init_and_device_error_reject_null():

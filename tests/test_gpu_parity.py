@@ -318,3 +318,52 @@ def test_graph_replays_match_eager_and_pipelined_schedule():
     db.pipelined_steps(list(range(4)), reps, stream, side)
     torch.cuda.synchronize()
     assert torch.equal(db.out, eager)
+
+
+@pytest.mark.parametrize("config", ["c1", "c2", "c3", "c4_dense", "c4_evict"])
+def test_stream_schedule(config):
+    """The persistent stream schedule (balanced unit runs across groups, boundary groups merged) against the
+    oracle on every workload."""
+    wl = workload(config)
+    steps = [0, wl.steps - 1]
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps, split_len=M.MURMUR_SPLIT_STREAM)
+    for i, s in enumerate(steps):
+        announce(f"attn {config} stream schedule step {s}")
+        ref, ref_lse = oracle_step(wl, s)
+        y, l = run_gpu(db, i)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+    assert int(db.ws[: db.NL * db.B * db.Hkv].abs().sum().item()) == 0  # tickets reset
+
+
+def test_stream_schedule_many_ragged_sequences():
+    """130 ragged sequences over 2 layers (more than one scan element per lane; many groups cut between
+    workgroups), both schedules, index-list and range modes."""
+    announce("attn stream schedule, 130 ragged sequences")
+    rng = np.random.default_rng(99)
+    B = 130
+    seg0 = np.stack([rng.integers(0, 20, B), rng.integers(0, 700, B), rng.integers(0, 8, B),
+                     rng.integers(0, 300, B)], axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.3, OFF, rng.integers(1, 400, B)), rng.integers(0, 200, B),
+                    rng.integers(0, 8, B), np.where(rng.random(B) < 0.3, OFF, rng.integers(1, 200, B)),
+                    rng.integers(0, 8, B)], axis=1).astype(np.int32)
+    wl = W.build("ragged", 31, 2, seg0, pol, steps=2, planted=False)
+    ref, ref_lse = oracle_step(wl, 1)
+    for split_len, use_ranges in ((M.MURMUR_SPLIT_STREAM, True), (M.MURMUR_SPLIT_STREAM, False), (0, True)):
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[1], split_len=split_len, use_ranges=use_ranges)
+        y, l = run_gpu(db, 0)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL, (split_len, use_ranges)
+
+
+def test_stream_schedule_more_workgroups_than_units():
+    """A max_keep far above the actual counts sizes the stream grid for more units than exist; the surplus
+    workgroups must stand aside (results right on two calls in a row, tickets back at zero)."""
+    wl = workload("c1")
+    steps = [0, wl.steps - 1]
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps, split_len=M.MURMUR_SPLIT_STREAM, max_keep=8192)
+    for i, s in enumerate(steps):
+        announce(f"attn c1 stream schedule, max_keep 8192, step {s}")
+        ref, ref_lse = oracle_step(wl, s)
+        for _ in range(2):
+            y, l = run_gpu(db, i)
+            assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+    assert int(db.ws[: db.NL * db.B * db.Hkv].abs().sum().item()) == 0
