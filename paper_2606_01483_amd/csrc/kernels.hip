@@ -107,16 +107,6 @@ static __device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-// Rank r of the retained list -> global position, from the six-piece table.
-static __device__ __forceinline__ int rank_to_pos(const int32_t (&rg)[2 * kPieces], int r) {
-#pragma unroll
-    for (int k = 0; k < kPieces; ++k) {
-        if (r < rg[2 * k + 1]) return rg[2 * k] + r;
-        r -= rg[2 * k + 1];
-    }
-    return -1;
-}
-
 // LDS tile of one wavefront: V^T for 128 head dims x 32 positions, in 16-byte
 // units (one head dim, eight positions).  Unit (d, q) -- q = position octet --
 // sits at q*128 + swz(d); the XOR swizzle and the half swap for odd d make both
@@ -212,52 +202,145 @@ static __device__ __forceinline__ void wave_acc_reset(WaveAcc &w) {
 }
 
 // Q^T as the MFMA B operand: lane (head n16, k-group c4) holds head dims
-// kc*32 + 8*c4 .. +8 for kc = 0..3.  Rows past the group are zero (their
-// address is clamped into the group so that nothing outside q is touched).
+// kc*32 + 8*c4 .. +8 for kc = 0..3.  Lanes past the group read the group's
+// last head, so every lane loads (no branch around the loads); their logits
+// fill S^T columns of no head of the group, which are never stored.
 static __device__ __forceinline__ void load_q(u32x4 (&qf)[4], const uint16_t *q, int64_t row_of_head0, int G,
                                               int n16, int c4) {
     const int hq = n16 < G ? n16 : G - 1;
-    const uint16_t *qrow = q + (row_of_head0 + hq) * kHeadDim;
+    const uint16_t *qrow = q + (row_of_head0 + hq) * kHeadDim + 8 * c4;
 #pragma unroll
-    for (int kc = 0; kc < 4; ++kc) qf[kc] = n16 < G ? load16(qrow + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
+    for (int kc = 0; kc < 4; ++kc) qf[kc] = load16(qrow + kc * 32);
 }
 
-// Where the ranks of a pass live: the six-piece range table (rg, in
-// registers) or the index list (idx_row).  Returns the position of rank
-// `rank`, -1 if rank >= r_end; sets bad_pos for positions outside the cache.
-static __device__ __forceinline__ int resolve_rank(int rank, int r_end, bool use_ranges, const int32_t (&rg)[2 * kPieces],
-                                                   const int32_t *idx_row, int max_len, int &bad_pos) {
-    if (rank >= r_end) return -1;
-    const int p = use_ranges ? rank_to_pos(rg, rank) : idx_row[rank];
-    if (p >= 0 && p < max_len) return p;
-    bad_pos = 1;
-    return -1;
+// The six-piece range table in cumulative form: rank r belongs to the last
+// piece k with r >= lo[k] (empty pieces are passed over by the next one) and
+// sits at position r + off[k].
+struct RangeTab {
+    int32_t lo[kPieces];
+    int32_t off[kPieces];
+};
+
+static __device__ __forceinline__ RangeTab make_tab(const int32_t (&rg)[2 * kPieces]) {
+    RangeTab t;
+    int32_t acc = 0;
+#pragma unroll
+    for (int k = 0; k < kPieces; ++k) {
+        t.lo[k] = acc;
+        t.off[k] = rg[2 * k] - acc;
+        acc += rg[2 * k + 1];
+    }
+    return t;
 }
 
-// Issues every K and V load of a pass.  mypos: position of rank r0 + (lane & 31)
-// (or -1); positions reach the loading lanes by __shfl.
-static __device__ __forceinline__ void load_pass(PassRegs &R, const uint16_t *kbase, const uint16_t *vbase,
-                                                 int64_t s_pos, int mypos, int n16, int c4) {
+// Position of rank r, and its piece, by a select chain (no branches).
+static __device__ __forceinline__ int tab_pos(const RangeTab &t, int r, int &piece) {
+    int p = r + t.off[0];
+    piece = 0;
+#pragma unroll
+    for (int k = 1; k < kPieces; ++k) {
+        const bool in = r >= t.lo[k];
+        p = in ? r + t.off[k] : p;
+        piece = in ? k : piece;
+    }
+    return p;
+}
+
+// Positions of the rows one lane loads in a pass of 32 ranks from r0: K rows
+// of ranks r0 + 16*blk + n16 (blk = 0, 1) and V rows of ranks r0 + 8*c4 + t
+// (t = 0..7).  Every lane loads, so ranks at or past the count, and positions
+// outside [0, max_len), read row 0 instead: their logits and V rows are masked
+// when the pass is computed.  A retained rank whose position is outside the
+// cache sets `bad` (the K ranks of the 64 lanes cover all 32 ranks).
+struct PassPos {
+    int32_t k[2];
+    int32_t v[8];
+};
+
+static __device__ __forceinline__ int keep_pos(int r, int p, int cnt, int max_len, int &bad) {
+    const bool live = r < cnt;
+    const bool inb = (uint32_t)p < (uint32_t)max_len;
+    bad |= live && !inb;
+    return live && inb ? p : 0;
+}
+
+static __device__ __forceinline__ void pass_pos_ranges(const RangeTab &t, int r0, int cnt, int max_len, int n16,
+                                                       int c4, PassPos &pp, int &bad) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-        const int pos = __shfl(mypos, 16 * blk + n16);
-        const uint16_t *row = kbase + (int64_t)(pos < 0 ? 0 : pos) * s_pos;
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) R.kf[blk][kc] = pos >= 0 ? load16(row + kc * 32 + 8 * c4) : u32x4{0, 0, 0, 0};
+        const int r = r0 + 16 * blk + n16;
+        int pc;
+        pp.k[blk] = keep_pos(r, tab_pos(t, r, pc), cnt, max_len, bad);
     }
+    // The eight V ranks of a lane are consecutive: one piece -> consecutive rows.
+    const int rv = r0 + 8 * c4;
+    int pc0, pc7;
+    const int p0 = tab_pos(t, rv, pc0);
+    const int p7 = tab_pos(t, rv + 7, pc7);
+    if (pc0 == pc7 && rv + 7 < cnt && p0 >= 0 && p7 < max_len) {
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const int pos = __shfl(mypos, 8 * c4 + t);
-        const uint16_t *row = vbase + (int64_t)(pos < 0 ? 0 : pos) * s_pos;
-        R.vf[t] = pos >= 0 ? load16(row + 8 * n16) : u32x4{0, 0, 0, 0};
+        for (int i = 0; i < 8; ++i) pp.v[i] = p0 + i;
+    } else {
+        int unused = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            int pc;
+            pp.v[i] = keep_pos(rv + i, tab_pos(t, rv + i, pc), cnt, max_len, unused);
+        }
     }
 }
+
+// Index-list entries of the same ranks, loaded ahead of the pass that uses
+// them.  The buffer resource spans the row's count, so ranks past it read 0
+// without a memory access (and a resource of 0 bytes reads nothing at all).
+struct IdxRegs {
+    int32_t k[2];
+    int32_t v[8];
+};
+
+static __device__ __forceinline__ void load_idx(IdxRegs &I, __amdgpu_buffer_rsrc_t row, int r0, int n16, int c4) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+        I.k[blk] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(row, (uint32_t)(r0 + 16 * blk + n16) * 4u, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        I.v[i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(row, (uint32_t)(r0 + 8 * c4 + i) * 4u, 0, 0);
+}
+
+static __device__ __forceinline__ void pass_pos_index(const IdxRegs &I, int r0, int cnt, int max_len, int n16,
+                                                      int c4, PassPos &pp, int &bad) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) pp.k[blk] = keep_pos(r0 + 16 * blk + n16, I.k[blk], cnt, max_len, bad);
+    int unused = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pp.v[i] = keep_pos(r0 + 8 * c4 + i, I.v[i], cnt, max_len, unused);
+}
+
+// K and V fragments of one pass, all loads issued unconditionally.  Keeping
+// every load outside control flow lets the compiler's wait counting stay
+// exact across the software pipeline: the wait before a pass's compute
+// covers that pass's loads only, never the loads issued after them.
+static __device__ __forceinline__ void issue_kv(PassRegs &R, const uint16_t *kbase, const uint16_t *vbase,
+                                                int64_t s_pos, const PassPos &pp, int n16, int c4) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+        const uint16_t *row = kbase + (int64_t)pp.k[blk] * s_pos + 8 * c4;
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) R.kf[blk][kc] = load16(row + kc * 32);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) R.vf[i] = load16(vbase + (int64_t)pp.v[i] * s_pos + 8 * n16);
+}
+
+// Keeps the instruction scheduler from moving anything across this point
+// (the consumer of one pass above the loads of the next, in particular).
+static __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // One pass: S^T = K Q^T, softmax update, O += P V.  `valid` = number of valid
 // ranks of the pass (1..32).  kOnline: fold into a running state (rescaling
 // what is there); otherwise the state is known to be empty.
 template <bool kOnline>
-static __device__ __forceinline__ void compute_pass(const PassRegs &R, const u32x4 (&qf)[4], int valid,
+static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&qf)[4], int valid,
                                                     float scale_log2, uint8_t *vt, WaveAcc &w, int n16, int c4) {
     // S^T: lane (head n16, c4), register i of block blk holds the logit of rank
     // r0 + 16*blk + 4*c4 + i.
@@ -317,6 +400,14 @@ static __device__ __forceinline__ void compute_pass(const PassRegs &R, const u32
         const uint32_t hi = pack_bf16(e0, e1);
         p_hi[wd] = hi;
         p_lo[wd] = pack_bf16(e0 - __builtin_bit_cast(float, hi << 16), e1 - __builtin_bit_cast(float, hi & 0xffff0000u));
+    }
+
+    // V rows of masked ranks were read from row 0: zero them so that 0 * V
+    // stays 0 whatever that row holds.
+    if (partial) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+            if (8 * c4 + t >= valid) R.vf[t] = u32x4{0, 0, 0, 0};
     }
 
     // V^T through LDS.  Lane (e = n16, octet c4) holds positions 8*c4 + t
@@ -497,14 +588,15 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
 // decode_attn, split schedule: one workgroup per (split, KV head, sequence,
 // layer).  Each of its four wavefronts takes passes of 32 retained positions,
 // interleaved over the split.  kMultiPass: splits longer than one workgroup
-// pass keep an online softmax across passes and have the next pass's loads in
-// flight while the current one is computed; otherwise every wavefront makes at
-// most one pass.  The last workgroup of each group merges the splits.
-// The leading scalar arguments are the ones the first memory accesses need;
-// the build preloads them into SGPRs so no kernel-argument load precedes the
+// pass keep an online softmax across passes, with the next pass's loads in
+// flight while the current one is computed; otherwise every wavefront makes
+// at most one pass.  kRanges: positions from the range table, else from the
+// index list.  The last workgroup of each group merges the splits.  The
+// leading scalar arguments are the ones the first memory accesses need; the
+// build preloads them into SGPRs so no kernel-argument load precedes the
 // range-table load.
 // ---------------------------------------------------------------------------
-template <bool kMultiPass>
+template <bool kMultiPass, bool kRanges>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ count,
                                                           const int32_t *__restrict__ ranges,
                                                           const int32_t *__restrict__ idx,
@@ -535,42 +627,81 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int r_begin = split * a.split_len;
     const int r_end = min(r_begin + a.split_len, cnt);
 
-    int32_t rg[2 * kPieces];
-    const bool use_ranges = ranges != nullptr;
+    RangeTab tab;
+    __amdgpu_buffer_rsrc_t irow;
+    if (kRanges) {
+        int32_t rg[2 * kPieces];
 #pragma unroll
-    for (int k = 0; k < 2 * kPieces; ++k) rg[k] = use_ranges ? ranges[b * 2 * kPieces + k] : 0;
-    const int32_t *idx_row = idx + (int64_t)b * max_keep;
+        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = ranges[b * 2 * kPieces + k];
+        tab = make_tab(rg);
+    } else {
+        irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
+    }
 
     const int64_t row0 = (int64_t)lb * a.Hq + g * G;  // first output row of the group
     u32x4 qf[4];
     load_q(qf, q, row0, G, n16, c4);
-    const uint16_t *kbase = a.k + layer * a.s_layer + b * a.s_b + g * a.s_h;
-    const uint16_t *vbase = a.v + layer * a.s_layer + b * a.s_b + g * a.s_h;
+    const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
+    const uint16_t *kbase = a.k + kv_off;
+    const uint16_t *vbase = a.v + kv_off;
     uint8_t *vt = smem + wave * kVtBytesPerWave;
 
     WaveAcc w;
     wave_acc_reset(w);
-    {
-        int r0 = r_begin + wave * kWaveTile;
-        PassRegs cur;
-        if (r0 < r_end)
-            load_pass(cur, kbase, vbase, a.s_pos,
-                      resolve_rank(r0 + (lane & 31), r_end, use_ranges, rg, idx_row, a.max_len, w.bad_pos), n16, c4);
-        if (kMultiPass) {
-            for (; r0 < r_end; r0 += kSplitUnit) {
-                PassRegs nxt;
-                const int rn = r0 + kSplitUnit;
-                const bool more = rn < r_end;
-                if (more)
-                    load_pass(nxt, kbase, vbase, a.s_pos,
-                              resolve_rank(rn + (lane & 31), r_end, use_ranges, rg, idx_row, a.max_len, w.bad_pos), n16,
-                              c4);
-                compute_pass<true>(cur, qf, min(kWaveTile, r_end - r0), a.scale_log2, vt, w, n16, c4);
-                if (more) cur = nxt;
-            }
-        } else if (r0 < r_end) {
-            compute_pass<false>(cur, qf, min(kWaveTile, r_end - r0), a.scale_log2, vt, w, n16, c4);
+    int r = r_begin + wave * kWaveTile;
+    auto positions = [&](const IdxRegs &I, int r0, PassPos &pp) {
+        if (kRanges) pass_pos_ranges(tab, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
+        else pass_pos_index(I, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
+    };
+    if (kMultiPass) {
+        // Two register sets, A and B, alternate between the pass being
+        // computed and the pass being loaded; the loop is unrolled twice so
+        // that the roles swap without register copies.
+        PassRegs RA, RB;
+        IdxRegs IA, IB;
+        PassPos pp;
+        if (!kRanges) {
+            load_idx(IA, irow, r, n16, c4);
+            load_idx(IB, irow, r + kSplitUnit, n16, c4);
         }
+        positions(IA, r, pp);
+        issue_kv(RA, kbase, vbase, a.s_pos, pp, n16, c4);
+        for (;;) {
+            // RA: pass r in flight; IB: index entries of pass r + 128.
+            if (r + kSplitUnit < r_end) {
+                if (!kRanges) load_idx(IA, irow, r + 2 * kSplitUnit, n16, c4);
+                positions(IB, r + kSplitUnit, pp);
+                issue_kv(RB, kbase, vbase, a.s_pos, pp, n16, c4);
+                sched_fence();
+                compute_pass<true>(RA, qf, kWaveTile, a.scale_log2, vt, w, n16, c4);
+                sched_fence();
+            } else {
+                if (r < r_end) compute_pass<true>(RA, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
+                break;
+            }
+            r += kSplitUnit;
+            // RB: pass r in flight; IA: index entries of pass r + 128.
+            if (r + kSplitUnit < r_end) {
+                if (!kRanges) load_idx(IB, irow, r + 2 * kSplitUnit, n16, c4);
+                positions(IA, r + kSplitUnit, pp);
+                issue_kv(RA, kbase, vbase, a.s_pos, pp, n16, c4);
+                sched_fence();
+                compute_pass<true>(RB, qf, kWaveTile, a.scale_log2, vt, w, n16, c4);
+                sched_fence();
+            } else {
+                compute_pass<true>(RB, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
+                break;
+            }
+            r += kSplitUnit;
+        }
+    } else if (r < r_end) {
+        PassRegs R;
+        IdxRegs I;
+        PassPos pp;
+        if (!kRanges) load_idx(I, irow, r, n16, c4);
+        positions(I, r, pp);
+        issue_kv(R, kbase, vbase, a.s_pos, pp, n16, c4);
+        compute_pass<false>(R, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
     }
 
     const int wg_bad_pos = __syncthreads_or(w.bad_pos);
@@ -591,15 +722,18 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
 // is the sequence of 128-position units of every (layer, sequence, KV head)
 // group in (layer, sequence, KV head) order; workgroup p takes the contiguous
 // units [p*U/P, (p+1)*U/P) and streams through them with the next unit's
-// loads in flight, across group boundaries.  A group it covers whole is
-// written directly; a group cut by a range boundary leaves a partial in slot
-// 2p (its first segment) or 2p+1 (its last), and the last contributor merges.
-// Per-sequence counts, range tables and unit offsets are staged in LDS.
+// loads (K, V, the query of its group and, for index lists, the entries of
+// the unit after) in flight, across group boundaries.  A group it covers
+// whole is written directly; a group cut by a range boundary leaves a partial
+// in slot 2p (its first segment) or 2p+1 (its last), and the last contributor
+// merges.  Per-sequence counts, range tables and unit offsets are staged in
+// LDS.
 // ---------------------------------------------------------------------------
 struct UnitPos {
     int layer, b, g, k;  // k: unit index within the group
 };
 
+template <bool kRanges>
 __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *__restrict__ count,
                                                                  const int32_t *__restrict__ ranges,
                                                                  const int32_t *__restrict__ idx,
@@ -610,7 +744,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     __shared__ int s_last;
     __shared__ int32_t s_cnt[kStreamMaxB];      // counts clamped to [0, max_keep]
     __shared__ int32_t s_pre[kStreamMaxB + 1];  // Hkv * (units of the sequences before b), b = 0..B
-    __shared__ int32_t s_rg[kStreamMaxB][2 * kPieces];
+    __shared__ int32_t s_rg[kRanges ? kStreamMaxB : 1][2 * kPieces];
     __shared__ uint32_t s_bad[kStreamMaxB / 32];  // sequences with an invalid count
 
     const int tid = threadIdx.x;
@@ -619,7 +753,6 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
     const int Hkv = a.Hkv, G = a.G;
-    const bool use_ranges = ranges != nullptr;
 
     // ---- per-sequence tables -------------------------------------------------
     if (tid < kStreamMaxB / 32) s_bad[tid] = 0;
@@ -631,7 +764,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         s_cnt[t] = cc;
         s_pre[t + 1] = cc > kSplitUnit ? (cc + kSplitUnit - 1) / kSplitUnit : 1;  // units, at least one
         if (badc) atomicOr(&s_bad[t >> 5], 1u << (t & 31));
-        if (use_ranges) {
+        if (kRanges) {
 #pragma unroll
             for (int k = 0; k < 2 * kPieces; ++k) s_rg[t][k] = ranges[t * 2 * kPieces + k];
         }
@@ -705,81 +838,131 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         }
         return x;
     };
-    auto issue_unit = [&](const UnitPos &x, PassRegs &R, int &bad_pos) {
-        const int cnt = s_cnt[x.b];
-        const int r0 = x.k * kSplitUnit + wave * kWaveTile;
-        if (r0 >= cnt) return;
-        int32_t rg[2 * kPieces];
-#pragma unroll
-        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = use_ranges ? s_rg[x.b][k] : 0;
-        const int32_t *idx_row = idx + (int64_t)x.b * max_keep;
-        const int64_t off = x.layer * a.s_layer + x.b * a.s_b + x.g * a.s_h;
-        load_pass(R, a.k + off, a.v + off, a.s_pos,
-                  resolve_rank(r0 + (lane & 31), cnt, use_ranges, rg, idx_row, a.max_len, bad_pos), n16, c4);
-    };
+    auto same_group = [](const UnitPos &x, const UnitPos &y) { return x.layer == y.layer && x.b == y.b && x.g == y.g; };
+    auto first_rank = [&](const UnitPos &x) { return x.k * kSplitUnit + wave * kWaveTile; };
     auto row_of = [&](const UnitPos &x) { return ((int64_t)x.layer * B + x.b) * a.Hq + x.g * G; };
+    // Index-list row of unit x; a unit that does not exist reads nothing.
+    auto irow_of = [&](const UnitPos &x, bool exists) {
+        return raw_buffer(idx + (int64_t)x.b * max_keep, exists ? (uint32_t)s_cnt[x.b] * 4u : 0u);
+    };
+    // Issues every load of unit x: K, V and the query of its group.
+    auto issue = [&](const UnitPos &x, const IdxRegs &I, PassRegs &R, u32x4 (&qx)[4], int &bad) {
+        const int cnt = s_cnt[x.b];
+        PassPos pp;
+        if (kRanges) {
+            int32_t rg[2 * kPieces];
+#pragma unroll
+            for (int k = 0; k < 2 * kPieces; ++k) rg[k] = s_rg[x.b][k];
+            pass_pos_ranges(make_tab(rg), first_rank(x), cnt, a.max_len, n16, c4, pp, bad);
+        } else {
+            pass_pos_index(I, first_rank(x), cnt, a.max_len, n16, c4, pp, bad);
+        }
+        const int64_t off = x.layer * a.s_layer + x.b * a.s_b + x.g * a.s_h;
+        issue_kv(R, a.k + off, a.v + off, a.s_pos, pp, n16, c4);
+        load_q(qx, q, row_of(x), G, n16, c4);
+    };
 
     uint8_t *vt = smem + wave * kVtBytesPerWave;
     float *o_lds = reinterpret_cast<float *>(smem);
     WaveAcc w;
     wave_acc_reset(w);
-    u32x4 qf[4], qn[4];
-    load_q(qf, q, row_of(cur), G, n16, c4);
-    PassRegs R, Rn;
-    issue_unit(cur, R, w.bad_pos);
     int seg_k0 = cur.k;  // first unit of the current segment within its group
 
-    for (; u < u_end; ++u) {
-        const bool has_next = u + 1 < u_end;
-        const UnitPos nxt = advance(cur);
-        const bool next_new_group = !(nxt.layer == cur.layer && nxt.b == cur.b && nxt.g == cur.g);
-        int next_bad = 0;  // invalid positions met while resolving the next unit
-        if (has_next) {
-            issue_unit(nxt, Rn, next_bad);
-            if (next_new_group) load_q(qn, q, row_of(nxt), G, n16, c4);
+    auto compute = [&](const UnitPos &x, PassRegs &R, const u32x4 (&qx)[4]) {
+        const int valid = s_cnt[x.b] - first_rank(x);
+        if (valid > 0) compute_pass<true>(R, qx, min(kWaveTile, valid), a.scale_log2, vt, w, n16, c4);
+    };
+    // The segment of group x in this workgroup ends with unit x.
+    auto seg_end = [&](const UnitPos &x) {
+        const bool bad_count = (s_bad[x.b >> 5] >> (x.b & 31)) & 1u;
+        const int wg_bad_pos = __syncthreads_or(w.bad_pos);
+        const bool bad = wg_bad_pos || bad_count;
+        combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
+        const int ub = units_of(x.b);
+        const bool whole = seg_k0 == 0 && x.k == ub - 1;
+        const int64_t s_g = x.layer * U_layer + s_pre[x.b] + (int64_t)x.g * ub;  // group's first unit
+        const uint32_t slot = (uint32_t)(2 * p + (u_begin < s_g ? 1 : 0));
+        const int64_t row0 = row_of(x);
+        write_result(a, o_lds, cl, G, tid, row0, whole, slot);
+        if (bad && tid == 0)
+            raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
+        if (!whole) {
+            const int64_t first = owner(s_g), last = owner(s_g + ub - 1);
+            const int grp = (int)(((int64_t)x.layer * B + x.b) * Hkv + x.g);
+            if (take_ticket(a, grp, (int)(last - first + 1), tid, s_last)) {
+                merge_partials(
+                    a, (int)(last - first + 1),
+                    [&](int i) {
+                        const int64_t pp = first + i;
+                        return (uint32_t)(2 * pp + ((pp * U / P) < s_g ? 1 : 0));
+                    },
+                    G, tid, row0);
+            }
         }
-        {
-            const int valid = s_cnt[cur.b] - (cur.k * kSplitUnit + wave * kWaveTile);
-            if (valid > 0) compute_pass<true>(R, qf, min(kWaveTile, valid), a.scale_log2, vt, w, n16, c4);
-        }
-        if (!has_next || next_new_group) {
-            // The segment of group `cur` in this workgroup ends here.
-            const bool bad_count = (s_bad[cur.b >> 5] >> (cur.b & 31)) & 1u;
-            const int wg_bad_pos = __syncthreads_or(w.bad_pos);
-            const bool bad = wg_bad_pos || bad_count;
-            combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
-            const int ub = units_of(cur.b);
-            const bool whole = seg_k0 == 0 && cur.k == ub - 1;
-            const int64_t s_g = cur.layer * U_layer + s_pre[cur.b] + (int64_t)cur.g * ub;  // group's first unit
-            const uint32_t slot = (uint32_t)(2 * p + (u_begin < s_g ? 1 : 0));
-            const int64_t row0 = row_of(cur);
-            write_result(a, o_lds, cl, G, tid, row0, whole, slot);
-            if (bad && tid == 0)
-                raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
-            if (!whole) {
-                const int64_t first = owner(s_g), last = owner(s_g + ub - 1);
-                const int grp = (int)(((int64_t)cur.layer * B + cur.b) * Hkv + cur.g);
-                if (take_ticket(a, grp, (int)(last - first + 1), tid, s_last)) {
-                    merge_partials(
-                        a, (int)(last - first + 1),
-                        [&](int i) {
-                            const int64_t pp = first + i;
-                            return (uint32_t)(2 * pp + ((pp * U / P) < s_g ? 1 : 0));
-                        },
-                        G, tid, row0);
+        __syncthreads();  // the next pass reuses the LDS tiles
+        wave_acc_reset(w);
+        seg_k0 = 0;
+    };
+
+    // Two register sets, A and B, alternate between the unit being computed
+    // and the unit being loaded; the loop is unrolled twice so that the roles
+    // swap without register copies.  The last unit of the workgroup takes the
+    // branch without loads.
+    PassRegs RA, RB;
+    u32x4 qA[4], qB[4];
+    IdxRegs IA, IB;
+    int next_bad = 0;  // invalid positions met while resolving the next unit
+    if (!kRanges) {
+        load_idx(IA, irow_of(cur, true), first_rank(cur), n16, c4);
+        const UnitPos n1 = advance(cur);
+        load_idx(IB, irow_of(n1, u + 1 < u_end), first_rank(n1), n16, c4);
+    }
+    issue(cur, IA, RA, qA, w.bad_pos);
+    for (;;) {
+        {   // RA/qA: unit u in flight; IB: index entries of unit u + 1
+            const bool more = u + 1 < u_end;
+            const UnitPos nxt = advance(cur);
+            if (more) {
+                if (!kRanges) {
+                    const UnitPos nn = advance(nxt);
+                    load_idx(IA, irow_of(nn, u + 2 < u_end), first_rank(nn), n16, c4);
                 }
+                issue(nxt, IB, RB, qB, next_bad);
+                sched_fence();
+                compute(cur, RA, qA);
+                sched_fence();
+            } else {
+                compute(cur, RA, qA);
             }
-            __syncthreads();  // the next pass reuses the LDS tiles
-            wave_acc_reset(w);
-            seg_k0 = 0;
-            if (has_next && next_new_group) {
-#pragma unroll
-                for (int kc = 0; kc < 4; ++kc) qf[kc] = qn[kc];
-            }
+            if (!more || !same_group(nxt, cur)) seg_end(cur);
+            w.bad_pos |= next_bad;
+            next_bad = 0;
+            if (!more) break;
+            cur = nxt;
+            ++u;
         }
-        w.bad_pos |= next_bad;
-        cur = nxt;
-        R = Rn;
+        {   // RB/qB: unit u in flight; IA: index entries of unit u + 1
+            const bool more = u + 1 < u_end;
+            const UnitPos nxt = advance(cur);
+            if (more) {
+                if (!kRanges) {
+                    const UnitPos nn = advance(nxt);
+                    load_idx(IB, irow_of(nn, u + 2 < u_end), first_rank(nn), n16, c4);
+                }
+                issue(nxt, IA, RA, qA, next_bad);
+                sched_fence();
+                compute(cur, RB, qB);
+                sched_fence();
+            } else {
+                compute(cur, RB, qB);
+            }
+            if (!more || !same_group(nxt, cur)) seg_end(cur);
+            w.bad_pos |= next_bad;
+            next_bad = 0;
+            if (!more) break;
+            cur = nxt;
+            ++u;
+        }
     }
 }
 
@@ -798,20 +981,28 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
     return (int)hipGetLastError();
 }
 
-int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
+template <bool kRanges>
+static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.stream_wg > 0) {
-        hipLaunchKernelGGL(decode_attn_stream_kernel, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
-                           (hipStream_t)stream, a.count, a.ranges, a.idx, a.q, a.max_keep, a.B, a);
-        return (int)hipGetLastError();
+        hipLaunchKernelGGL(decode_attn_stream_kernel<kRanges>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
+                           stream, a.count, a.ranges, a.idx, a.q, a.max_keep, a.B, a);
+        return;
     }
     const dim3 grid((unsigned)a.n_split, (unsigned)a.Hkv, (unsigned)(a.NL * a.B));
-    // Splits of more than one pass per wavefront double-buffer their loads.
+    // Splits of more than one pass per wavefront pipeline their loads.
     if (a.split_len > kSplitUnit)
-        hipLaunchKernelGGL(decode_attn_kernel<true>, grid, dim3(kWavesPerWg * 64), 0, (hipStream_t)stream, a.count,
+        hipLaunchKernelGGL((decode_attn_kernel<true, kRanges>), grid, dim3(kWavesPerWg * 64), 0, stream, a.count,
                            a.ranges, a.idx, a.q, a.max_keep, a.B, a);
     else
-        hipLaunchKernelGGL(decode_attn_kernel<false>, grid, dim3(kWavesPerWg * 64), 0, (hipStream_t)stream, a.count,
+        hipLaunchKernelGGL((decode_attn_kernel<false, kRanges>), grid, dim3(kWavesPerWg * 64), 0, stream, a.count,
                            a.ranges, a.idx, a.q, a.max_keep, a.B, a);
+}
+
+int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
+    if (a.ranges)
+        launch_decode_attn_mode<true>(a, (hipStream_t)stream);
+    else
+        launch_decode_attn_mode<false>(a, (hipStream_t)stream);
     return (int)hipGetLastError();
 }
 
