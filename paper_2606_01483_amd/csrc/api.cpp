@@ -57,14 +57,22 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
         return p;
     }
     if (split_len <= 0) {
-        // Enough workgroups to cover the chip about twice (kTargetWorkgroups),
-        // otherwise as few splits as possible: every split adds a partial that
-        // the merge has to read back.  At most kMaxAutoSplits splits.
-        int64_t want = (kTargetWorkgroups + groups - 1) / groups;
-        if (want > kMaxAutoSplits) want = kMaxAutoSplits;
-        if (want > units) want = units;
-        if (want < 1) want = 1;
-        const int64_t per = (units + want - 1) / want;
+        // Few units: one pass per wavefront (the light single-pass kernel, which
+        // several workgroups share a compute unit with).  Otherwise the
+        // LDS-staged kernel, which takes a whole compute unit: as many splits
+        // as keep one dispatch round (kRoundWorkgroups), fewer when there are
+        // more groups than that, at most kMaxAutoSplits.
+        int64_t per;
+        if (groups * units <= kSinglePassMaxUnits) {
+            per = 1;
+        } else {
+            int64_t want = kRoundWorkgroups / groups;
+            if (want > kMaxAutoSplits) want = kMaxAutoSplits;
+            if (want > units) want = units;
+            if (want < 1) want = 1;
+            per = (units + want - 1) / want;
+            if (per < 2) per = 2;
+        }
         split_len = (int32_t)(per * kSplitUnit);
     }
     p.split_len = split_len;
@@ -171,6 +179,9 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     if (B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1 || kv->n_layers < 1 || kv->max_len < 1)
         return fail(MURMUR_EINVAL, "B, Hq, Hkv, max_keep, kv->n_layers and kv->max_len must be >= 1");
     if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+    if (max_keep > kMaxKeep)
+        return fail(MURMUR_EUNSUPPORTED, "max_keep %d exceeds %d (index-list offsets are 32-bit byte offsets)",
+                    max_keep, kMaxKeep);
     if (D != kHeadDim) return fail(MURMUR_EUNSUPPORTED, "head_dim %d is not supported (only %d)", D, kHeadDim);
     if (Hq / Hkv > kMaxGroup)
         return fail(MURMUR_EUNSUPPORTED, "query heads per KV head %d exceeds %d", Hq / Hkv, kMaxGroup);

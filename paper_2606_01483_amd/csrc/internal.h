@@ -15,7 +15,8 @@ constexpr int kWaveTile = 32;     // retained positions one wavefront handles pe
 constexpr int kWavesPerWg = 4;
 constexpr int kSplitUnit = kWaveTile * kWavesPerWg;  // 128 positions: one pass of a workgroup
 constexpr int kMaxAutoSplits = 64;
-constexpr int kTargetWorkgroups = 512;  // about two workgroups per compute unit of the 256
+constexpr int kRoundWorkgroups = 256;     // one workgroup per compute unit
+constexpr int kSinglePassMaxUnits = 512;  // below this many units the automatic split is one pass
 // Stream schedule: one persistent workgroup per compute unit of the 256,
 // chosen automatically once there are at least kStreamMinUnits units of 128
 // positions; sequences' tables live in LDS, so at most kStreamMaxB sequences.
@@ -24,6 +25,7 @@ constexpr int kStreamMaxB = 256;
 // Splits one merge can combine: it stages 2 * n_split * G + 2 * G floats in
 // the workgroup's 32 KiB of V-tile LDS.
 constexpr int kMaxMergeSplits = 240;
+constexpr int kMaxKeep = 1 << 28;  // retained positions per sequence the attention accepts
 constexpr int kMergeBatch = 8;  // splits whose partials one merging thread loads at once
 
 // Launch description of one decode_attn call, fully validated by the caller.

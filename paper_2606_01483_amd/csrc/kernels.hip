@@ -336,21 +336,16 @@ static __device__ __forceinline__ void issue_kv(PassRegs &R, const uint16_t *kba
 // (the consumer of one pass above the loads of the next, in particular).
 static __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
-// One pass: S^T = K Q^T, softmax update, O += P V.  `valid` = number of valid
-// ranks of the pass (1..32).  kOnline: fold into a running state (rescaling
-// what is there); otherwise the state is known to be empty.
+// Softmax update of one pass from its S^T tile (lane (head n16, c4), register
+// i of block blk: logit of rank 16*blk + 4*c4 + i of the pass): masks ranks
+// at or past `valid`, folds the pass into the running (max, sum) and rescales
+// O, and returns P as the A operand of O = P V in k order (4*c4 + 0..3,
+// 16 + 4*c4 + 0..3), split into bf16 hi + lo so that hi + lo carries ~16
+// mantissa bits.  kOnline: fold into a running state; otherwise the state is
+// known to be empty.
 template <bool kOnline>
-static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&qf)[4], int valid,
-                                                    float scale_log2, uint8_t *vt, WaveAcc &w, int n16, int c4) {
-    // S^T: lane (head n16, c4), register i of block blk holds the logit of rank
-    // r0 + 16*blk + 4*c4 + i.
-    f32x4 s[2];
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(R.kf[blk][kc], qf[kc], s[blk]);
-    }
+static __device__ __forceinline__ void softmax_step(const f32x4 (&s)[2], int valid, float scale_log2, WaveAcc &w,
+                                                    int c4, u32x4 &p_hi, u32x4 &p_lo) {
     // Logits in log2 units; ranks past `valid` are masked (a partial pass).
     float x[2][4];
     const bool partial = valid < kWaveTile;
@@ -389,10 +384,6 @@ static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&q
         w.l_run = psum;
     }
     w.m_run = m_new;
-
-    // P as the A operand of O = P V, k order (4*c4 + 0..3, 16 + 4*c4 + 0..3),
-    // split into bf16 hi + lo so that hi + lo carries ~16 mantissa bits.
-    u32x4 p_hi, p_lo;
 #pragma unroll
     for (int wd = 0; wd < 4; ++wd) {
         const int blk = wd >> 1, i0 = (wd & 1) * 2;
@@ -401,6 +392,23 @@ static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&q
         p_hi[wd] = hi;
         p_lo[wd] = pack_bf16(e0 - __builtin_bit_cast(float, hi << 16), e1 - __builtin_bit_cast(float, hi & 0xffff0000u));
     }
+}
+
+// One pass from registers: S^T = K Q^T, softmax update, O += P V.  `valid` =
+// number of valid ranks of the pass (1..32).
+template <bool kOnline>
+static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&qf)[4], int valid,
+                                                    float scale_log2, uint8_t *vt, WaveAcc &w, int n16, int c4) {
+    f32x4 s[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+        s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(R.kf[blk][kc], qf[kc], s[blk]);
+    }
+    const bool partial = valid < kWaveTile;
+    u32x4 p_hi, p_lo;
+    softmax_step<kOnline>(s, valid, scale_log2, w, c4, p_hi, p_lo);
 
     // V rows of masked ranks were read from row 0: zero them so that 0 * V
     // stays 0 whatever that row holds.
@@ -442,6 +450,198 @@ static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&q
     }
     // The next pass overwrites this wave's tile only after these reads have
     // returned (their results feed the MFMAs above).
+}
+
+// ---------------------------------------------------------------------------
+// LDS-staged passes.  K and V rows go from HBM straight into LDS with gfx950's
+// direct-to-LDS loads (no registers hold data in flight, so a wavefront can
+// keep a whole pass loading while it computes the previous one), the MFMA K
+// operands come back with ds_read_b128 and the V operands with the
+// transposing ds_read_b64_tr_b16, which needs no VALU transpose.
+//
+// Tile of one pass (K or V): 32 rows of 256 bytes; 16-byte chunk c of row r
+// sits at slot c ^ (r & 15), which keeps both operand reads bank-conflict
+// free.  A direct-to-LDS load writes lane l's 16 bytes at base + 16*l, so load
+// j (0..7) fills rows 4j .. 4j+3 and lane l fetches chunk (l & 15) ^ (row & 15)
+// of row 4j + (l >> 4).
+//
+// The LDS reads run in inline assembly that ends with its own lgkmcnt wait
+// (outputs early-clobber: a read's result may land before a later read of the
+// same block has taken its address):
+// the compiler's wait insertion assumes any LDS read may depend on every
+// direct-to-LDS load in flight and would drain the pipeline; the waits for
+// the loads are placed by hand instead (wait_vm), counting only loads issued
+// by this wavefront after the ones awaited, so a wait can be longer than
+// needed but never shorter.
+// ---------------------------------------------------------------------------
+constexpr int kTileRowBytes = kHeadDim * 2;            // 256
+constexpr int kTileBytes = kWaveTile * kTileRowBytes;  // 8 KiB
+constexpr int kStageBytes = 2 * kTileBytes;            // K tile, then V tile
+constexpr int kIdxSlotBytes = 256;                     // index entries of one pass (32 of 64 words used)
+constexpr int kStageLoads = 16;                        // direct-to-LDS loads of one pass (dma_pass)
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+static __device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+}
+
+template <int N>
+static __device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// The 16 direct-to-LDS loads of one pass (8 for K, then 8 for V) into `stage`.
+// pos[j]: in-bounds position of the row whose rank is r0 + 4j + (lane >> 4).
+static __device__ __forceinline__ void dma_pass(uint8_t *stage, const uint16_t *kbase, const uint16_t *vbase,
+                                                int64_t s_pos, const int32_t (&pos)[8], int lane) {
+    const int q = lane >> 4, sl = lane & 15;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int c = sl ^ ((4 * j + q) & 15);
+        __builtin_amdgcn_global_load_lds(kbase + (int64_t)pos[j] * s_pos + 8 * c, (lds_void_t *)(stage + j * 1024),
+                                         16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int c = sl ^ ((4 * j + q) & 15);
+        __builtin_amdgcn_global_load_lds(vbase + (int64_t)pos[j] * s_pos + 8 * c,
+                                         (lds_void_t *)(stage + kTileBytes + j * 1024), 16, 0, 0);
+    }
+}
+
+// Positions for dma_pass from the range table.  Ranks at or past r_end read
+// the row of rank r0 (their logits are masked and their weights are exactly
+// zero); a retained rank outside [0, max_len) sets `bad` and reads a clamped
+// row.  When the pass lies in one piece (the common case; the test is uniform
+// over the wavefront) the rows are consecutive.
+static __device__ __forceinline__ void dma_pos_ranges(const RangeTab &t, int r0, int r_end, int max_len, int q,
+                                                      int32_t (&pos)[8], int &bad) {
+    const int valid = min(kWaveTile, r_end - r0);
+    int pc0, pcl;
+    const int p0 = tab_pos(t, r0, pc0);
+    const int pl = tab_pos(t, r0 + valid - 1, pcl);
+    const bool p0ok = (uint32_t)p0 < (uint32_t)max_len;
+    if (pc0 == pcl && p0ok && pl < max_len) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int d = 4 * j + q;
+            pos[j] = p0 + (d < valid ? d : 0);
+        }
+    } else {
+        const int fb = p0ok ? p0 : 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int r = r0 + 4 * j + q;
+            int pc;
+            const int p = tab_pos(t, r, pc);
+            const bool live = r < r_end, inb = (uint32_t)p < (uint32_t)max_len;
+            bad |= live && !inb;
+            pos[j] = live && inb ? p : fb;
+        }
+    }
+}
+
+// Index entries of one pass into an LDS slot with one direct-to-LDS load:
+// word 8q + j holds the entry of rank r0 + 4j + q (q = 0..3, j = 0..7), so a
+// lane reads its eight entries as two 16-byte words.  The buffer resource
+// spans the row's count; lanes past it (and lanes 32..63) read zeros.
+static __device__ __forceinline__ void dma_idx(uint8_t *slot, __amdgpu_buffer_rsrc_t irow, int r0, int lane) {
+    const uint32_t voff = lane < 32 ? (uint32_t)(r0 + (lane & 7) * 4 + (lane >> 3)) * 4u : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(irow, (lds_void_t *)slot, 4, voff, 0, 0, 0);
+}
+
+static __device__ __forceinline__ void dma_pos_index(const uint8_t *slot, int r0, int r_end, int max_len, int q,
+                                                     int32_t (&pos)[8], int &bad) {
+    u32x4 e0, e1;
+    uint32_t w0;
+    asm volatile("ds_read_b128 %0, %3\n\tds_read_b128 %1, %3 offset:16\n\tds_read_b32 %2, %4\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(e0), "=&v"(e1), "=&v"(w0)
+                 : "v"(lds_addr(slot) + 32u * q), "v"(lds_addr(slot))
+                 : "memory");
+    const int p0 = (int)w0;  // entry of rank r0
+    const int fb = (uint32_t)p0 < (uint32_t)max_len ? p0 : 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int r = r0 + 4 * j + q;
+        const int p = (int)(j < 4 ? e0[j] : e1[j - 4]);
+        const bool live = r < r_end, inb = (uint32_t)p < (uint32_t)max_len;
+        bad |= live && !inb;
+        pos[j] = live && inb ? p : fb;
+    }
+}
+
+// One pass from an LDS stage: operand reads, S^T = K Q^T, softmax update,
+// O += P V.
+template <bool kOnline>
+static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, const u32x4 (&qf)[4], int valid,
+                                                        float scale_log2, WaveAcc &w, int n16, int c4) {
+    const uint32_t kt = lds_addr(stage), vt = kt + kTileBytes;
+    // K operand (blk, kc): row 16*blk + n16, chunk 4*kc + c4 (row & 15 == n16);
+    // blk 1 is 16 rows (4096 bytes) further.
+    uint32_t ka[4];
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) ka[kc] = kt + n16 * kTileRowBytes + (((4 * kc + c4) ^ n16) << 4);
+    // V operand (db, h) of lane (i = n16, c4): row 16*h + 4*c4 + i/4, head dims
+    // 16*db + 4*(i%4) .. +3, i.e. chunk 2*db + (i%4)/2, half i & 1; the row's
+    // low four bits are 4*c4 + i/4 for both h (h = 1 is 4096 bytes further).
+    const int vr = 4 * c4 + (n16 >> 2);
+    uint32_t va[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+        va[db] = vt + vr * kTileRowBytes + (((2 * db + ((n16 & 3) >> 1)) ^ vr) << 4) + (n16 & 1) * 8;
+    u32x4 kf[8];
+    u32x2 vf[16];
+    asm volatile(
+        "ds_read_b128 %0, %24\n\t"
+        "ds_read_b128 %1, %25\n\t"
+        "ds_read_b128 %2, %26\n\t"
+        "ds_read_b128 %3, %27\n\t"
+        "ds_read_b128 %4, %24 offset:4096\n\t"
+        "ds_read_b128 %5, %25 offset:4096\n\t"
+        "ds_read_b128 %6, %26 offset:4096\n\t"
+        "ds_read_b128 %7, %27 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %8, %28\n\t"
+        "ds_read_b64_tr_b16 %9, %28 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %10, %29\n\t"
+        "ds_read_b64_tr_b16 %11, %29 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %12, %30\n\t"
+        "ds_read_b64_tr_b16 %13, %30 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %14, %31\n\t"
+        "ds_read_b64_tr_b16 %15, %31 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %16, %32\n\t"
+        "ds_read_b64_tr_b16 %17, %32 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %18, %33\n\t"
+        "ds_read_b64_tr_b16 %19, %33 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %20, %34\n\t"
+        "ds_read_b64_tr_b16 %21, %34 offset:4096\n\t"
+        "ds_read_b64_tr_b16 %22, %35\n\t"
+        "ds_read_b64_tr_b16 %23, %35 offset:4096\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(kf[0]), "=&v"(kf[1]), "=&v"(kf[2]), "=&v"(kf[3]), "=&v"(kf[4]), "=&v"(kf[5]), "=&v"(kf[6]), "=&v"(kf[7]),
+          "=&v"(vf[0]), "=&v"(vf[1]), "=&v"(vf[2]), "=&v"(vf[3]), "=&v"(vf[4]), "=&v"(vf[5]), "=&v"(vf[6]), "=&v"(vf[7]),
+          "=&v"(vf[8]), "=&v"(vf[9]), "=&v"(vf[10]), "=&v"(vf[11]), "=&v"(vf[12]), "=&v"(vf[13]), "=&v"(vf[14]),
+          "=&v"(vf[15])
+        : "v"(ka[0]), "v"(ka[1]), "v"(ka[2]), "v"(ka[3]), "v"(va[0]), "v"(va[1]), "v"(va[2]), "v"(va[3]), "v"(va[4]),
+          "v"(va[5]), "v"(va[6]), "v"(va[7])
+        : "memory");
+    f32x4 s[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+        s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(kf[4 * blk + kc], qf[kc], s[blk]);
+    }
+    u32x4 p_hi, p_lo;
+    softmax_step<kOnline>(s, valid, scale_log2, w, c4, p_hi, p_lo);
+    // B operand of head dims 16*db .. +15: positions 4*c4 .. +3 (h = 0) and
+    // 16 + 4*c4 .. +3 (h = 1), the k order of P.
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+        const u32x4 bv = u32x4{vf[2 * db][0], vf[2 * db][1], vf[2 * db + 1][0], vf[2 * db + 1][1]};
+        w.acc[db] = mfma16x16x32(p_hi, bv, w.acc[db]);
+        w.acc[db] = mfma16x16x32(p_lo, bv, w.acc[db]);
+    }
 }
 
 // LDS shared by the combine step of both schedules.
@@ -707,6 +907,115 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int wg_bad_pos = __syncthreads_or(w.bad_pos);
     const bool bad = wg_bad_pos || bad_count;
     float *o_lds = reinterpret_cast<float *>(smem);  // [wave][16][128], reuses the V tiles
+    combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
+    write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
+    if (bad && tid == 0)
+        raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
+    if (a.n_split == 1) return;
+    if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
+    const uint32_t pbase = (uint32_t)grp * a.n_split;
+    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0);
+}
+
+// ---------------------------------------------------------------------------
+// decode_attn, split schedule with LDS-staged passes, for splits of more than
+// one workgroup pass: grid and split layout as decode_attn_kernel; each
+// wavefront double-buffers its passes in two LDS stages (K and V, 16 KiB per
+// stage), issuing the next pass's direct-to-LDS loads before computing the
+// current one.  Index lists are staged too, one pass ahead of the rows.
+// ---------------------------------------------------------------------------
+template <bool kRanges>
+__global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__restrict__ count,
+                                                              const int32_t *__restrict__ ranges,
+                                                              const int32_t *__restrict__ idx,
+                                                              const uint16_t *__restrict__ q, int32_t max_keep,
+                                                              int32_t B, const AttnLaunch a) {
+    __shared__ __attribute__((aligned(16))) uint8_t stages[kWavesPerWg][2][kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kRanges ? 1 : kWavesPerWg][2][kIdxSlotBytes];
+    __shared__ CombineLds cl;
+    __shared__ int s_last;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int n16 = lane & 15;
+    const int c4 = lane >> 4;
+
+    const int split = blockIdx.x;
+    const int g = blockIdx.y;
+    const int lb = blockIdx.z;
+    const int b = lb % B;
+    const int layer = lb / B;
+    const int grp = lb * a.Hkv + g;
+    const int G = a.G;
+
+    int cnt = count[b];
+    const bool bad_count = cnt < 1 || cnt > max_keep;
+    if (bad_count) cnt = cnt < 0 ? 0 : (cnt > max_keep ? max_keep : cnt);
+    const int r_begin = split * a.split_len;
+    const int r_end = min(r_begin + a.split_len, cnt);
+
+    RangeTab tab;
+    __amdgpu_buffer_rsrc_t irow;
+    if (kRanges) {
+        int32_t rg[2 * kPieces];
+#pragma unroll
+        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = ranges[b * 2 * kPieces + k];
+        tab = make_tab(rg);
+    } else {
+        irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
+    }
+
+    const int64_t row0 = (int64_t)lb * a.Hq + g * G;
+    u32x4 qf[4];
+    load_q(qf, q, row0, G, n16, c4);
+    const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
+    const uint16_t *kbase = a.k + kv_off;
+    const uint16_t *vbase = a.v + kv_off;
+    uint8_t *st[2] = {&stages[wave][0][0], &stages[wave][1][0]};
+    uint8_t *ring[2] = {&idx_ring[kRanges ? 0 : wave][0][0], &idx_ring[kRanges ? 0 : wave][1][0]};
+
+    WaveAcc w;
+    wave_acc_reset(w);
+    int r = r_begin + wave * kWaveTile;
+    if (r < r_end) {
+        int32_t pos[8];
+        if (kRanges) {
+            dma_pos_ranges(tab, r, r_end, a.max_len, c4, pos, w.bad_pos);
+        } else {
+            dma_idx(ring[0], irow, r, lane);
+            dma_idx(ring[1], irow, r + kSplitUnit, lane);
+            wait_vm<1>();
+            dma_pos_index(ring[0], r, r_end, a.max_len, c4, pos, w.bad_pos);
+        }
+        dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane);
+        for (int k = 0;; r += kSplitUnit, ++k) {
+            const uint8_t *cur = st[k & 1];
+            if (r + kSplitUnit < r_end) {
+                if (kRanges) {
+                    dma_pos_ranges(tab, r + kSplitUnit, r_end, a.max_len, c4, pos, w.bad_pos);
+                } else {
+                    wait_vm<kStageLoads>();  // entries of the next pass (issued before this pass's rows)
+                    dma_pos_index(ring[(k + 1) & 1], r + kSplitUnit, r_end, a.max_len, c4, pos, w.bad_pos);
+                    dma_idx(ring[k & 1], irow, r + 2 * kSplitUnit, lane);
+                }
+                dma_pass(st[(k + 1) & 1], kbase, vbase, a.s_pos, pos, lane);
+                if (kRanges)
+                    wait_vm<kStageLoads>();  // this pass's rows; the next pass's stay in flight
+                else
+                    wait_vm<kStageLoads + 1>();
+                compute_pass_lds<true>(cur, qf, kWaveTile, a.scale_log2, w, n16, c4);
+            } else {
+                wait_vm<0>();
+                compute_pass_lds<true>(cur, qf, min(kWaveTile, r_end - r), a.scale_log2, w, n16, c4);
+                break;
+            }
+        }
+    }
+
+    const int wg_bad_pos = __syncthreads_or(w.bad_pos);
+    const bool bad = wg_bad_pos || bad_count;
+    float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // [wave][16][128], reuses the stages
     combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
     write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
     if (bad && tid == 0)
@@ -991,7 +1300,7 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     const dim3 grid((unsigned)a.n_split, (unsigned)a.Hkv, (unsigned)(a.NL * a.B));
     // Splits of more than one pass per wavefront pipeline their loads.
     if (a.split_len > kSplitUnit)
-        hipLaunchKernelGGL((decode_attn_kernel<true, kRanges>), grid, dim3(kWavesPerWg * 64), 0, stream, a.count,
+        hipLaunchKernelGGL(decode_attn_lds_kernel<kRanges>, grid, dim3(kWavesPerWg * 64), 0, stream, a.count,
                            a.ranges, a.idx, a.q, a.max_keep, a.B, a);
     else
         hipLaunchKernelGGL((decode_attn_kernel<false, kRanges>), grid, dim3(kWavesPerWg * 64), 0, stream, a.count,

@@ -112,6 +112,7 @@ def call_attn(a):
     (dict(split_len=100), M.MURMUR_EINVAL),
     (dict(split_len=-128), M.MURMUR_EINVAL),
     (dict(split_len=-2), M.MURMUR_EINVAL),
+    (dict(max_keep=(1 << 28) + 1), M.MURMUR_EUNSUPPORTED),
     (dict(split_len=M.MURMUR_SPLIT_STREAM, B=300), M.MURMUR_EUNSUPPORTED),
     (dict(q=FAKE + 8), M.MURMUR_EINVAL),
     (dict(ws=FAKE + 64), M.MURMUR_EINVAL),
