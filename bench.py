@@ -1,10 +1,12 @@
 #!/usr/bin/env python3
 """Decode-attention benchmark on one MI355X: µs per decode step and achieved HBM GB/s.
 
-One step is the whole hot path on one batch: murmur_evict_compact (retained
-lists from the eviction policy) then murmur_decode_attn (split-K GQA attention
-over the retained K/V with the log-sum-exp merge), on synthetic inputs already
-resident in HBM.  Default workload: 12 chunks of 300 s (2250 speech tokens, 32
+One step is the whole hot path on one batch: the retained sets from the
+eviction policy, then split-K GQA attention over the retained K/V with the
+log-sum-exp merge, on synthetic inputs already resident in HBM.  The step's
+value times the single-launch murmur_decode_step (retained-set outputs
+written); murmur_evict_compact followed by murmur_decode_attn is timed beside
+it (step_two_launches_us).  Default workload: 12 chunks of 300 s (2250 speech tokens, 32
 prompt tokens, 600-1200 output tokens), speech window 562 with delay 512,
 output window 256, 1 layer, GQA 28/4, head_dim 128, bf16.
 
@@ -140,6 +142,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
 
     for i in range(warmup):
         db.step(i % n_steps, i % replicas)
+        db.step_fused(i % n_steps, i % replicas)
     torch.cuda.synchronize()
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during warm-up")
@@ -176,10 +179,16 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) * 1e3
 
-    # Whole steps (evict_compact then decode_attn on one stream), captured once into a graph and replayed.
-    log("timing the steps as a replayed HIP graph")
+    # Whole steps, captured once into a graph and replayed: the single-launch murmur_decode_step (the
+    # step's value, retained-set outputs written), and murmur_evict_compact + murmur_decode_attn.
+    log("timing the fused steps as a replayed HIP graph")
+    fused_graph = capture(lambda: [db.step_fused(order[i], rep[i]) for i in range(steps)])
+    step_us = time_graph(fused_graph) / steps
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during the timed fused steps")
+    log("timing the two-launch steps as a replayed HIP graph")
     step_graph = capture(lambda: [db.step(order[i], rep[i]) for i in range(steps)])
-    step_us = time_graph(step_graph) / steps
+    two_launch_us = time_graph(step_graph) / steps
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during the timed steps")
 
@@ -213,13 +222,14 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
                    "retained_per_step": int(np.mean([int(counts[o].sum()) for o in order])),
                    "kv_replicas": replicas, "selection": "ranges" if use_ranges else "index list",
                    "split_len": db.split_len or "auto"},
+        "step_two_launches_us": round(two_launch_us, 3),
         "decode_attn_us": round(attn_us, 3),
         "decode_attn_event_bracket_us": {"mean": round(float(bracket_us.mean()), 3),
                                          "median": round(float(np.median(bracket_us)), 3),
                                          "p90": round(float(np.percentile(bracket_us, 90)), 3)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": committed_traffic(config),
-                     "kernel": "decode_attn_kernel", "alg_bytes_per_launch": int(alg_bytes)},
+                     "kernel": "decode_attn", "alg_bytes_per_launch": int(alg_bytes)},
     }
     if cpu:
         threads = max(1, min(16, len(os.sched_getaffinity(0))))

@@ -117,7 +117,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 1
+#define MURMUR_ABI_VERSION 2
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -199,6 +199,26 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  * MURMUR_DEVERR_POSITION and MURMUR_DEVERR_COUNT. */
 int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *idx_dev, const int32_t *ranges_dev,
                        const int32_t *count_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                       float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                       void *ws_dev, size_t ws_bytes, murmur_stream_t stream);
+
+/* One whole decode step in one launch: the retained set of every sequence
+ * (Section 3.2: Algorithms 1-2 and Equation 2, as murmur_evict_compact) and
+ * the attention over it (Equation 1, as murmur_decode_attn).  Each attention
+ * workgroup derives its sequence's six pieces from seg_dev/pol_dev in closed
+ * form, so nothing waits for a separate eviction launch; the results are
+ * those of murmur_evict_compact followed by murmur_decode_attn with the range
+ * table, bit for bit in the retained sets.
+ *   seg_dev, pol_dev, pol_per_seq: as murmur_evict_compact;
+ *   idx_dev, count_dev, ranges_dev: nullable outputs, written as
+ *               murmur_evict_compact writes them (idx_dev [B][max_keep]);
+ *   every other argument: as murmur_decode_attn (same workspace size).
+ * Device errors: MURMUR_DEVERR_POLICY and MURMUR_DEVERR_OVERFLOW as
+ * murmur_evict_compact, MURMUR_DEVERR_COUNT for the same sequences (their
+ * outputs are NaN), MURMUR_DEVERR_POSITION as murmur_decode_attn. */
+int murmur_decode_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                       const void *q_dev, const murmur_kv *kv, int32_t *idx_dev, int32_t *count_dev,
+                       int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
                        float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
                        void *ws_dev, size_t ws_bytes, murmur_stream_t stream);
 

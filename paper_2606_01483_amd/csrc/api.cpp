@@ -12,6 +12,9 @@
 
 #define MURMUR_EXPORT extern "C" __attribute__((visibility("default")))
 
+static_assert(sizeof(murmur_seg) == 4 * sizeof(int32_t), "the kernels read murmur_seg as four int32");
+static_assert(sizeof(murmur_policy) == 5 * sizeof(int32_t), "the kernels read murmur_policy as five int32");
+
 namespace murmur {
 namespace {
 
@@ -110,6 +113,97 @@ int check_host_policy(const murmur_seg *seg, const murmur_policy *pol, int32_t p
 }  // namespace
 }  // namespace murmur
 
+namespace murmur {
+namespace {
+
+// Validation and launch description shared by murmur_decode_attn and
+// murmur_decode_step (everything but where the retained sets come from).
+int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv,
+                 int32_t D, float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                 void *ws_dev, size_t ws_bytes, AttnLaunch &a) {
+    if (!q_dev || !kv || !out_dev || !ws_dev)
+        return fail(MURMUR_EINVAL, "q_dev, kv, out_dev and ws_dev must not be NULL");
+    if (!kv->k || !kv->v) return fail(MURMUR_EINVAL, "kv->k and kv->v must not be NULL");
+    if (B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1 || kv->n_layers < 1 || kv->max_len < 1)
+        return fail(MURMUR_EINVAL, "B, Hq, Hkv, max_keep, kv->n_layers and kv->max_len must be >= 1");
+    if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+    if (max_keep > kMaxKeep)
+        return fail(MURMUR_EUNSUPPORTED, "max_keep %d exceeds %d (index-list offsets are 32-bit byte offsets)",
+                    max_keep, kMaxKeep);
+    if (D != kHeadDim) return fail(MURMUR_EUNSUPPORTED, "head_dim %d is not supported (only %d)", D, kHeadDim);
+    if (Hq / Hkv > kMaxGroup)
+        return fail(MURMUR_EUNSUPPORTED, "query heads per KV head %d exceeds %d", Hq / Hkv, kMaxGroup);
+    if (out_dtype != MURMUR_DTYPE_BF16 && out_dtype != MURMUR_DTYPE_F32)
+        return fail(MURMUR_EINVAL, "out_dtype must be MURMUR_DTYPE_BF16 or MURMUR_DTYPE_F32 (got %d)", out_dtype);
+    if (!isfinite(scale)) return fail(MURMUR_EINVAL, "scale must be finite");
+    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kSplitUnit != 0))
+        return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
+                    kSplitUnit, split_len);
+    if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
+        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
+    const int64_t strides[4] = {kv->stride_layer, kv->stride_b, kv->stride_h, kv->stride_pos};
+    for (int i = 0; i < 4; ++i)
+        if (strides[i] < 0 || strides[i] % 8 != 0)
+            return fail(MURMUR_EINVAL, "KV strides must be non-negative multiples of 8 elements");
+    if (kv->stride_pos < kHeadDim && kv->max_len > 1)
+        return fail(MURMUR_EINVAL, "kv->stride_pos (%lld) must be >= head_dim", (long long)kv->stride_pos);
+    if (!aligned(q_dev, 16) || !aligned(kv->k, 16) || !aligned(kv->v, 16))
+        return fail(MURMUR_EINVAL, "q_dev, kv->k and kv->v must be 16-byte aligned");
+    if (!aligned(out_dev, 16) || !aligned(lse_dev, 4))
+        return fail(MURMUR_EINVAL, "out_dev must be 16-byte and lse_dev 4-byte aligned");
+    if (!aligned(ws_dev, 256)) return fail(MURMUR_EINVAL, "ws_dev must be 256-byte aligned");
+
+    const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
+    if (ws_bytes < plan.total)
+        return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
+    if (!plan.stream_wg && plan.n_split > kMaxMergeSplits)
+        return fail(MURMUR_EINVAL, "split_len %d gives %d splits for max_keep %d; at most %d are supported",
+                    plan.split_len, plan.n_split, max_keep, kMaxMergeSplits);
+    if (plan.o_bytes >= ((size_t)1 << 31))
+        return fail(MURMUR_EINVAL, "split partials of %zu bytes exceed the 2 GiB a launch can address; use a longer "
+                    "split_len", plan.o_bytes);
+    if ((int64_t)kv->n_layers * B > 65535 || Hkv > 65535 || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
+        return fail(MURMUR_EINVAL, "problem too large for one launch (n_layers * B = %lld, Hkv = %d)",
+                    (long long)kv->n_layers * B, Hkv);
+
+    a = AttnLaunch{};
+    a.q = (const uint16_t *)q_dev;
+    a.k = (const uint16_t *)kv->k;
+    a.v = (const uint16_t *)kv->v;
+    a.s_layer = kv->stride_layer;
+    a.s_b = kv->stride_b;
+    a.s_h = kv->stride_h;
+    a.s_pos = kv->stride_pos;
+    a.out = out_dev;
+    a.lse = lse_dev;
+    uint8_t *ws = (uint8_t *)ws_dev;
+    a.ticket = (int32_t *)ws;
+    // Partials exist for split schedules of more than one split and for the stream schedule.
+    const bool partials = plan.ml_bytes > 0;
+    if (partials != (plan.stream_wg > 0 || plan.n_split > 1))
+        return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
+    a.part_ml = partials ? (float *)(ws + plan.ticket_bytes) : nullptr;
+    a.part_o = partials ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
+    a.part_ml_bytes = (uint32_t)plan.ml_bytes;
+    a.part_o_bytes = (uint32_t)plan.o_bytes;
+    a.max_len = kv->max_len;
+    a.max_keep = max_keep;
+    a.B = B;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = Hq / Hkv;
+    a.NL = kv->n_layers;
+    a.split_len = plan.split_len;
+    a.n_split = plan.n_split;
+    a.stream_wg = plan.stream_wg;
+    a.out_f32 = out_dtype == MURMUR_DTYPE_F32;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    return ok();
+}
+
+}  // namespace
+}  // namespace murmur
+
 using namespace murmur;
 
 MURMUR_EXPORT int murmur_abi_version(void) { return MURMUR_ABI_VERSION; }
@@ -167,95 +261,51 @@ MURMUR_EXPORT int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_byte
     return ok();
 }
 
-MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *idx_dev,
-                                     const int32_t *ranges_dev, const int32_t *count_dev, int32_t max_keep,
-                                     int32_t B, int32_t Hq, int32_t Hkv, int32_t D, float scale, int32_t split_len,
-                                     void *out_dev, int32_t out_dtype, float *lse_dev, void *ws_dev, size_t ws_bytes,
-                                     murmur_stream_t stream) {
-    if (!q_dev || !kv || !count_dev || !out_dev || !ws_dev)
-        return fail(MURMUR_EINVAL, "q_dev, kv, count_dev, out_dev and ws_dev must not be NULL");
-    if (!kv->k || !kv->v) return fail(MURMUR_EINVAL, "kv->k and kv->v must not be NULL");
+MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *idx_dev, const int32_t *ranges_dev,
+                                     const int32_t *count_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                     float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                                     void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
+    if (!count_dev) return fail(MURMUR_EINVAL, "count_dev must not be NULL");
     if (!idx_dev && !ranges_dev) return fail(MURMUR_EINVAL, "one of idx_dev and ranges_dev is required");
-    if (B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1 || kv->n_layers < 1 || kv->max_len < 1)
-        return fail(MURMUR_EINVAL, "B, Hq, Hkv, max_keep, kv->n_layers and kv->max_len must be >= 1");
-    if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
-    if (max_keep > kMaxKeep)
-        return fail(MURMUR_EUNSUPPORTED, "max_keep %d exceeds %d (index-list offsets are 32-bit byte offsets)",
-                    max_keep, kMaxKeep);
-    if (D != kHeadDim) return fail(MURMUR_EUNSUPPORTED, "head_dim %d is not supported (only %d)", D, kHeadDim);
-    if (Hq / Hkv > kMaxGroup)
-        return fail(MURMUR_EUNSUPPORTED, "query heads per KV head %d exceeds %d", Hq / Hkv, kMaxGroup);
-    if (out_dtype != MURMUR_DTYPE_BF16 && out_dtype != MURMUR_DTYPE_F32)
-        return fail(MURMUR_EINVAL, "out_dtype must be MURMUR_DTYPE_BF16 or MURMUR_DTYPE_F32 (got %d)", out_dtype);
-    if (!isfinite(scale)) return fail(MURMUR_EINVAL, "scale must be finite");
-    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kSplitUnit != 0))
-        return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
-                    kSplitUnit, split_len);
-    if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
-        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
-    const int64_t strides[4] = {kv->stride_layer, kv->stride_b, kv->stride_h, kv->stride_pos};
-    for (int i = 0; i < 4; ++i)
-        if (strides[i] < 0 || strides[i] % 8 != 0)
-            return fail(MURMUR_EINVAL, "KV strides must be non-negative multiples of 8 elements");
-    if (kv->stride_pos < kHeadDim && kv->max_len > 1)
-        return fail(MURMUR_EINVAL, "kv->stride_pos (%lld) must be >= head_dim", (long long)kv->stride_pos);
-    if (!aligned(q_dev, 16) || !aligned(kv->k, 16) || !aligned(kv->v, 16))
-        return fail(MURMUR_EINVAL, "q_dev, kv->k and kv->v must be 16-byte aligned");
-    if (!aligned(out_dev, 16) || !aligned(lse_dev, 4) ||
-        !aligned(count_dev, 4) || !aligned(idx_dev, 4) || !aligned(ranges_dev, 4))
-        return fail(MURMUR_EINVAL, "out/lse/count/idx/ranges pointers are misaligned");
-    if (!aligned(ws_dev, 256)) return fail(MURMUR_EINVAL, "ws_dev must be 256-byte aligned");
-
-    const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
-    if (ws_bytes < plan.total)
-        return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
-    if (!plan.stream_wg && plan.n_split > kMaxMergeSplits)
-        return fail(MURMUR_EINVAL, "split_len %d gives %d splits for max_keep %d; at most %d are supported",
-                    plan.split_len, plan.n_split, max_keep, kMaxMergeSplits);
-    if (plan.o_bytes >= ((size_t)1 << 31))
-        return fail(MURMUR_EINVAL, "split partials of %zu bytes exceed the 2 GiB a launch can address; use a longer "
-                    "split_len", plan.o_bytes);
-    if ((int64_t)kv->n_layers * B > 65535 || Hkv > 65535 || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
-        return fail(MURMUR_EINVAL, "problem too large for one launch (n_layers * B = %lld, Hkv = %d)",
-                    (long long)kv->n_layers * B, Hkv);
-
-    AttnLaunch a{};
-    a.q = (const uint16_t *)q_dev;
-    a.k = (const uint16_t *)kv->k;
-    a.v = (const uint16_t *)kv->v;
-    a.s_layer = kv->stride_layer;
-    a.s_b = kv->stride_b;
-    a.s_h = kv->stride_h;
-    a.s_pos = kv->stride_pos;
+    if (!aligned(count_dev, 4) || !aligned(idx_dev, 4) || !aligned(ranges_dev, 4))
+        return fail(MURMUR_EINVAL, "count/idx/ranges pointers must be 4-byte aligned");
+    AttnLaunch a;
+    const int rc = prepare_attn(q_dev, kv, max_keep, B, Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev,
+                                ws_dev, ws_bytes, a);
+    if (rc != MURMUR_OK) return rc;
+    a.src0 = count_dev;
+    a.src1 = ranges_dev;
     a.idx = idx_dev;
-    a.ranges = ranges_dev;
-    a.count = count_dev;
-    a.out = out_dev;
-    a.lse = lse_dev;
-    uint8_t *ws = (uint8_t *)ws_dev;
-    a.ticket = (int32_t *)ws;
-    // Partials exist for split schedules of more than one split and for the stream schedule.
-    const bool partials = plan.ml_bytes > 0;
-    if (partials != (plan.stream_wg > 0 || plan.n_split > 1))
-        return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
-    a.part_ml = partials ? (float *)(ws + plan.ticket_bytes) : nullptr;
-    a.part_o = partials ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
-    a.part_ml_bytes = (uint32_t)plan.ml_bytes;
-    a.part_o_bytes = (uint32_t)plan.o_bytes;
-    a.max_len = kv->max_len;
-    a.max_keep = max_keep;
-    a.B = B;
-    a.Hq = Hq;
-    a.Hkv = Hkv;
-    a.G = Hq / Hkv;
-    a.NL = kv->n_layers;
-    a.split_len = plan.split_len;
-    a.n_split = plan.n_split;
-    a.stream_wg = plan.stream_wg;
-    a.out_f32 = out_dtype == MURMUR_DTYPE_F32;
-    a.scale_log2 = scale * 1.4426950408889634f;
+    a.src_mode = ranges_dev ? kSrcRanges : kSrcIndex;
     const int e = launch_decode_attn(a, stream);
     if (e != 0) return fail(MURMUR_EHIP, "decode_attn launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                                     const void *q_dev, const murmur_kv *kv, int32_t *idx_dev, int32_t *count_dev,
+                                     int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                     float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                                     void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
+    if (!seg_dev || !pol_dev) return fail(MURMUR_EINVAL, "seg_dev and pol_dev must not be NULL");
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
+        !aligned(ranges_dev, 4))
+        return fail(MURMUR_EINVAL, "seg/pol/idx/count/ranges pointers must be 4-byte aligned");
+    if ((int64_t)B * max_keep > ((int64_t)1 << 40)) return fail(MURMUR_EINVAL, "B * max_keep too large");
+    AttnLaunch a;
+    const int rc = prepare_attn(q_dev, kv, max_keep, B, Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev,
+                                ws_dev, ws_bytes, a);
+    if (rc != MURMUR_OK) return rc;
+    a.src0 = reinterpret_cast<const int32_t *>(seg_dev);
+    a.src1 = reinterpret_cast<const int32_t *>(pol_dev);
+    a.pol_per_seq = pol_per_seq;
+    a.src_mode = kSrcLayout;
+    a.idx_out = idx_dev;
+    a.count_out = count_dev;
+    a.ranges_out = ranges_dev;
+    const int e = launch_decode_attn(a, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "decode_step launch failed: %s", hip_error_text(e));
     return ok();
 }
 

@@ -29,14 +29,22 @@ constexpr int kMaxKeep = 1 << 28;  // retained positions per sequence the attent
 constexpr int kMergeBatch = 8;  // splits whose partials one merging thread loads at once
 
 // Launch description of one decode_attn call, fully validated by the caller.
+// Where the attention takes the retained sets from (see AttnLaunch::src0/src1).
+enum SrcMode : int32_t { kSrcIndex = 0, kSrcRanges = 1, kSrcLayout = 2 };
+
 struct AttnLaunch {
+    // kSrcIndex / kSrcRanges: src0 = counts [B], src1 = range tables [B][6][2]
+    // (kSrcRanges); kSrcLayout: src0 = layouts (murmur_seg [B]), src1 =
+    // policies (murmur_policy [1] or [B], pol_per_seq).
+    const int32_t *src0;
+    const int32_t *src1;
+    int32_t src_mode, pol_per_seq;
+    int32_t *idx_out, *count_out, *ranges_out;  // kSrcLayout: optional evict_compact outputs
     const uint16_t *q;
     const uint16_t *k;
     const uint16_t *v;
     int64_t s_layer, s_b, s_h, s_pos;
     const int32_t *idx;
-    const int32_t *ranges;
-    const int32_t *count;
     void *out;
     float *lse;
     int32_t *ticket;   // [groups]

@@ -644,6 +644,74 @@ static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, co
     }
 }
 
+// ---------------------------------------------------------------------------
+// Where the retained set of a sequence comes from.  kSrcIndex: counts and the
+// index list; kSrcRanges: counts and the six-piece range table; kSrcLayout
+// (the fused decode step): the layouts and policies themselves, the pieces
+// computed in closed form by every workgroup that needs them, and the
+// evict_compact outputs written by one workgroup per sequence.
+// ---------------------------------------------------------------------------
+// Count of sequence b and, unless kSrcIndex, its range table.  p0/p1: counts
+// and range tables, or (kSrcLayout) layouts (murmur_seg [B]) and policies
+// (murmur_policy [1] or [B]).  An invalid layout or policy gives count 0 and
+// sets policy_bad.
+template <int kSrc>
+static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t *p1, int b, int32_t pol_per_seq,
+                                                int32_t (&rg)[2 * kPieces], int &policy_bad) {
+    if (kSrc == kSrcLayout) {
+        const int32_t *sg = p0 + 4 * b;
+        const int32_t *pl = p1 + (pol_per_seq ? 5 * b : 0);
+        Pieces pc;
+        if (retained_pieces(sg[0], sg[1], sg[2], sg[3], pl[0], pl[1], pl[2], pl[3], pl[4], &pc) != 0) {
+            policy_bad = 1;
+#pragma unroll
+            for (int k = 0; k < 2 * kPieces; ++k) rg[k] = 0;
+            return 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) {
+            rg[2 * k] = pc.start[k];
+            rg[2 * k + 1] = pc.len[k];
+        }
+        return pc.count;
+    }
+    if (kSrc == kSrcRanges) {
+#pragma unroll
+        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = p1[b * 2 * kPieces + k];
+    }
+    return p0[b];
+}
+
+// The evict_compact outputs of sequence b (each one only if the caller passed
+// its buffer) and its device errors: count (0 for an invalid layout or
+// policy), range table, ascending index list padded with -1 (its first
+// max_keep entries when the count exceeds max_keep).  Block-wide.
+static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b, int cnt, int policy_bad,
+                                                      const int32_t (&rg)[2 * kPieces], int max_keep, int tid) {
+    if (tid == 0) {
+        if (a.count_out) a.count_out[b] = cnt;
+        if (policy_bad) raise_device_error(MURMUR_DEVERR_POLICY);
+        else if (cnt > max_keep) raise_device_error(MURMUR_DEVERR_OVERFLOW);
+    }
+    if (a.ranges_out && tid < 2 * kPieces) {
+        int32_t v = 0;
+#pragma unroll
+        for (int k = 0; k < 2 * kPieces; ++k) v = tid == k ? rg[k] : v;
+        a.ranges_out[b * 2 * kPieces + tid] = v;
+    }
+    if (a.idx_out) {
+        int32_t *row = a.idx_out + (int64_t)b * max_keep;
+        int off = 0;
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) {
+            const int n = rg[2 * k + 1] < max_keep - off ? rg[2 * k + 1] : max_keep - off;
+            for (int t = tid; t < n; t += kWavesPerWg * 64) row[off + t] = rg[2 * k] + t;
+            off += n;
+        }
+        for (int r = off + tid; r < max_keep; r += kWavesPerWg * 64) row[r] = -1;
+    }
+}
+
 // LDS shared by the combine step of both schedules.
 struct CombineLds {
     float ml[kWavesPerWg][kMaxGroup][2];  // per wave and head: max (log2 units), sum
@@ -785,20 +853,17 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
 }
 
 // ---------------------------------------------------------------------------
-// decode_attn, split schedule: one workgroup per (split, KV head, sequence,
-// layer).  Each of its four wavefronts takes passes of 32 retained positions,
-// interleaved over the split.  kMultiPass: splits longer than one workgroup
-// pass keep an online softmax across passes, with the next pass's loads in
-// flight while the current one is computed; otherwise every wavefront makes
-// at most one pass.  kRanges: positions from the range table, else from the
-// index list.  The last workgroup of each group merges the splits.  The
+// decode_attn, split schedule, splits of one workgroup pass (128 retained
+// positions): one workgroup per (split, KV head, sequence, layer), each of its
+// four wavefronts one pass of 32 positions, the loads of the pass issued
+// straight from registers.  kSrc: where the retained set comes from.  The last workgroup of each group merges the splits.  The
 // leading scalar arguments are the ones the first memory accesses need; the
 // build preloads them into SGPRs so no kernel-argument load precedes the
 // range-table load.
 // ---------------------------------------------------------------------------
-template <bool kMultiPass, bool kRanges>
-__global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ count,
-                                                          const int32_t *__restrict__ ranges,
+template <int kSrc>
+__global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ src0,
+                                                          const int32_t *__restrict__ src1,
                                                           const int32_t *__restrict__ idx,
                                                           const uint16_t *__restrict__ q, int32_t max_keep,
                                                           int32_t B, const AttnLaunch a) {
@@ -821,22 +886,18 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int grp = lb * a.Hkv + g;  // ((layer * B) + b) * Hkv + g
     const int G = a.G;
 
-    int cnt = count[b];
-    const bool bad_count = cnt < 1 || cnt > max_keep;
-    if (bad_count) cnt = cnt < 0 ? 0 : (cnt > max_keep ? max_keep : cnt);
+    int32_t rg[2 * kPieces];
+    int policy_bad = 0;
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, a.pol_per_seq, rg, policy_bad);
+    const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
+    const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
     const int r_begin = split * a.split_len;
     const int r_end = min(r_begin + a.split_len, cnt);
 
     RangeTab tab;
     __amdgpu_buffer_rsrc_t irow;
-    if (kRanges) {
-        int32_t rg[2 * kPieces];
-#pragma unroll
-        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = ranges[b * 2 * kPieces + k];
-        tab = make_tab(rg);
-    } else {
-        irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
-    }
+    if (kSrc != kSrcIndex) tab = make_tab(rg);
+    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
 
     const int64_t row0 = (int64_t)lb * a.Hq + g * G;  // first output row of the group
     u32x4 qf[4];
@@ -850,55 +911,14 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     wave_acc_reset(w);
     int r = r_begin + wave * kWaveTile;
     auto positions = [&](const IdxRegs &I, int r0, PassPos &pp) {
-        if (kRanges) pass_pos_ranges(tab, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
+        if (kSrc != kSrcIndex) pass_pos_ranges(tab, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
         else pass_pos_index(I, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
     };
-    if (kMultiPass) {
-        // Two register sets, A and B, alternate between the pass being
-        // computed and the pass being loaded; the loop is unrolled twice so
-        // that the roles swap without register copies.
-        PassRegs RA, RB;
-        IdxRegs IA, IB;
-        PassPos pp;
-        if (!kRanges) {
-            load_idx(IA, irow, r, n16, c4);
-            load_idx(IB, irow, r + kSplitUnit, n16, c4);
-        }
-        positions(IA, r, pp);
-        issue_kv(RA, kbase, vbase, a.s_pos, pp, n16, c4);
-        for (;;) {
-            // RA: pass r in flight; IB: index entries of pass r + 128.
-            if (r + kSplitUnit < r_end) {
-                if (!kRanges) load_idx(IA, irow, r + 2 * kSplitUnit, n16, c4);
-                positions(IB, r + kSplitUnit, pp);
-                issue_kv(RB, kbase, vbase, a.s_pos, pp, n16, c4);
-                sched_fence();
-                compute_pass<true>(RA, qf, kWaveTile, a.scale_log2, vt, w, n16, c4);
-                sched_fence();
-            } else {
-                if (r < r_end) compute_pass<true>(RA, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
-                break;
-            }
-            r += kSplitUnit;
-            // RB: pass r in flight; IA: index entries of pass r + 128.
-            if (r + kSplitUnit < r_end) {
-                if (!kRanges) load_idx(IB, irow, r + 2 * kSplitUnit, n16, c4);
-                positions(IA, r + kSplitUnit, pp);
-                issue_kv(RA, kbase, vbase, a.s_pos, pp, n16, c4);
-                sched_fence();
-                compute_pass<true>(RB, qf, kWaveTile, a.scale_log2, vt, w, n16, c4);
-                sched_fence();
-            } else {
-                compute_pass<true>(RB, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
-                break;
-            }
-            r += kSplitUnit;
-        }
-    } else if (r < r_end) {
+    if (r < r_end) {
         PassRegs R;
         IdxRegs I;
         PassPos pp;
-        if (!kRanges) load_idx(I, irow, r, n16, c4);
+        if (kSrc == kSrcIndex) load_idx(I, irow, r, n16, c4);
         positions(I, r, pp);
         issue_kv(R, kbase, vbase, a.s_pos, pp, n16, c4);
         compute_pass<false>(R, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
@@ -909,6 +929,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     float *o_lds = reinterpret_cast<float *>(smem);  // [wave][16][128], reuses the V tiles
     combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
     write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
+    if (kSrc == kSrcLayout && split == 0 && g == 0 && layer == 0) write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
@@ -924,14 +945,14 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
 // stage), issuing the next pass's direct-to-LDS loads before computing the
 // current one.  Index lists are staged too, one pass ahead of the rows.
 // ---------------------------------------------------------------------------
-template <bool kRanges>
-__global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__restrict__ count,
-                                                              const int32_t *__restrict__ ranges,
+template <int kSrc>
+__global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__restrict__ src0,
+                                                              const int32_t *__restrict__ src1,
                                                               const int32_t *__restrict__ idx,
                                                               const uint16_t *__restrict__ q, int32_t max_keep,
                                                               int32_t B, const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t stages[kWavesPerWg][2][kStageBytes];
-    __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kRanges ? 1 : kWavesPerWg][2][kIdxSlotBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kSrc != kSrcIndex ? 1 : kWavesPerWg][2][kIdxSlotBytes];
     __shared__ CombineLds cl;
     __shared__ int s_last;
 
@@ -949,22 +970,18 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const int grp = lb * a.Hkv + g;
     const int G = a.G;
 
-    int cnt = count[b];
-    const bool bad_count = cnt < 1 || cnt > max_keep;
-    if (bad_count) cnt = cnt < 0 ? 0 : (cnt > max_keep ? max_keep : cnt);
+    int32_t rg[2 * kPieces];
+    int policy_bad = 0;
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, a.pol_per_seq, rg, policy_bad);
+    const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
+    const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
     const int r_begin = split * a.split_len;
     const int r_end = min(r_begin + a.split_len, cnt);
 
     RangeTab tab;
     __amdgpu_buffer_rsrc_t irow;
-    if (kRanges) {
-        int32_t rg[2 * kPieces];
-#pragma unroll
-        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = ranges[b * 2 * kPieces + k];
-        tab = make_tab(rg);
-    } else {
-        irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
-    }
+    if (kSrc != kSrcIndex) tab = make_tab(rg);
+    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
 
     const int64_t row0 = (int64_t)lb * a.Hq + g * G;
     u32x4 qf[4];
@@ -973,14 +990,14 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
     uint8_t *st[2] = {&stages[wave][0][0], &stages[wave][1][0]};
-    uint8_t *ring[2] = {&idx_ring[kRanges ? 0 : wave][0][0], &idx_ring[kRanges ? 0 : wave][1][0]};
+    uint8_t *ring[2] = {&idx_ring[kSrc != kSrcIndex ? 0 : wave][0][0], &idx_ring[kSrc != kSrcIndex ? 0 : wave][1][0]};
 
     WaveAcc w;
     wave_acc_reset(w);
     int r = r_begin + wave * kWaveTile;
     if (r < r_end) {
         int32_t pos[8];
-        if (kRanges) {
+        if (kSrc != kSrcIndex) {
             dma_pos_ranges(tab, r, r_end, a.max_len, c4, pos, w.bad_pos);
         } else {
             dma_idx(ring[0], irow, r, lane);
@@ -992,7 +1009,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
         for (int k = 0;; r += kSplitUnit, ++k) {
             const uint8_t *cur = st[k & 1];
             if (r + kSplitUnit < r_end) {
-                if (kRanges) {
+                if (kSrc != kSrcIndex) {
                     dma_pos_ranges(tab, r + kSplitUnit, r_end, a.max_len, c4, pos, w.bad_pos);
                 } else {
                     wait_vm<kStageLoads>();  // entries of the next pass (issued before this pass's rows)
@@ -1000,7 +1017,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
                     dma_idx(ring[k & 1], irow, r + 2 * kSplitUnit, lane);
                 }
                 dma_pass(st[(k + 1) & 1], kbase, vbase, a.s_pos, pos, lane);
-                if (kRanges)
+                if (kSrc != kSrcIndex)
                     wait_vm<kStageLoads>();  // this pass's rows; the next pass's stay in flight
                 else
                     wait_vm<kStageLoads + 1>();
@@ -1018,6 +1035,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // [wave][16][128], reuses the stages
     combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
     write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
+    if (kSrc == kSrcLayout && split == 0 && g == 0 && layer == 0) write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
@@ -1042,9 +1060,9 @@ struct UnitPos {
     int layer, b, g, k;  // k: unit index within the group
 };
 
-template <bool kRanges>
-__global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *__restrict__ count,
-                                                                 const int32_t *__restrict__ ranges,
+template <int kSrc>
+__global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *__restrict__ src0,
+                                                                 const int32_t *__restrict__ src1,
                                                                  const int32_t *__restrict__ idx,
                                                                  const uint16_t *__restrict__ q, int32_t max_keep,
                                                                  int32_t B, const AttnLaunch a) {
@@ -1053,7 +1071,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     __shared__ int s_last;
     __shared__ int32_t s_cnt[kStreamMaxB];      // counts clamped to [0, max_keep]
     __shared__ int32_t s_pre[kStreamMaxB + 1];  // Hkv * (units of the sequences before b), b = 0..B
-    __shared__ int32_t s_rg[kRanges ? kStreamMaxB : 1][2 * kPieces];
+    __shared__ int32_t s_rg[kSrc != kSrcIndex ? kStreamMaxB : 1][2 * kPieces];
     __shared__ uint32_t s_bad[kStreamMaxB / 32];  // sequences with an invalid count
 
     const int tid = threadIdx.x;
@@ -1067,15 +1085,17 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     if (tid < kStreamMaxB / 32) s_bad[tid] = 0;
     __syncthreads();
     for (int t = tid; t < B; t += blockDim.x) {
-        const int c = count[t];
+        int32_t rg[2 * kPieces];
+        int policy_bad = 0;
+        const int c = seq_count<kSrc>(src0, src1, t, a.pol_per_seq, rg, policy_bad);
         const bool badc = c < 1 || c > max_keep;
         const int cc = c < 0 ? 0 : (c > max_keep ? max_keep : c);
         s_cnt[t] = cc;
         s_pre[t + 1] = cc > kSplitUnit ? (cc + kSplitUnit - 1) / kSplitUnit : 1;  // units, at least one
         if (badc) atomicOr(&s_bad[t >> 5], 1u << (t & 31));
-        if (kRanges) {
+        if (kSrc != kSrcIndex) {
 #pragma unroll
-            for (int k = 0; k < 2 * kPieces; ++k) s_rg[t][k] = ranges[t * 2 * kPieces + k];
+            for (int k = 0; k < 2 * kPieces; ++k) s_rg[t][k] = rg[k];
         }
     }
     __syncthreads();
@@ -1158,7 +1178,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     auto issue = [&](const UnitPos &x, const IdxRegs &I, PassRegs &R, u32x4 (&qx)[4], int &bad) {
         const int cnt = s_cnt[x.b];
         PassPos pp;
-        if (kRanges) {
+        if (kSrc != kSrcIndex) {
             int32_t rg[2 * kPieces];
 #pragma unroll
             for (int k = 0; k < 2 * kPieces; ++k) rg[k] = s_rg[x.b][k];
@@ -1221,7 +1241,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     u32x4 qA[4], qB[4];
     IdxRegs IA, IB;
     int next_bad = 0;  // invalid positions met while resolving the next unit
-    if (!kRanges) {
+    if (kSrc == kSrcIndex) {
         load_idx(IA, irow_of(cur, true), first_rank(cur), n16, c4);
         const UnitPos n1 = advance(cur);
         load_idx(IB, irow_of(n1, u + 1 < u_end), first_rank(n1), n16, c4);
@@ -1232,7 +1252,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
             const bool more = u + 1 < u_end;
             const UnitPos nxt = advance(cur);
             if (more) {
-                if (!kRanges) {
+                if (kSrc == kSrcIndex) {
                     const UnitPos nn = advance(nxt);
                     load_idx(IA, irow_of(nn, u + 2 < u_end), first_rank(nn), n16, c4);
                 }
@@ -1254,7 +1274,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
             const bool more = u + 1 < u_end;
             const UnitPos nxt = advance(cur);
             if (more) {
-                if (!kRanges) {
+                if (kSrc == kSrcIndex) {
                     const UnitPos nn = advance(nxt);
                     load_idx(IB, irow_of(nn, u + 2 < u_end), first_rank(nn), n16, c4);
                 }
@@ -1271,6 +1291,14 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
             if (!more) break;
             cur = nxt;
             ++u;
+        }
+    }
+    if (kSrc == kSrcLayout) {  // the evict_compact outputs, sequences spread over the workgroups
+        for (int bb = (int)p; bb < B; bb += (int)P) {
+            int32_t rg[2 * kPieces];
+            int policy_bad = 0;
+            const int c = seq_count<kSrc>(src0, src1, bb, a.pol_per_seq, rg, policy_bad);
+            write_retained(a, bb, c, policy_bad, rg, max_keep, tid);
         }
     }
 }
@@ -1290,28 +1318,30 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
     return (int)hipGetLastError();
 }
 
-template <bool kRanges>
+template <int kSrc>
 static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.stream_wg > 0) {
-        hipLaunchKernelGGL(decode_attn_stream_kernel<kRanges>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
-                           stream, a.count, a.ranges, a.idx, a.q, a.max_keep, a.B, a);
+        hipLaunchKernelGGL(decode_attn_stream_kernel<kSrc>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
+                           stream, a.src0, a.src1, a.idx, a.q, a.max_keep, a.B, a);
         return;
     }
     const dim3 grid((unsigned)a.n_split, (unsigned)a.Hkv, (unsigned)(a.NL * a.B));
-    // Splits of more than one pass per wavefront pipeline their loads.
+    // Splits of more than one pass stage their passes in LDS.
     if (a.split_len > kSplitUnit)
-        hipLaunchKernelGGL(decode_attn_lds_kernel<kRanges>, grid, dim3(kWavesPerWg * 64), 0, stream, a.count,
-                           a.ranges, a.idx, a.q, a.max_keep, a.B, a);
+        hipLaunchKernelGGL(decode_attn_lds_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
+                           a.idx, a.q, a.max_keep, a.B, a);
     else
-        hipLaunchKernelGGL((decode_attn_kernel<false, kRanges>), grid, dim3(kWavesPerWg * 64), 0, stream, a.count,
-                           a.ranges, a.idx, a.q, a.max_keep, a.B, a);
+        hipLaunchKernelGGL(decode_attn_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1, a.idx,
+                           a.q, a.max_keep, a.B, a);
 }
 
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
-    if (a.ranges)
-        launch_decode_attn_mode<true>(a, (hipStream_t)stream);
+    if (a.src_mode == kSrcLayout)
+        launch_decode_attn_mode<kSrcLayout>(a, (hipStream_t)stream);
+    else if (a.src_mode == kSrcRanges)
+        launch_decode_attn_mode<kSrcRanges>(a, (hipStream_t)stream);
     else
-        launch_decode_attn_mode<false>(a, (hipStream_t)stream);
+        launch_decode_attn_mode<kSrcIndex>(a, (hipStream_t)stream);
     return (int)hipGetLastError();
 }
 

@@ -5,8 +5,9 @@ Memory plumbing only (torch allocates, the HIP kernels compute):
     consecutive timed steps can read different addresses (cold caches);
   * per-step layouts [steps][B][4] and queries [steps][NL][B][Hq][D];
   * retained lists, counts, range tables, outputs and the split workspace.
-A step is murmur_evict_compact followed by murmur_decode_attn, both enqueued on
-the current torch stream with no host synchronisation.
+A step is murmur_evict_compact followed by murmur_decode_attn, or the single
+murmur_decode_step launch, enqueued on the current torch stream with no host
+synchronisation.
 """
 from __future__ import annotations
 
@@ -78,6 +79,14 @@ class DecodeBatch:
     def step(self, i: int, replica: int = 0, stream=None) -> None:
         self.evict(i, stream)
         self.attend(i, replica, stream)
+
+    def step_fused(self, i: int, replica: int = 0, stream=None, buf: int = 0, outputs: bool = True) -> None:
+        """murmur_decode_step for the i-th step: eviction and attention in one launch, the retained-set
+        outputs (index list, count, range table) written into buffer set `buf` when `outputs`."""
+        idx, count, ranges = self.sets[buf] if outputs else (None, None, None)
+        M.murmur_decode_step(self.seg[i], self.pol, 1, self.q[i], self.kv[replica], idx, count, ranges,
+                             self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale, self.split_len,
+                             self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes, stream)
 
     def pipelined_steps(self, steps: list[int], replicas: list[int], attn_stream, evict_stream) -> None:
         """Enqueue the given steps with the eviction of step k+1 overlapping the attention of step k.

@@ -76,6 +76,9 @@ def _load():
     lib.murmur_decode_attn.restype = ctypes.c_int
     lib.murmur_decode_attn.argtypes = [vp, ctypes.POINTER(murmur_kv), vp, vp, vp, i32, i32, i32, i32, i32,
                                        ctypes.c_float, i32, vp, i32, vp, vp, sz, vp]
+    lib.murmur_decode_step.restype = ctypes.c_int
+    lib.murmur_decode_step.argtypes = [vp, vp, i32, vp, ctypes.POINTER(murmur_kv), vp, vp, vp, i32, i32, i32, i32, i32,
+                                       ctypes.c_float, i32, vp, i32, vp, vp, sz, vp]
     lib.murmur_device_error.restype = ctypes.c_int
     lib.murmur_device_error.argtypes = [vp, i32p]
     _lib = lib
@@ -186,6 +189,16 @@ def murmur_decode_attn(q_dev, kv: murmur_kv, idx_dev, ranges_dev, count_dev, max
                                       _addr(count_dev), max_keep, B, Hq, Hkv, D, float(scale), split_len,
                                       _addr(out_dev), out_dtype, _addr(lse_dev), _addr(ws_dev), ws_bytes,
                                       _stream(stream)))
+
+
+def murmur_decode_step(seg_dev, pol_dev, pol_per_seq: int, q_dev, kv: murmur_kv, idx_dev, count_dev, ranges_dev,
+                       max_keep: int, B: int, Hq: int, Hkv: int, D: int, scale: float, split_len: int, out_dev,
+                       out_dtype: int, lse_dev, ws_dev, ws_bytes: int, stream=None) -> None:
+    """Eviction and attention of one decode step in one launch; idx/count/ranges outputs are optional."""
+    _check(_load().murmur_decode_step(_addr(seg_dev), _addr(pol_dev), pol_per_seq, _addr(q_dev), ctypes.byref(kv),
+                                      _addr(idx_dev), _addr(count_dev), _addr(ranges_dev), max_keep, B, Hq, Hkv, D,
+                                      float(scale), split_len, _addr(out_dev), out_dtype, _addr(lse_dev),
+                                      _addr(ws_dev), ws_bytes, _stream(stream)))
 
 
 def murmur_device_error(stream=None) -> int:

@@ -37,14 +37,14 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 8
+    assert len(names) == 9
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 1
+    assert M.murmur_abi_version() == 2
 
 
 def test_retained_count_host_matches_oracle():
@@ -175,3 +175,26 @@ def test_workspace_init_and_device_error_reject_null():
     assert lib.murmur_decode_attn_workspace_init(None, 1024, 0) == M.MURMUR_EINVAL
     assert lib.murmur_decode_attn_workspace_init(FAKE + 4, 1024, 0) == M.MURMUR_EINVAL
     assert lib.murmur_device_error(0, None) == M.MURMUR_EINVAL
+
+
+def call_step(a, seg=FAKE, pol=FAKE, pol_per_seq=0):
+    return M.lib().murmur_decode_step(seg, pol, pol_per_seq, a["q"], ctypes.byref(a["kv"]), a["idx"], a["count"],
+                                      a["ranges"], a["max_keep"], a["B"], a["Hq"], a["Hkv"], a["D"], a["scale"],
+                                      a["split_len"], a["out"], a["out_dtype"], a["lse"], a["ws"], a["ws_bytes"], 0)
+
+
+@pytest.mark.parametrize("over,step_kw,code", [
+    ({}, dict(seg=None), M.MURMUR_EINVAL),
+    ({}, dict(pol=None), M.MURMUR_EINVAL),
+    ({}, dict(pol_per_seq=2), M.MURMUR_EINVAL),
+    ({}, dict(seg=FAKE + 2), M.MURMUR_EINVAL),
+    (dict(idx=FAKE + 1), {}, M.MURMUR_EINVAL),
+    (dict(q=None), {}, M.MURMUR_EINVAL),
+    (dict(D=64), {}, M.MURMUR_EUNSUPPORTED),
+    (dict(split_len=100), {}, M.MURMUR_EINVAL),
+    (dict(max_keep=0), {}, M.MURMUR_EINVAL),
+    (dict(ws_bytes=1000), {}, M.MURMUR_ENOSPACE),
+])
+def test_decode_step_rejects(over, step_kw, code):
+    assert call_step(attn_args(**over), **step_kw) == code
+    assert M.murmur_last_error() != ""

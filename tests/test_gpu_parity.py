@@ -367,3 +367,118 @@ def test_stream_schedule_more_workgroups_than_units():
             y, l = run_gpu(db, i)
             assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
     assert int(db.ws[: db.NL * db.B * db.Hkv].abs().sum().item()) == 0
+
+
+# ---- murmur_decode_step: eviction and attention in one launch ------------------------------------
+
+def check_retained_outputs(db, wl, s, buf=0):
+    """The fused step's retained-set outputs against the oracle, bit for bit."""
+    ref_idx, ref_cnt = oracle.retained(wl.seg(s), wl.policy, max_keep=db.max_keep)
+    idx, cnt, rng = (t.cpu().numpy() for t in db.sets[buf])
+    assert np.array_equal(cnt, ref_cnt)
+    assert np.array_equal(idx, ref_idx)
+    for b in range(db.B):
+        assert expand(rng[b]) == ref_idx[b, :ref_cnt[b]].tolist()
+
+
+@pytest.mark.parametrize("config", ["c1", "c2", "c3", "c4_dense", "c4_evict"])
+def test_decode_step_fused(config):
+    """murmur_decode_step against the oracle on both schedules: attention to the fp32 bar, the index
+    list, counts and range tables it writes bit-exact."""
+    wl = workload(config)
+    steps = [0, wl.steps - 1]
+    for split_len in (0, M.MURMUR_SPLIT_STREAM):
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps, split_len=split_len)
+        for i, s in enumerate(steps):
+            announce(f"decode_step {config} step {s} split_len {split_len}")
+            ref, ref_lse = oracle_step(wl, s)
+            for t in db.sets[0]:
+                t.fill_(-7)
+            db.out.fill_(float("nan"))
+            db.step_fused(i)
+            torch.cuda.synchronize()
+            y = db.out.float().cpu().numpy().astype(np.float64)
+            l = db.lse.cpu().numpy().astype(np.float64)
+            assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+            check_retained_outputs(db, wl, s)
+        assert int(db.ws[: db.NL * db.B * db.Hkv].abs().sum().item()) == 0
+
+
+def test_decode_step_fused_ragged_and_without_outputs():
+    """130 ragged sequences with per-sequence policies, retained-set outputs written and not."""
+    announce("decode_step, 130 ragged sequences")
+    rng = np.random.default_rng(123)
+    B = 130
+    seg0 = np.stack([rng.integers(0, 20, B), rng.integers(0, 700, B), rng.integers(0, 8, B),
+                     rng.integers(0, 300, B)], axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.3, OFF, rng.integers(1, 400, B)), rng.integers(0, 200, B),
+                    rng.integers(0, 8, B), np.where(rng.random(B) < 0.3, OFF, rng.integers(1, 200, B)),
+                    rng.integers(0, 8, B)], axis=1).astype(np.int32)
+    wl = W.build("ragged", 37, 2, seg0, pol, steps=2, planted=False)
+    ref, ref_lse = oracle_step(wl, 1)
+    for split_len in (0, 256, M.MURMUR_SPLIT_STREAM):
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[1], split_len=split_len)
+        for outputs in (True, False):
+            db.out.fill_(float("nan"))
+            db.step_fused(0, outputs=outputs)
+            torch.cuda.synchronize()
+            y = db.out.float().cpu().numpy().astype(np.float64)
+            l = db.lse.cpu().numpy().astype(np.float64)
+            assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL, (split_len, outputs)
+        check_retained_outputs(db, wl, 1)
+
+
+def test_decode_step_fused_device_errors():
+    """An invalid policy and a count above max_keep: the evict_compact outputs and errors, NaN attention."""
+    announce("decode_step device errors")
+    wl = workload("c1")
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[0])
+    bad_pol = torch.tensor([[0, 0, 0, 0, 0]], dtype=torch.int32, device="cuda")  # out_window 0: invalid
+    idx, cnt, rng = db.sets[0]
+    M.murmur_decode_step(db.seg[0], bad_pol, 0, db.q[0], db.kv[0], idx, cnt, rng, db.max_keep, db.B, db.Hq, db.Hkv,
+                         db.D, wl.scale, 0, db.out, db.out_dtype, db.lse, db.ws, db.ws_bytes)
+    torch.cuda.synchronize()
+    assert M.murmur_device_error() == M.MURMUR_DEVERR_POLICY | M.MURMUR_DEVERR_COUNT
+    assert torch.isnan(db.out).all().item()
+    assert cnt.cpu().tolist() == [0] and (idx == -1).all().item() and (rng == 0).all().item()
+    true_cnt = int(oracle.retained(wl.seg(0), wl.policy)[1][0])
+    small = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[0], max_keep=true_cnt - 5)
+    small.step_fused(0)
+    torch.cuda.synchronize()
+    assert M.murmur_device_error() == M.MURMUR_DEVERR_OVERFLOW | M.MURMUR_DEVERR_COUNT
+    assert torch.isnan(small.out).all().item()
+    ref_idx, _ = oracle.retained(wl.seg(0), wl.policy)
+    assert small.count.cpu().tolist() == [true_cnt]
+    assert np.array_equal(small.idx.cpu().numpy()[0], ref_idx[0, : true_cnt - 5])
+
+
+def test_decode_step_fused_graph_replays():
+    """Fused steps captured into a HIP graph replay to the eager result every time."""
+    announce("decode_step graph replays")
+    wl = workload("c3")
+    steps = [0, 1, 2]
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps)
+    outs = []
+    for i in range(len(steps)):
+        db.step_fused(i)
+        torch.cuda.synchronize()
+        outs.append(db.out.clone())
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        db.step_fused(0, stream=s)  # warm-up on the capture stream
+        g.capture_begin()
+        for i in range(len(steps)):
+            db.step_fused(i, stream=s)
+        g.capture_end()
+    torch.cuda.current_stream().wait_stream(s)
+    for _ in range(3):
+        db.out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(db.out, outs[-1])
+        db.step_fused(0)
+        torch.cuda.synchronize()
+        assert torch.equal(db.out, outs[0])
