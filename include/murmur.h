@@ -176,9 +176,12 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  *   q_dev:      bf16 [n_layers][B][Hq][D], contiguous, 16-byte aligned;
  *   kv:         host struct describing the bf16 K/V caches (see murmur_kv);
  *   ranges_dev: nullable [B][6][2] range table from murmur_evict_compact; when
- *               given it is used and idx_dev is not read;
+ *               given it is used, each sequence's count is the table's total
+ *               length (what murmur_evict_compact writes to count_dev), and
+ *               neither idx_dev nor count_dev is read;
  *   idx_dev:    [B][max_keep] positions (used when ranges_dev is NULL);
- *   count_dev:  [B] retained counts;
+ *   count_dev:  [B] retained counts (required with idx_dev; may be NULL with
+ *               ranges_dev);
  *   D:          head_dim, must be 128; Hq/Hkv must be in [1, 16];
  *   scale:      logit scale (1/sqrt(D) for unscaled queries), finite;
  *   split_len:  the work schedule.  A positive multiple of 128: each (layer,
@@ -194,8 +197,9 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  *               stores the fp32 accumulation);
  *   lse_dev:    nullable fp32 [n_layers][B][Hq], natural log;
  *   ws_dev:     workspace of ws_bytes >= murmur_decode_attn_workspace(...).
- * Accumulation is fp32 throughout.  Errors: MURMUR_EINVAL, MURMUR_EUNSUPPORTED,
- * MURMUR_ENOSPACE (workspace), MURMUR_EHIP; device errors
+ * Accumulation is fp32 throughout.  Errors: MURMUR_EINVAL, MURMUR_EUNSUPPORTED
+ * (head_dim, group size, max_keep above 2^28), MURMUR_ENOSPACE (workspace),
+ * MURMUR_EHIP; device errors
  * MURMUR_DEVERR_POSITION and MURMUR_DEVERR_COUNT. */
 int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *idx_dev, const int32_t *ranges_dev,
                        const int32_t *count_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,

@@ -162,9 +162,9 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     if (plan.o_bytes >= ((size_t)1 << 31))
         return fail(MURMUR_EINVAL, "split partials of %zu bytes exceed the 2 GiB a launch can address; use a longer "
                     "split_len", plan.o_bytes);
-    if ((int64_t)kv->n_layers * B > 65535 || Hkv > 65535 || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
-        return fail(MURMUR_EINVAL, "problem too large for one launch (n_layers * B = %lld, Hkv = %d)",
-                    (long long)kv->n_layers * B, Hkv);
+    if ((int64_t)kv->n_layers * Hkv > 65535 || B > 65535 || (int64_t)kv->n_layers * B * Hq > 0x7fffffffLL)
+        return fail(MURMUR_EINVAL, "problem too large for one launch (n_layers * Hkv = %lld, B = %d)",
+                    (long long)kv->n_layers * Hkv, B);
 
     a = AttnLaunch{};
     a.q = (const uint16_t *)q_dev;
@@ -265,15 +265,15 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
                                      const int32_t *count_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
                                      float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
                                      void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
-    if (!count_dev) return fail(MURMUR_EINVAL, "count_dev must not be NULL");
     if (!idx_dev && !ranges_dev) return fail(MURMUR_EINVAL, "one of idx_dev and ranges_dev is required");
+    if (!ranges_dev && !count_dev) return fail(MURMUR_EINVAL, "count_dev is required with an index list");
     if (!aligned(count_dev, 4) || !aligned(idx_dev, 4) || !aligned(ranges_dev, 4))
         return fail(MURMUR_EINVAL, "count/idx/ranges pointers must be 4-byte aligned");
     AttnLaunch a;
     const int rc = prepare_attn(q_dev, kv, max_keep, B, Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev,
                                 ws_dev, ws_bytes, a);
     if (rc != MURMUR_OK) return rc;
-    a.src0 = count_dev;
+    a.src0 = ranges_dev ? nullptr : count_dev;  // a range table carries its own counts
     a.src1 = ranges_dev;
     a.idx = idx_dev;
     a.src_mode = ranges_dev ? kSrcRanges : kSrcIndex;

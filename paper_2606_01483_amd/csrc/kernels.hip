@@ -332,6 +332,18 @@ static __device__ __forceinline__ void issue_kv(PassRegs &R, const uint16_t *kba
     for (int i = 0; i < 8; ++i) R.vf[i] = load16(vbase + (int64_t)pp.v[i] * s_pos + 8 * n16);
 }
 
+// Forces uniform values into scalar registers at this point: the scalar loads
+// they come from are then issued together, ahead of one wait, instead of
+// being sunk to their first use behind earlier waits.
+template <typename T>
+static __device__ __forceinline__ void materialize_one(const T &x) {
+    asm volatile("" ::"s"(x));
+}
+template <typename... T>
+static __device__ __forceinline__ void materialize(const T &...x) {
+    (materialize_one(x), ...);
+}
+
 // Keeps the instruction scheduler from moving anything across this point
 // (the consumer of one pass above the loads of the next, in particular).
 static __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
@@ -652,7 +664,8 @@ static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, co
 // evict_compact outputs written by one workgroup per sequence.
 // ---------------------------------------------------------------------------
 // Count of sequence b and, unless kSrcIndex, its range table.  p0/p1: counts
-// and range tables, or (kSrcLayout) layouts (murmur_seg [B]) and policies
+// (kSrcIndex) or range tables (kSrcRanges, the count being the table's total
+// length), or (kSrcLayout) layouts (murmur_seg [B]) and policies
 // (murmur_policy [1] or [B]).  An invalid layout or policy gives count 0 and
 // sets policy_bad.
 template <int kSrc>
@@ -661,8 +674,11 @@ static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t
     if (kSrc == kSrcLayout) {
         const int32_t *sg = p0 + 4 * b;
         const int32_t *pl = p1 + (pol_per_seq ? 5 * b : 0);
+        const int32_t s0 = sg[0], s1 = sg[1], s2 = sg[2], s3 = sg[3];
+        const int32_t w0 = pl[0], w1 = pl[1], w2 = pl[2], w3 = pl[3], w4 = pl[4];
+        materialize(s0, s1, s2, s3, w0, w1, w2, w3, w4);  // both rows in one round trip
         Pieces pc;
-        if (retained_pieces(sg[0], sg[1], sg[2], sg[3], pl[0], pl[1], pl[2], pl[3], pl[4], &pc) != 0) {
+        if (retained_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, &pc) != 0) {
             policy_bad = 1;
 #pragma unroll
             for (int k = 0; k < 2 * kPieces; ++k) rg[k] = 0;
@@ -675,9 +691,13 @@ static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t
         }
         return pc.count;
     }
-    if (kSrc == kSrcRanges) {
+    if (kSrc == kSrcRanges) {  // the count is the table's total length
+        int c = 0;
 #pragma unroll
         for (int k = 0; k < 2 * kPieces; ++k) rg[k] = p1[b * 2 * kPieces + k];
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) c += rg[2 * k + 1];
+        return c;
     }
     return p0[b];
 }
@@ -854,7 +874,7 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
 
 // ---------------------------------------------------------------------------
 // decode_attn, split schedule, splits of one workgroup pass (128 retained
-// positions): one workgroup per (split, KV head, sequence, layer), each of its
+// positions): one workgroup per (split, layer and KV head, sequence), each of its
 // four wavefronts one pass of 32 positions, the loads of the pass issued
 // straight from registers.  kSrc: where the retained set comes from.  The last workgroup of each group merges the splits.  The
 // leading scalar arguments are the ones the first memory accesses need; the
@@ -866,7 +886,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
                                                           const int32_t *__restrict__ src1,
                                                           const int32_t *__restrict__ idx,
                                                           const uint16_t *__restrict__ q, int32_t max_keep,
-                                                          int32_t B, const AttnLaunch a) {
+                                                          int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
+                                                          const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
     __shared__ CombineLds cl;
     __shared__ int s_last;
@@ -878,17 +899,19 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int c4 = lane >> 4;
 
     // Grid: x = split, y = KV head, z = layer * B + sequence.
+    // Grid: x = split, y = layer * Hkv + KV head, z = sequence.  The
+    // sequence's retained-set description is loaded first: the first K/V loads
+    // wait for it and for nothing else.
     const int split = blockIdx.x;
-    const int g = blockIdx.y;
-    const int lb = blockIdx.z;
-    const int b = lb % B;
-    const int layer = lb / B;
-    const int grp = lb * a.Hkv + g;  // ((layer * B) + b) * Hkv + g
-    const int G = a.G;
-
+    const int b = blockIdx.z;
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, a.pol_per_seq, rg, policy_bad);
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, rg, policy_bad);
+    const int layer = (int)blockIdx.y / Hkv;
+    const int g = (int)blockIdx.y - layer * Hkv;
+    const int lb = layer * B + b;
+    const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
+    const int Hq = Hkv * G;
     const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
     const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
     const int r_begin = split * a.split_len;
@@ -897,9 +920,9 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     RangeTab tab;
     __amdgpu_buffer_rsrc_t irow;
     if (kSrc != kSrcIndex) tab = make_tab(rg);
-    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
+    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)max_keep * 4u);  // ranks past the count are masked
 
-    const int64_t row0 = (int64_t)lb * a.Hq + g * G;  // first output row of the group
+    const int64_t row0 = (int64_t)lb * Hq + g * G;  // first output row of the group
     u32x4 qf[4];
     load_q(qf, q, row0, G, n16, c4);
     const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
@@ -910,6 +933,10 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     WaveAcc w;
     wave_acc_reset(w);
     int r = r_begin + wave * kWaveTile;
+    materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
+    if (kSrc != kSrcIndex)
+        materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
+                    tab.off[3], tab.off[4], tab.off[5]);
     auto positions = [&](const IdxRegs &I, int r0, PassPos &pp) {
         if (kSrc != kSrcIndex) pass_pos_ranges(tab, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
         else pass_pos_index(I, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
@@ -950,7 +977,8 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
                                                               const int32_t *__restrict__ src1,
                                                               const int32_t *__restrict__ idx,
                                                               const uint16_t *__restrict__ q, int32_t max_keep,
-                                                              int32_t B, const AttnLaunch a) {
+                                                              int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
+                                                          const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t stages[kWavesPerWg][2][kStageBytes];
     __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kSrc != kSrcIndex ? 1 : kWavesPerWg][2][kIdxSlotBytes];
     __shared__ CombineLds cl;
@@ -962,17 +990,19 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
 
+    // Grid: x = split, y = layer * Hkv + KV head, z = sequence.  The
+    // sequence's retained-set description is loaded first: the first K/V loads
+    // wait for it and for nothing else.
     const int split = blockIdx.x;
-    const int g = blockIdx.y;
-    const int lb = blockIdx.z;
-    const int b = lb % B;
-    const int layer = lb / B;
-    const int grp = lb * a.Hkv + g;
-    const int G = a.G;
-
+    const int b = blockIdx.z;
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, a.pol_per_seq, rg, policy_bad);
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, rg, policy_bad);
+    const int layer = (int)blockIdx.y / Hkv;
+    const int g = (int)blockIdx.y - layer * Hkv;
+    const int lb = layer * B + b;
+    const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
+    const int Hq = Hkv * G;
     const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
     const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
     const int r_begin = split * a.split_len;
@@ -981,9 +1011,9 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     RangeTab tab;
     __amdgpu_buffer_rsrc_t irow;
     if (kSrc != kSrcIndex) tab = make_tab(rg);
-    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)cnt * 4u);
+    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)max_keep * 4u);  // ranks past the count are masked
 
-    const int64_t row0 = (int64_t)lb * a.Hq + g * G;
+    const int64_t row0 = (int64_t)lb * Hq + g * G;
     u32x4 qf[4];
     load_q(qf, q, row0, G, n16, c4);
     const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
@@ -995,6 +1025,10 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     WaveAcc w;
     wave_acc_reset(w);
     int r = r_begin + wave * kWaveTile;
+    materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
+    if (kSrc != kSrcIndex)
+        materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
+                    tab.off[3], tab.off[4], tab.off[5]);
     if (r < r_end) {
         int32_t pos[8];
         if (kSrc != kSrcIndex) {
@@ -1065,7 +1099,8 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
                                                                  const int32_t *__restrict__ src1,
                                                                  const int32_t *__restrict__ idx,
                                                                  const uint16_t *__restrict__ q, int32_t max_keep,
-                                                                 int32_t B, const AttnLaunch a) {
+                                                                 int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
+                                                          const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
     __shared__ CombineLds cl;
     __shared__ int s_last;
@@ -1079,7 +1114,6 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     const int wave = tid >> 6;
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
-    const int Hkv = a.Hkv, G = a.G;
 
     // ---- per-sequence tables -------------------------------------------------
     if (tid < kStreamMaxB / 32) s_bad[tid] = 0;
@@ -1087,7 +1121,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     for (int t = tid; t < B; t += blockDim.x) {
         int32_t rg[2 * kPieces];
         int policy_bad = 0;
-        const int c = seq_count<kSrc>(src0, src1, t, a.pol_per_seq, rg, policy_bad);
+        const int c = seq_count<kSrc>(src0, src1, t, pol_per_seq, rg, policy_bad);
         const bool badc = c < 1 || c > max_keep;
         const int cc = c < 0 ? 0 : (c > max_keep ? max_keep : c);
         s_cnt[t] = cc;
@@ -1297,7 +1331,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         for (int bb = (int)p; bb < B; bb += (int)P) {
             int32_t rg[2 * kPieces];
             int policy_bad = 0;
-            const int c = seq_count<kSrc>(src0, src1, bb, a.pol_per_seq, rg, policy_bad);
+            const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, rg, policy_bad);
             write_retained(a, bb, c, policy_bad, rg, max_keep, tid);
         }
     }
@@ -1322,17 +1356,17 @@ template <int kSrc>
 static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.stream_wg > 0) {
         hipLaunchKernelGGL(decode_attn_stream_kernel<kSrc>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
-                           stream, a.src0, a.src1, a.idx, a.q, a.max_keep, a.B, a);
+                           stream, a.src0, a.src1, a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
         return;
     }
-    const dim3 grid((unsigned)a.n_split, (unsigned)a.Hkv, (unsigned)(a.NL * a.B));
+    const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
     // Splits of more than one pass stage their passes in LDS.
     if (a.split_len > kSplitUnit)
         hipLaunchKernelGGL(decode_attn_lds_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
-                           a.idx, a.q, a.max_keep, a.B, a);
+                           a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
     else
         hipLaunchKernelGGL(decode_attn_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1, a.idx,
-                           a.q, a.max_keep, a.B, a);
+                           a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
 }
 
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
