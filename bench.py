@@ -82,6 +82,53 @@ def committed_traffic(config: str) -> float | None:
         return None
 
 
+def summarize_trace(directory: str, top: int = 8) -> str:
+    """Markdown table of a rocprofv3 --kernel-trace --stats run (its *kernel_stats.csv)."""
+    import csv
+    import glob
+    path = sorted(glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True))[0]
+    rows = list(csv.DictReader(open(path)))
+    out = ["| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns | Std dev |", "|---|---|---|---|---|---|---|---|"]
+    for r in rows[:top]:
+        name = r["Name"] if len(r["Name"]) <= 72 else r["Name"][:69] + "..."
+        out.append(f"| {name} | {r['Calls']} | {r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | {r['Percentage']} | "
+                   f"{r['MinNs']} | {r['MaxNs']} | {float(r['StdDev']):.0f} |")
+    return "\n".join(out)
+
+
+def _pmc_per_dispatch(directory: str, name_part: str) -> tuple[float, int]:
+    """Mean counter value (KiB) per dispatch of the kernels whose name contains name_part."""
+    import csv
+    import glob
+    path = sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True))[0]
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path)) if name_part in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"no dispatch of a kernel named like {name_part!r} in {path}")
+    return sum(vals) / len(vals), len(vals)
+
+
+def summarize_pmc(config: str, kernel: str, fetch_dir: str, write_dir: str, copy_fetch_dir: str,
+                  copy_write_dir: str, copy_mib: int, alg_bytes: int) -> str:
+    """Body of profiles/decode_attn_<config>_traffic.txt: FETCH_SIZE and WRITE_SIZE per dispatch of
+    `kernel`, each scaled by what the same counter reads for a plain device copy of copy_mib MiB."""
+    f_kib, nf = _pmc_per_dispatch(fetch_dir, kernel)
+    w_kib, nw = _pmc_per_dispatch(write_dir, kernel)
+    cf_kib, _ = _pmc_per_dispatch(copy_fetch_dir, "copyBuffer")
+    cw_kib, _ = _pmc_per_dispatch(copy_write_dir, "copyBuffer")
+    f_scale, w_scale = copy_mib * 1024 / cf_kib, copy_mib * 1024 / cw_kib
+    traffic = (f_kib * f_scale + w_kib * w_scale) * 1024
+    return "\n".join([
+        f"# Scale factors: a plain {copy_mib} MiB device copy (__amd_rocclr_copyBuffer) reads FETCH_SIZE "
+        f"{cf_kib:.1f} KiB and WRITE_SIZE {cw_kib:.1f} KiB per dispatch,",
+        f"# so FETCH_SIZE is scaled by {f_scale:.4f} and WRITE_SIZE by {w_scale:.4f}.",
+        f"# {kernel}: FETCH_SIZE mean {f_kib:.1f} KiB over {nf} dispatches, WRITE_SIZE mean {w_kib:.1f} KiB over {nw}.",
+        f"kernel: {kernel}", f"workload: {config}", f"fetch_kib_per_dispatch: {f_kib:.1f}",
+        f"write_kib_per_dispatch: {w_kib:.1f}", f"fetch_scale: {f_scale:.4f}", f"write_scale: {w_scale:.4f}",
+        f"algorithmic_bytes_per_launch: {alg_bytes}", f"traffic_bytes_per_launch: {traffic:.0f}",
+        f"traffic_over_algorithmic: {traffic / alg_bytes:.3f}", f"kernel_source_sha256_16: {kernel_source_hash()}",
+    ])
+
+
 def copy_reference(mbytes: int, reps: int) -> dict:
     """A plain device copy of known size, the reference for scaling the PMC byte counters."""
     import torch
@@ -252,7 +299,19 @@ def main() -> int:
     ap.add_argument("--all", action="store_true", help="one JSON line per workload (c1 .. c5), no CPU baseline")
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MB",
                     help="only run plain device copies of this many MiB (PMC counter reference)")
+    ap.add_argument("--summarize-trace", metavar="DIR", help="print the kernel table of a rocprofv3 --stats run")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="print the traffic summary from four rocprofv3 --pmc runs")
+    ap.add_argument("--pmc-kernel", default="decode_attn_kernel<1>", help="kernel name part for --summarize-pmc")
+    ap.add_argument("--copy-mib", type=int, default=256, help="copy size of the --copy-reference runs")
+    ap.add_argument("--alg-bytes", type=int, default=0, help="algorithmic bytes per launch (bench JSON)")
     args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return 0
+    if args.summarize_pmc:
+        print(summarize_pmc(args.config, args.pmc_kernel, *args.summarize_pmc, args.copy_mib, args.alg_bytes))
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this decode path has no multi-GPU mode (got --gpus {args.gpus})",
               file=sys.stderr)
