@@ -732,53 +732,49 @@ static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b
     }
 }
 
-// LDS shared by the combine step of both schedules.
-struct CombineLds {
-    float ml[kWavesPerWg][kMaxGroup][2];  // per wave and head: max (log2 units), sum
-    float mlf[kMaxGroup][2];              // per head: workgroup max, workgroup sum (NaN when bad)
+// Combine of a workgroup's four wavefronts.  Each wavefront publishes its
+// state -- (max, sum) per head and its unscaled O rows -- into LDS regions no
+// other wavefront touches before the workgroup barrier that follows; after
+// the barrier the threads writing the result rescale and add the four states
+// as they read them.  One barrier and no dependent LDS round trip between.
+struct __attribute__((aligned(16))) CombineLds {
+    float ml[kMaxGroup][kWavesPerWg][2];  // per head and wavefront: max (log2 units), sum
 };
+constexpr int kOStride = kHeadDim + 4;                  // floats per published O row (padded: conflict-free stores)
+constexpr int kOWaveBytes = kMaxGroup * kOStride * 4;   // 8448: a wavefront's published rows
+static_assert(kOWaveBytes >= kVtBytesPerWave && kOWaveBytes % 16 == 0,
+              "a wavefront's LDS slot holds its V tile, then its published rows");
 
-// Merges the four wavefronts' states of one (layer, sequence, KV head) in LDS.
-// Afterwards o_lds[w][h][d] holds wave w's O rescaled to the workgroup max,
-// whose sum over w is the workgroup's unnormalised O; cl.mlf holds (max, sum).
-// Block-wide: every thread calls it.
-static __device__ __forceinline__ void combine_waves(const WaveAcc &w, bool bad, float *o_lds, CombineLds &cl,
-                                                     int G, int tid, int wave, int n16, int c4) {
+static __device__ __forceinline__ void publish_wave(const WaveAcc &w, float *o_w, CombineLds &cl, int wave, int n16,
+                                                    int c4) {
     if (c4 == 0) {
-        cl.ml[wave][n16][0] = w.m_run;
-        cl.ml[wave][n16][1] = w.l_run;
+        cl.ml[n16][wave][0] = w.m_run;
+        cl.ml[n16][wave][1] = w.l_run;
     }
-    __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int h = 4 * c4 + i;
-        if (h < G) {
-            const float mx = fmaxf(fmaxf(cl.ml[0][h][0], cl.ml[1][h][0]), fmaxf(cl.ml[2][h][0], cl.ml[3][h][0]));
-            const float mine = cl.ml[wave][h][0];
-            const float f = mine == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mine - mx);
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int db = 0; db < 8; ++db) o_lds[(wave * kMaxGroup + h) * kHeadDim + 16 * db + n16] = w.acc[db][i] * f;
-        }
-    }
-    if (tid < G) {
-        const float mx = fmaxf(fmaxf(cl.ml[0][tid][0], cl.ml[1][tid][0]), fmaxf(cl.ml[2][tid][0], cl.ml[3][tid][0]));
-        float L = 0.f;
-#pragma unroll
-        for (int wv = 0; wv < kWavesPerWg; ++wv) {
-            const float mw = cl.ml[wv][tid][0];
-            L += cl.ml[wv][tid][1] * (mw == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mw - mx));
-        }
-        cl.mlf[tid][0] = mx;
-        cl.mlf[tid][1] = bad ? __builtin_nanf("") : L;
-    }
-    __syncthreads();
+        for (int db = 0; db < 8; ++db) o_w[(4 * c4 + i) * kOStride + 16 * db + n16] = w.acc[db][i];
 }
 
-static __device__ __forceinline__ f32x4 combined_o(const float *o_lds, int h, int d0) {
-    f32x4 O = *reinterpret_cast<const f32x4 *>(&o_lds[h * kHeadDim + d0]);
+// The workgroup's state of head h, head dims d0 .. d0+3, from the published
+// states: M = max over the wavefronts, L and O rescaled to M.  wave_stride:
+// floats between consecutive wavefronts' regions.
+static __device__ __forceinline__ void gather_head(const float *o_lds, int wave_stride, const CombineLds &cl, int h,
+                                                   int d0, float &M, float &L, f32x4 &O) {
+    const f32x4 a01 = *reinterpret_cast<const f32x4 *>(&cl.ml[h][0][0]);
+    const f32x4 a23 = *reinterpret_cast<const f32x4 *>(&cl.ml[h][2][0]);
+    const float m[kWavesPerWg] = {a01[0], a01[2], a23[0], a23[2]};
+    const float l[kWavesPerWg] = {a01[1], a01[3], a23[1], a23[3]};
+    M = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+    L = 0.f;
+    O = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int wv = 1; wv < kWavesPerWg; ++wv) O += *reinterpret_cast<const f32x4 *>(&o_lds[(wv * kMaxGroup + h) * kHeadDim + d0]);
-    return O;
+    for (int wv = 0; wv < kWavesPerWg; ++wv) {
+        const float f = m[wv] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[wv] - M);
+        L += l[wv] * f;
+        O += f * *reinterpret_cast<const f32x4 *>(&o_lds[wv * wave_stride + h * kOStride + d0]);
+    }
 }
 
 // Normalised output of four head dims and, from the thread owning d0 == 0, the lse.
@@ -794,13 +790,17 @@ static __device__ __forceinline__ void store_output(const AttnLaunch &a, int64_t
 }
 
 // Writes the workgroup's combined result: the output itself when it covered
-// the whole (layer, sequence, KV head), else a partial in slot `slot`.
-static __device__ __forceinline__ void write_result(const AttnLaunch &a, const float *o_lds, const CombineLds &cl,
-                                                    int G, int tid, int64_t row0, bool whole, uint32_t slot) {
+// the whole (layer, sequence, KV head), else a partial in slot `slot`.  bad:
+// the sum becomes NaN (and so do the outputs).
+static __device__ __forceinline__ void write_result(const AttnLaunch &a, const float *o_lds, int wave_stride,
+                                                    const CombineLds &cl, bool bad, int G, int tid, int64_t row0,
+                                                    bool whole, uint32_t slot) {
     for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        const f32x4 O = combined_o(o_lds, h, d0);
-        const float mx = cl.mlf[h][0], L = cl.mlf[h][1];
+        float mx, L;
+        f32x4 O;
+        gather_head(o_lds, wave_stride, cl, h, d0, mx, L, O);
+        if (bad) L = __builtin_nanf("");
         if (whole) {
             store_output(a, row0 + h, d0, O, mx, L);
         } else {
@@ -888,7 +888,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
                                                           const uint16_t *__restrict__ q, int32_t max_keep,
                                                           int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
                                                           const AttnLaunch a) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
+    __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kOWaveBytes];  // V tiles, then O rows
     __shared__ CombineLds cl;
     __shared__ int s_last;
 
@@ -928,7 +928,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
-    uint8_t *vt = smem + wave * kVtBytesPerWave;
+    uint8_t *vt = smem + wave * kOWaveBytes;  // this wavefront's V tile, later its O rows
 
     WaveAcc w;
     wave_acc_reset(w);
@@ -951,11 +951,12 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
         compute_pass<false>(R, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
     }
 
+    float *o_lds = reinterpret_cast<float *>(smem);  // each wavefront's O rows over its own V tile
+    publish_wave(w, o_lds + wave * (kOWaveBytes / 4), cl, wave, n16, c4);
     const int wg_bad_pos = __syncthreads_or(w.bad_pos);
     const bool bad = wg_bad_pos || bad_count;
-    float *o_lds = reinterpret_cast<float *>(smem);  // [wave][16][128], reuses the V tiles
-    combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
-    write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
+    write_result(a, o_lds, kOWaveBytes / 4, cl, bad, G, tid, row0, a.n_split == 1,
+                 (uint32_t)grp * a.n_split + split);
     if (kSrc == kSrcLayout && split == 0 && g == 0 && layer == 0) write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
@@ -1064,11 +1065,13 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
         }
     }
 
+    float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // each wavefront's O rows in its own stages
+    constexpr int kStageWaveFloats = 2 * kStageBytes / 4;
+    publish_wave(w, o_lds + wave * kStageWaveFloats, cl, wave, n16, c4);
     const int wg_bad_pos = __syncthreads_or(w.bad_pos);
     const bool bad = wg_bad_pos || bad_count;
-    float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // [wave][16][128], reuses the stages
-    combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
-    write_result(a, o_lds, cl, G, tid, row0, a.n_split == 1, (uint32_t)grp * a.n_split + split);
+    write_result(a, o_lds, kStageWaveFloats, cl, bad, G, tid, row0, a.n_split == 1,
+                 (uint32_t)grp * a.n_split + split);
     if (kSrc == kSrcLayout && split == 0 && g == 0 && layer == 0) write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
@@ -1101,7 +1104,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
                                                                  const uint16_t *__restrict__ q, int32_t max_keep,
                                                                  int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
                                                           const AttnLaunch a) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kVtBytesPerWave];
+    __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kOWaveBytes];  // V tiles, then O rows
     __shared__ CombineLds cl;
     __shared__ int s_last;
     __shared__ int32_t s_cnt[kStreamMaxB];      // counts clamped to [0, max_keep]
@@ -1225,7 +1228,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         load_q(qx, q, row_of(x), G, n16, c4);
     };
 
-    uint8_t *vt = smem + wave * kVtBytesPerWave;
+    uint8_t *vt = smem + wave * kOWaveBytes;
     float *o_lds = reinterpret_cast<float *>(smem);
     WaveAcc w;
     wave_acc_reset(w);
@@ -1238,15 +1241,15 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     // The segment of group x in this workgroup ends with unit x.
     auto seg_end = [&](const UnitPos &x) {
         const bool bad_count = (s_bad[x.b >> 5] >> (x.b & 31)) & 1u;
+        publish_wave(w, o_lds + wave * (kOWaveBytes / 4), cl, wave, n16, c4);
         const int wg_bad_pos = __syncthreads_or(w.bad_pos);
         const bool bad = wg_bad_pos || bad_count;
-        combine_waves(w, bad, o_lds, cl, G, tid, wave, n16, c4);
         const int ub = units_of(x.b);
         const bool whole = seg_k0 == 0 && x.k == ub - 1;
         const int64_t s_g = x.layer * U_layer + s_pre[x.b] + (int64_t)x.g * ub;  // group's first unit
         const uint32_t slot = (uint32_t)(2 * p + (u_begin < s_g ? 1 : 0));
         const int64_t row0 = row_of(x);
-        write_result(a, o_lds, cl, G, tid, row0, whole, slot);
+        write_result(a, o_lds, kOWaveBytes / 4, cl, bad, G, tid, row0, whole, slot);
         if (bad && tid == 0)
             raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
         if (!whole) {
