@@ -834,9 +834,66 @@ static __device__ __forceinline__ bool take_ticket(const AttnLaunch &a, int grp,
 // gives the slot of the i-th.  Each thread owns four consecutive head dims of
 // one head and folds the partials in batches whose loads are all in flight
 // together.  Block-wide.
+// Many partials (more than 2 * kMergeBatch): the (max, sum) pairs of every
+// partial and head are staged in LDS first (one load per pair, shared by the
+// threads of a head), so the overall max is known before any O value arrives;
+// the O values then stream through two register batches, the next batch's
+// loads in flight while the current one is accumulated (loads past the last
+// partial re-read it with a zero weight, so every load is unconditional).
+// s_ml: LDS scratch of n * G * 2 floats, free by the time the merge runs.
+template <typename SlotOf>
+static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
+                                               int64_t row0, float *s_ml) {
+    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+    constexpr int kThreads = kWavesPerWg * 64;
+    for (int e = tid; e < n * G; e += kThreads) {
+        const int i = e / G, h = e - i * G;
+        const uint32_t prow = slot_of(i) * G + h;
+        s_ml[2 * e] = load_coherent1(rml, prow * 8);
+        s_ml[2 * e + 1] = load_coherent1(rml, prow * 8 + 4);
+    }
+    __syncthreads();
+    for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
+        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
+        float M = kNegInf;
+        for (int i = 0; i < n; ++i) M = fmaxf(M, s_ml[2 * (i * G + h)]);
+        float L = 0.f;
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
+        auto load_batch = [&](int base, f32x4 (&o)[kMergeBatch]) {
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k)
+                o[k] = load_coherent4(ro, ((slot_of(min(base + k, n - 1)) * G + h) * kHeadDim + d0) * 4);
+        };
+        auto add_batch = [&](int base, const f32x4 (&o)[kMergeBatch]) {
+#pragma unroll
+            for (int k = 0; k < kMergeBatch; ++k) {
+                const int i = base + k;
+                const float m = s_ml[2 * (min(i, n - 1) * G + h)], l = s_ml[2 * (min(i, n - 1) * G + h) + 1];
+                const float f = (i >= n || m == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m - M);
+                L += l * f;
+                O += o[k] * f;
+            }
+        };
+        f32x4 ba[kMergeBatch], bb[kMergeBatch];
+        load_batch(0, ba);
+        for (int base = 0; base < n; base += 2 * kMergeBatch) {
+            load_batch(base + kMergeBatch, bb);
+            add_batch(base, ba);
+            load_batch(base + 2 * kMergeBatch, ba);
+            add_batch(base + kMergeBatch, bb);
+        }
+        store_output(a, row0 + h, d0, O, M, L);
+    }
+}
+
 template <typename SlotOf>
 static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
-                                                      int64_t row0) {
+                                                      int64_t row0, float *s_ml) {
+    if (n > 2 * kMergeBatch) {
+        merge_many(a, n, slot_of, G, tid, row0, s_ml);
+        return;
+    }
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
     for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
@@ -889,6 +946,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
                                                           int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
                                                           const AttnLaunch a) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kOWaveBytes];  // V tiles, then O rows
+    static_assert(kMaxMergeSplits * kMaxGroup * 2 * 4 <= sizeof(smem), "merge scratch fits the tile LDS");
     __shared__ CombineLds cl;
     __shared__ int s_last;
 
@@ -963,7 +1021,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     if (a.n_split == 1) return;
     if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
     const uint32_t pbase = (uint32_t)grp * a.n_split;
-    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0);
+    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0,
+                   reinterpret_cast<float *>(smem));
 }
 
 // ---------------------------------------------------------------------------
@@ -1078,7 +1137,8 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     if (a.n_split == 1) return;
     if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
     const uint32_t pbase = (uint32_t)grp * a.n_split;
-    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0);
+    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0,
+                   reinterpret_cast<float *>(&stages[0][0][0]));
 }
 
 // ---------------------------------------------------------------------------
@@ -1454,7 +1514,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
                     const int64_t pp = first + j;
                     return (uint32_t)(2 * pp + ((pp * U / P) < s_g ? 1 : 0));
                 },
-                G, tid, pend_row0[i]);
+                G, tid, pend_row0[i], reinterpret_cast<float *>(&stages[0][0][0]));
         }
     }
 
