@@ -155,11 +155,14 @@ int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev
 
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
  * (0 = the automatic choice, MURMUR_SPLIT_STREAM, or positions per split).
- * The workspace holds the split partials and a ticket counter per (layer,
- * sequence, kv-head).  It must be zero-filled once
+ * The workspace holds ticket counters (one per (layer, sequence, kv-head)
+ * group that is split, or two per stream workgroup) in a region at its start
+ * whose size depends on ws_bytes alone (4 bytes per KiB, rounded up to 256),
+ * and the split partials after that region.  It must be zero-filled once
  * before its first use (or reset with murmur_decode_attn_workspace_init);
- * every completed call leaves the tickets at zero again.  Calls that share a
- * workspace must not run concurrently. */
+ * every completed call leaves the tickets at zero again.  Calls of any shapes
+ * may share a workspace as long as they pass the same ws_bytes (at least what
+ * this function returns for each of them) and do not run concurrently. */
 int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
                                  int32_t split_len, size_t *bytes);
 

@@ -39,6 +39,8 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
 
+size_t ticket_region(size_t ws_bytes) { return round_up(4 * ((ws_bytes + 1023) / 1024), 256); }
+
 WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
                              int32_t split_len) {
     WorkspacePlan p{};
@@ -46,45 +48,59 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     const int64_t groups = (int64_t)n_layers * B * Hkv;
     const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
     p.groups = groups;
-    p.ticket_bytes = round_up((size_t)groups * sizeof(int32_t), 256);
     const bool stream = split_len == MURMUR_SPLIT_STREAM;
     if (stream) {
-        // Persistent workgroups, each leaving at most two partial segments.
+        // Persistent workgroups, each leaving at most two partial segments; a
+        // group cut between workgroups takes the ticket of its first
+        // contributor's last slot.
         const int64_t wg = groups * units < kStreamWorkgroups ? groups * units : kStreamWorkgroups;
         p.stream_wg = (int32_t)(wg < 1 ? 1 : wg);
         p.split_len = 0;
         p.n_split = 0;
+        p.tickets = 2 * (int64_t)p.stream_wg;
         p.ml_bytes = round_up((size_t)2 * p.stream_wg * G * 2 * sizeof(float), 256);
         p.o_bytes = round_up((size_t)2 * p.stream_wg * G * kHeadDim * sizeof(float), 256);
-        p.total = p.ticket_bytes + p.ml_bytes + p.o_bytes;
+    } else {
+        if (split_len <= 0) {
+            // Few units: one pass per wavefront (the light single-pass kernel,
+            // which several workgroups share a compute unit with), as long as one
+            // merge can combine that many splits.  Otherwise the LDS-staged
+            // kernel, which takes a whole compute unit: as many splits as keep
+            // one dispatch round (kRoundWorkgroups), fewer when there are more
+            // groups than that, at most kMaxAutoSplits.
+            int64_t per;
+            if (groups * units <= kSinglePassMaxUnits && units <= kMaxMergeSplits) {
+                per = 1;
+            } else {
+                int64_t want = kRoundWorkgroups / groups;
+                if (want > kMaxAutoSplits) want = kMaxAutoSplits;
+                if (want > units) want = units;
+                if (want < 1) want = 1;
+                per = (units + want - 1) / want;
+                if (per < 2) per = 2;
+            }
+            split_len = (int32_t)(per * kSplitUnit);
+        }
+        p.split_len = split_len;
+        p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
+        if (p.n_split > 1) {
+            p.tickets = groups;
+            p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
+            p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
+        }
+    }
+    // The smallest size whose ticket region holds the tickets and leaves room
+    // for the partials, with 256 bytes to spare so that any larger size does
+    // too (the region grows by 256 bytes at a time).
+    const size_t part = p.ml_bytes + p.o_bytes;
+    if (part == 0 && p.tickets == 0) {
+        p.total = 256;
         return p;
     }
-    if (split_len <= 0) {
-        // Few units: one pass per wavefront (the light single-pass kernel, which
-        // several workgroups share a compute unit with).  Otherwise the
-        // LDS-staged kernel, which takes a whole compute unit: as many splits
-        // as keep one dispatch round (kRoundWorkgroups), fewer when there are
-        // more groups than that, at most kMaxAutoSplits.
-        int64_t per;
-        if (groups * units <= kSinglePassMaxUnits) {
-            per = 1;
-        } else {
-            int64_t want = kRoundWorkgroups / groups;
-            if (want > kMaxAutoSplits) want = kMaxAutoSplits;
-            if (want > units) want = units;
-            if (want < 1) want = 1;
-            per = (units + want - 1) / want;
-            if (per < 2) per = 2;
-        }
-        split_len = (int32_t)(per * kSplitUnit);
-    }
-    p.split_len = split_len;
-    p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
-    if (p.n_split > 1) {
-        p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
-        p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
-    }
-    p.total = p.ticket_bytes + p.ml_bytes + p.o_bytes;
+    size_t total = round_up(part + 512, 256);
+    if (total < (size_t)p.tickets * 1024) total = round_up((size_t)p.tickets * 1024, 256);
+    while (total < ticket_region(total) + part + 256) total += 256;
+    p.total = total;
     return p;
 }
 
@@ -177,13 +193,17 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     a.out = out_dev;
     a.lse = lse_dev;
     uint8_t *ws = (uint8_t *)ws_dev;
+    // Tickets in the ticket region at the start, partials after it; the split
+    // depends only on ws_bytes (see murmur_decode_attn_workspace).
+    const size_t region = ticket_region(ws_bytes);
     a.ticket = (int32_t *)ws;
     // Partials exist for split schedules of more than one split and for the stream schedule.
     const bool partials = plan.ml_bytes > 0;
-    if (partials != (plan.stream_wg > 0 || plan.n_split > 1))
+    if (partials != (plan.stream_wg > 0 || plan.n_split > 1) || region < (size_t)plan.tickets * 4 ||
+        region + plan.ml_bytes + plan.o_bytes > ws_bytes)
         return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
-    a.part_ml = partials ? (float *)(ws + plan.ticket_bytes) : nullptr;
-    a.part_o = partials ? (float *)(ws + plan.ticket_bytes + plan.ml_bytes) : nullptr;
+    a.part_ml = partials ? (float *)(ws + region) : nullptr;
+    a.part_o = partials ? (float *)(ws + region + plan.ml_bytes) : nullptr;
     a.part_ml_bytes = (uint32_t)plan.ml_bytes;
     a.part_o_bytes = (uint32_t)plan.o_bytes;
     a.max_len = kv->max_len;

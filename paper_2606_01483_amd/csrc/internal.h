@@ -47,7 +47,7 @@ struct AttnLaunch {
     const int32_t *idx;
     void *out;
     float *lse;
-    int32_t *ticket;   // [groups]
+    int32_t *ticket;   // split schedule: [groups]; stream schedule: [2 * workgroups]
     float *part_ml;    // [groups][n_split][G][2]  (running max in log2 units, sum)
     float *part_o;     // [groups][n_split][G][128]
     uint32_t part_ml_bytes, part_o_bytes;  // extents of the two partial arrays (< 2^31)
@@ -62,8 +62,15 @@ struct WorkspacePlan {
     int32_t n_split;
     int32_t stream_wg;  // > 0: stream schedule
     int64_t groups;
-    size_t ticket_bytes, ml_bytes, o_bytes, total;
+    int64_t tickets;  // ticket counters the launch uses
+    size_t ml_bytes, o_bytes, total;
 };
+
+// Bytes at the start of a workspace of ws_bytes that hold the tickets (the
+// partials follow).  Depends on the size alone, so calls of different shapes
+// that share a workspace place their tickets alike, and never where another
+// call left partials.
+size_t ticket_region(size_t ws_bytes);
 
 // Split choice and workspace layout; deterministic in its arguments.
 WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,

@@ -1387,7 +1387,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     // Tickets of the cut groups, taken after the stream.
     int n_pending = 0;
     int64_t pend_sg[2] = {0, 0}, pend_row0[2] = {0, 0};
-    int pend_grp[2] = {0, 0}, pend_ub[2] = {0, 0};
+    int pend_ub[2] = {0, 0};
 
     // The segment of group x in this workgroup ends with unit x, computed from stage `stg`.
     auto seg_end = [&](const UnitPos &x, int stg) {
@@ -1443,7 +1443,6 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         if (!whole) {
             pend_sg[n_pending] = s_g;
             pend_row0[n_pending] = row0;
-            pend_grp[n_pending] = (int)(((int64_t)x.layer * B + x.b) * Hkv + x.g);
             pend_ub[n_pending] = ub;
             ++n_pending;
         }
@@ -1507,7 +1506,9 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     for (int i = 0; i < n_pending; ++i) {
         const int64_t s_g = pend_sg[i];
         const int64_t first = owner(s_g), last = owner(s_g + pend_ub[i] - 1);
-        if (take_ticket(a, pend_grp[i], (int)(last - first + 1), tid, s_last)) {
+        // The group's ticket is that of its first contributor's last segment
+        // (slot 2 * first + 1): one per cut group, at most 2P tickets.
+        if (take_ticket(a, (int)(2 * first + 1), (int)(last - first + 1), tid, s_last)) {
             merge_partials(
                 a, (int)(last - first + 1),
                 [&](int j) {

@@ -139,28 +139,58 @@ def test_evict_compact_rejects():
     assert lib.murmur_evict_compact(FAKE, FAKE, 0, 12, FAKE + 2, 10, FAKE, None, 0) == M.MURMUR_EINVAL
 
 
+def rnd(x):
+    return (x + 255) // 256 * 256
+
+
+def ticket_region(ws_bytes):
+    """Bytes at the start of a workspace that hold the tickets: 4 per KiB of workspace, rounded up."""
+    return rnd(4 * -(-ws_bytes // 1024))
+
+
+def split_partials(groups, n_split, G):
+    # (m, l) and 128 outputs per (group, split, head)
+    return rnd(groups * n_split * G * 2 * 4) + rnd(groups * n_split * G * 128 * 4)
+
+
+def check_plan(ws, partials, tickets):
+    """The workspace holds its ticket region and the partials, with room to spare, and so does any larger one."""
+    for w in (ws, ws + 1, ws + 255, ws + 256, ws + 65536, ws + 65536 * 3 + 77, 2 * ws):
+        assert ticket_region(w) >= 4 * tickets and ticket_region(w) + partials <= w, w
+    assert ws - 256 < max(ticket_region(ws) + partials + 256, rnd(tickets * 1024)) + 256  # and it is the smallest
+
+
 def test_workspace_sizing():
-    def rnd(x):
-        return (x + 255) // 256 * 256
     ws = M.murmur_decode_attn_workspace(1, 12, 28, 4, 850)
-    # 336 units of 128 positions: split schedule, 48 tickets, 7 splits of 128 positions:
-    # 48*7*7 partials of (m, l) and of 128 outputs
-    assert ws == 256 + rnd(48 * 7 * 7 * 2 * 4) + rnd(48 * 7 * 7 * 128 * 4)
-    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 100) == 256  # one split: tickets only
+    # 336 units of 128 positions: split schedule, 48 groups, 7 splits of 128 positions
+    check_plan(ws, split_partials(48, 7, 7), 48)
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 100) == 256  # one split: nothing to merge
     assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 1024) == 256
     # an explicit split length on a long list
-    n_split = -(-35160 // 640)
-    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, 640) == \
-        256 + rnd(4 * n_split * 7 * 2 * 4) + rnd(4 * n_split * 7 * 128 * 4)
-    # automatic split of 1100 units over 4 groups: 64 splits of 5 units
-    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160) == \
-        256 + rnd(4 * 55 * 7 * 2 * 4) + rnd(4 * 55 * 7 * 128 * 4)
-    # the stream schedule: 256 workgroups with two partial slots each
-    stream = 256 + rnd(2 * 256 * 7 * 2 * 4) + rnd(2 * 256 * 7 * 128 * 4)
-    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, M.MURMUR_SPLIT_STREAM) == stream
+    ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, 640)
+    check_plan(ws, split_partials(4, -(-35160 // 640), 7), 4)
+    # automatic split of 1100 units over 4 groups: 55 splits of 5 units
+    ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160)
+    check_plan(ws, split_partials(4, 55, 7), 4)
+    assert ws < split_partials(4, 56, 7)
+    # one group of 300 units: too many one-pass splits to merge, so 60 splits of 5 units
+    ws = M.murmur_decode_attn_workspace(1, 1, 7, 1, 300 * 128)
+    check_plan(ws, split_partials(1, 60, 7), 1)
+    assert ws < split_partials(1, 61, 7)
+    # many groups of two splits
+    ws = M.murmur_decode_attn_workspace(28, 256, 4, 4, 512, 256)
+    check_plan(ws, split_partials(28 * 256 * 4, 2, 1), 28 * 256 * 4)
+    # the stream schedule with one head per group: the tickets set the size
+    ws = M.murmur_decode_attn_workspace(1, 12, 4, 4, 35160, M.MURMUR_SPLIT_STREAM)
+    check_plan(ws, rnd(2 * 256 * 1 * 2 * 4) + rnd(2 * 256 * 1 * 128 * 4), 512)
+    assert ws == rnd(512 * 1024)
+    # the stream schedule: 256 workgroups with two partial slots and two tickets each
+    ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, M.MURMUR_SPLIT_STREAM)
+    stream = rnd(2 * 256 * 7 * 2 * 4) + rnd(2 * 256 * 7 * 128 * 4)
+    check_plan(ws, stream, 512)
     # forced stream on a tiny problem: as many workgroups as units (4 groups x 2 units)
-    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 192, M.MURMUR_SPLIT_STREAM) == \
-        256 + rnd(2 * 8 * 7 * 2 * 4) + rnd(2 * 8 * 7 * 128 * 4)
+    ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 192, M.MURMUR_SPLIT_STREAM)
+    check_plan(ws, rnd(2 * 8 * 7 * 2 * 4) + rnd(2 * 8 * 7 * 128 * 4), 16)
     with pytest.raises(M.MurmurError):
         M.murmur_decode_attn_workspace(1, 12, 28, 5, 850)
     with pytest.raises(M.MurmurError):
@@ -168,6 +198,16 @@ def test_workspace_sizing():
     with pytest.raises(M.MurmurError) as e:
         M.murmur_decode_attn_workspace(1, 300, 28, 4, 850, M.MURMUR_SPLIT_STREAM)
     assert e.value.code == M.MURMUR_EUNSUPPORTED
+
+
+def test_decode_attn_accepts_any_larger_workspace():
+    """Host validation (the workspace plan included) passes for the exact size and for larger ones; with no
+    GPU the launch itself then fails with MURMUR_EHIP."""
+    for split_len in (0, 256, M.MURMUR_SPLIT_STREAM):
+        ws = M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, split_len)
+        for w in (ws, ws + 1, ws + 65536 + 13, 4 * ws):
+            assert call_attn(attn_args(split_len=split_len, ws_bytes=w)) == M.MURMUR_EHIP, (split_len, w)
+        assert call_attn(attn_args(split_len=split_len, ws_bytes=ws - 1)) == M.MURMUR_ENOSPACE
 
 
 def test_workspace_init_and_device_error_reject_null():
