@@ -187,9 +187,10 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  *               ranges_dev);
  *   D:          head_dim, must be 128; Hq/Hkv must be in [1, 16];
  *   scale:      logit scale (1/sqrt(D) for unscaled queries), finite;
- *   split_len:  the work schedule.  A positive multiple of 128: each (layer,
+ *   split_len:  the work schedule.  A positive multiple of 32: each (layer,
  *               sequence, KV head) is cut into splits of that many retained
- *               positions, one workgroup each, merged by log-sum-exp.
+ *               positions, one workgroup each (its four wavefronts take
+ *               passes of 32 positions in turn), merged by log-sum-exp.
  *               MURMUR_SPLIT_STREAM: persistent workgroups, one per compute
  *               unit, stream balanced runs of 128-position units across all
  *               groups; only groups cut by a run boundary are merged (at most

@@ -152,9 +152,9 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     if (out_dtype != MURMUR_DTYPE_BF16 && out_dtype != MURMUR_DTYPE_F32)
         return fail(MURMUR_EINVAL, "out_dtype must be MURMUR_DTYPE_BF16 or MURMUR_DTYPE_F32 (got %d)", out_dtype);
     if (!isfinite(scale)) return fail(MURMUR_EINVAL, "scale must be finite");
-    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kSplitUnit != 0))
+    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kWaveTile != 0))
         return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
-                    kSplitUnit, split_len);
+                    kWaveTile, split_len);
     if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
         return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
     const int64_t strides[4] = {kv->stride_layer, kv->stride_b, kv->stride_h, kv->stride_pos};
@@ -262,9 +262,9 @@ MURMUR_EXPORT int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int3
     if (n_layers < 1 || B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1)
         return fail(MURMUR_EINVAL, "n_layers, B, Hq, Hkv and max_keep must be >= 1");
     if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
-    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kSplitUnit != 0))
+    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kWaveTile != 0))
         return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
-                    kSplitUnit, split_len);
+                    kWaveTile, split_len);
     if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
         return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
     *bytes = plan_workspace(n_layers, B, Hq, Hkv, max_keep, split_len).total;

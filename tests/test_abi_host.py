@@ -194,7 +194,10 @@ def test_workspace_sizing():
     with pytest.raises(M.MurmurError):
         M.murmur_decode_attn_workspace(1, 12, 28, 5, 850)
     with pytest.raises(M.MurmurError):
-        M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 64)
+        M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 48)  # not a multiple of 32
+    # splits of 64 and of 192 positions (multiples of one wavefront pass)
+    check_plan(M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 64), split_partials(48, 14, 7), 48)
+    check_plan(M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 192), split_partials(48, 5, 7), 48)
     with pytest.raises(M.MurmurError) as e:
         M.murmur_decode_attn_workspace(1, 300, 28, 4, 850, M.MURMUR_SPLIT_STREAM)
     assert e.value.code == M.MURMUR_EUNSUPPORTED

@@ -200,9 +200,15 @@ def test_split_count_invariance():
     wl = workload("c3")
     ref, ref_lse = oracle_step(wl, 0)
     outs = []
-    for split_len in (0, 128, 256, 512, 1024):
+    for split_len in (0, 32, 96, 128, 160, 192, 256, 512, 1024):
         announce(f"attn c3 split_len {split_len}")
         db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, split_len=split_len, steps=[0])
+        y, l = run_gpu(db, 0)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+        outs.append(y)
+    for split_len in (96, 160, 192):  # index lists too, splits of a whole and a partial pass per wavefront
+        announce(f"attn c3 split_len {split_len} index list")
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, split_len=split_len, steps=[0], use_ranges=False)
         y, l = run_gpu(db, 0)
         assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
         outs.append(y)
