@@ -62,15 +62,22 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
         p.o_bytes = round_up((size_t)2 * p.stream_wg * G * kHeadDim * sizeof(float), 256);
     } else {
         if (split_len <= 0) {
-            // Few units: one pass per wavefront (the light single-pass kernel,
-            // which several workgroups share a compute unit with), as long as one
-            // merge can combine that many splits.  Otherwise the LDS-staged
+            // Few units (and no more splits than one merge combines): splits of
+            // one or two passes per wavefront from registers, as many as fill one
+            // dispatch round (kRoundWorkgroups) with equal shares, so no compute
+            // unit holds twice the work of another.  Otherwise the LDS-staged
             // kernel, which takes a whole compute unit: as many splits as keep
-            // one dispatch round (kRoundWorkgroups), fewer when there are more
-            // groups than that, at most kMaxAutoSplits.
+            // one dispatch round, fewer when there are more groups than that, at
+            // most kMaxAutoSplits.
             int64_t per;
             if (groups * units <= kSinglePassMaxUnits && units <= kMaxMergeSplits) {
-                per = 1;
+                int64_t n = kRoundWorkgroups / groups;
+                if (n < 1) n = 1;
+                int64_t len = (((int64_t)max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
+                if (len < kSplitUnit) len = kSplitUnit;
+                if (len > 2 * kSplitUnit) len = 2 * kSplitUnit;
+                split_len = (int32_t)len;
+                per = 0;
             } else {
                 int64_t want = kRoundWorkgroups / groups;
                 if (want > kMaxAutoSplits) want = kMaxAutoSplits;
@@ -79,7 +86,7 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
                 per = (units + want - 1) / want;
                 if (per < 2) per = 2;
             }
-            split_len = (int32_t)(per * kSplitUnit);
+            if (per > 0) split_len = (int32_t)(per * kSplitUnit);
         }
         p.split_len = split_len;
         p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);

@@ -930,15 +930,17 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
 }
 
 // ---------------------------------------------------------------------------
-// decode_attn, split schedule, splits of one workgroup pass (128 retained
-// positions): one workgroup per (split, layer and KV head, sequence), each of its
-// four wavefronts one pass of 32 positions, the loads of the pass issued
-// straight from registers.  kSrc: where the retained set comes from.  The last workgroup of each group merges the splits.  The
-// leading scalar arguments are the ones the first memory accesses need; the
-// build preloads them into SGPRs so no kernel-argument load precedes the
-// range-table load.
+// decode_attn, split schedule, splits of up to kPasses workgroup passes (128
+// retained positions each): one workgroup per (split, layer and KV head,
+// sequence); wavefront w takes the passes of 32 positions at w*32 and, with
+// two passes, w*32 + 128, all their loads issued up front into registers, so
+// the compute unit's whole share is in flight at once.  kSrc: where the
+// retained set comes from.  The last workgroup of each group merges the
+// splits.  The leading scalar arguments are the ones the first memory
+// accesses need; the build preloads them into SGPRs so no kernel-argument load
+// precedes the range-table load.
 // ---------------------------------------------------------------------------
-template <int kSrc>
+template <int kSrc, int kPasses>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ src0,
                                                           const int32_t *__restrict__ src1,
                                                           const int32_t *__restrict__ idx,
@@ -956,7 +958,6 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
 
-    // Grid: x = split, y = KV head, z = layer * B + sequence.
     // Grid: x = split, y = layer * Hkv + KV head, z = sequence.  The
     // sequence's retained-set description is loaded first: the first K/V loads
     // wait for it and for nothing else.
@@ -995,18 +996,27 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
+    // Ranks past the split's end load row 0 (the same row in every lane).
     auto positions = [&](const IdxRegs &I, int r0, PassPos &pp) {
-        if (kSrc != kSrcIndex) pass_pos_ranges(tab, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
-        else pass_pos_index(I, r0, cnt, a.max_len, n16, c4, pp, w.bad_pos);
+        if (kSrc != kSrcIndex) pass_pos_ranges(tab, r0, r_end, a.max_len, n16, c4, pp, w.bad_pos);
+        else pass_pos_index(I, r0, r_end, a.max_len, n16, c4, pp, w.bad_pos);
     };
     if (r < r_end) {
-        PassRegs R;
-        IdxRegs I;
+        PassRegs R[kPasses];
+        IdxRegs I[kPasses];
         PassPos pp;
-        if (kSrc == kSrcIndex) load_idx(I, irow, r, n16, c4);
-        positions(I, r, pp);
-        issue_kv(R, kbase, vbase, a.s_pos, pp, n16, c4);
-        compute_pass<false>(R, qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
+        if (kSrc == kSrcIndex)
+#pragma unroll
+            for (int p = 0; p < kPasses; ++p) load_idx(I[p], irow, r + p * kSplitUnit, n16, c4);
+#pragma unroll
+        for (int p = 0; p < kPasses; ++p) {
+            positions(I[p], r + p * kSplitUnit, pp);
+            issue_kv(R[p], kbase, vbase, a.s_pos, pp, n16, c4);
+        }
+        compute_pass<false>(R[0], qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
+        if (kPasses > 1 && r + kSplitUnit < r_end)
+            compute_pass<true>(R[kPasses - 1], qf, min(kWaveTile, r_end - r - kSplitUnit), a.scale_log2, vt, w, n16,
+                               c4);
     }
 
     float *o_lds = reinterpret_cast<float *>(smem);  // each wavefront's O rows over its own V tile
@@ -1552,13 +1562,17 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
         return;
     }
     const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
-    // Splits of more than one pass stage their passes in LDS.
-    if (a.split_len > kSplitUnit)
+    // Splits of up to two passes run from registers; longer splits stage their
+    // passes in LDS.
+    if (a.split_len > 2 * kSplitUnit)
         hipLaunchKernelGGL(decode_attn_lds_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
                            a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
+    else if (a.split_len > kSplitUnit)
+        hipLaunchKernelGGL((decode_attn_kernel<kSrc, 2>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
+                           a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
     else
-        hipLaunchKernelGGL(decode_attn_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1, a.idx,
-                           a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
+        hipLaunchKernelGGL((decode_attn_kernel<kSrc, 1>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
+                           a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
 }
 
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {

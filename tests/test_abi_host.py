@@ -162,8 +162,11 @@ def check_plan(ws, partials, tickets):
 
 def test_workspace_sizing():
     ws = M.murmur_decode_attn_workspace(1, 12, 28, 4, 850)
-    # 336 units of 128 positions: split schedule, 48 groups, 7 splits of 128 positions
-    check_plan(ws, split_partials(48, 7, 7), 48)
+    # 48 groups of 850 positions: 5 splits of 192 positions fill one round of 256 workgroups (240)
+    check_plan(ws, split_partials(48, 5, 7), 48)
+    assert ws < split_partials(48, 6, 7)
+    # 4 groups of 2592: splits of at least one full pass (128 positions), 21 of them
+    check_plan(M.murmur_decode_attn_workspace(1, 1, 28, 4, 2592), split_partials(4, 21, 7), 4)
     assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 100) == 256  # one split: nothing to merge
     assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 1024) == 256
     # an explicit split length on a long list
