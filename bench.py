@@ -302,7 +302,7 @@ def main() -> int:
     ap.add_argument("--summarize-trace", metavar="DIR", help="print the kernel table of a rocprofv3 --stats run")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="print the traffic summary from four rocprofv3 --pmc runs")
-    ap.add_argument("--pmc-kernel", default="decode_attn_kernel<1>", help="kernel name part for --summarize-pmc")
+    ap.add_argument("--pmc-kernel", default="decode_attn_kernel<1, 2>", help="kernel name part for --summarize-pmc")
     ap.add_argument("--copy-mib", type=int, default=256, help="copy size of the --copy-reference runs")
     ap.add_argument("--alg-bytes", type=int, default=0, help="algorithmic bytes per launch (bench JSON)")
     args = ap.parse_args()
