@@ -1037,22 +1037,29 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
 
 // ---------------------------------------------------------------------------
 // decode_attn, split schedule with LDS-staged passes, for splits of more than
-// one workgroup pass: grid and split layout as decode_attn_kernel; each
-// wavefront double-buffers its passes in two LDS stages (K and V, 16 KiB per
-// stage), issuing the next pass's direct-to-LDS loads before computing the
-// current one.  Index lists are staged too, one pass ahead of the rows.
+// two workgroup passes: grid and split layout as decode_attn_kernel.  With
+// kStages = 2 each wavefront double-buffers its passes in two LDS stages (K
+// and V, 16 KiB per stage), issuing the next pass's direct-to-LDS loads before
+// computing the current one; the workgroup takes 128 KiB of LDS, a compute
+// unit to itself.  With kStages = 1 (grids of more than one dispatch round)
+// each wavefront loads a pass, waits and computes it: 64 KiB, so two
+// workgroups share a compute unit and one's prologue, epilogue and dispatch
+// gap overlap the other's loads.  Index lists are staged too, one pass ahead
+// of the rows.
 // ---------------------------------------------------------------------------
-template <int kSrc>
+template <int kSrc, int kStages>
 __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__restrict__ src0,
                                                               const int32_t *__restrict__ src1,
                                                               const int32_t *__restrict__ idx,
                                                               const uint16_t *__restrict__ q, int32_t max_keep,
                                                               int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
                                                           const AttnLaunch a) {
-    __shared__ __attribute__((aligned(16))) uint8_t stages[kWavesPerWg][2][kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t stages[kWavesPerWg][kStages][kStageBytes];
     __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kSrc != kSrcIndex ? 1 : kWavesPerWg][2][kIdxSlotBytes];
     __shared__ CombineLds cl;
     __shared__ int s_last;
+    static_assert(kMaxMergeSplits * kMaxGroup * 2 * 4 <= sizeof(stages) && kOWaveBytes <= kStages * kStageBytes,
+                  "merge scratch and published rows fit the stages");
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1089,7 +1096,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
-    uint8_t *st[2] = {&stages[wave][0][0], &stages[wave][1][0]};
+    uint8_t *st[2] = {&stages[wave][0][0], &stages[wave][kStages - 1][0]};
     uint8_t *ring[2] = {&idx_ring[kSrc != kSrcIndex ? 0 : wave][0][0], &idx_ring[kSrc != kSrcIndex ? 0 : wave][1][0]};
 
     WaveAcc w;
@@ -1099,7 +1106,26 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
-    if (r < r_end) {
+    if (r < r_end && kStages == 1) {
+        int32_t pos[8];
+        if (kSrc == kSrcIndex) {
+            dma_idx(ring[0], irow, r, lane);
+            dma_idx(ring[1], irow, r + kSplitUnit, lane);
+        }
+        for (int k = 0;; r += kSplitUnit, ++k) {
+            if (kSrc != kSrcIndex) {
+                dma_pos_ranges(tab, r, r_end, a.max_len, c4, pos, w.bad_pos);
+            } else {
+                wait_vm<1>();  // this pass's entries; the next pass's may stay in flight
+                dma_pos_index(ring[k & 1], r, r_end, a.max_len, c4, pos, w.bad_pos);
+            }
+            dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane);
+            wait_vm<0>();
+            compute_pass_lds<true>(st[0], qf, min(kWaveTile, r_end - r), a.scale_log2, w, n16, c4);
+            if (r + kSplitUnit >= r_end) break;
+            if (kSrc == kSrcIndex) dma_idx(ring[k & 1], irow, r + 2 * kSplitUnit, lane);  // its slot is read
+        }
+    } else if (r < r_end) {
         int32_t pos[8];
         if (kSrc != kSrcIndex) {
             dma_pos_ranges(tab, r, r_end, a.max_len, c4, pos, w.bad_pos);
@@ -1135,7 +1161,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     }
 
     float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // each wavefront's O rows in its own stages
-    constexpr int kStageWaveFloats = 2 * kStageBytes / 4;
+    constexpr int kStageWaveFloats = kStages * kStageBytes / 4;
     publish_wave(w, o_lds + wave * kStageWaveFloats, cl, wave, n16, c4);
     const int wg_bad_pos = __syncthreads_or(w.bad_pos);
     const bool bad = wg_bad_pos || bad_count;
@@ -1563,9 +1589,14 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     }
     const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
     // Splits of up to two passes run from registers; longer splits stage their
-    // passes in LDS.
-    if (a.split_len > 2 * kSplitUnit)
-        hipLaunchKernelGGL(decode_attn_lds_kernel<kSrc>, grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
+    // passes in LDS, double-buffered within one dispatch round, else one stage
+    // per wavefront and two workgroups per compute unit.
+    const bool one_round = (int64_t)a.n_split * a.NL * a.Hkv * a.B <= kRoundWorkgroups;
+    if (a.split_len > 2 * kSplitUnit && one_round)
+        hipLaunchKernelGGL((decode_attn_lds_kernel<kSrc, 2>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
+                           a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
+    else if (a.split_len > 2 * kSplitUnit)
+        hipLaunchKernelGGL((decode_attn_lds_kernel<kSrc, 1>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
                            a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
     else if (a.split_len > kSplitUnit)
         hipLaunchKernelGGL((decode_attn_kernel<kSrc, 2>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,

@@ -264,6 +264,29 @@ def test_workspace_shared_across_shapes():
         assert tickets_clear(ws, ws_bytes), (wl.name, split_len, i)
 
 
+def test_multi_round_grid_both_modes():
+    """4 layers x 24 sequences x 4 KV heads of 500-900 retained positions: 384 whole-group workgroups, more than
+    one dispatch round, so the LDS-staged kernel runs with one stage per wavefront (two workgroups per compute
+    unit); index lists and range tables, fp32 and bf16 outputs."""
+    rng = np.random.default_rng(77)
+    B = 24
+    seg0 = np.stack([np.full(B, 32), rng.integers(1800, 2250, B), np.zeros(B, dtype=np.int64),
+                     rng.integers(300, 1200, B)], axis=1).astype(np.int32)
+    pol = np.stack([seg0[:, 1] // 4, np.full(B, 512), np.zeros(B, dtype=np.int64), np.full(B, 256),
+                    np.zeros(B, dtype=np.int64)], axis=1).astype(np.int32)
+    wl = W.build("rounds", 43, 4, seg0, pol, steps=2, planted=True)
+    ref, ref_lse = oracle_step(wl, 1)
+    for use_ranges in (True, False):
+        announce(f"attn 384 whole groups, one-stage LDS kernel, ranges={use_ranges}")
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[1], use_ranges=use_ranges)
+        assert db.split_len == 0
+        y, l = run_gpu(db, 0)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL, use_ranges
+        db16 = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_BF16, steps=[1], use_ranges=use_ranges)
+        y16, _ = run_gpu(db16, 0)
+        assert bf16_excess(y16, ref) <= REL_TOL, use_ranges
+
+
 @pytest.mark.parametrize("hq,hkv", [(28, 4), (4, 4), (16, 1), (12, 3)])
 def test_attn_edge_shapes(hq, hkv):
     announce(f"attn edge shapes hq={hq} hkv={hkv}")
