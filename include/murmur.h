@@ -64,6 +64,7 @@ enum {
     MURMUR_DEVERR_POLICY = 2,    /* evict_compact: invalid layout or policy for a sequence */
     MURMUR_DEVERR_POSITION = 4,  /* decode_attn: retained position outside [0, max_len) */
     MURMUR_DEVERR_COUNT = 8,     /* decode_attn: count outside [1, max_keep] */
+    MURMUR_DEVERR_CAPACITY = 16, /* decode_step_ring: the output ring cannot hold the retained outputs */
 };
 
 /* One sequence (audio chunk) of the batch, Section 3.2's layout
@@ -117,7 +118,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 2
+#define MURMUR_ABI_VERSION 3
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -229,6 +230,63 @@ int murmur_decode_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, 
                        int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
                        float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
                        void *ws_dev, size_t ws_bytes, murmur_stream_t stream);
+
+/* Physical eviction storage (Section 3.2: evicted entries leave the cache).
+ * The output region of each sequence's cache holds its out_sink output sinks
+ * at rows o0 .. o0+out_sink-1 (o0 = prompt_pre + speech_len + prompt_mid),
+ * then a ring of out_capacity rows: 0-based output token i >= out_sink lives
+ * at row o0 + out_sink + (i - out_sink) mod out_capacity.  A row is reused
+ * only by a token that enters Algorithm 1's window after the row's previous
+ * token has left it, so a cache of prompt_pre + speech_len + prompt_mid +
+ * out_sink + out_capacity rows per sequence (instead of one row per generated
+ * token) serves the whole decode.  Requirements per sequence: out_capacity
+ * >= out_window when output eviction is on; with it off (out_window = -1),
+ * out_len - out_sink <= out_capacity.  Prompt and speech rows are unchanged.
+ *   out_capacity: ring rows (>= 1), the same for every sequence;
+ *   k_new, v_new: device bf16 [n_layers][B][Hkv][D], contiguous, 16-byte
+ *                 aligned: the current token's keys and values (the token
+ *                 whose output index is out_len - 1). */
+typedef struct murmur_ring {
+    int32_t out_capacity;
+    const void *k_new;
+    const void *v_new;
+} murmur_ring;
+
+/* Host-only (no GPU): where the retained set of each sequence lies in ring
+ * storage.  ranges[b][6][2] (nullable): six (start, length) row pieces that
+ * hold exactly the tokens of murmur_evict_compact's pieces (same count):
+ * prompt_pre, speech sinks, speech window, prompt_mid, then the output part
+ * in at most two pieces -- piece 4 holds the output sinks and, when the
+ * window wraps around the ring, its newer part (ring rows from 0), piece 5
+ * the rest of the window.  cur_row[b] (nullable): the row of the current
+ * token.  Errors: MURMUR_EINVAL as murmur_retained_count_host, or when the
+ * ring cannot hold the retained outputs (see murmur_ring). */
+int murmur_ring_layout_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
+                            int32_t out_capacity, int32_t *ranges, int32_t *cur_row);
+
+/* One decode step on ring storage, in one launch: the retained set in
+ * storage rows (as murmur_ring_layout_host), the attention of the current
+ * token over it (Equation 1, as murmur_decode_step) and the append of the
+ * current token's K/V into its ring row.  The attention reads the current
+ * token from k_new/v_new, and no retained row is the one being written (it
+ * held a token that has just left the window), so the append and the
+ * attention do not race.  kv describes the ring storage (max_len >= the
+ * rows above); the call writes row cur_row of every (layer, sequence, KV
+ * head) of kv->k and kv->v, which must therefore be writable.
+ *   idx_dev, count_dev, ranges_dev: nullable outputs as murmur_decode_step,
+ *               in storage rows (idx in piece order, not ascending);
+ *   split_len:  as murmur_decode_attn, except MURMUR_SPLIT_STREAM
+ *               (MURMUR_EUNSUPPORTED);
+ *   every other argument: as murmur_decode_step.
+ * Device errors: those of murmur_decode_step, and MURMUR_DEVERR_CAPACITY for
+ * a sequence whose ring cannot hold its retained outputs (count 0, NaN
+ * outputs, nothing appended). */
+int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                            const murmur_ring *ring, const void *q_dev, const murmur_kv *kv, int32_t *idx_dev,
+                            int32_t *count_dev, int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq,
+                            int32_t Hkv, int32_t D, float scale, int32_t split_len, void *out_dev,
+                            int32_t out_dtype, float *lse_dev, void *ws_dev, size_t ws_bytes,
+                            murmur_stream_t stream);
 
 /* Synchronises `stream`, returns the device error word of the current device
  * in *code (0 = none) and clears it.  Not for use inside a captured graph. */

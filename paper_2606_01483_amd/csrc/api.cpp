@@ -336,6 +336,76 @@ MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_pol
     return ok();
 }
 
+MURMUR_EXPORT int murmur_ring_layout_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq,
+                                          int32_t B, int32_t out_capacity, int32_t *ranges, int32_t *cur_row) {
+    if (!seg || !pol) return fail(MURMUR_EINVAL, "seg and pol must not be NULL");
+    if (B < 1) return fail(MURMUR_EINVAL, "B must be >= 1 (got %d)", B);
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (out_capacity < 1) return fail(MURMUR_EINVAL, "out_capacity must be >= 1 (got %d)", out_capacity);
+    for (int32_t b = 0; b < B; ++b) {
+        const murmur_seg &s = seg[b];
+        const murmur_policy &p = pol[pol_per_seq ? b : 0];
+        Pieces pc;
+        int32_t cur = 0;
+        const int rc = ring_pieces(s.prompt_pre, s.speech_len, s.prompt_mid, s.out_len, p.speech_window,
+                                   p.speech_delay, p.speech_sink, p.out_window, p.out_sink, out_capacity, &pc, &cur);
+        if (rc == -2)
+            return fail(MURMUR_EINVAL, "sequence %d: a ring of %d rows cannot hold the retained outputs (out_len %d, "
+                        "out_window %d, out_sink %d)", b, out_capacity, s.out_len, p.out_window, p.out_sink);
+        if (rc != 0)
+            return fail(MURMUR_EINVAL,
+                        "sequence %d: invalid layout or policy (seg %d/%d/%d/%d, policy %d/%d/%d/%d/%d)", b,
+                        s.prompt_pre, s.speech_len, s.prompt_mid, s.out_len, p.speech_window, p.speech_delay,
+                        p.speech_sink, p.out_window, p.out_sink);
+        if (ranges)
+            for (int k = 0; k < kPieces; ++k) {
+                ranges[(int64_t)b * 2 * kPieces + 2 * k] = pc.start[k];
+                ranges[(int64_t)b * 2 * kPieces + 2 * k + 1] = pc.len[k];
+            }
+        if (cur_row) cur_row[b] = cur;
+    }
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                                          const murmur_ring *ring, const void *q_dev, const murmur_kv *kv,
+                                          int32_t *idx_dev, int32_t *count_dev, int32_t *ranges_dev, int32_t max_keep,
+                                          int32_t B, int32_t Hq, int32_t Hkv, int32_t D, float scale,
+                                          int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                                          void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
+    if (!seg_dev || !pol_dev || !ring) return fail(MURMUR_EINVAL, "seg_dev, pol_dev and ring must not be NULL");
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (!ring->k_new || !ring->v_new) return fail(MURMUR_EINVAL, "ring->k_new and ring->v_new must not be NULL");
+    if (!aligned(ring->k_new, 16) || !aligned(ring->v_new, 16))
+        return fail(MURMUR_EINVAL, "ring->k_new and ring->v_new must be 16-byte aligned");
+    if (ring->out_capacity < 1)
+        return fail(MURMUR_EINVAL, "ring->out_capacity must be >= 1 (got %d)", ring->out_capacity);
+    if (split_len == MURMUR_SPLIT_STREAM)
+        return fail(MURMUR_EUNSUPPORTED, "ring storage runs on the split schedules (split_len 0 or a multiple of %d)",
+                    kWaveTile);
+    if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
+        !aligned(ranges_dev, 4))
+        return fail(MURMUR_EINVAL, "seg/pol/idx/count/ranges pointers must be 4-byte aligned");
+    if ((int64_t)B * max_keep > ((int64_t)1 << 40)) return fail(MURMUR_EINVAL, "B * max_keep too large");
+    AttnLaunch a;
+    const int rc = prepare_attn(q_dev, kv, max_keep, B, Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev,
+                                ws_dev, ws_bytes, a);
+    if (rc != MURMUR_OK) return rc;
+    a.src0 = reinterpret_cast<const int32_t *>(seg_dev);
+    a.src1 = reinterpret_cast<const int32_t *>(pol_dev);
+    a.pol_per_seq = pol_per_seq;
+    a.src_mode = kSrcRing;
+    a.idx_out = idx_dev;
+    a.count_out = count_dev;
+    a.ranges_out = ranges_dev;
+    a.ring_cap = ring->out_capacity;
+    a.k_new = (const uint16_t *)ring->k_new;
+    a.v_new = (const uint16_t *)ring->v_new;
+    const int e = launch_decode_attn(a, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "decode_step_ring launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
 MURMUR_EXPORT int murmur_device_error(murmur_stream_t stream, int32_t *code) {
     if (!code) return fail(MURMUR_EINVAL, "code must not be NULL");
     const int e = read_and_clear_device_error(stream, code);

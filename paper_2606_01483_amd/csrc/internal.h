@@ -30,16 +30,21 @@ constexpr int kMergeBatch = 8;  // splits whose partials one merging thread load
 
 // Launch description of one decode_attn call, fully validated by the caller.
 // Where the attention takes the retained sets from (see AttnLaunch::src0/src1).
-enum SrcMode : int32_t { kSrcIndex = 0, kSrcRanges = 1, kSrcLayout = 2 };
+enum SrcMode : int32_t { kSrcIndex = 0, kSrcRanges = 1, kSrcLayout = 2, kSrcRing = 3 };
 
 struct AttnLaunch {
     // kSrcIndex / kSrcRanges: src0 = counts [B], src1 = range tables [B][6][2]
-    // (kSrcRanges); kSrcLayout: src0 = layouts (murmur_seg [B]), src1 =
-    // policies (murmur_policy [1] or [B], pol_per_seq).
+    // (kSrcRanges); kSrcLayout and kSrcRing: src0 = layouts (murmur_seg [B]),
+    // src1 = policies (murmur_policy [1] or [B], pol_per_seq).
     const int32_t *src0;
     const int32_t *src1;
     int32_t src_mode, pol_per_seq;
-    int32_t *idx_out, *count_out, *ranges_out;  // kSrcLayout: optional evict_compact outputs
+    int32_t *idx_out, *count_out, *ranges_out;  // kSrcLayout / kSrcRing: optional evict_compact outputs
+    // kSrcRing: output ring rows, and the current token's K/V [NL][B][Hkv][D]
+    // (read instead of its ring row, then appended there).
+    int32_t ring_cap;
+    const uint16_t *k_new;
+    const uint16_t *v_new;
     const uint16_t *q;
     const uint16_t *k;
     const uint16_t *v;

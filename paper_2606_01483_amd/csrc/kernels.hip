@@ -316,20 +316,38 @@ static __device__ __forceinline__ void pass_pos_index(const IdxRegs &I, int r0, 
     for (int i = 0; i < 8; ++i) pp.v[i] = keep_pos(r0 + 8 * c4 + i, I.v[i], cnt, max_len, unused);
 }
 
+// The current token in ring storage: rows at position `cur` are read from
+// the K/V passed with the call instead of the cache, whose row `cur` this
+// launch overwrites (kRing only; otherwise cur is never compared).
+struct NewRows {
+    int32_t cur;
+    const uint16_t *k;
+    const uint16_t *v;
+};
+
+template <bool kRing>
+static __device__ __forceinline__ const uint16_t *row_ptr(const uint16_t *base, int p, int64_t s_pos,
+                                                          const NewRows &nr, const uint16_t *fresh) {
+    const uint16_t *row = base + (int64_t)p * s_pos;
+    return kRing && p == nr.cur ? fresh : row;
+}
+
 // K and V fragments of one pass, all loads issued unconditionally.  Keeping
 // every load outside control flow lets the compiler's wait counting stay
 // exact across the software pipeline: the wait before a pass's compute
 // covers that pass's loads only, never the loads issued after them.
+template <bool kRing>
 static __device__ __forceinline__ void issue_kv(PassRegs &R, const uint16_t *kbase, const uint16_t *vbase,
-                                                int64_t s_pos, const PassPos &pp, int n16, int c4) {
+                                                int64_t s_pos, const PassPos &pp, int n16, int c4,
+                                                const NewRows &nr) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-        const uint16_t *row = kbase + (int64_t)pp.k[blk] * s_pos + 8 * c4;
+        const uint16_t *row = row_ptr<kRing>(kbase, pp.k[blk], s_pos, nr, nr.k) + 8 * c4;
 #pragma unroll
         for (int kc = 0; kc < 4; ++kc) R.kf[blk][kc] = load16(row + kc * 32);
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) R.vf[i] = load16(vbase + (int64_t)pp.v[i] * s_pos + 8 * n16);
+    for (int i = 0; i < 8; ++i) R.vf[i] = load16(row_ptr<kRing>(vbase, pp.v[i], s_pos, nr, nr.v) + 8 * n16);
 }
 
 // Forces uniform values into scalar registers at this point: the scalar loads
@@ -505,19 +523,23 @@ static __device__ __forceinline__ void wait_vm() {
 
 // The 16 direct-to-LDS loads of one pass (8 for K, then 8 for V) into `stage`.
 // pos[j]: in-bounds position of the row whose rank is r0 + 4j + (lane >> 4).
+// ring: compare positions with nr.cur (a constant at every call site).
 static __device__ __forceinline__ void dma_pass(uint8_t *stage, const uint16_t *kbase, const uint16_t *vbase,
-                                                int64_t s_pos, const int32_t (&pos)[8], int lane) {
+                                                int64_t s_pos, const int32_t (&pos)[8], int lane, bool ring,
+                                                const NewRows &nr) {
     const int q = lane >> 4, sl = lane & 15;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int c = sl ^ ((4 * j + q) & 15);
-        __builtin_amdgcn_global_load_lds(kbase + (int64_t)pos[j] * s_pos + 8 * c, (lds_void_t *)(stage + j * 1024),
-                                         16, 0, 0);
+        const uint16_t *kr = kbase + (int64_t)pos[j] * s_pos;
+        __builtin_amdgcn_global_load_lds((ring && pos[j] == nr.cur ? nr.k : kr) + 8 * c,
+                                         (lds_void_t *)(stage + j * 1024), 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int c = sl ^ ((4 * j + q) & 15);
-        __builtin_amdgcn_global_load_lds(vbase + (int64_t)pos[j] * s_pos + 8 * c,
+        const uint16_t *vr = vbase + (int64_t)pos[j] * s_pos;
+        __builtin_amdgcn_global_load_lds((ring && pos[j] == nr.cur ? nr.v : vr) + 8 * c,
                                          (lds_void_t *)(stage + kTileBytes + j * 1024), 16, 0, 0);
     }
 }
@@ -665,21 +687,29 @@ static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, co
 // ---------------------------------------------------------------------------
 // Count of sequence b and, unless kSrcIndex, its range table.  p0/p1: counts
 // (kSrcIndex) or range tables (kSrcRanges, the count being the table's total
-// length), or (kSrcLayout) layouts (murmur_seg [B]) and policies
-// (murmur_policy [1] or [B]).  An invalid layout or policy gives count 0 and
-// sets policy_bad.
+// length), or (kSrcLayout, kSrcRing) layouts (murmur_seg [B]) and policies
+// (murmur_policy [1] or [B]).  kSrcRing gives the pieces in ring-storage rows
+// of ring_cap output slots and the row of the current token in `cur`.  An
+// invalid layout or policy gives count 0 and sets policy_bad to 1 (2: the
+// ring cannot hold the retained outputs).
 template <int kSrc>
 static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t *p1, int b, int32_t pol_per_seq,
-                                                int32_t (&rg)[2 * kPieces], int &policy_bad) {
-    if (kSrc == kSrcLayout) {
+                                                int32_t ring_cap, int32_t (&rg)[2 * kPieces], int &policy_bad,
+                                                int32_t &cur) {
+    if (kSrc == kSrcLayout || kSrc == kSrcRing) {
         const int32_t *sg = p0 + 4 * b;
         const int32_t *pl = p1 + (pol_per_seq ? 5 * b : 0);
         const int32_t s0 = sg[0], s1 = sg[1], s2 = sg[2], s3 = sg[3];
         const int32_t w0 = pl[0], w1 = pl[1], w2 = pl[2], w3 = pl[3], w4 = pl[4];
-        materialize(s0, s1, s2, s3, w0, w1, w2, w3, w4);  // both rows in one round trip
+        if (kSrc == kSrcRing)
+            materialize(s0, s1, s2, s3, w0, w1, w2, w3, w4, ring_cap);  // one round trip
+        else
+            materialize(s0, s1, s2, s3, w0, w1, w2, w3, w4);  // both rows in one round trip
         Pieces pc;
-        if (retained_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, &pc) != 0) {
-            policy_bad = 1;
+        const int rc = kSrc == kSrcRing ? ring_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, ring_cap, &pc, &cur)
+                                        : retained_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, &pc);
+        if (rc != 0) {
+            policy_bad = rc == -2 ? 2 : 1;
 #pragma unroll
             for (int k = 0; k < 2 * kPieces; ++k) rg[k] = 0;
             return 0;
@@ -710,7 +740,7 @@ static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b
                                                       const int32_t (&rg)[2 * kPieces], int max_keep, int tid) {
     if (tid == 0) {
         if (a.count_out) a.count_out[b] = cnt;
-        if (policy_bad) raise_device_error(MURMUR_DEVERR_POLICY);
+        if (policy_bad) raise_device_error(policy_bad == 2 ? MURMUR_DEVERR_CAPACITY : MURMUR_DEVERR_POLICY);
         else if (cnt > max_keep) raise_device_error(MURMUR_DEVERR_OVERFLOW);
     }
     if (a.ranges_out && tid < 2 * kPieces) {
@@ -730,6 +760,21 @@ static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b
         }
         for (int r = off + tid; r < max_keep; r += kWavesPerWg * 64) row[r] = -1;
     }
+}
+
+// Ring storage: copies the current token's K and V rows (256 bytes each) of
+// this (layer, sequence, KV head) into its ring row `cur`, unless the layout,
+// policy or ring is invalid or the row lies outside the cache.  No workgroup
+// of this launch reads that row (positions equal to cur read nr.k / nr.v).
+// Block-wide; threads 0-15 copy K, 16-31 copy V.
+static __device__ __forceinline__ void append_new_row(const AttnLaunch &a, const NewRows &nr, const uint16_t *kbase,
+                                                      const uint16_t *vbase, int policy_bad, int tid) {
+    if (policy_bad || (uint32_t)nr.cur >= (uint32_t)a.max_len || tid >= 32) return;
+    const int c = tid & 15;
+    const bool is_v = tid >= 16;
+    const u32x4 x = load16((is_v ? nr.v : nr.k) + 8 * c);
+    uint16_t *dst = const_cast<uint16_t *>(is_v ? vbase : kbase) + (int64_t)nr.cur * a.s_pos + 8 * c;
+    *reinterpret_cast<u32x4 *>(dst) = x;
 }
 
 // Combine of a workgroup's four wavefronts.  Each wavefront publishes its
@@ -965,7 +1010,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int b = blockIdx.z;
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, rg, policy_bad);
+    int32_t cur = -1;
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, a.ring_cap, rg, policy_bad, cur);
     const int layer = (int)blockIdx.y / Hkv;
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
@@ -987,12 +1033,19 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
+    constexpr bool kRing = kSrc == kSrcRing;
+    NewRows nr{cur, nullptr, nullptr};
+    if (kRing) {
+        nr.k = a.k_new + (int64_t)grp * kHeadDim;
+        nr.v = a.v_new + (int64_t)grp * kHeadDim;
+    }
     uint8_t *vt = smem + wave * kOWaveBytes;  // this wavefront's V tile, later its O rows
 
     WaveAcc w;
     wave_acc_reset(w);
     int r = r_begin + wave * kWaveTile;
     materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
+    if (kRing) materialize(nr.k, nr.v, nr.cur);
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
@@ -1011,7 +1064,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
 #pragma unroll
         for (int p = 0; p < kPasses; ++p) {
             positions(I[p], r + p * kSplitUnit, pp);
-            issue_kv(R[p], kbase, vbase, a.s_pos, pp, n16, c4);
+            issue_kv<kRing>(R[p], kbase, vbase, a.s_pos, pp, n16, c4, nr);
         }
         compute_pass<false>(R[0], qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
         if (kPasses > 1 && r + kSplitUnit < r_end)
@@ -1025,7 +1078,9 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kOWaveBytes / 4, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
-    if (kSrc == kSrcLayout && split == 0 && g == 0 && layer == 0) write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
+    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 && layer == 0)
+        write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
+    if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
@@ -1074,7 +1129,8 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const int b = blockIdx.z;
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, rg, policy_bad);
+    int32_t cur = -1;
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, a.ring_cap, rg, policy_bad, cur);
     const int layer = (int)blockIdx.y / Hkv;
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
@@ -1096,6 +1152,12 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
+    constexpr bool kRing = kSrc == kSrcRing;
+    NewRows nr{cur, nullptr, nullptr};
+    if (kRing) {
+        nr.k = a.k_new + (int64_t)grp * kHeadDim;
+        nr.v = a.v_new + (int64_t)grp * kHeadDim;
+    }
     uint8_t *st[2] = {&stages[wave][0][0], &stages[wave][kStages - 1][0]};
     uint8_t *ring[2] = {&idx_ring[kSrc != kSrcIndex ? 0 : wave][0][0], &idx_ring[kSrc != kSrcIndex ? 0 : wave][1][0]};
 
@@ -1103,6 +1165,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     wave_acc_reset(w);
     int r = r_begin + wave * kWaveTile;
     materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
+    if (kRing) materialize(nr.k, nr.v, nr.cur);
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
@@ -1119,7 +1182,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
                 wait_vm<1>();  // this pass's entries; the next pass's may stay in flight
                 dma_pos_index(ring[k & 1], r, r_end, a.max_len, c4, pos, w.bad_pos);
             }
-            dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane);
+            dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
             wait_vm<0>();
             compute_pass_lds<true>(st[0], qf, min(kWaveTile, r_end - r), a.scale_log2, w, n16, c4);
             if (r + kSplitUnit >= r_end) break;
@@ -1135,7 +1198,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
             wait_vm<1>();
             dma_pos_index(ring[0], r, r_end, a.max_len, c4, pos, w.bad_pos);
         }
-        dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane);
+        dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
         for (int k = 0;; r += kSplitUnit, ++k) {
             const uint8_t *cur = st[k & 1];
             if (r + kSplitUnit < r_end) {
@@ -1146,7 +1209,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
                     dma_pos_index(ring[(k + 1) & 1], r + kSplitUnit, r_end, a.max_len, c4, pos, w.bad_pos);
                     dma_idx(ring[k & 1], irow, r + 2 * kSplitUnit, lane);
                 }
-                dma_pass(st[(k + 1) & 1], kbase, vbase, a.s_pos, pos, lane);
+                dma_pass(st[(k + 1) & 1], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
                 if (kSrc != kSrcIndex)
                     wait_vm<kStageLoads>();  // this pass's rows; the next pass's stay in flight
                 else
@@ -1167,7 +1230,9 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kStageWaveFloats, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
-    if (kSrc == kSrcLayout && split == 0 && g == 0 && layer == 0) write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
+    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 && layer == 0)
+        write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
+    if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
@@ -1308,7 +1373,8 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
     for (int t = tid; t < B; t += blockDim.x) {
         int32_t rg[2 * kPieces];
         int policy_bad = 0;
-        const int c = seq_count<kSrc>(src0, src1, t, pol_per_seq, rg, policy_bad);
+        int32_t unused_cur;
+        const int c = seq_count<kSrc>(src0, src1, t, pol_per_seq, 0, rg, policy_bad, unused_cur);
         const bool badc = c < 1 || c > max_keep;
         const int cc = c < 0 ? 0 : (c > max_keep ? max_keep : c);
         s_cnt[t] = cc;
@@ -1414,7 +1480,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         }
         dma_query(&q_slot[qs][0], q + row_of(x) * kHeadDim, G, lane);
         const int64_t off = x.layer * a.s_layer + x.b * a.s_b + x.g * a.s_h;
-        dma_pass(stage, a.k + off, a.v + off, a.s_pos, pos, lane);
+        dma_pass(stage, a.k + off, a.v + off, a.s_pos, pos, lane, false, NewRows{-1, nullptr, nullptr});
     };
 
     WaveAcc w;
@@ -1559,7 +1625,8 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         for (int bb = (int)p; bb < B; bb += (int)P) {
             int32_t rg[2 * kPieces];
             int policy_bad = 0;
-            const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, rg, policy_bad);
+            int32_t unused_cur;
+            const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, 0, rg, policy_bad, unused_cur);
             write_retained(a, bb, c, policy_bad, rg, max_keep, tid);
         }
     }
@@ -1582,10 +1649,12 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 
 template <int kSrc>
 static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
-    if (a.stream_wg > 0) {
-        hipLaunchKernelGGL(decode_attn_stream_kernel<kSrc>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64), 0,
-                           stream, a.src0, a.src1, a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
-        return;
+    if constexpr (kSrc != kSrcRing) {  // ring storage runs on the split schedules only
+        if (a.stream_wg > 0) {
+            hipLaunchKernelGGL(decode_attn_stream_kernel<kSrc>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64),
+                               0, stream, a.src0, a.src1, a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
+            return;
+        }
     }
     const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
     // Splits of up to two passes run from registers; longer splits stage their
@@ -1607,7 +1676,9 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
 }
 
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
-    if (a.src_mode == kSrcLayout)
+    if (a.src_mode == kSrcRing)
+        launch_decode_attn_mode<kSrcRing>(a, (hipStream_t)stream);
+    else if (a.src_mode == kSrcLayout)
         launch_decode_attn_mode<kSrcLayout>(a, (hipStream_t)stream);
     else if (a.src_mode == kSrcRanges)
         launch_decode_attn_mode<kSrcRanges>(a, (hipStream_t)stream);

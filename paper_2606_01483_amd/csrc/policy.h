@@ -107,4 +107,51 @@ MURMUR_HD inline int retained_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, 
     return 0;
 }
 
+// Physical eviction storage: the output region of a sequence holds its
+// n_sink output sinks at slots 0 .. n_sink-1, followed by a ring of `cap`
+// slots; 0-based output token i >= n_sink lives at slot
+// n_sink + (i - n_sink) mod cap.  A token whose slot is reused by a later
+// one is exactly a token Algorithm 1 has evicted, as long as the window fits
+// the ring (cap >= w) or, with output eviction off, as long as no slot has
+// been reused yet (j - n_sink <= cap).  Prompt and speech positions are
+// unchanged, so the storage of a sequence spans
+// prompt_pre + speech_len + prompt_mid + n_sink + cap rows.
+//
+// Rewrites the pieces of retained_pieces (same count) into storage
+// positions and gives the slot of the current token j.  The output part
+// stays within two pieces: when the window wraps around the ring, its newer
+// part starts at ring slot 0, right after the sinks, and joins them in
+// piece 4; the older part is piece 5.  Pieces are then in storage order of
+// rows, not in order of position.  Returns 0, -1 for an invalid layout or
+// policy (as retained_pieces), or -2 when the ring cannot hold the retained
+// outputs (cap < 1, cap < w, or output eviction off and j - n_sink > cap).
+MURMUR_HD inline int ring_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s, int32_t d,
+                                 int32_t n_ss, int32_t w_o, int32_t n_so, int32_t cap, Pieces *out, int32_t *cur) {
+    if (retained_pieces(p_pre, l_s, p_mid, j, w_s, d, n_ss, w_o, n_so, out) != 0) return -1;
+    if (cap < 1 || (w_o >= 1 && cap < w_o)) return -2;
+    const int64_t rows = (int64_t)p_pre + l_s + p_mid + n_so + cap;
+    if (rows > 0x7fffffffLL) return -1;
+    const int32_t out0 = p_pre + l_s + p_mid;
+    const int32_t last = j - 1;  // 0-based output index of the current token
+    *cur = out0 + (last < n_so ? last : n_so + (last - n_so) % cap);
+    if (out->len[5] == 0) {
+        // Every output token 0 .. j-1 is kept (one piece from the region's
+        // start): the ring must not have wrapped yet.
+        if (j > n_so && j - n_so > cap) return -2;
+        return 0;
+    }
+    // Window [w0, j) of w_o tokens, all past the sinks (w0 > n_so).
+    const int32_t w0 = j - w_o;
+    const int32_t a = (w0 - n_so) % cap;
+    const int32_t ring0 = out0 + n_so;
+    if (a + w_o <= cap) {
+        out->start[5] = ring0 + a;
+    } else {
+        out->len[4] = n_so + (a + w_o - cap);  // sinks, then ring slots 0 .. a + w_o - cap - 1
+        out->start[5] = ring0 + a;
+        out->len[5] = cap - a;
+    }
+    return 0;
+}
+
 }  // namespace murmur

@@ -127,3 +127,106 @@ class DecodeBatch:
         n = self.NL * self.B * self.Hq
         sel = self.B * M.N_PIECES * 2 * 4 if self.use_ranges else self.B * self.max_keep * 4
         return n * self.D * 2 + n * self.D * out_b + n * 4 + self.B * 4 + sel
+
+
+def ring_rows(seg_row, n_sink: int, cap: int) -> int:
+    """Rows of ring storage one sequence needs: prompts, speech, output sinks and `cap` ring rows."""
+    p_pre, l_s, p_mid, _ = (int(x) for x in seg_row)
+    return p_pre + l_s + p_mid + int(n_sink) + int(cap)
+
+
+def ring_prefill(cache: np.ndarray, seg: np.ndarray, n_sink: np.ndarray, cap: int, rows: int) -> np.ndarray:
+    """Places a sequence-ordered cache [NL, B, Hkv, L, D] into ring storage [NL, B, Hkv, rows, D] as it
+    stands after output tokens 0 .. out_len-1 have been appended (the layout of include/murmur.h's
+    murmur_ring): prompts and speech in place, output sinks after them, and each of the last `cap`
+    later tokens at its ring row.  Rows that hold no token are zero."""
+    seg = np.asarray(seg).reshape(-1, 4)
+    NL, B, Hkv, _, D = cache.shape
+    st = np.zeros((NL, B, Hkv, rows, D), dtype=cache.dtype)
+    for b in range(B):
+        p_pre, l_s, p_mid, j = (int(x) for x in seg[b])
+        out0, ns = p_pre + l_s + p_mid, int(n_sink[b])
+        st[:, b, :, :out0] = cache[:, b, :, :out0]
+        ks = min(ns, j)
+        st[:, b, :, out0:out0 + ks] = cache[:, b, :, out0:out0 + ks]
+        tok = np.arange(max(ns, j - cap), j)  # the ring tokens still in storage
+        st[:, b, :, out0 + ns + (tok - ns) % cap] = cache[:, b, :, out0 + tok]
+    return st
+
+
+class RingBatch:
+    """Decode steps on ring storage (murmur_decode_step_ring): eviction, attention and the append of the
+    current token in one launch per step.
+
+    Memory plumbing only: the ring storage [R][NL][B][Hkv][rows][D] (R replicas for cold reads), per-step
+    layouts, queries and current-token K/V [steps][NL][B][Hkv][D], outputs and workspace.  `storage`
+    (optional, uint16 bf16 bits [NL, B, Hkv, rows, D]) replaces the prefill of the first step's state."""
+
+    def __init__(self, wl: Workload, cap: int, device: str = "cuda", replicas: int = 1,
+                 out_dtype: int = M.MURMUR_DTYPE_BF16, split_len: int = 0, steps: list[int] | None = None,
+                 storage: tuple[np.ndarray, np.ndarray] | None = None):
+        self.wl = wl
+        self.cap = int(cap)
+        self.device = torch.device(device)
+        self.steps = list(range(wl.steps)) if steps is None else list(steps)
+        self.out_dtype = out_dtype
+        self.split_len = split_len
+        B, NL, Hq, Hkv, D = wl.batch, wl.n_layers, wl.hq, wl.hkv, wl.head_dim
+        self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
+        n_sink = wl.policy[:, 4]
+        counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[1] for s in self.steps]
+        self.max_keep = int(max(counts))
+        seg_before = wl.seg(self.steps[0])
+        seg_before[:, 3] -= 1  # the state before the first step: its token is not appended yet
+        self.rows = max(ring_rows(seg_before[b], n_sink[b], cap) for b in range(B))
+        self.rows = (self.rows + 7) // 8 * 8
+        if storage is None:
+            storage = (ring_prefill(wl.k, seg_before, n_sink, cap, self.rows),
+                       ring_prefill(wl.v, seg_before, n_sink, cap, self.rows))
+        dev = self.device
+        self.replicas = replicas
+        k0 = torch.from_numpy(np.ascontiguousarray(storage[0])).view(torch.bfloat16)
+        v0 = torch.from_numpy(np.ascontiguousarray(storage[1])).view(torch.bfloat16)
+        self.k = torch.empty((replicas,) + tuple(k0.shape), dtype=torch.bfloat16, device=dev)
+        self.v = torch.empty_like(self.k)
+        for r in range(replicas):
+            self.k[r].copy_(k0)
+            self.v[r].copy_(v0)
+        self.kv = [M.kv_from_tensors(self.k[r], self.v[r]) for r in range(replicas)]
+
+        self.seg = torch.from_numpy(np.stack([wl.seg(s) for s in self.steps]).astype(np.int32)).to(dev)
+        self.pol = torch.from_numpy(np.ascontiguousarray(wl.policy, dtype=np.int32)).to(dev)
+        self.q = torch.from_numpy(np.stack([wl.q(s) for s in self.steps])).view(torch.bfloat16).to(dev)
+        # The current token's K/V of every step, taken from the sequence-ordered cache.
+        knew = np.empty((len(self.steps), NL, B, Hkv, D), dtype=np.uint16)
+        vnew = np.empty_like(knew)
+        for i, s in enumerate(self.steps):
+            seg = wl.seg(s)
+            for b in range(B):
+                p = int(seg[b, 0] + seg[b, 1] + seg[b, 2] + seg[b, 3]) - 1
+                knew[i, :, b] = wl.k[:, b, :, p]
+                vnew[i, :, b] = wl.v[:, b, :, p]
+        self.k_new = torch.from_numpy(knew).view(torch.bfloat16).to(dev)
+        self.v_new = torch.from_numpy(vnew).view(torch.bfloat16).to(dev)
+        self.ring = [M.make_ring(cap, self.k_new[i], self.v_new[i]) for i in range(len(self.steps))]
+
+        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
+        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.ranges = torch.zeros((B, M.N_PIECES, 2), dtype=torch.int32, device=dev)
+        odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
+        self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
+        self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
+        self.ws_bytes = M.murmur_decode_attn_workspace(NL, B, Hq, Hkv, self.max_keep, split_len)
+        self.ws = torch.zeros(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.int32, device=dev)
+
+    def step(self, i: int, replica: int = 0, stream=None, outputs: bool = True) -> None:
+        """murmur_decode_step_ring for the i-th step of this batch on storage replica `replica`."""
+        idx, count, ranges = (self.idx, self.count, self.ranges) if outputs else (None, None, None)
+        M.murmur_decode_step_ring(self.seg[i], self.pol, 1, self.ring[i], self.q[i], self.kv[replica], idx, count,
+                                  ranges, self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale,
+                                  self.split_len, self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes,
+                                  stream)
+
+    def resident_bytes(self) -> int:
+        """Bytes of one replica of the ring storage (K and V)."""
+        return 2 * self.k[0].numel() * 2

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libmurmur.so")
 MURMUR_OK, MURMUR_EINVAL, MURMUR_EUNSUPPORTED, MURMUR_ENOSPACE, MURMUR_EHIP = 0, -1, -2, -3, -4
 MURMUR_DTYPE_BF16, MURMUR_DTYPE_F32 = 1, 2
 MURMUR_DEVERR_OVERFLOW, MURMUR_DEVERR_POLICY, MURMUR_DEVERR_POSITION, MURMUR_DEVERR_COUNT = 1, 2, 4, 8
+MURMUR_DEVERR_CAPACITY = 16
 N_PIECES = 6
 SPLIT_UNIT = 128
 MURMUR_SPLIT_STREAM = -1
@@ -40,6 +41,10 @@ class murmur_kv(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("n_layers", ctypes.c_int32),
                 ("max_len", ctypes.c_int32), ("stride_layer", ctypes.c_int64), ("stride_b", ctypes.c_int64),
                 ("stride_h", ctypes.c_int64), ("stride_pos", ctypes.c_int64)]
+
+
+class murmur_ring(ctypes.Structure):
+    _fields_ = [("out_capacity", ctypes.c_int32), ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p)]
 
 
 class MurmurError(RuntimeError):
@@ -79,6 +84,13 @@ def _load():
     lib.murmur_decode_step.restype = ctypes.c_int
     lib.murmur_decode_step.argtypes = [vp, vp, i32, vp, ctypes.POINTER(murmur_kv), vp, vp, vp, i32, i32, i32, i32, i32,
                                        ctypes.c_float, i32, vp, i32, vp, vp, sz, vp]
+    lib.murmur_ring_layout_host.restype = ctypes.c_int
+    lib.murmur_ring_layout_host.argtypes = [ctypes.POINTER(murmur_seg), ctypes.POINTER(murmur_policy), i32, i32, i32,
+                                            i32p, i32p]
+    lib.murmur_decode_step_ring.restype = ctypes.c_int
+    lib.murmur_decode_step_ring.argtypes = [vp, vp, i32, ctypes.POINTER(murmur_ring), vp, ctypes.POINTER(murmur_kv),
+                                            vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, i32, vp, i32, vp,
+                                            vp, sz, vp]
     lib.murmur_device_error.restype = ctypes.c_int
     lib.murmur_device_error.argtypes = [vp, i32p]
     _lib = lib
@@ -199,6 +211,38 @@ def murmur_decode_step(seg_dev, pol_dev, pol_per_seq: int, q_dev, kv: murmur_kv,
                                       _addr(idx_dev), _addr(count_dev), _addr(ranges_dev), max_keep, B, Hq, Hkv, D,
                                       float(scale), split_len, _addr(out_dev), out_dtype, _addr(lse_dev),
                                       _addr(ws_dev), ws_bytes, _stream(stream)))
+
+
+def murmur_ring_layout_host(seg, pol, out_capacity: int, pol_per_seq: int | None = None):
+    """Host-only ring-storage layout.  Returns (ranges int32 [B, 6, 2], cur_row int32 [B])."""
+    seg_np = np.ascontiguousarray(seg, dtype=np.int32).reshape(-1, 4)
+    pol_np = np.ascontiguousarray(pol, dtype=np.int32)
+    if pol_per_seq is None:
+        pol_per_seq = 1 if pol_np.ndim == 2 and pol_np.shape[0] > 1 else 0
+    B = seg_np.shape[0]
+    ranges = np.zeros((B, N_PIECES, 2), dtype=np.int32)
+    cur = np.zeros(B, dtype=np.int32)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    _check(_load().murmur_ring_layout_host(_segs(seg_np), _pols(pol_np), pol_per_seq, B, int(out_capacity),
+                                           ranges.ctypes.data_as(i32p), cur.ctypes.data_as(i32p)))
+    return ranges, cur
+
+
+def make_ring(out_capacity: int, k_new, v_new) -> murmur_ring:
+    """murmur_ring from the ring size and the current token's K/V (device tensors [NL, B, Hkv, D] or addresses)."""
+    return murmur_ring(int(out_capacity), _addr(k_new), _addr(v_new))
+
+
+def murmur_decode_step_ring(seg_dev, pol_dev, pol_per_seq: int, ring: murmur_ring, q_dev, kv: murmur_kv, idx_dev,
+                            count_dev, ranges_dev, max_keep: int, B: int, Hq: int, Hkv: int, D: int, scale: float,
+                            split_len: int, out_dev, out_dtype: int, lse_dev, ws_dev, ws_bytes: int,
+                            stream=None) -> None:
+    """Eviction, attention and the current token's append on ring storage, in one launch."""
+    _check(_load().murmur_decode_step_ring(_addr(seg_dev), _addr(pol_dev), pol_per_seq, ctypes.byref(ring),
+                                           _addr(q_dev), ctypes.byref(kv), _addr(idx_dev), _addr(count_dev),
+                                           _addr(ranges_dev), max_keep, B, Hq, Hkv, D, float(scale), split_len,
+                                           _addr(out_dev), out_dtype, _addr(lse_dev), _addr(ws_dev), ws_bytes,
+                                           _stream(stream)))
 
 
 def murmur_device_error(stream=None) -> int:

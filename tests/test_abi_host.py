@@ -13,6 +13,7 @@ import pytest
 import torch
 
 import oracle
+from oracle import ring as OR
 from paper_2606_01483_amd import _build
 from paper_2606_01483_amd import murmur as M
 
@@ -37,14 +38,14 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 11
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 2
+    assert M.murmur_abi_version() == 3
 
 
 def test_retained_count_host_matches_oracle():
@@ -244,3 +245,87 @@ def call_step(a, seg=FAKE, pol=FAKE, pol_per_seq=0):
 def test_decode_step_rejects(over, step_kw, code):
     assert call_step(attn_args(**over), **step_kw) == code
     assert M.murmur_last_error() != ""
+
+
+# ---- ring storage (host layout and argument checks) ----------------------------------------------
+
+def expand(ranges_row):
+    out = []
+    for start, length in ranges_row:
+        out.extend(range(int(start), int(start) + int(length)))
+    return out
+
+
+def test_ring_layout_host_matches_oracle_rows():
+    """The six storage pieces hold exactly the oracle's retained tokens, mapped to their ring rows, and
+    cur_row is the row the current token is written to (400 random layouts and policies)."""
+    rng = np.random.default_rng(21)
+    B = 400
+    w_o = np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 120, B))
+    n_so = rng.integers(0, 8, B)
+    j = rng.integers(1, 600, B)
+    seg = np.stack([rng.integers(0, 40, B), rng.integers(0, 400, B), rng.integers(0, 20, B), j],
+                   axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 300, B)), rng.integers(0, 300, B),
+                    rng.integers(0, 30, B), w_o, n_so], axis=1).astype(np.int32)
+    for cap in (130, 700):
+        ok = (w_o <= cap) & ((w_o != OFF) | (j - n_so <= cap))
+        seg_ok, pol_ok = seg[ok], pol[ok]
+        ranges, cur = M.murmur_ring_layout_host(seg_ok, pol_ok, cap, 1)
+        idx, cnt = oracle.retained(seg_ok, pol_ok)
+        rows = OR.storage_rows(idx, cnt, seg_ok, pol_ok[:, 4], cap)
+        for b in range(seg_ok.shape[0]):
+            got = expand(ranges[b])
+            assert sorted(got) == sorted(rows[b]) and len(got) == int(cnt[b])
+            out0 = int(seg_ok[b, 0] + seg_ok[b, 1] + seg_ok[b, 2])
+            assert cur[b] == OR.ring_row(int(seg_ok[b, 3]) - 1, out0, int(pol_ok[b, 4]), cap)
+            assert np.all(ranges[b, :, 1] >= 0)
+
+
+def test_ring_layout_host_rejects_rings_too_small():
+    seg = np.array([[32, 100, 0, 50]], dtype=np.int32)
+    with pytest.raises(M.MurmurError):
+        M.murmur_ring_layout_host(seg, np.array([OFF, 0, 0, 64, 0]), 63)  # cap < window
+    with pytest.raises(M.MurmurError):
+        M.murmur_ring_layout_host(seg, np.array([OFF, 0, 0, OFF, 2]), 47)  # keep-all, 48 ring tokens
+    M.murmur_ring_layout_host(seg, np.array([OFF, 0, 0, OFF, 2]), 48)
+    with pytest.raises(M.MurmurError):
+        M.murmur_ring_layout_host(seg, np.array([OFF, 0, 0, 8, 0]), 0)
+
+
+def call_ring_step(a, ring, seg=FAKE, pol=FAKE):
+    return M.lib().murmur_decode_step_ring(seg, pol, 0, ctypes.byref(ring) if ring is not None else None, a["q"],
+                                           ctypes.byref(a["kv"]), a["idx"], a["count"], a["ranges"], a["max_keep"],
+                                           a["B"], a["Hq"], a["Hkv"], a["D"], a["scale"], a["split_len"], a["out"],
+                                           a["out_dtype"], a["lse"], a["ws"], a["ws_bytes"], 0)
+
+
+@pytest.mark.parametrize("over,ring,code", [
+    ({}, None, M.MURMUR_EINVAL),
+    ({}, M.murmur_ring(0, FAKE, FAKE), M.MURMUR_EINVAL),
+    ({}, M.murmur_ring(256, None, FAKE), M.MURMUR_EINVAL),
+    ({}, M.murmur_ring(256, FAKE + 8, FAKE), M.MURMUR_EINVAL),
+    (dict(split_len=M.MURMUR_SPLIT_STREAM), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_EUNSUPPORTED),
+    (dict(D=64), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_EUNSUPPORTED),
+    (dict(ws_bytes=1000), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_ENOSPACE),
+])
+def test_decode_step_ring_rejects(over, ring, code):
+    assert call_ring_step(attn_args(**over), ring) == code
+    assert M.murmur_last_error() != ""
+
+
+def test_ring_prefill_matches_the_oracle_appends():
+    """decode.ring_prefill (the bench's placement of a prefilled state) equals the oracle's literal
+    sequence of appends, row for row."""
+    from paper_2606_01483_amd.decode import ring_prefill
+    rng = np.random.default_rng(5)
+    for _ in range(40):
+        B = 3
+        seg = np.stack([rng.integers(0, 9, B), rng.integers(0, 30, B), rng.integers(0, 5, B),
+                        rng.integers(1, 90, B)], axis=1).astype(np.int32)
+        n_so = rng.integers(0, 5, B)
+        cap = int(rng.integers(1, 40))
+        L = int((seg.sum(axis=1)).max())
+        cache = rng.integers(1, 60000, size=(2, B, 2, L, 4)).astype(np.uint16)
+        rows = max(OR.storage_len(seg[b], n_so[b], cap) for b in range(B))
+        assert np.array_equal(ring_prefill(cache, seg, n_so, cap, rows), OR.append_all(cache, seg, n_so, cap, rows))
