@@ -160,8 +160,50 @@ def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
                       f"{wl.hq} heads), retained set + fp64 attention, {threads} threads, {dt:.1f} s wall"}
 
 
+def replicas_for(wl, kv_step: list[int]) -> int:
+    """KV replicas to rotate over so that consecutive steps read more than 2.2 x the Infinity Cache
+    (at most 24 GB of replicas)."""
+    replicas = max(1, math.ceil(2.2 * MALL_BYTES / min(kv_step)))
+    return min(replicas, max(1, (24 << 30) // (wl.k.nbytes * 2)))
+
+
+def ring_capacity(wl, n_steps: int) -> int:
+    """Ring rows for a workload: its largest output window, or, where output eviction is off, every
+    output token the measured steps generate beyond the sinks."""
+    cap = 1
+    last_j = wl.seg(n_steps - 1)[:, 3]
+    for b in range(wl.batch):
+        w_o, n_so = int(wl.policy[b, 3]), int(wl.policy[b, 4])
+        cap = max(cap, w_o if w_o >= 1 else int(last_j[b]) - n_so)
+    return cap
+
+
+def ring_timing(wl, n_steps: int, steps: int, warmup: int, replicas: int, split_len: int, capture,
+                time_graph) -> dict:
+    """The same steps on ring storage (murmur_decode_step_ring: retained set, attention and the append
+    of the current token in one launch), timed as a replayed graph, with the storage it needs."""
+    from paper_2606_01483_amd import murmur as M
+    from paper_2606_01483_amd.decode import RingBatch
+    cap = ring_capacity(wl, n_steps)
+    log(f"ring storage: {cap} output rows, {replicas} replica(s)")
+    rb = RingBatch(wl, cap, replicas=replicas, split_len=split_len if split_len >= 0 else 0,
+                   steps=list(range(n_steps)))
+    for i in range(warmup):
+        rb.step(i % n_steps, i % replicas)
+    graph = capture(lambda: [rb.step(i % n_steps, i % replicas) for i in range(steps)])
+    ring_us = time_graph(graph) / steps
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during the timed ring steps")
+    last = wl.seg(n_steps - 1)
+    linear_rows = int(last.sum(axis=1).max())  # rows per sequence of the sequence-ordered cache at the last step
+    per_row = wl.n_layers * wl.batch * wl.hkv * wl.head_dim * 2 * 2
+    return {"step_us": round(ring_us, 3), "out_capacity": cap, "rows_per_sequence": rb.rows,
+            "rows_per_sequence_linear": linear_rows, "kv_resident_bytes": rb.rows * per_row,
+            "kv_resident_bytes_linear": linear_rows * per_row}
+
+
 def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, cpu_budget: float,
-        split_len: int, use_ranges: bool) -> dict:
+        split_len: int, use_ranges: bool, with_ring: bool = True) -> dict:
     import torch
     from paper_2606_01483_amd import murmur as M
     from paper_2606_01483_amd import workloads as W
@@ -176,9 +218,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[0] for s in range(n_steps)]
     kv_step = [int(c.sum()) * wl.n_layers * wl.hkv * 2 * wl.head_dim * 2 for c in counts]
     if replicas is None:
-        replicas = max(1, math.ceil(2.2 * MALL_BYTES / min(kv_step)))
-        cache_bytes = wl.k.nbytes * 2
-        replicas = min(replicas, max(1, (24 << 30) // cache_bytes))
+        replicas = replicas_for(wl, kv_step)
     log(f"uploading: {replicas} KV replica(s) of {wl.k.nbytes * 2 / 1e6:.1f} MB")
     db = DecodeBatch(wl, replicas=replicas, out_dtype=M.MURMUR_DTYPE_BF16, split_len=split_len,
                      use_ranges=use_ranges, steps=list(range(n_steps)))
@@ -248,6 +288,10 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during the timed decode_attn launches")
 
+    ring = None
+    if with_ring:
+        ring = ring_timing(wl, n_steps, steps, warmup, replicas_for(wl, kv_step), split_len, capture, time_graph)
+
     io = db.io_bytes()
     alg_bytes = float(kv_step[order[0]] + io)  # every launch of the decode_attn graph reads this set
     achieved = float(alg_bytes / (attn_us * 1e-6) / 1e9)
@@ -278,11 +322,80 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": committed_traffic(config),
                      "kernel": "decode_attn", "alg_bytes_per_launch": int(alg_bytes)},
     }
+    if ring is not None:
+        res["ring"] = ring
     if cpu:
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
         log(f"timing the fp64 oracle on {threads} host threads")
         res["cpu_baseline"] = cpu_baseline(wl, cpu_budget, threads)
     return res
+
+
+def ablation(samples: int, reps: int, split_len: int) -> list[dict]:
+    """Decode-attention time of every eviction preset of the paper's ablations over a whole decode of
+    2700 output tokens (batch 16, 300 s chunks): the fused step is timed at `samples` evenly spaced
+    steps (a graph of `reps` launches per step, each on the next KV replica) and averaged, next to the
+    exact ratio of dense to retained positions summed over all 2700 steps."""
+    import torch
+    from paper_2606_01483_amd import murmur as M
+    from paper_2606_01483_amd import workloads as W
+    from paper_2606_01483_amd.decode import DecodeBatch
+
+    torch.cuda.init()
+    M.lib()
+    log("ablation: drawing the 16-chunk cache")
+    base = W.ablation_workload("full")
+    T = base.steps
+    sample_steps = sorted({int(round(k * (T - 1) / (samples - 1))) for k in range(samples)})
+    dense = np.array([int(base.seg(s)[:, :4].sum()) for s in range(T)], dtype=np.float64)
+    out = []
+    full_us = None
+    for name, pol in W.ABLATION_PRESETS.items():
+        wl = W.with_policy(base, pol)
+        kept = np.array([int(M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[0].sum()) for s in range(T)],
+                        dtype=np.float64)
+        kv_min = int(kept[sample_steps].min()) * wl.hkv * 2 * wl.head_dim * 2
+        replicas = min(max(1, math.ceil(2.2 * MALL_BYTES / kv_min)), max(1, (24 << 30) // (wl.k.nbytes * 2)))
+        log(f"ablation {name}: {replicas} replica(s)")
+        db = DecodeBatch(wl, replicas=replicas, split_len=split_len, steps=sample_steps)
+        stream = torch.cuda.current_stream()
+        per_step = []
+        for i in range(len(sample_steps)):
+            for r in range(2):
+                db.step_fused(i, r % replicas, outputs=False)
+            graph = torch.cuda.CUDAGraph()
+            cap = torch.cuda.Stream()
+            cap.wait_stream(stream)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=cap):
+                for r in range(reps):
+                    db.step_fused(i, r % replicas, outputs=False)
+            torch.cuda.synchronize()
+            graph.replay()
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            t0.record(stream)
+            graph.replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            per_step.append(t0.elapsed_time(t1) * 1e3 / reps)
+            del graph
+        if M.murmur_device_error() != 0:
+            raise RuntimeError(f"device error in ablation preset {name}")
+        us = float(np.mean(per_step))
+        if full_us is None:
+            full_us = us
+        out.append({"preset": name, "policy": list(map(int, pol)), "batch": wl.batch, "outputs": T,
+                    "sample_steps": len(sample_steps), "attn_step_us_mean": round(us, 3),
+                    "attn_step_us_first_last": [round(per_step[0], 3), round(per_step[-1], 3)],
+                    "kept_fraction_mean": round(float(np.mean(kept / dense)), 4),
+                    "kept_fraction_last": round(float(kept[-1] / dense[-1]), 4),
+                    "dense_over_kept_positions": round(float(dense.sum() / kept.sum()), 4),
+                    "measured_speedup_vs_full": round(full_us / us, 4)})
+        print(json.dumps(out[-1]), flush=True)
+        del db
+        torch.cuda.empty_cache()
+    return out
 
 
 def main() -> int:
@@ -295,8 +408,12 @@ def main() -> int:
     ap.add_argument("--split-len", type=int, default=0)
     ap.add_argument("--index-list", action="store_true", help="attend from the index list instead of ranges")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ring", action="store_true", help="skip the ring-storage timing")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
     ap.add_argument("--all", action="store_true", help="one JSON line per workload (c1 .. c5), no CPU baseline")
+    ap.add_argument("--ablation", action="store_true",
+                    help="one JSON line per eviction preset of the paper's ablations (batch 16, 2700 outputs)")
+    ap.add_argument("--ablation-samples", type=int, default=12)
     ap.add_argument("--copy-reference", type=int, default=0, metavar="MB",
                     help="only run plain device copies of this many MiB (PMC counter reference)")
     ap.add_argument("--summarize-trace", metavar="DIR", help="print the kernel table of a rocprofv3 --stats run")
@@ -316,17 +433,21 @@ def main() -> int:
         print(f"bench.py runs on one GPU only: this decode path has no multi-GPU mode (got --gpus {args.gpus})",
               file=sys.stderr)
         return 2
+    if args.ablation:
+        ablation(args.ablation_samples, max(4, args.steps // 4), args.split_len)
+        return 0
     if args.copy_reference:
         print(json.dumps(copy_reference(args.copy_reference, 8)), flush=True)
         return 0
     if args.all:
         from paper_2606_01483_amd import workloads as W
         for cfg in W.CONFIGS:
-            res = run(cfg, args.steps, args.warmup, None, False, 0.0, args.split_len, not args.index_list)
+            res = run(cfg, args.steps, args.warmup, None, False, 0.0, args.split_len, not args.index_list,
+                      not args.no_ring)
             print(json.dumps(res), flush=True)
         return 0
     res = run(args.config, args.steps, args.warmup, args.replicas, not args.no_cpu_baseline, args.cpu_budget,
-              args.split_len, not args.index_list)
+              args.split_len, not args.index_list, not args.no_ring)
     print(json.dumps(res), flush=True)
     return 0
 

@@ -241,3 +241,41 @@ def _layout(name, seed, n_layers, seg0, pol, steps, planted) -> Layout:
 
 
 CONFIGS = ("c1", "c2", "c3", "c4_dense", "c4_evict", "c5")
+
+# Eviction policies of the paper's ablations, all on 300 s chunks decoded in a batch of 16 (Section 4,
+# Tables 2-4): (speech_window, speech_delay, speech_sink, out_window, out_sink).  Table 3 varies
+# Algorithm 1's sinks / window; Table 4 Algorithm 2's delay / window (its "S / W" columns); Table 2
+# combines output s4 w1024 with speech d512 w1024.
+ABLATION_PRESETS = {
+    "full": (OFF, 0, 0, OFF, 0),
+    "out s4 w1024": (OFF, 0, 0, 1024, 4),
+    "out s4 w512": (OFF, 0, 0, 512, 4),
+    "out s4 w256": (OFF, 0, 0, 256, 4),
+    "out s8 w1024": (OFF, 0, 0, 1024, 8),
+    "out s8 w512": (OFF, 0, 0, 512, 8),
+    "out s8 w256": (OFF, 0, 0, 256, 8),
+    "speech d256 w1024": (1024, 256, 0, OFF, 0),
+    "speech d256 w1538": (1538, 256, 0, OFF, 0),
+    "speech d512 w1024": (1024, 512, 0, OFF, 0),
+    "speech d512 w1538": (1538, 512, 0, OFF, 0),
+    "both: out s4 w1024 + speech d512 w1024": (1024, 512, 0, 1024, 4),
+}
+ABLATION_BATCH = 16
+ABLATION_OUTPUTS = 2700  # output tokens per 300 s chunk (Equation 3's example)
+
+
+def ablation_workload(preset: str = "full", n_outputs: int = ABLATION_OUTPUTS) -> Workload:
+    """A batch of 16 chunks of 300 s (32 prompt + 2250 speech tokens) decoded from the first output token
+    to n_outputs under one of ABLATION_PRESETS; step s generates output token s + 1.  The caches do not
+    depend on the preset (same seed), so presets can share one draw via with_policy()."""
+    seg0 = np.tile(np.array([[32, 2250, 0, 0]], dtype=np.int32), (ABLATION_BATCH, 1))
+    return build("ablation", 1006, 1, seg0, np.array(ABLATION_PRESETS[preset], dtype=np.int32), n_outputs,
+                 planted=False)
+
+
+def with_policy(wl: Workload, policy) -> Workload:
+    """The same workload (same arrays) under another policy, [5] or [B, 5]."""
+    pol = np.ascontiguousarray(policy, dtype=np.int32)
+    if pol.ndim == 1:
+        pol = np.repeat(pol.reshape(1, 5), wl.batch, axis=0)
+    return dataclasses.replace(wl, policy=pol)

@@ -179,6 +179,28 @@ def test_attn_workloads(config):
         assert lse_err(l, ref_lse) <= LSE_TOL
 
 
+@pytest.mark.parametrize("preset", list(W.ABLATION_PRESETS))
+def test_ablation_presets(preset):
+    """Every eviction preset of the paper's ablations (batch 16, 300 s chunks) at the first, a middle and
+    the last of 2700 decode steps: retained sets bit for bit (fused step outputs) and attention."""
+    if "ablation" not in _cache:
+        _cache["ablation"] = W.ablation_workload()
+    wl = W.with_policy(_cache["ablation"], W.ABLATION_PRESETS[preset])
+    steps = [0, 1349, wl.steps - 1]
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=steps)
+    for i, s in enumerate(steps):
+        announce(f"ablation preset {preset!r} step {s}")
+        db.step_fused(i)
+        torch.cuda.synchronize()
+        idx, cnt = oracle.retained(wl.seg(s), wl.policy, db.max_keep)
+        assert np.array_equal(db.count.cpu().numpy(), cnt)
+        assert np.array_equal(db.idx.cpu().numpy(), idx)
+        ref, ref_lse = oracle.attend(wl.q(s), wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=THREADS)
+        y = db.out.float().cpu().numpy()
+        assert rel_err_fp32(y, ref) <= REL_TOL
+        assert lse_err(db.lse.cpu().numpy(), ref_lse) <= LSE_TOL
+
+
 def test_attn_28_layers_sampled():
     """The 28-layer workload at full size: every output is computed on the GPU in one launch per step;
     the oracle checks a sample of (layer, sequence) pairs and the bf16 store path."""
