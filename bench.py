@@ -47,6 +47,7 @@ DESCRIPTIONS = {
     "c4_evict": "single-pass hour with eviction: speech window 2048 (delay 512), output window 512",
     "c5": "28 layers x 12 chunks: speech U{1800..2250}, output U{300..1200}, speech window L_s/4 (delay 512), "
           "output window 256, all layers in one launch",
+    "c5_layers": "c5 with its first 4 layers dense and the eviction policy on the other 24 (per-layer policies)",
 }
 
 
@@ -147,10 +148,17 @@ def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
     qs = [wl.q(s) for s in range(wl.steps)]
     t0 = time.perf_counter()
     n = 0
+    per_layer = wl.policy.ndim == 3
     while True:
         s = n % wl.steps
-        idx, cnt = oracle.retained(wl.seg(s), wl.policy)
-        oracle.attend(qs[s], wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=threads)
+        if per_layer:  # the retained set of each layer's policy, attended layer by layer
+            for layer in range(wl.n_layers):
+                idx, cnt = oracle.retained(wl.seg(s), wl.policy[layer])
+                sl = slice(layer, layer + 1)
+                oracle.attend(qs[s][sl], wl.k[sl], wl.v[sl], idx, cnt, scale=wl.scale, n_threads=threads)
+        else:
+            idx, cnt = oracle.retained(wl.seg(s), wl.policy)
+            oracle.attend(qs[s], wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=threads)
         n += 1
         if time.perf_counter() - t0 > budget_s:
             break
@@ -170,11 +178,13 @@ def replicas_for(wl, kv_step: list[int]) -> int:
 def ring_capacity(wl, n_steps: int) -> int:
     """Ring rows for a workload: its largest output window, or, where output eviction is off, every
     output token the measured steps generate beyond the sinks."""
+    from paper_2606_01483_amd.decode import layer_policies
     cap = 1
     last_j = wl.seg(n_steps - 1)[:, 3]
-    for b in range(wl.batch):
-        w_o, n_so = int(wl.policy[b, 3]), int(wl.policy[b, 4])
-        cap = max(cap, w_o if w_o >= 1 else int(last_j[b]) - n_so)
+    for pol in layer_policies(wl):
+        for b in range(wl.batch):
+            w_o, n_so = int(pol[b, 3]), int(pol[b, 4])
+            cap = max(cap, w_o if w_o >= 1 else int(last_j[b]) - n_so)
     return cap
 
 
@@ -207,7 +217,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     import torch
     from paper_2606_01483_amd import murmur as M
     from paper_2606_01483_amd import workloads as W
-    from paper_2606_01483_amd.decode import DecodeBatch
+    from paper_2606_01483_amd.decode import DecodeBatch, retained_counts
 
     torch.cuda.init()
     M.lib()
@@ -215,8 +225,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     n_steps = max(lay.steps, steps)
     log(f"workload {config}: drawing inputs ({n_steps} steps)")
     wl = W.make(config, steps=n_steps)
-    counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[0] for s in range(n_steps)]
-    kv_step = [int(c.sum()) * wl.n_layers * wl.hkv * 2 * wl.head_dim * 2 for c in counts]
+    counts = [retained_counts(wl, s) for s in range(n_steps)]  # [NL, B] per step
+    kv_step = [int(c.sum()) * wl.hkv * 2 * wl.head_dim * 2 for c in counts]
     if replicas is None:
         replicas = replicas_for(wl, kv_step)
     log(f"uploading: {replicas} KV replica(s) of {wl.k.nbytes * 2 / 1e6:.1f} MB")
@@ -226,24 +236,29 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
 
     order = [i % n_steps for i in range(steps)]
     rep = [i % replicas for i in range(steps)]
+    # Per-layer policies run on the fused step only: it is then also the kernel the roofline is taken on.
+    two_launch = not db.per_layer
 
     for i in range(warmup):
-        db.step(i % n_steps, i % replicas)
+        if two_launch:
+            db.step(i % n_steps, i % replicas)
         db.step_fused(i % n_steps, i % replicas)
     torch.cuda.synchronize()
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during warm-up")
 
-    # Per-launch event brackets (diagnostic: they include each launch's dispatch latency).
-    log("timing decode_attn launches with HIP event brackets")
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for i in range(steps):
-        db.evict(order[i])
-        evs[i][0].record(stream)
-        db.attend(order[i], rep[i])
-        evs[i][1].record(stream)
-    torch.cuda.synchronize()
-    bracket_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    bracket_us = None
+    if two_launch:
+        # Per-launch event brackets (diagnostic: they include each launch's dispatch latency).
+        log("timing decode_attn launches with HIP event brackets")
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for i in range(steps):
+            db.evict(order[i])
+            evs[i][0].record(stream)
+            db.attend(order[i], rep[i])
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        bracket_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
 
     def capture(fn):
         graph = torch.cuda.CUDAGraph()
@@ -273,27 +288,32 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     step_us = time_graph(fused_graph) / steps
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during the timed fused steps")
-    log("timing the two-launch steps as a replayed HIP graph")
-    step_graph = capture(lambda: [db.step(order[i], rep[i]) for i in range(steps)])
-    two_launch_us = time_graph(step_graph) / steps
-    if M.murmur_device_error() != 0:
-        raise RuntimeError("device error during the timed steps")
+    io = db.io_bytes()
+    if two_launch:
+        log("timing the two-launch steps as a replayed HIP graph")
+        step_graph = capture(lambda: [db.step(order[i], rep[i]) for i in range(steps)])
+        two_launch_us = time_graph(step_graph) / steps
+        if M.murmur_device_error() != 0:
+            raise RuntimeError("device error during the timed steps")
 
-    # decode_attn alone: the same launches back to back (retained set of the first timed step, each launch
-    # reading the next KV replica), so the mean is the kernel's own duration.
-    log("timing decode_attn launches as a replayed HIP graph")
-    db.evict(order[0])
-    attn_graph = capture(lambda: [db.attend(order[i], rep[i]) for i in range(steps)])
-    attn_us = time_graph(attn_graph) / steps
-    if M.murmur_device_error() != 0:
-        raise RuntimeError("device error during the timed decode_attn launches")
+        # decode_attn alone: the same launches back to back (retained set of the first timed step, each
+        # launch reading the next KV replica), so the mean is the kernel's own duration.
+        log("timing decode_attn launches as a replayed HIP graph")
+        db.evict(order[0])
+        attn_graph = capture(lambda: [db.attend(order[i], rep[i]) for i in range(steps)])
+        attn_us = time_graph(attn_graph) / steps
+        if M.murmur_device_error() != 0:
+            raise RuntimeError("device error during the timed decode_attn launches")
+        alg_bytes = float(kv_step[order[0]] + io)  # every launch of the decode_attn graph reads this set
+    else:
+        two_launch_us = None
+        attn_us = step_us
+        alg_bytes = float(np.mean([kv_step[o] for o in order]) + io)
 
     ring = None
     if with_ring:
         ring = ring_timing(wl, n_steps, steps, warmup, replicas_for(wl, kv_step), split_len, capture, time_graph)
 
-    io = db.io_bytes()
-    alg_bytes = float(kv_step[order[0]] + io)  # every launch of the decode_attn graph reads this set
     achieved = float(alg_bytes / (attn_us * 1e-6) / 1e9)
     res = {
         "metric": METRIC,
@@ -310,17 +330,18 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         "data": "synthetic",
         "config": {"workload": f"{config}: {DESCRIPTIONS[config]}", "batch": wl.batch, "layers": wl.n_layers,
                    "q_heads": wl.hq, "kv_heads": wl.hkv, "head_dim": wl.head_dim,
-                   "retained_per_step": int(np.mean([int(counts[o].sum()) for o in order])),
+                   "retained_per_step": int(np.mean([int(counts[o].sum()) for o in order]) / wl.n_layers),
                    "kv_replicas": replicas, "selection": "ranges" if use_ranges else "index list",
                    "split_len": db.split_len or "auto"},
-        "step_two_launches_us": round(two_launch_us, 3),
+        "step_two_launches_us": round(two_launch_us, 3) if two_launch else None,
         "decode_attn_us": round(attn_us, 3),
-        "decode_attn_event_bracket_us": {"mean": round(float(bracket_us.mean()), 3),
-                                         "median": round(float(np.median(bracket_us)), 3),
-                                         "p90": round(float(np.percentile(bracket_us, 90)), 3)},
+        "decode_attn_event_bracket_us": None if bracket_us is None else {
+            "mean": round(float(bracket_us.mean()), 3), "median": round(float(np.median(bracket_us)), 3),
+            "p90": round(float(np.percentile(bracket_us, 90)), 3)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": committed_traffic(config),
-                     "kernel": "decode_attn", "alg_bytes_per_launch": int(alg_bytes)},
+                     "kernel": "decode_attn" if two_launch else "decode_step (fused; per-layer policies)",
+                     "alg_bytes_per_launch": int(alg_bytes)},
     }
     if ring is not None:
         res["ring"] = ring
@@ -403,7 +424,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="c3", help="workload: c1, c2, c3, c4_dense, c4_evict, c5")
+    ap.add_argument("--config", default="c3", help="workload: c1, c2, c3, c4_dense, c4_evict, c5, c5_layers")
     ap.add_argument("--replicas", type=int, default=None, help="KV cache replicas to rotate over (default: auto)")
     ap.add_argument("--split-len", type=int, default=0)
     ap.add_argument("--index-list", action="store_true", help="attend from the index list instead of ranges")

@@ -55,6 +55,16 @@ enum {
 
 enum { MURMUR_DTYPE_BF16 = 1, MURMUR_DTYPE_F32 = 2 };
 
+/* Policy array layouts (the pol_per_seq argument, a bit set).  The array holds
+ * [per layer ? n_layers : 1][per sequence ? B : 1] murmur_policy records;
+ * (layer, sequence b) uses record
+ *   (PER_LAYER ? layer * (PER_SEQ ? B : 1) : 0) + (PER_SEQ ? b : 0).
+ * PER_LAYER is accepted by the fused steps only (the paper finds the speech
+ * sparsity on 24 of its model's 28 layers, Section 1 and Section 2.3, so a
+ * model may keep some layers dense); it makes their retained-set outputs
+ * per layer too. */
+enum { MURMUR_POL_PER_SEQ = 1, MURMUR_POL_PER_LAYER = 2 };
+
 /* split_len value selecting the persistent stream schedule of murmur_decode_attn. */
 #define MURMUR_SPLIT_STREAM (-1)
 
@@ -118,7 +128,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 3
+#define MURMUR_ABI_VERSION 4
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -218,9 +228,15 @@ int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *id
  * form, so nothing waits for a separate eviction launch; the results are
  * those of murmur_evict_compact followed by murmur_decode_attn with the range
  * table, bit for bit in the retained sets.
- *   seg_dev, pol_dev, pol_per_seq: as murmur_evict_compact;
+ *   seg_dev:    device [B], as murmur_evict_compact;
+ *   pol_dev, pol_per_seq: device policy records in the layout the
+ *               MURMUR_POL_* bits of pol_per_seq give (0..3);
  *   idx_dev, count_dev, ranges_dev: nullable outputs, written as
- *               murmur_evict_compact writes them (idx_dev [B][max_keep]);
+ *               murmur_evict_compact writes them (idx_dev [B][max_keep]),
+ *               with MURMUR_POL_PER_LAYER one set per layer
+ *               ([n_layers][B][max_keep], [n_layers][B], [n_layers][B][6][2]);
+ *   split_len:  as murmur_decode_attn; MURMUR_SPLIT_STREAM takes per-sequence
+ *               policies only (MURMUR_EUNSUPPORTED with MURMUR_POL_PER_LAYER);
  *   every other argument: as murmur_decode_attn (same workspace size).
  * Device errors: MURMUR_DEVERR_POLICY and MURMUR_DEVERR_OVERFLOW as
  * murmur_evict_compact, MURMUR_DEVERR_COUNT for the same sequences (their
@@ -275,6 +291,8 @@ int murmur_ring_layout_host(const murmur_seg *seg, const murmur_policy *pol, int
  * head) of kv->k and kv->v, which must therefore be writable.
  *   idx_dev, count_dev, ranges_dev: nullable outputs as murmur_decode_step,
  *               in storage rows (idx in piece order, not ascending);
+ *   pol_per_seq: MURMUR_POL_* bits as murmur_decode_step (the ring must hold
+ *               the retained outputs of every layer's policy);
  *   split_len:  as murmur_decode_attn, except MURMUR_SPLIT_STREAM
  *               (MURMUR_EUNSUPPORTED);
  *   every other argument: as murmur_decode_step.

@@ -315,7 +315,10 @@ MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_pol
                                      float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
                                      void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
     if (!seg_dev || !pol_dev) return fail(MURMUR_EINVAL, "seg_dev and pol_dev must not be NULL");
-    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (pol_per_seq < 0 || pol_per_seq > (MURMUR_POL_PER_SEQ | MURMUR_POL_PER_LAYER))
+        return fail(MURMUR_EINVAL, "pol_per_seq must be a set of MURMUR_POL_* bits (0..3, got %d)", pol_per_seq);
+    if ((pol_per_seq & MURMUR_POL_PER_LAYER) && split_len == MURMUR_SPLIT_STREAM)
+        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes per-sequence policies only");
     if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
         !aligned(ranges_dev, 4))
         return fail(MURMUR_EINVAL, "seg/pol/idx/count/ranges pointers must be 4-byte aligned");
@@ -374,7 +377,8 @@ MURMUR_EXPORT int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmu
                                           int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
                                           void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
     if (!seg_dev || !pol_dev || !ring) return fail(MURMUR_EINVAL, "seg_dev, pol_dev and ring must not be NULL");
-    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (pol_per_seq < 0 || pol_per_seq > (MURMUR_POL_PER_SEQ | MURMUR_POL_PER_LAYER))
+        return fail(MURMUR_EINVAL, "pol_per_seq must be a set of MURMUR_POL_* bits (0..3, got %d)", pol_per_seq);
     if (!ring->k_new || !ring->v_new) return fail(MURMUR_EINVAL, "ring->k_new and ring->v_new must not be NULL");
     if (!aligned(ring->k_new, 16) || !aligned(ring->v_new, 16))
         return fail(MURMUR_EINVAL, "ring->k_new and ring->v_new must be 16-byte aligned");

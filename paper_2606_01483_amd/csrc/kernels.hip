@@ -685,20 +685,27 @@ static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, co
 // computed in closed form by every workgroup that needs them, and the
 // evict_compact outputs written by one workgroup per sequence.
 // ---------------------------------------------------------------------------
+// Row of the policy array that applies to (layer, sequence b): the array is
+// [per layer ? NL : 1][per sequence ? B : 1] policies (MURMUR_POL_* bits).
+static __device__ __forceinline__ int policy_row(int32_t pol_mode, int layer, int b, int B) {
+    const int per_seq = pol_mode & MURMUR_POL_PER_SEQ;
+    return ((pol_mode & MURMUR_POL_PER_LAYER) ? layer * (per_seq ? B : 1) : 0) + (per_seq ? b : 0);
+}
+
 // Count of sequence b and, unless kSrcIndex, its range table.  p0/p1: counts
 // (kSrcIndex) or range tables (kSrcRanges, the count being the table's total
 // length), or (kSrcLayout, kSrcRing) layouts (murmur_seg [B]) and policies
-// (murmur_policy [1] or [B]).  kSrcRing gives the pieces in ring-storage rows
+// (murmur_policy rows, see policy_row).  kSrcRing gives the pieces in ring-storage rows
 // of ring_cap output slots and the row of the current token in `cur`.  An
 // invalid layout or policy gives count 0 and sets policy_bad to 1 (2: the
 // ring cannot hold the retained outputs).
 template <int kSrc>
-static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t *p1, int b, int32_t pol_per_seq,
-                                                int32_t ring_cap, int32_t (&rg)[2 * kPieces], int &policy_bad,
-                                                int32_t &cur) {
+static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t *p1, int b, int32_t pol_mode,
+                                                int layer, int B, int32_t ring_cap, int32_t (&rg)[2 * kPieces],
+                                                int &policy_bad, int32_t &cur) {
     if (kSrc == kSrcLayout || kSrc == kSrcRing) {
         const int32_t *sg = p0 + 4 * b;
-        const int32_t *pl = p1 + (pol_per_seq ? 5 * b : 0);
+        const int32_t *pl = p1 + 5 * policy_row(pol_mode, layer, b, B);
         const int32_t s0 = sg[0], s1 = sg[1], s2 = sg[2], s3 = sg[3];
         const int32_t w0 = pl[0], w1 = pl[1], w2 = pl[2], w3 = pl[3], w4 = pl[4];
         if (kSrc == kSrcRing)
@@ -1011,8 +1018,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
     int32_t cur = -1;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, a.ring_cap, rg, policy_bad, cur);
     const int layer = (int)blockIdx.y / Hkv;
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur);
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
     const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
@@ -1078,8 +1085,10 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kOWaveBytes / 4, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
-    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 && layer == 0)
-        write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
+    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 &&
+        (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
+        write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
+                       max_keep, tid);
     if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
@@ -1130,8 +1139,8 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
     int32_t cur = -1;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, a.ring_cap, rg, policy_bad, cur);
     const int layer = (int)blockIdx.y / Hkv;
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur);
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
     const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
@@ -1230,8 +1239,10 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kStageWaveFloats, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
-    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 && layer == 0)
-        write_retained(a, b, cnt_seq, policy_bad, rg, max_keep, tid);
+    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 &&
+        (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
+        write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
+                       max_keep, tid);
     if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
@@ -1374,7 +1385,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
         int32_t rg[2 * kPieces];
         int policy_bad = 0;
         int32_t unused_cur;
-        const int c = seq_count<kSrc>(src0, src1, t, pol_per_seq, 0, rg, policy_bad, unused_cur);
+        const int c = seq_count<kSrc>(src0, src1, t, pol_per_seq, 0, B, 0, rg, policy_bad, unused_cur);
         const bool badc = c < 1 || c > max_keep;
         const int cc = c < 0 ? 0 : (c > max_keep ? max_keep : c);
         s_cnt[t] = cc;
@@ -1626,7 +1637,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
             int32_t rg[2 * kPieces];
             int policy_bad = 0;
             int32_t unused_cur;
-            const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, 0, rg, policy_bad, unused_cur);
+            const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, 0, B, 0, rg, policy_bad, unused_cur);
             write_retained(a, bb, c, policy_bad, rg, max_keep, tid);
         }
     }

@@ -18,6 +18,24 @@ from . import murmur as M
 from .workloads import Workload
 
 
+def pol_mode(policy: np.ndarray) -> int:
+    """MURMUR_POL_* bits of a workload's policy array: [B, 5] per sequence, [NL, B, 5] per layer too."""
+    return M.MURMUR_POL_PER_SEQ | (M.MURMUR_POL_PER_LAYER if np.ndim(policy) == 3 else 0)
+
+
+def layer_policies(wl: Workload) -> list[np.ndarray]:
+    """The [B, 5] policy of every layer."""
+    if np.ndim(wl.policy) == 3:
+        return [wl.policy[layer] for layer in range(wl.n_layers)]
+    return [wl.policy] * wl.n_layers
+
+
+def retained_counts(wl: Workload, step: int) -> np.ndarray:
+    """Retained counts [NL, B] at a step, from the host closed form (murmur_retained_count_host)."""
+    seg = wl.seg(step)
+    return np.stack([M.murmur_retained_count_host(seg, pol, 1)[0] for pol in layer_policies(wl)])
+
+
 class DecodeBatch:
     def __init__(self, wl: Workload, device: str = "cuda", replicas: int = 1, out_dtype: int = M.MURMUR_DTYPE_BF16,
                  split_len: int = 0, use_ranges: bool = True, steps: list[int] | None = None,
@@ -32,7 +50,9 @@ class DecodeBatch:
         self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
 
         # Sizing from the host closed form over every step this batch will run.
-        counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[1] for s in self.steps]
+        self.pol_mode = pol_mode(wl.policy)
+        self.per_layer = bool(self.pol_mode & M.MURMUR_POL_PER_LAYER)
+        counts = [int(retained_counts(wl, s).max()) for s in self.steps]
         self.max_keep = int(max(counts)) if max_keep is None else int(max_keep)
 
         dev = self.device
@@ -54,9 +74,11 @@ class DecodeBatch:
 
         # Two sets of retained-set buffers, so that the eviction of the next step can run while the
         # attention of the current one still reads its set.
-        self.sets = [(torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev),
-                      torch.zeros(B, dtype=torch.int32, device=dev),
-                      torch.zeros((B, M.N_PIECES, 2), dtype=torch.int32, device=dev)) for _ in range(2)]
+        # (with per-layer policies the fused step writes one set per layer: [NL][B] rows)
+        rows = NL * B if self.per_layer else B
+        self.sets = [(torch.full((rows, self.max_keep), -1, dtype=torch.int32, device=dev),
+                      torch.zeros(rows, dtype=torch.int32, device=dev),
+                      torch.zeros((rows, M.N_PIECES, 2), dtype=torch.int32, device=dev)) for _ in range(2)]
         self.idx, self.count, self.ranges = self.sets[0]
         odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
         self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
@@ -66,6 +88,8 @@ class DecodeBatch:
 
     def evict(self, i: int, stream=None, buf: int = 0) -> None:
         """murmur_evict_compact for the i-th step of this batch into retained-set buffer `buf`."""
+        if self.per_layer:
+            raise ValueError("per-layer policies run on the fused step only")
         idx, count, ranges = self.sets[buf]
         M.murmur_evict_compact(self.seg[i], self.pol, 1, self.B, idx, self.max_keep, count, ranges, stream)
 
@@ -84,7 +108,7 @@ class DecodeBatch:
         """murmur_decode_step for the i-th step: eviction and attention in one launch, the retained-set
         outputs (index list, count, range table) written into buffer set `buf` when `outputs`."""
         idx, count, ranges = self.sets[buf] if outputs else (None, None, None)
-        M.murmur_decode_step(self.seg[i], self.pol, 1, self.q[i], self.kv[replica], idx, count, ranges,
+        M.murmur_decode_step(self.seg[i], self.pol, self.pol_mode, self.q[i], self.kv[replica], idx, count, ranges,
                              self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale, self.split_len,
                              self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes, stream)
 
@@ -117,14 +141,15 @@ class DecodeBatch:
         attn_stream.wait_stream(evict_stream)
 
     def kv_bytes_read(self, i: int) -> int:
-        """Algorithmic K/V bytes of step i: retained positions x layers x KV heads x (K + V) x D x 2 B."""
-        counts, _ = M.murmur_retained_count_host(self.wl.seg(self.steps[i]), self.wl.policy, 1)
-        return int(counts.sum()) * self.NL * self.Hkv * 2 * self.D * 2
+        """Algorithmic K/V bytes of step i: retained positions of every layer x KV heads x (K + V) x D x 2 B."""
+        return int(retained_counts(self.wl, self.steps[i]).sum()) * self.Hkv * 2 * self.D * 2
 
     def io_bytes(self) -> int:
         """Algorithmic bytes besides K/V: queries, outputs, lse, count and range table (or index list)."""
         out_b = 4 if self.out_dtype == M.MURMUR_DTYPE_F32 else 2
         n = self.NL * self.B * self.Hq
+        if self.per_layer:  # the fused step reads layouts and per-layer policies
+            return n * self.D * 2 + n * self.D * out_b + n * 4 + self.B * 16 + self.NL * self.B * 20
         sel = self.B * M.N_PIECES * 2 * 4 if self.use_ranges else self.B * self.max_keep * 4
         return n * self.D * 2 + n * self.D * out_b + n * 4 + self.B * 4 + sel
 
@@ -173,8 +198,11 @@ class RingBatch:
         self.split_len = split_len
         B, NL, Hq, Hkv, D = wl.batch, wl.n_layers, wl.hq, wl.hkv, wl.head_dim
         self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
-        n_sink = wl.policy[:, 4]
-        counts = [M.murmur_retained_count_host(wl.seg(s), wl.policy, 1)[1] for s in self.steps]
+        self.pol_mode = pol_mode(wl.policy)
+        n_sink = layer_policies(wl)[0][:, 4]  # the output sinks precede the ring: one count per sequence
+        if any(not np.array_equal(p[:, 4], n_sink) for p in layer_policies(wl)):
+            raise ValueError("ring storage needs the same output sink count in every layer")
+        counts = [int(retained_counts(wl, s).max()) for s in self.steps]
         self.max_keep = int(max(counts))
         seg_before = wl.seg(self.steps[0])
         seg_before[:, 3] -= 1  # the state before the first step: its token is not appended yet
@@ -210,9 +238,10 @@ class RingBatch:
         self.v_new = torch.from_numpy(vnew).view(torch.bfloat16).to(dev)
         self.ring = [M.make_ring(cap, self.k_new[i], self.v_new[i]) for i in range(len(self.steps))]
 
-        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
-        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
-        self.ranges = torch.zeros((B, M.N_PIECES, 2), dtype=torch.int32, device=dev)
+        rows = NL * B if self.pol_mode & M.MURMUR_POL_PER_LAYER else B
+        self.idx = torch.full((rows, self.max_keep), -1, dtype=torch.int32, device=dev)
+        self.count = torch.zeros(rows, dtype=torch.int32, device=dev)
+        self.ranges = torch.zeros((rows, M.N_PIECES, 2), dtype=torch.int32, device=dev)
         odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
         self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
         self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
@@ -222,7 +251,8 @@ class RingBatch:
     def step(self, i: int, replica: int = 0, stream=None, outputs: bool = True) -> None:
         """murmur_decode_step_ring for the i-th step of this batch on storage replica `replica`."""
         idx, count, ranges = (self.idx, self.count, self.ranges) if outputs else (None, None, None)
-        M.murmur_decode_step_ring(self.seg[i], self.pol, 1, self.ring[i], self.q[i], self.kv[replica], idx, count,
+        M.murmur_decode_step_ring(self.seg[i], self.pol, self.pol_mode, self.ring[i], self.q[i], self.kv[replica],
+                                  idx, count,
                                   ranges, self.max_keep, self.B, self.Hq, self.Hkv, self.D, self.wl.scale,
                                   self.split_len, self.out, self.out_dtype, self.lse, self.ws, self.ws_bytes,
                                   stream)

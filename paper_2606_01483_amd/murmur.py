@@ -19,6 +19,7 @@ MURMUR_OK, MURMUR_EINVAL, MURMUR_EUNSUPPORTED, MURMUR_ENOSPACE, MURMUR_EHIP = 0,
 MURMUR_DTYPE_BF16, MURMUR_DTYPE_F32 = 1, 2
 MURMUR_DEVERR_OVERFLOW, MURMUR_DEVERR_POLICY, MURMUR_DEVERR_POSITION, MURMUR_DEVERR_COUNT = 1, 2, 4, 8
 MURMUR_DEVERR_CAPACITY = 16
+MURMUR_POL_PER_SEQ, MURMUR_POL_PER_LAYER = 1, 2
 N_PIECES = 6
 SPLIT_UNIT = 128
 MURMUR_SPLIT_STREAM = -1

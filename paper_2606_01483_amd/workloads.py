@@ -61,7 +61,8 @@ class Workload:
 
     seg0:   int32 [B, 4] (prompt_pre, speech_len, prompt_mid, out_len) before step 0;
             at step s the current token is output number out_len0 + s + 1.
-    policy: int32 [B, 5] (speech_window, speech_delay, speech_sink, out_window, out_sink).
+    policy: int32 [B, 5] (speech_window, speech_delay, speech_sink, out_window, out_sink),
+            or [NL, B, 5] for a policy per layer.
     k, v:   uint16 bf16 bits [NL, B, Hkv, max_len, D]; positions past a sequence's
             last step hold bf16 NaN, so reading them cannot go unnoticed.
     """
@@ -129,6 +130,8 @@ def build(name: str, seed: int, n_layers: int, seg0: np.ndarray, policy: np.ndar
     policy = np.ascontiguousarray(policy, dtype=np.int32)
     if policy.ndim == 1:
         policy = np.repeat(policy.reshape(1, 5), B, axis=0)
+    if policy.ndim == 3 and policy.shape != (n_layers, B, 5):
+        raise ValueError("a per-layer policy is [n_layers, B, 5]")
     final_len = seg0[:, 0].astype(np.int64) + seg0[:, 1] + seg0[:, 2] + seg0[:, 3] + steps
     max_len = int(final_len.max())
     max_len = (max_len + 7) // 8 * 8
@@ -196,6 +199,7 @@ def layout(config: str, steps: int | None = None) -> Layout:
     c4_evict  the same with speech window 2048 (delay 512) and output window 512.
     c5        28 layers x 12 chunks: speech U{1800..2250}, output U{300..1200}, speech window
               floor(L_s/4) (delay 512), output window 256, planted keys, 256 steps.
+    c5_layers c5 with its first 4 layers dense (no eviction) and the c5 policy on the other 24.
     """
     if config == "c1":
         seed = 1001
@@ -229,6 +233,14 @@ def layout(config: str, steps: int | None = None) -> Layout:
         pol = np.stack([l_s // 4, np.full(12, 512), np.zeros(12), np.full(12, 256), np.zeros(12)],
                        axis=1).astype(np.int32)
         return _layout("c5", seed, 28, seg0, pol, steps or 256, planted=True)
+    if config == "c5_layers":
+        # c5 with the first DENSE_LAYERS layers dense: the paper finds the speech sparsity on 24 of the
+        # 28 layers (Section 1, Section 2.3), strongest in the deeper ones.
+        base = layout("c5", steps)
+        pol = np.repeat(base.policy[None], base.n_layers, axis=0)
+        pol[:DENSE_LAYERS] = np.array([OFF, 0, 0, OFF, 0], dtype=np.int32)
+        return Layout(name="c5_layers", seed=base.seed, n_layers=base.n_layers, steps=base.steps, seg0=base.seg0,
+                      policy=pol, planted=True)
     raise KeyError(f"unknown workload {config!r}")
 
 
@@ -241,6 +253,8 @@ def _layout(name, seed, n_layers, seg0, pol, steps, planted) -> Layout:
 
 
 CONFIGS = ("c1", "c2", "c3", "c4_dense", "c4_evict", "c5")
+DENSE_LAYERS = 4
+EXTRA_CONFIGS = ("c5_layers",)  # per-layer policies: fused steps only
 
 # Eviction policies of the paper's ablations, all on 300 s chunks decoded in a batch of 16 (Section 4,
 # Tables 2-4): (speech_window, speech_delay, speech_sink, out_window, out_sink).  Table 3 varies

@@ -45,7 +45,7 @@ def test_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 3
+    assert M.murmur_abi_version() == 4
 
 
 def test_retained_count_host_matches_oracle():
@@ -233,7 +233,9 @@ def call_step(a, seg=FAKE, pol=FAKE, pol_per_seq=0):
 @pytest.mark.parametrize("over,step_kw,code", [
     ({}, dict(seg=None), M.MURMUR_EINVAL),
     ({}, dict(pol=None), M.MURMUR_EINVAL),
-    ({}, dict(pol_per_seq=2), M.MURMUR_EINVAL),
+    ({}, dict(pol_per_seq=4), M.MURMUR_EINVAL),
+    ({}, dict(pol_per_seq=-1), M.MURMUR_EINVAL),
+    (dict(split_len=M.MURMUR_SPLIT_STREAM), dict(pol_per_seq=M.MURMUR_POL_PER_LAYER), M.MURMUR_EUNSUPPORTED),
     ({}, dict(seg=FAKE + 2), M.MURMUR_EINVAL),
     (dict(idx=FAKE + 1), {}, M.MURMUR_EINVAL),
     (dict(q=None), {}, M.MURMUR_EINVAL),
