@@ -306,6 +306,41 @@ int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmur_policy *pol_
                             int32_t out_dtype, float *lse_dev, void *ws_dev, size_t ws_bytes,
                             murmur_stream_t stream);
 
+/* Chunked inference, host only (Section 3.1).  Packs the speech segments a
+ * voice-activity detector found into chunks of at most max_chunk seconds,
+ * greedily in time order, so that the chunks tile the recording from 0:
+ * chunk i covers [chunk_start[i], chunk_start[i] + chunk_len[i]) and
+ * chunk_start[i] is the sum of the lengths before it, the offset of
+ * Equation 4.  A chunk takes the next segment while that segment ends within
+ * max_chunk of the chunk's start; it then ends where the next segment begins
+ * (so it keeps the silence after its last segment), or max_chunk after its
+ * start if that comes first.  A segment longer than max_chunk is cut at
+ * chunk boundaries; no other segment is cut (a chunk whose limit falls
+ * inside such a segment ends where the segment begins, even if it then holds
+ * only silence: the offsets need the tiling).  The last chunk ends at audio_len or max_chunk after its start,
+ * whichever comes first; a recording without segments gives no chunk.
+ *   seg_start, seg_end: [n_seg] seconds, 0 <= start < end <= audio_len,
+ *               sorted by start, not overlapping (n_seg may be 0);
+ *   chunk_start[i] equals the sum of chunk_len[0 .. i-1] up to rounding;
+ *   chunk_of_seg: [n_seg] (nullable) chunk holding each segment's start;
+ *   chunk_start, chunk_len: [max_chunks] outputs; *n_chunks: chunks written.
+ *   speech_tokens (nullable): [max_chunks] speech tokens of each chunk at
+ *               tokens_per_s (the speech_len of its murmur_seg: the chunk's
+ *               length times the rate, rounded to nearest).
+ * Errors: MURMUR_EINVAL (unsorted or overlapping segments, a segment outside
+ * [0, audio_len], max_chunk <= 0, tokens_per_s < 0), MURMUR_ENOSPACE (more
+ * than max_chunks chunks; *n_chunks then holds the number needed). */
+int murmur_plan_chunks(const double *seg_start, const double *seg_end, int32_t n_seg, double audio_len,
+                       double max_chunk, double tokens_per_s, int32_t *chunk_of_seg, double *chunk_start,
+                       double *chunk_len, int32_t *speech_tokens, int32_t max_chunks, int32_t *n_chunks);
+
+/* Equation 4: absolute timestamps from chunk-relative ones,
+ * t[k] = t_local[k] + offset(chunk[k]), offset(i) = chunk_len[0] + ... +
+ * chunk_len[i-1].  Host only.  Errors: MURMUR_EINVAL for a chunk index
+ * outside [0, n_chunks) or a negative chunk length. */
+int murmur_chunk_timestamps(const double *t_local, const int32_t *chunk, int32_t n, const double *chunk_len,
+                            int32_t n_chunks, double *t);
+
 /* Synchronises `stream`, returns the device error word of the current device
  * in *code (0 = none) and clears it.  Not for use inside a captured graph. */
 int murmur_device_error(murmur_stream_t stream, int32_t *code);

@@ -410,6 +410,87 @@ MURMUR_EXPORT int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmu
     return ok();
 }
 
+MURMUR_EXPORT int murmur_plan_chunks(const double *seg_start, const double *seg_end, int32_t n_seg,
+                                     double audio_len, double max_chunk, double tokens_per_s, int32_t *chunk_of_seg,
+                                     double *chunk_start, double *chunk_len, int32_t *speech_tokens,
+                                     int32_t max_chunks, int32_t *n_chunks) {
+    if (!n_chunks || (n_seg > 0 && (!seg_start || !seg_end)) || (max_chunks > 0 && (!chunk_start || !chunk_len)))
+        return fail(MURMUR_EINVAL, "missing segment or chunk arrays");
+    if (n_seg < 0 || max_chunks < 0) return fail(MURMUR_EINVAL, "n_seg and max_chunks must be >= 0");
+    if (!(max_chunk > 0) || !(audio_len >= 0) || !(tokens_per_s >= 0) || !isfinite(audio_len) ||
+        !isfinite(max_chunk) || !isfinite(tokens_per_s))
+        return fail(MURMUR_EINVAL, "audio_len and tokens_per_s must be >= 0 and max_chunk > 0, all finite");
+    for (int32_t i = 0; i < n_seg; ++i) {
+        if (!(seg_start[i] >= 0) || !(seg_end[i] > seg_start[i]) || !(seg_end[i] <= audio_len))
+            return fail(MURMUR_EINVAL, "segment %d [%g, %g) is empty or outside [0, %g]", i, seg_start[i], seg_end[i],
+                        audio_len);
+        if (i > 0 && seg_start[i] < seg_end[i - 1])
+            return fail(MURMUR_EINVAL, "segment %d starts before segment %d ends (unsorted or overlapping)", i, i - 1);
+    }
+    // Pass 1: chunk boundaries.  `speech`: the open chunk holds (part of) a segment.
+    int32_t n = 0;
+    auto emit = [&](double start, double len) {
+        if (n < max_chunks) {
+            chunk_start[n] = start;
+            chunk_len[n] = len;
+            if (speech_tokens) speech_tokens[n] = (int32_t)llround(len * tokens_per_s);
+        }
+        ++n;
+    };
+    double start = 0.0;
+    bool speech = false;
+    for (int32_t i = 0; i < n_seg;) {
+        if (seg_end[i] - start <= max_chunk) {  // segment i (or what is left of it) ends within the chunk
+            speech = true;
+            ++i;
+            continue;
+        }
+        // Segment i does not end within the chunk: close the chunk max_chunk after its start, unless that
+        // falls inside segment i and the segment can stay whole (it fits a chunk of its own) or the chunk
+        // already holds speech before it: then where the segment begins.
+        double end = start + max_chunk;
+        const bool whole = seg_end[i] - seg_start[i] <= max_chunk;
+        if ((speech || whole) && seg_start[i] < end) end = seg_start[i];
+        emit(start, end - start);
+        start = end;
+        speech = false;
+    }
+    // The last chunk keeps the silence after the last segment, up to audio_len or max_chunk after its start.
+    if (n_seg > 0) emit(start, (audio_len < start + max_chunk ? audio_len : start + max_chunk) - start);
+    *n_chunks = n;
+    if (n > max_chunks) return fail(MURMUR_ENOSPACE, "%d chunks needed, %d allowed", n, max_chunks);
+    // Pass 2: the chunk holding each segment's start (chunks are in time order).
+    if (chunk_of_seg) {
+        int32_t c = 0;
+        for (int32_t i = 0; i < n_seg; ++i) {
+            while (c + 1 < n && chunk_start[c + 1] <= seg_start[i]) ++c;
+            chunk_of_seg[i] = c;
+        }
+    }
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_chunk_timestamps(const double *t_local, const int32_t *chunk, int32_t n,
+                                          const double *chunk_len, int32_t n_chunks, double *t) {
+    if (n < 0 || n_chunks < 0) return fail(MURMUR_EINVAL, "n and n_chunks must be >= 0");
+    if (n > 0 && (!t_local || !chunk || !t || !chunk_len)) return fail(MURMUR_EINVAL, "missing arrays");
+    for (int32_t c = 0; c < n_chunks; ++c)
+        if (!(chunk_len[c] >= 0)) return fail(MURMUR_EINVAL, "chunk %d has a negative length", c);
+    for (int32_t k = 0; k < n; ++k)
+        if (chunk[k] < 0 || chunk[k] >= n_chunks)
+            return fail(MURMUR_EINVAL, "timestamp %d names chunk %d of %d", k, chunk[k], n_chunks);
+    // offset(i): the lengths of the chunks before i, accumulated in order.
+    double *offset = new double[n_chunks > 0 ? n_chunks : 1];
+    double acc = 0.0;
+    for (int32_t c = 0; c < n_chunks; ++c) {
+        offset[c] = acc;
+        acc += chunk_len[c];
+    }
+    for (int32_t k = 0; k < n; ++k) t[k] = t_local[k] + offset[chunk[k]];
+    delete[] offset;
+    return ok();
+}
+
 MURMUR_EXPORT int murmur_device_error(murmur_stream_t stream, int32_t *code) {
     if (!code) return fail(MURMUR_EINVAL, "code must not be NULL");
     const int e = read_and_clear_device_error(stream, code);

@@ -92,6 +92,12 @@ def _load():
     lib.murmur_decode_step_ring.argtypes = [vp, vp, i32, ctypes.POINTER(murmur_ring), vp, ctypes.POINTER(murmur_kv),
                                             vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, i32, vp, i32, vp,
                                             vp, sz, vp]
+    f64p = ctypes.POINTER(ctypes.c_double)
+    lib.murmur_plan_chunks.restype = ctypes.c_int
+    lib.murmur_plan_chunks.argtypes = [f64p, f64p, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32p,
+                                       f64p, f64p, i32p, i32, i32p]
+    lib.murmur_chunk_timestamps.restype = ctypes.c_int
+    lib.murmur_chunk_timestamps.argtypes = [f64p, i32p, i32, f64p, i32, f64p]
     lib.murmur_device_error.restype = ctypes.c_int
     lib.murmur_device_error.argtypes = [vp, i32p]
     _lib = lib
@@ -244,6 +250,42 @@ def murmur_decode_step_ring(seg_dev, pol_dev, pol_per_seq: int, ring: murmur_rin
                                            _addr(ranges_dev), max_keep, B, Hq, Hkv, D, float(scale), split_len,
                                            _addr(out_dev), out_dtype, _addr(lse_dev), _addr(ws_dev), ws_bytes,
                                            _stream(stream)))
+
+
+def murmur_plan_chunks(seg_start, seg_end, audio_len: float, max_chunk: float = 300.0,
+                       tokens_per_s: float = 7.5):
+    """Chunked inference plan (host only).  Returns (chunk_start, chunk_len, speech_tokens, chunk_of_seg)."""
+    s0 = np.ascontiguousarray(seg_start, dtype=np.float64)
+    s1 = np.ascontiguousarray(seg_end, dtype=np.float64)
+    n_seg = int(s0.shape[0])
+    f64p, i32p = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)
+    n = ctypes.c_int32(0)
+    cap = max(1, n_seg + 1)
+    while True:
+        cs, cl = np.zeros(cap), np.zeros(cap)
+        tok, of = np.zeros(cap, dtype=np.int32), np.zeros(max(1, n_seg), dtype=np.int32)
+        rc = _load().murmur_plan_chunks(s0.ctypes.data_as(f64p), s1.ctypes.data_as(f64p), n_seg, float(audio_len),
+                                        float(max_chunk), float(tokens_per_s), of.ctypes.data_as(i32p),
+                                        cs.ctypes.data_as(f64p), cl.ctypes.data_as(f64p), tok.ctypes.data_as(i32p),
+                                        cap, ctypes.byref(n))
+        if rc == MURMUR_ENOSPACE and n.value > cap:
+            cap = n.value
+            continue
+        _check(rc)
+        k = n.value
+        return cs[:k], cl[:k], tok[:k], of[:n_seg]
+
+
+def murmur_chunk_timestamps(t_local, chunk, chunk_len):
+    """Equation 4 (host only): absolute timestamps from chunk-relative ones."""
+    tl = np.ascontiguousarray(t_local, dtype=np.float64)
+    ch = np.ascontiguousarray(chunk, dtype=np.int32)
+    cl = np.ascontiguousarray(chunk_len, dtype=np.float64)
+    out = np.zeros_like(tl)
+    f64p, i32p = ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)
+    _check(_load().murmur_chunk_timestamps(tl.ctypes.data_as(f64p), ch.ctypes.data_as(i32p), int(tl.shape[0]),
+                                           cl.ctypes.data_as(f64p), int(cl.shape[0]), out.ctypes.data_as(f64p)))
+    return out
 
 
 def murmur_device_error(stream=None) -> int:
