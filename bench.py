@@ -168,6 +168,31 @@ def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
                       f"{wl.hq} heads), retained set + fp64 attention, {threads} threads, {dt:.1f} s wall"}
 
 
+def read_ceiling(nbytes: int, steps: int, capture, time_graph, workgroups: int = 256) -> dict:
+    """The practical read ceiling: murmur_read_probe (a plain read-only streaming kernel, one workgroup
+    per compute unit) over the same byte count as one attention launch, each launch of a replayed graph
+    reading the next of enough regions to defeat the Infinity Cache; and over 1 GiB."""
+    import torch
+    from paper_2606_01483_amd import murmur as M
+    nbytes = max(16, nbytes // 16 * 16)
+    regions = max(2, math.ceil(2.2 * MALL_BYTES / nbytes))
+    buf = torch.empty(regions * nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(workgroups, dtype=torch.int32, device="cuda")
+    log(f"read ceiling: {nbytes / 1e6:.1f} MB x {regions} regions")
+    graph = capture(lambda: [M.murmur_read_probe(buf[(i % regions) * nbytes:], nbytes, workgroups, sink)
+                             for i in range(steps)])
+    us = time_graph(graph) / steps
+    del graph, buf
+    gib = 1 << 30
+    big = torch.empty(2 * gib, dtype=torch.uint8, device="cuda")
+    graph = capture(lambda: [M.murmur_read_probe(big[(i % 2) * gib:], gib, workgroups, sink) for i in range(8)])
+    us_gib = time_graph(graph) / 8
+    del graph, big
+    torch.cuda.empty_cache()
+    return {"bytes": nbytes, "workgroups": workgroups, "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1),
+            "us_1GiB": round(us_gib, 3), "GBps_1GiB": round(gib / us_gib / 1e3, 1)}
+
+
 def replicas_for(wl, kv_step: list[int]) -> int:
     """KV replicas to rotate over so that consecutive steps read more than 2.2 x the Infinity Cache
     (at most 24 GB of replicas)."""
@@ -310,6 +335,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         attn_us = step_us
         alg_bytes = float(np.mean([kv_step[o] for o in order]) + io)
 
+    ceiling = read_ceiling(int(alg_bytes), steps, capture, time_graph)
+
     ring = None
     if with_ring:
         ring = ring_timing(wl, n_steps, steps, warmup, replicas_for(wl, kv_step), split_len, capture, time_graph)
@@ -343,6 +370,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
                      "kernel": "decode_attn" if two_launch else "decode_step (fused; per-layer policies)",
                      "alg_bytes_per_launch": int(alg_bytes)},
     }
+    res["read_ceiling"] = ceiling
+    res["roofline"]["frac_of_read_ceiling"] = round(achieved / ceiling["GBps"], 4)
     if ring is not None:
         res["ring"] = ring
     if cpu:

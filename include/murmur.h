@@ -341,6 +341,18 @@ int murmur_plan_chunks(const double *seg_start, const double *seg_end, int32_t n
 int murmur_chunk_timestamps(const double *t_local, const int32_t *chunk, int32_t n, const double *chunk_len,
                             int32_t n_chunks, double *t);
 
+/* Measurement only (not part of the method): a plain read-only streaming
+ * kernel, the practical ceiling the attention's achieved HBM bandwidth is
+ * compared with.  n_workgroups workgroups of 256 threads each read a
+ * contiguous share of buf_dev[0, bytes) with 16-byte loads, eight per
+ * thread in flight, and keep an XOR of what they read; sink_dev
+ * [n_workgroups] (4-byte aligned) is written only if that XOR equals a fixed
+ * pattern, so the loads are not optimised away and nearly nothing is
+ * written.  buf_dev 16-byte aligned, bytes a positive multiple of 16,
+ * n_workgroups in [1, 65535].  Errors: MURMUR_EINVAL, MURMUR_EHIP. */
+int murmur_read_probe(const void *buf_dev, size_t bytes, int32_t n_workgroups, uint32_t *sink_dev,
+                      murmur_stream_t stream);
+
 /* Synchronises `stream`, returns the device error word of the current device
  * in *code (0 = none) and clears it.  Not for use inside a captured graph. */
 int murmur_device_error(murmur_stream_t stream, int32_t *code);

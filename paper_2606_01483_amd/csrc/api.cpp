@@ -491,6 +491,18 @@ MURMUR_EXPORT int murmur_chunk_timestamps(const double *t_local, const int32_t *
     return ok();
 }
 
+MURMUR_EXPORT int murmur_read_probe(const void *buf_dev, size_t bytes, int32_t n_workgroups, uint32_t *sink_dev,
+                                    murmur_stream_t stream) {
+    if (!buf_dev || !sink_dev) return fail(MURMUR_EINVAL, "buf_dev and sink_dev must not be NULL");
+    if (!aligned(buf_dev, 16) || !aligned(sink_dev, 4))
+        return fail(MURMUR_EINVAL, "buf_dev must be 16-byte and sink_dev 4-byte aligned");
+    if (bytes == 0 || bytes % 16 != 0) return fail(MURMUR_EINVAL, "bytes must be a positive multiple of 16");
+    if (n_workgroups < 1 || n_workgroups > 65535) return fail(MURMUR_EINVAL, "n_workgroups must be in [1, 65535]");
+    const int e = launch_read_probe(buf_dev, (int64_t)(bytes / 16), n_workgroups, sink_dev, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "read_probe launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
 MURMUR_EXPORT int murmur_device_error(murmur_stream_t stream, int32_t *code) {
     if (!code) return fail(MURMUR_EINVAL, "code must not be NULL");
     const int e = read_and_clear_device_error(stream, code);

@@ -86,6 +86,7 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
                          int32_t *idx, int32_t max_keep, int32_t *count, int32_t *ranges, murmur_stream_t stream);
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream);
 int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream);
+int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, uint32_t *sink, murmur_stream_t stream);
 int read_and_clear_device_error(murmur_stream_t stream, int32_t *code);
 const char *hip_error_text(int err);
 

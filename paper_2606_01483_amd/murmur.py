@@ -98,6 +98,8 @@ def _load():
                                        f64p, f64p, i32p, i32, i32p]
     lib.murmur_chunk_timestamps.restype = ctypes.c_int
     lib.murmur_chunk_timestamps.argtypes = [f64p, i32p, i32, f64p, i32, f64p]
+    lib.murmur_read_probe.restype = ctypes.c_int
+    lib.murmur_read_probe.argtypes = [vp, sz, i32, vp, vp]
     lib.murmur_device_error.restype = ctypes.c_int
     lib.murmur_device_error.argtypes = [vp, i32p]
     _lib = lib
@@ -286,6 +288,12 @@ def murmur_chunk_timestamps(t_local, chunk, chunk_len):
     _check(_load().murmur_chunk_timestamps(tl.ctypes.data_as(f64p), ch.ctypes.data_as(i32p), int(tl.shape[0]),
                                            cl.ctypes.data_as(f64p), int(cl.shape[0]), out.ctypes.data_as(f64p)))
     return out
+
+
+def murmur_read_probe(buf_dev, nbytes: int, n_workgroups: int, sink_dev, stream=None) -> None:
+    """Read-only streaming probe over buf_dev[0, nbytes) (measurement of the practical read ceiling)."""
+    _check(_load().murmur_read_probe(_addr(buf_dev), int(nbytes), int(n_workgroups), _addr(sink_dev),
+                                     _stream(stream)))
 
 
 def murmur_device_error(stream=None) -> int:

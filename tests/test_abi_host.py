@@ -38,7 +38,7 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -331,3 +331,12 @@ def test_ring_prefill_matches_the_oracle_appends():
         cache = rng.integers(1, 60000, size=(2, B, 2, L, 4)).astype(np.uint16)
         rows = max(OR.storage_len(seg[b], n_so[b], cap) for b in range(B))
         assert np.array_equal(ring_prefill(cache, seg, n_so, cap, rows), OR.append_all(cache, seg, n_so, cap, rows))
+
+
+def test_read_probe_rejects():
+    lib = M.lib()
+    assert lib.murmur_read_probe(None, 1024, 256, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 1000, 256, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 0, 256, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 1024, 0, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE + 8, 1024, 256, FAKE, 0) == M.MURMUR_EINVAL
