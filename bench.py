@@ -237,6 +237,27 @@ def ring_timing(wl, n_steps: int, steps: int, warmup: int, replicas: int, split_
             "kv_resident_bytes_linear": linear_rows * per_row}
 
 
+def paged_timing(wl, n_steps: int, steps: int, warmup: int, replicas: int, split_len: int, capture,
+                 time_graph, block_size: int = 16) -> dict:
+    """The same steps on a paged cache (blocks of 16 rows in one pool, [block][slot][kv head][D], a random block
+    table): murmur_evict_compact_paged + murmur_decode_attn over the pool's rows, and the attention alone."""
+    from paper_2606_01483_amd import murmur as M
+    from paper_2606_01483_amd.decode import PagedBatch
+    log(f"paged cache: blocks of {block_size}, {replicas} replica(s)")
+    pb = PagedBatch(wl, block_size, replicas=replicas, split_len=split_len, steps=list(range(n_steps)))
+    for i in range(warmup):
+        pb.step(i % n_steps, i % replicas)
+    graph = capture(lambda: [pb.step(i % n_steps, i % replicas) for i in range(steps)])
+    step_us = time_graph(graph) / steps
+    pb.evict(0)
+    graph = capture(lambda: [pb.attend(0, i % replicas) for i in range(steps)])
+    attn_us = time_graph(graph) / steps
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during the timed paged steps")
+    return {"block_size": block_size, "pool_layout": "block, slot, kv head, head dim",
+            "step_two_launches_us": round(step_us, 3), "decode_attn_us": round(attn_us, 3)}
+
+
 def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, cpu_budget: float,
         split_len: int, use_ranges: bool, with_ring: bool = True) -> dict:
     import torch
@@ -340,6 +361,9 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     ring = None
     if with_ring:
         ring = ring_timing(wl, n_steps, steps, warmup, replicas_for(wl, kv_step), split_len, capture, time_graph)
+    paged = None
+    if with_ring and two_launch and split_len >= 0:
+        paged = paged_timing(wl, n_steps, steps, warmup, replicas_for(wl, kv_step), split_len, capture, time_graph)
 
     achieved = float(alg_bytes / (attn_us * 1e-6) / 1e9)
     res = {
@@ -374,6 +398,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     res["roofline"]["frac_of_read_ceiling"] = round(achieved / ceiling["GBps"], 4)
     if ring is not None:
         res["ring"] = ring
+    if paged is not None:
+        res["paged"] = paged
     if cpu:
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
         log(f"timing the fp64 oracle on {threads} host threads")

@@ -75,6 +75,7 @@ enum {
     MURMUR_DEVERR_POSITION = 4,  /* decode_attn: retained position outside [0, max_len) */
     MURMUR_DEVERR_COUNT = 8,     /* decode_attn: count outside [1, max_keep] */
     MURMUR_DEVERR_CAPACITY = 16, /* decode_step_ring: the output ring cannot hold the retained outputs */
+    MURMUR_DEVERR_BLOCK = 32,    /* evict_compact_paged: a retained position past the block table */
 };
 
 /* One sequence (audio chunk) of the batch, Section 3.2's layout
@@ -128,7 +129,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 4
+#define MURMUR_ABI_VERSION 5
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -163,6 +164,29 @@ int murmur_retained_count_host(const murmur_seg *seg, const murmur_policy *pol, 
 int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
                          int32_t B, int32_t *idx_dev, int32_t max_keep, int32_t *count_dev,
                          int32_t *ranges_dev, murmur_stream_t stream);
+
+/* Paged KV cache (the block tables of a paged-attention engine such as vLLM,
+ * the paper's second engine, Section 3.1): every sequence's positions live
+ * in blocks of block_size rows of one shared pool, position p of sequence b
+ * in pool row block_table[b][p / block_size] * block_size + p % block_size.
+ * murmur_evict_compact_paged emits the retained set of every sequence (as
+ * murmur_evict_compact) with the index list in pool rows, ready for
+ * murmur_decode_attn in index-list mode over a murmur_kv that describes the
+ * pool as one sequence of rows: stride_b = 0, max_len = pool rows, and for a
+ * pool laid out [block][slot][kv_head][D] stride_pos = Hkv*D, stride_h = D
+ * (or [kv_head][block][slot][D]: stride_pos = D, stride_h = pool rows * D).
+ *   block_table_dev: device int32 [B][max_blocks], physical block numbers;
+ *   block_size: a power of two;
+ *   count_dev, ranges_dev: as murmur_evict_compact (ranges in sequence
+ *               positions, not pool rows).
+ * Errors as murmur_evict_compact; device error MURMUR_DEVERR_BLOCK (entry -1)
+ * for a retained position past max_blocks blocks.  Table entries are not
+ * range-checked here: a row outside the pool is reported by
+ * murmur_decode_attn (MURMUR_DEVERR_POSITION, NaN outputs). */
+int murmur_evict_compact_paged(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                               int32_t B, const int32_t *block_table_dev, int32_t max_blocks, int32_t block_size,
+                               int32_t *idx_dev, int32_t max_keep, int32_t *count_dev, int32_t *ranges_dev,
+                               murmur_stream_t stream);
 
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
  * (0 = the automatic choice, MURMUR_SPLIT_STREAM, or positions per split).

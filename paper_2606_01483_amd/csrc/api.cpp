@@ -258,8 +258,34 @@ MURMUR_EXPORT int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_p
         return fail(MURMUR_EINVAL, "device pointers must be 4-byte aligned");
     if ((int64_t)B * max_keep > ((int64_t)1 << 40)) return fail(MURMUR_EINVAL, "B * max_keep too large");
     const int e = launch_evict_compact(seg_dev, pol_dev, pol_per_seq, B, idx_dev, max_keep, count_dev, ranges_dev,
-                                       stream);
+                                       nullptr, 0, 0, stream);
     if (e != 0) return fail(MURMUR_EHIP, "evict_compact launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_evict_compact_paged(const murmur_seg *seg_dev, const murmur_policy *pol_dev,
+                                             int32_t pol_per_seq, int32_t B, const int32_t *block_table_dev,
+                                             int32_t max_blocks, int32_t block_size, int32_t *idx_dev,
+                                             int32_t max_keep, int32_t *count_dev, int32_t *ranges_dev,
+                                             murmur_stream_t stream) {
+    if (!seg_dev || !pol_dev || !idx_dev || !count_dev || !block_table_dev)
+        return fail(MURMUR_EINVAL, "seg_dev, pol_dev, block_table_dev, idx_dev and count_dev must not be NULL");
+    if (B < 1) return fail(MURMUR_EINVAL, "B must be >= 1 (got %d)", B);
+    if (max_keep < 1) return fail(MURMUR_EINVAL, "max_keep must be >= 1 (got %d)", max_keep);
+    if (max_blocks < 1) return fail(MURMUR_EINVAL, "max_blocks must be >= 1 (got %d)", max_blocks);
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (block_size < 1 || block_size > (1 << 20) || (block_size & (block_size - 1)) != 0)
+        return fail(MURMUR_EINVAL, "block_size must be a power of two in [1, 2^20] (got %d)", block_size);
+    if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
+        !aligned(ranges_dev, 4) || !aligned(block_table_dev, 4))
+        return fail(MURMUR_EINVAL, "device pointers must be 4-byte aligned");
+    if ((int64_t)B * max_keep > ((int64_t)1 << 40) || (int64_t)B * max_blocks > ((int64_t)1 << 40))
+        return fail(MURMUR_EINVAL, "B * max_keep or B * max_blocks too large");
+    int log2_bs = 0;
+    while ((1 << log2_bs) < block_size) ++log2_bs;
+    const int e = launch_evict_compact(seg_dev, pol_dev, pol_per_seq, B, idx_dev, max_keep, count_dev, ranges_dev,
+                                       block_table_dev, max_blocks, log2_bs, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "evict_compact_paged launch failed: %s", hip_error_text(e));
     return ok();
 }
 

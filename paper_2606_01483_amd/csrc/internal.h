@@ -83,7 +83,8 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
 
 // Kernel launchers (kernels.hip).  They return a hipError_t value as int.
 int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
-                         int32_t *idx, int32_t max_keep, int32_t *count, int32_t *ranges, murmur_stream_t stream);
+                         int32_t *idx, int32_t max_keep, int32_t *count, int32_t *ranges, const int32_t *bt,
+                         int32_t max_blocks, int32_t log2_bs, murmur_stream_t stream);
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream);
 int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream);
 int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, uint32_t *sink, murmur_stream_t stream);

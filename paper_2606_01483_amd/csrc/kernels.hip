@@ -38,11 +38,27 @@ static __device__ __forceinline__ void raise_device_error(int32_t bit) { atomicO
 // ---------------------------------------------------------------------------
 // evict_compact: one workgroup per sequence.
 // ---------------------------------------------------------------------------
+// With a block table (paged cache, bt != null) the index list holds physical
+// rows: position p of sequence b lives in row bt[b][p / bs] * bs + p % bs
+// (bs = 1 << log2_bs); a position past the table's max_blocks entries gives
+// -1 and MURMUR_DEVERR_BLOCK.
+static __device__ __forceinline__ int32_t paged_row(const int32_t *bt_row, int32_t max_blocks, int32_t log2_bs,
+                                                    int32_t p, int &bad) {
+    const int32_t blk = p >> log2_bs;
+    if (blk >= max_blocks) {
+        bad = 1;
+        return -1;
+    }
+    return (bt_row[blk] << log2_bs) | (p & ((1 << log2_bs) - 1));
+}
+
 __global__ __launch_bounds__(256) void evict_compact_kernel(const murmur_seg *__restrict__ seg,
                                                             const murmur_policy *__restrict__ pol,
                                                             int32_t pol_per_seq, int32_t max_keep,
                                                             int32_t *__restrict__ idx, int32_t *__restrict__ count,
-                                                            int32_t *__restrict__ ranges) {
+                                                            int32_t *__restrict__ ranges,
+                                                            const int32_t *__restrict__ bt, int32_t max_blocks,
+                                                            int32_t log2_bs) {
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
     const murmur_seg s = seg[b];
@@ -69,14 +85,20 @@ __global__ __launch_bounds__(256) void evict_compact_kernel(const murmur_seg *__
         ranges[b * 2 * kPieces + tid] = (tid & 1) ? pc.len[k] : pc.start[k];
     }
     int off = 0;
+    int bad_block = 0;
+    const int32_t *bt_row = bt ? bt + (int64_t)b * max_blocks : nullptr;
 #pragma unroll
     for (int k = 0; k < kPieces; ++k) {
         const int n = pc.len[k] < max_keep - off ? pc.len[k] : max_keep - off;
-        for (int t = tid; t < n; t += blockDim.x) row[off + t] = pc.start[k] + t;
+        for (int t = tid; t < n; t += blockDim.x) {
+            const int32_t p = pc.start[k] + t;
+            row[off + t] = bt_row ? paged_row(bt_row, max_blocks, log2_bs, p, bad_block) : p;
+        }
         off += pc.len[k];
         if (off >= max_keep) break;
     }
     for (int r = pc.count + tid; r < max_keep; r += blockDim.x) row[r] = -1;
+    if (bad_block) raise_device_error(MURMUR_DEVERR_BLOCK);
 }
 
 // ---------------------------------------------------------------------------
@@ -1675,9 +1697,10 @@ __global__ void workspace_init_kernel(int32_t *ticket, int64_t n) {
 // launchers
 // ---------------------------------------------------------------------------
 int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
-                         int32_t *idx, int32_t max_keep, int32_t *count, int32_t *ranges, murmur_stream_t stream) {
+                         int32_t *idx, int32_t max_keep, int32_t *count, int32_t *ranges, const int32_t *bt,
+                         int32_t max_blocks, int32_t log2_bs, murmur_stream_t stream) {
     hipLaunchKernelGGL(evict_compact_kernel, dim3(B), dim3(256), 0, (hipStream_t)stream, seg, pol, pol_per_seq,
-                       max_keep, idx, count, ranges);
+                       max_keep, idx, count, ranges, bt, max_blocks, log2_bs);
     return (int)hipGetLastError();
 }
 

@@ -260,3 +260,92 @@ class RingBatch:
     def resident_bytes(self) -> int:
         """Bytes of one replica of the ring storage (K and V)."""
         return 2 * self.k[0].numel() * 2
+
+
+class PagedBatch:
+    """Decode steps on a paged KV cache: one shared pool of blocks of `block_size` rows and a block table per
+    sequence (a random placement of its blocks, seeded).  A step is murmur_evict_compact_paged (the retained
+    set as pool rows) followed by murmur_decode_attn in index-list mode over the pool.
+
+    Memory plumbing only: the pool [R][NL][rows][Hkv][D] ("flash": block, slot, head) or [R][NL][Hkv][rows][D]
+    ("head"), R replicas for cold reads, the block table [B][max_blocks], per-step layouts and queries,
+    outputs and workspace."""
+
+    def __init__(self, wl: Workload, block_size: int = 16, layout: str = "flash", device: str = "cuda",
+                 replicas: int = 1, out_dtype: int = M.MURMUR_DTYPE_BF16, split_len: int = 0,
+                 steps: list[int] | None = None, seed: int = 0, spare_blocks: int = 7):
+        if np.ndim(wl.policy) == 3:
+            raise ValueError("paged steps take per-sequence policies")
+        self.wl = wl
+        self.bs = int(block_size)
+        self.layout = layout
+        self.device = torch.device(device)
+        self.steps = list(range(wl.steps)) if steps is None else list(steps)
+        self.out_dtype = out_dtype
+        self.split_len = split_len
+        B, NL, Hq, Hkv, D = wl.batch, wl.n_layers, wl.hq, wl.hkv, wl.head_dim
+        self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
+        self.max_keep = int(max(int(retained_counts(wl, s).max()) for s in self.steps))
+        last = wl.seg(self.steps[-1])
+        self.lengths = last.sum(axis=1).astype(np.int64)  # positions each sequence fills by the last step
+        per_seq = -(-self.lengths // self.bs)
+        self.max_blocks = int(per_seq.max())
+        self.n_blocks = int(per_seq.sum()) + spare_blocks
+        rng = np.random.default_rng(seed)
+        perm = rng.permutation(self.n_blocks)
+        self.block_table = np.zeros((B, self.max_blocks), dtype=np.int32)
+        o = 0
+        for b in range(B):
+            self.block_table[b, :per_seq[b]] = perm[o:o + per_seq[b]]
+            o += int(per_seq[b])
+        self.rows = self.n_blocks * self.bs
+        dev = self.device
+        self.replicas = replicas
+        k0 = torch.from_numpy(self.pool(wl.k)).view(torch.bfloat16)
+        v0 = torch.from_numpy(self.pool(wl.v)).view(torch.bfloat16)
+        self.k = torch.empty((replicas,) + tuple(k0.shape), dtype=torch.bfloat16, device=dev)
+        self.v = torch.empty_like(self.k)
+        for r in range(replicas):
+            self.k[r].copy_(k0)
+            self.v[r].copy_(v0)
+        if layout == "flash":
+            strides = (self.rows * Hkv * D, 0, D, Hkv * D)
+        else:
+            strides = (Hkv * self.rows * D, 0, self.rows * D, D)
+        self.kv = [M.make_kv(self.k[r], self.v[r], NL, self.rows, strides) for r in range(replicas)]
+        self.bt = torch.from_numpy(self.block_table).to(dev)
+        self.seg = torch.from_numpy(np.stack([wl.seg(s) for s in self.steps]).astype(np.int32)).to(dev)
+        self.pol = torch.from_numpy(np.ascontiguousarray(wl.policy, dtype=np.int32)).to(dev)
+        self.q = torch.from_numpy(np.stack([wl.q(s) for s in self.steps])).view(torch.bfloat16).to(dev)
+        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
+        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
+        odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
+        self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
+        self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
+        self.ws_bytes = M.murmur_decode_attn_workspace(NL, B, Hq, Hkv, self.max_keep, split_len)
+        self.ws = torch.zeros(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.int32, device=dev)
+
+    def pool(self, cache: np.ndarray) -> np.ndarray:
+        """The pool of a sequence-ordered cache [NL, B, Hkv, L, D] (positions up to each sequence's length)."""
+        NL, B, Hkv, _, D = cache.shape
+        flash = np.zeros((NL, self.rows, Hkv, D), dtype=cache.dtype)
+        for b in range(B):
+            n = int(self.lengths[b])
+            for i in range(-(-n // self.bs)):
+                lo, hi = i * self.bs, min((i + 1) * self.bs, n)
+                r0 = int(self.block_table[b, i]) * self.bs
+                flash[:, r0:r0 + hi - lo] = cache[:, b, :, lo:hi].transpose(0, 2, 1, 3)
+        return flash if self.layout == "flash" else np.ascontiguousarray(flash.transpose(0, 2, 1, 3))
+
+    def evict(self, i: int, stream=None) -> None:
+        M.murmur_evict_compact_paged(self.seg[i], self.pol, 1, self.B, self.bt, self.max_blocks, self.bs, self.idx,
+                                     self.max_keep, self.count, None, stream)
+
+    def attend(self, i: int, replica: int = 0, stream=None) -> None:
+        M.murmur_decode_attn(self.q[i], self.kv[replica], self.idx, None, self.count, self.max_keep, self.B,
+                             self.Hq, self.Hkv, self.D, self.wl.scale, self.split_len, self.out, self.out_dtype,
+                             self.lse, self.ws, self.ws_bytes, stream)
+
+    def step(self, i: int, replica: int = 0, stream=None) -> None:
+        self.evict(i, stream)
+        self.attend(i, replica, stream)

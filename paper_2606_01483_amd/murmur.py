@@ -20,6 +20,7 @@ MURMUR_DTYPE_BF16, MURMUR_DTYPE_F32 = 1, 2
 MURMUR_DEVERR_OVERFLOW, MURMUR_DEVERR_POLICY, MURMUR_DEVERR_POSITION, MURMUR_DEVERR_COUNT = 1, 2, 4, 8
 MURMUR_DEVERR_CAPACITY = 16
 MURMUR_POL_PER_SEQ, MURMUR_POL_PER_LAYER = 1, 2
+MURMUR_DEVERR_BLOCK = 32
 N_PIECES = 6
 SPLIT_UNIT = 128
 MURMUR_SPLIT_STREAM = -1
@@ -75,6 +76,8 @@ def _load():
                                                i32p, i32p]
     lib.murmur_evict_compact.restype = ctypes.c_int
     lib.murmur_evict_compact.argtypes = [vp, vp, i32, i32, vp, i32, vp, vp, vp]
+    lib.murmur_evict_compact_paged.restype = ctypes.c_int
+    lib.murmur_evict_compact_paged.argtypes = [vp, vp, i32, i32, vp, i32, i32, vp, i32, vp, vp, vp]
     lib.murmur_decode_attn_workspace.restype = ctypes.c_int
     lib.murmur_decode_attn_workspace.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.murmur_decode_attn_workspace_init.restype = ctypes.c_int
@@ -179,6 +182,15 @@ def murmur_evict_compact(seg_dev, pol_dev, pol_per_seq: int, B: int, idx_dev, ma
     count_dev: int32 [B]; ranges_dev: int32 [B, 6, 2] or None."""
     _check(_load().murmur_evict_compact(_addr(seg_dev), _addr(pol_dev), pol_per_seq, B, _addr(idx_dev), max_keep,
                                         _addr(count_dev), _addr(ranges_dev), _stream(stream)))
+
+
+def murmur_evict_compact_paged(seg_dev, pol_dev, pol_per_seq: int, B: int, block_table_dev, max_blocks: int,
+                               block_size: int, idx_dev, max_keep: int, count_dev, ranges_dev=None,
+                               stream=None) -> None:
+    """murmur_evict_compact with the index list in rows of a paged pool (block_table_dev int32 [B, max_blocks])."""
+    _check(_load().murmur_evict_compact_paged(_addr(seg_dev), _addr(pol_dev), pol_per_seq, B, _addr(block_table_dev),
+                                              max_blocks, block_size, _addr(idx_dev), max_keep, _addr(count_dev),
+                                              _addr(ranges_dev), _stream(stream)))
 
 
 def murmur_decode_attn_workspace(n_layers: int, B: int, Hq: int, Hkv: int, max_keep: int, split_len: int = 0) -> int:

@@ -38,14 +38,14 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 4
+    assert M.murmur_abi_version() == 5
 
 
 def test_retained_count_host_matches_oracle():
@@ -340,3 +340,20 @@ def test_read_probe_rejects():
     assert lib.murmur_read_probe(FAKE, 0, 256, FAKE, 0) == M.MURMUR_EINVAL
     assert lib.murmur_read_probe(FAKE, 1024, 0, FAKE, 0) == M.MURMUR_EINVAL
     assert lib.murmur_read_probe(FAKE + 8, 1024, 256, FAKE, 0) == M.MURMUR_EINVAL
+
+
+def test_evict_compact_paged_rejects():
+    lib = M.lib()
+    good = dict(seg=FAKE, pol=FAKE, per=0, B=12, bt=FAKE, mb=64, bs=16, idx=FAKE, mk=850, cnt=FAKE)
+
+    def call(**over):
+        a = dict(good, **over)
+        return lib.murmur_evict_compact_paged(a["seg"], a["pol"], a["per"], a["B"], a["bt"], a["mb"], a["bs"],
+                                              a["idx"], a["mk"], a["cnt"], None, 0)
+    assert call(bt=None) == M.MURMUR_EINVAL
+    assert call(bs=12) == M.MURMUR_EINVAL     # not a power of two
+    assert call(bs=0) == M.MURMUR_EINVAL
+    assert call(mb=0) == M.MURMUR_EINVAL
+    assert call(per=2) == M.MURMUR_EINVAL
+    assert call(bt=FAKE + 2) == M.MURMUR_EINVAL
+    assert call(B=0) == M.MURMUR_EINVAL
