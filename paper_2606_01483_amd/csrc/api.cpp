@@ -71,12 +71,28 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
             // most kMaxAutoSplits.
             int64_t per;
             if (groups * units <= kSinglePassMaxUnits && units <= kMaxMergeSplits) {
-                int64_t n = kRoundWorkgroups / groups;
-                if (n < 1) n = 1;
-                int64_t len = (((int64_t)max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
-                if (len < kSplitUnit) len = kSplitUnit;
-                if (len > 2 * kSplitUnit) len = 2 * kSplitUnit;
-                split_len = (int32_t)len;
+                // The split count that minimises an estimate of the launch time: each compute unit streams
+                // its split at kCuBytesPerUs, and more than one split adds the merge chain (store, ticket,
+                // loading the partials).  At most one dispatch round; splits of 1 or 2 passes.
+                const int64_t n_max = kRoundWorkgroups / groups < 1 ? 1 : kRoundWorkgroups / groups;
+                const double group_bytes = (double)max_keep * 4.0 * kHeadDim;  // K and V rows of one KV head
+                const double part_bytes = (double)G * (kHeadDim + 2) * 4.0;
+                int64_t best_len = 0;
+                double best = 0.0;
+                for (int64_t n = 1; n <= n_max; ++n) {
+                    int64_t len = (((int64_t)max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
+                    if (len < kSplitUnit) len = kSplitUnit;
+                    if (len > 2 * kSplitUnit) continue;  // more than two passes: the LDS-staged kernel's range
+                    const int64_t ns = ((int64_t)max_keep + len - 1) / len;
+                    const double t = group_bytes / ns / kCuBytesPerUs +
+                                     (ns > 1 ? kMergeChainUs + ns * part_bytes / kCuBytesPerUs : 0.0);
+                    if (best_len == 0 || t < best) {
+                        best = t;
+                        best_len = len;
+                    }
+                }
+                if (best_len == 0) best_len = 2 * kSplitUnit;
+                split_len = (int32_t)best_len;
                 per = 0;
             } else {
                 int64_t want = kRoundWorkgroups / groups;

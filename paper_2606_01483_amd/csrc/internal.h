@@ -27,6 +27,11 @@ constexpr int kStreamMaxB = 256;
 constexpr int kMaxMergeSplits = 240;
 constexpr int kMaxKeep = 1 << 28;  // retained positions per sequence the attention accepts
 constexpr int kMergeBatch = 8;  // splits whose partials one merging thread loads at once
+// Split-choice model (measured on MI355X): one compute unit streams about 40 GB/s from HBM however many
+// wavefronts it runs, and the split-K merge chain (partial stores, ticket, loading the partials) costs
+// about 2.3 us on top of the data phase.
+constexpr double kCuBytesPerUs = 40e3;
+constexpr double kMergeChainUs = 2.3;
 
 // Launch description of one decode_attn call, fully validated by the caller.
 // Where the attention takes the retained sets from (see AttnLaunch::src0/src1).
