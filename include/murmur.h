@@ -352,7 +352,8 @@ int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmur_policy *pol_
  *               tokens_per_s (the speech_len of its murmur_seg: the chunk's
  *               length times the rate, rounded to nearest).
  * Errors: MURMUR_EINVAL (unsorted or overlapping segments, a segment outside
- * [0, audio_len], max_chunk <= 0, tokens_per_s < 0), MURMUR_ENOSPACE (more
+ * [0, audio_len], max_chunk <= 0, tokens_per_s < 0, audio_len / max_chunk or
+ * n_seg above 2^24, max_chunk * tokens_per_s above 2e9), MURMUR_ENOSPACE (more
  * than max_chunks chunks; *n_chunks then holds the number needed). */
 int murmur_plan_chunks(const double *seg_start, const double *seg_end, int32_t n_seg, double audio_len,
                        double max_chunk, double tokens_per_s, int32_t *chunk_of_seg, double *chunk_start,

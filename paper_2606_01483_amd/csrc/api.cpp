@@ -462,6 +462,8 @@ MURMUR_EXPORT int murmur_plan_chunks(const double *seg_start, const double *seg_
     if (!(max_chunk > 0) || !(audio_len >= 0) || !(tokens_per_s >= 0) || !isfinite(audio_len) ||
         !isfinite(max_chunk) || !isfinite(tokens_per_s))
         return fail(MURMUR_EINVAL, "audio_len and tokens_per_s must be >= 0 and max_chunk > 0, all finite");
+    if (audio_len / max_chunk > (double)(1 << 24) || max_chunk * tokens_per_s > 2e9 || n_seg > (1 << 24))
+        return fail(MURMUR_EINVAL, "more than 2^24 chunks or segments, or more than 2e9 speech tokens per chunk");
     for (int32_t i = 0; i < n_seg; ++i) {
         if (!(seg_start[i] >= 0) || !(seg_end[i] > seg_start[i]) || !(seg_end[i] <= audio_len))
             return fail(MURMUR_EINVAL, "segment %d [%g, %g) is empty or outside [0, %g]", i, seg_start[i], seg_end[i],

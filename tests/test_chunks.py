@@ -153,5 +153,7 @@ def test_plan_chunks_rejects_bad_input():
         M.murmur_plan_chunks([0.0], [10.0], 100.0, max_chunk=0.0)
     with pytest.raises(M.MurmurError):
         M.murmur_chunk_timestamps([1.0], [3], [10.0, 10.0])        # no chunk 3
+    with pytest.raises(M.MurmurError):
+        M.murmur_plan_chunks([0.0], [10.0], 1e9, max_chunk=1.0)  # more than 2^24 chunks
     cs, cl, tok, of = M.murmur_plan_chunks([], [], 100.0)
     assert len(cs) == 0
