@@ -404,6 +404,9 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
         log(f"timing the fp64 oracle on {threads} host threads")
         res["cpu_baseline"] = cpu_baseline(wl, cpu_budget, threads)
+        log("timing the fp64 oracle on one host thread")
+        one = cpu_baseline(wl, max(1.0, cpu_budget / 3), 1)
+        res["cpu_baseline"]["single_thread"] = {"value": one["value"], "unit": one["unit"], "sample": one["sample"]}
     return res
 
 
