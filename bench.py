@@ -193,6 +193,37 @@ def read_ceiling(nbytes: int, steps: int, capture, time_graph, workgroups: int =
             "us_1GiB": round(us_gib, 3), "GBps_1GiB": round(gib / us_gib / 1e3, 1)}
 
 
+def oracle_parity(wl, db, i: int) -> dict:
+    """CPU-baseline leg: the fused step's bf16 output for step i (all layers, sequences and heads) against the
+    fp64 oracle: the largest error relative to max(|ref|, rms of the 128-wide row), and the same after
+    subtracting half a bf16 ulp of the reference (what the bf16 store alone may add)."""
+    import torch
+    import oracle
+    db.step_fused(i, 0)
+    torch.cuda.synchronize()
+    y = db.out.float().cpu().numpy().astype(np.float64)
+    lse = db.lse.cpu().numpy().astype(np.float64)
+    s = db.steps[i]
+    seg, q = wl.seg(s), wl.q(s)
+    if wl.policy.ndim == 3:
+        parts = []
+        for layer in range(wl.n_layers):
+            idx, cnt = oracle.retained(seg, wl.policy[layer])
+            sl = slice(layer, layer + 1)
+            parts.append(oracle.attend(q[sl], wl.k[sl], wl.v[sl], idx, cnt, scale=wl.scale, n_threads=16))
+        ref, ref_lse = np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
+    else:
+        idx, cnt = oracle.retained(seg, wl.policy)
+        ref, ref_lse = oracle.attend(q, wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=16)
+    denom = np.maximum(np.abs(ref), np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True)))
+    half_ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126))) - 8)
+    err = np.abs(y - ref)
+    return {"step": int(s), "max_rel_err_bf16_out": float(np.max(err / denom)),
+            "max_rel_err_beyond_bf16_rounding": float(np.max((err - half_ulp) / denom)),
+            "lse_max_err": float(np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse)))),
+            "tolerance": 2e-3}
+
+
 def replicas_for(wl, kv_step: list[int]) -> int:
     """KV replicas to rotate over so that consecutive steps read more than 2.2 x the Infinity Cache
     (at most 24 GB of replicas)."""
@@ -407,6 +438,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         log("timing the fp64 oracle on one host thread")
         one = cpu_baseline(wl, max(1.0, cpu_budget / 3), 1)
         res["cpu_baseline"]["single_thread"] = {"value": one["value"], "unit": one["unit"], "sample": one["sample"]}
+        log("checking one timed step against the oracle")
+        res["cpu_baseline"]["parity"] = oracle_parity(wl, db, order[0])
     return res
 
 
