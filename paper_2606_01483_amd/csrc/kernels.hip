@@ -1039,9 +1039,9 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const int b = blockIdx.z;
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
-    int32_t cur = -1;
+    int32_t cur_row = -1;  // ring storage: the current token's row
     const int layer = (int)blockIdx.y / Hkv;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur);
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
     const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
@@ -1063,7 +1063,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
     constexpr bool kRing = kSrc == kSrcRing;
-    NewRows nr{cur, nullptr, nullptr};
+    NewRows nr{cur_row, nullptr, nullptr};
     if (kRing) {
         nr.k = a.k_new + (int64_t)grp * kHeadDim;
         nr.v = a.v_new + (int64_t)grp * kHeadDim;
@@ -1160,9 +1160,9 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const int b = blockIdx.z;
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
-    int32_t cur = -1;
+    int32_t cur_row = -1;  // ring storage: the current token's row
     const int layer = (int)blockIdx.y / Hkv;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur);
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
     const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
@@ -1184,7 +1184,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
     constexpr bool kRing = kSrc == kSrcRing;
-    NewRows nr{cur, nullptr, nullptr};
+    NewRows nr{cur_row, nullptr, nullptr};
     if (kRing) {
         nr.k = a.k_new + (int64_t)grp * kHeadDim;
         nr.v = a.v_new + (int64_t)grp * kHeadDim;
