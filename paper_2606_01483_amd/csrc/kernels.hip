@@ -764,15 +764,19 @@ static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t
 // The evict_compact outputs of sequence b (each one only if the caller passed
 // its buffer) and its device errors: count (0 for an invalid layout or
 // policy), range table, ascending index list padded with -1 (its first
-// max_keep entries when the count exceeds max_keep).  Block-wide.
+// max_keep entries when the count exceeds max_keep).  Each caller writes the
+// index-list entries of ranks [r_lo, r_hi) (the splits of a sequence share
+// the list between them); the one with r_lo == 0 also writes the count, the
+// table and the errors.  Block-wide.
 static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b, int cnt, int policy_bad,
-                                                      const int32_t (&rg)[2 * kPieces], int max_keep, int tid) {
-    if (tid == 0) {
+                                                      const int32_t (&rg)[2 * kPieces], int max_keep, int tid,
+                                                      int r_lo, int r_hi) {
+    if (r_lo == 0 && tid == 0) {
         if (a.count_out) a.count_out[b] = cnt;
         if (policy_bad) raise_device_error(policy_bad == 2 ? MURMUR_DEVERR_CAPACITY : MURMUR_DEVERR_POLICY);
         else if (cnt > max_keep) raise_device_error(MURMUR_DEVERR_OVERFLOW);
     }
-    if (a.ranges_out && tid < 2 * kPieces) {
+    if (r_lo == 0 && a.ranges_out && tid < 2 * kPieces) {
         int32_t v = 0;
 #pragma unroll
         for (int k = 0; k < 2 * kPieces; ++k) v = tid == k ? rg[k] : v;
@@ -780,14 +784,16 @@ static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b
     }
     if (a.idx_out) {
         int32_t *row = a.idx_out + (int64_t)b * max_keep;
-        int off = 0;
+        const int hi = r_hi < max_keep ? r_hi : max_keep;
+        int off = 0;  // first rank of piece k
 #pragma unroll
         for (int k = 0; k < kPieces; ++k) {
             const int n = rg[2 * k + 1] < max_keep - off ? rg[2 * k + 1] : max_keep - off;
-            for (int t = tid; t < n; t += kWavesPerWg * 64) row[off + t] = rg[2 * k] + t;
+            const int lo = off > r_lo ? off : r_lo, e = off + n < hi ? off + n : hi;
+            for (int r = lo + tid; r < e; r += kWavesPerWg * 64) row[r] = rg[2 * k] + (r - off);
             off += n;
         }
-        for (int r = off + tid; r < max_keep; r += kWavesPerWg * 64) row[r] = -1;
+        for (int r = (off > r_lo ? off : r_lo) + tid; r < hi; r += kWavesPerWg * 64) row[r] = -1;
     }
 }
 
@@ -1107,10 +1113,10 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kOWaveBytes / 4, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
-    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 &&
+    if ((kSrc == kSrcLayout || kRing) && g == 0 &&
         (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
         write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
-                       max_keep, tid);
+                       max_keep, tid, r_begin, r_begin + a.split_len);
     if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
@@ -1261,10 +1267,10 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kStageWaveFloats, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
-    if ((kSrc == kSrcLayout || kRing) && split == 0 && g == 0 &&
+    if ((kSrc == kSrcLayout || kRing) && g == 0 &&
         (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
         write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
-                       max_keep, tid);
+                       max_keep, tid, r_begin, r_begin + a.split_len);
     if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
@@ -1660,7 +1666,7 @@ __global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *
             int policy_bad = 0;
             int32_t unused_cur;
             const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, 0, B, 0, rg, policy_bad, unused_cur);
-            write_retained(a, bb, c, policy_bad, rg, max_keep, tid);
+            write_retained(a, bb, c, policy_bad, rg, max_keep, tid, 0, max_keep);
         }
     }
 }
