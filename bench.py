@@ -289,6 +289,27 @@ def paged_timing(wl, n_steps: int, steps: int, warmup: int, replicas: int, split
             "step_two_launches_us": round(step_us, 3), "decode_attn_us": round(attn_us, 3)}
 
 
+def recycled_blocks(seg0, policy, block_size: int = 16, n_outputs: int = 2700) -> dict:
+    """Host-only: blocks of `block_size` positions the sequences hold over a decode from their layout to
+    n_outputs output tokens when every block no later step retains goes back to the pool before each step
+    (murmur_freeable_blocks_host), against the blocks they hold at the end without freeing."""
+    from paper_2606_01483_amd import murmur as M
+    seg0 = np.asarray(seg0, dtype=np.int32).reshape(-1, 4)
+    pol = np.ascontiguousarray(policy, dtype=np.int32)
+    B = seg0.shape[0]
+    peak = 0
+    for j in range(1, n_outputs + 1):
+        seg = seg0.copy()
+        seg[:, 3] = j
+        held = -(-seg.sum(axis=1) // block_size)  # logical blocks up to the current token
+        fb = M.murmur_freeable_blocks_host(seg, pol, block_size, 1 if pol.ndim == 2 else 0)
+        peak = max(peak, int((held - fb[:, :, 1].sum(axis=1)).sum()))
+    seg = seg0.copy()
+    seg[:, 3] = n_outputs
+    return {"block_size": block_size, "outputs": n_outputs, "peak_blocks": peak,
+            "blocks_without_freeing": int((-(-seg.sum(axis=1) // block_size)).sum())}
+
+
 def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, cpu_budget: float,
         split_len: int, use_ranges: bool, with_ring: bool = True) -> dict:
     import torch
@@ -431,6 +452,8 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         res["ring"] = ring
     if paged is not None:
         res["paged"] = paged
+        if np.ndim(wl.policy) < 3:
+            res["paged"]["recycled_to_2700_outputs"] = recycled_blocks(wl.seg0 * np.array([1, 1, 1, 0]), wl.policy)
     if cpu:
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
         log(f"timing the fp64 oracle on {threads} host threads")

@@ -75,7 +75,7 @@ enum {
     MURMUR_DEVERR_POSITION = 4,  /* decode_attn: retained position outside [0, max_len) */
     MURMUR_DEVERR_COUNT = 8,     /* decode_attn: count outside [1, max_keep] */
     MURMUR_DEVERR_CAPACITY = 16, /* decode_step_ring: the output ring cannot hold the retained outputs */
-    MURMUR_DEVERR_BLOCK = 32,    /* evict_compact_paged: a retained position past the block table */
+    MURMUR_DEVERR_BLOCK = 32,    /* evict_compact_paged: a retained position past the block table or in a freed block */
 };
 
 /* One sequence (audio chunk) of the batch, Section 3.2's layout
@@ -129,7 +129,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 5
+#define MURMUR_ABI_VERSION 6
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -180,13 +180,31 @@ int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev
  *   count_dev, ranges_dev: as murmur_evict_compact (ranges in sequence
  *               positions, not pool rows).
  * Errors as murmur_evict_compact; device error MURMUR_DEVERR_BLOCK (entry -1)
- * for a retained position past max_blocks blocks.  Table entries are not
- * range-checked here: a row outside the pool is reported by
- * murmur_decode_attn (MURMUR_DEVERR_POSITION, NaN outputs). */
+ * for a retained position past max_blocks blocks or in a block whose table
+ * entry is negative (a freed block, see murmur_freeable_blocks_host).  Other
+ * table entries are not range-checked here: a row outside the pool is
+ * reported by murmur_decode_attn (MURMUR_DEVERR_POSITION, NaN outputs). */
 int murmur_evict_compact_paged(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
                                int32_t B, const int32_t *block_table_dev, int32_t max_blocks, int32_t block_size,
                                int32_t *idx_dev, int32_t max_keep, int32_t *count_dev, int32_t *ranges_dev,
                                murmur_stream_t stream);
+
+/* Host-only (no GPU): the logical blocks of each sequence that hold only
+ * positions no decode step from out_len on retains again, so that a paged
+ * cache can return them to its pool (Section 3.2: an evicted entry leaves the
+ * KV cache).  These are the speech tokens behind the window that are not
+ * speech sinks, and the output tokens older than the window that are not
+ * output sinks: the window start of Algorithm 2 never decreases and the
+ * window of Algorithm 1 only moves forward.  Speech ahead of the window stays,
+ * since the window moves onto it.  blocks[b][2][2]: (first logical block,
+ * number of blocks) of the speech part, then of the output part, where
+ * logical block k holds positions [k*block_size, (k+1)*block_size); (0, 0)
+ * when no whole block qualifies.  The result at
+ * a later step contains the one at an earlier step, so a caller frees what is
+ * new.  block_size >= 1; pol_per_seq 0 or 1 (as murmur_evict_compact).
+ * Errors: MURMUR_EINVAL as murmur_retained_count_host. */
+int murmur_freeable_blocks_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
+                                int32_t block_size, int32_t *blocks);
 
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
  * (0 = the automatic choice, MURMUR_SPLIT_STREAM, or positions per split).

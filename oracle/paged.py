@@ -10,15 +10,22 @@ definitions, run literally:
   * ``pool_row``    -- that row;
   * ``build_pool``  -- a pool [NL, rows, Hkv, D] filled from a sequence-ordered cache by copying every
                        position to its row one by one;
-  * ``rows_of``     -- the pool rows of a list of retained positions.
+  * ``rows_of``     -- the pool rows of a list of retained positions;
+  * ``never_retained_again`` -- the positions of a sequence that no step from j to j + horizon
+                       retains (each step's retained set from the oracle's Algorithm 1/2 loops);
+  * ``freeable_blocks`` -- the logical blocks made only of such positions (Section 3.2: an evicted
+                       entry leaves the cache, so its block can go back to the pool).
 
 Pins (``tests/test_oracle_paged.py``): with the identity table of one sequence the pool row is the
 position; a pool built from any table reproduces the sequence-ordered cache at every position read back
-through the table.
+through the table; a hand-worked example of the freeable blocks (tiny workload at step 80); a block
+freeable at one step stays freeable at every later one; a longer horizon frees nothing more.
 """
 from __future__ import annotations
 
 import numpy as np
+
+from oracle import retained
 
 
 def pool_row(block_table_row, block_size: int, p: int) -> int:
@@ -42,3 +49,34 @@ def rows_of(idx: np.ndarray, count: np.ndarray, block_table: np.ndarray, block_s
         for r in range(int(count[b])):
             out[b, r] = pool_row(block_table[b], block_size, int(idx[b, r]))
     return out
+
+
+def default_horizon(seg_row, pol_row) -> int:
+    """Later steps to scan: enough for the speech window (one token per step once the delay has passed)
+    to reach every speech position, plus a margin."""
+    _, l_s, _, _ = (int(x) for x in seg_row)
+    return l_s + max(int(pol_row[1]), 1) + 4
+
+
+def never_retained_again(seg_row, pol_row, horizon: int | None = None) -> np.ndarray:
+    """Boolean mask over positions [0, length) of a sequence at step j = seg_row[3]: True where none of
+    the retained sets of steps j, j+1, .., j+horizon holds the position (the sequence grows by one output
+    token per step; positions past the current length are not part of the mask)."""
+    p_pre, l_s, p_mid, j = (int(x) for x in seg_row)
+    pol_row = np.asarray(pol_row, dtype=np.int32).reshape(5)
+    if horizon is None:
+        horizon = default_horizon(seg_row, pol_row)
+    length = p_pre + l_s + p_mid + j
+    kept = np.zeros(length, dtype=bool)
+    for jj in range(j, j + horizon + 1):
+        idx, cnt = retained(np.array([[p_pre, l_s, p_mid, jj]], dtype=np.int32), pol_row)
+        rows = idx[0, :int(cnt[0])]
+        kept[rows[rows < length]] = True
+    return ~kept
+
+
+def freeable_blocks(seg_row, pol_row, block_size: int, horizon: int | None = None) -> list[int]:
+    """Logical blocks k (positions [k*block_size, (k+1)*block_size)) that lie inside the current length
+    and hold only positions never retained again, ascending."""
+    free = never_retained_again(seg_row, pol_row, horizon)
+    return [k for k in range(len(free) // block_size) if free[k * block_size:(k + 1) * block_size].all()]

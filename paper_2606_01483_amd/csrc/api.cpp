@@ -305,6 +305,34 @@ MURMUR_EXPORT int murmur_evict_compact_paged(const murmur_seg *seg_dev, const mu
     return ok();
 }
 
+MURMUR_EXPORT int murmur_freeable_blocks_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq,
+                                             int32_t B, int32_t block_size, int32_t *blocks) {
+    if (!seg || !pol || !blocks) return fail(MURMUR_EINVAL, "seg, pol and blocks must not be NULL");
+    if (B < 1) return fail(MURMUR_EINVAL, "B must be >= 1 (got %d)", B);
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (block_size < 1) return fail(MURMUR_EINVAL, "block_size must be >= 1 (got %d)", block_size);
+    for (int32_t b = 0; b < B; ++b) {
+        const murmur_seg &s = seg[b];
+        const murmur_policy &p = pol[pol_per_seq ? b : 0];
+        int32_t ranges[2][2];
+        if (evicted_ranges(s.prompt_pre, s.speech_len, s.prompt_mid, s.out_len, p.speech_window, p.speech_delay,
+                           p.speech_sink, p.out_window, p.out_sink, ranges[0], ranges[1]) != 0)
+            return fail(MURMUR_EINVAL,
+                        "sequence %d: invalid layout or policy (seg %d/%d/%d/%d, policy %d/%d/%d/%d/%d)", b,
+                        s.prompt_pre, s.speech_len, s.prompt_mid, s.out_len, p.speech_window, p.speech_delay,
+                        p.speech_sink, p.out_window, p.out_sink);
+        // Whole blocks inside each range: from the first block that starts in it to the last that ends in it.
+        for (int k = 0; k < 2; ++k) {
+            const int64_t lo = ranges[k][0], hi = (int64_t)ranges[k][0] + ranges[k][1];
+            const int64_t first = (lo + block_size - 1) / block_size, end = hi / block_size;
+            int32_t *out = blocks + (int64_t)b * 4 + 2 * k;
+            out[0] = end > first ? (int32_t)first : 0;
+            out[1] = end > first ? (int32_t)(end - first) : 0;
+        }
+    }
+    return ok();
+}
+
 MURMUR_EXPORT int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv,
                                                int32_t max_keep, int32_t split_len, size_t *bytes) {
     if (!bytes) return fail(MURMUR_EINVAL, "bytes must not be NULL");

@@ -41,15 +41,18 @@ static __device__ __forceinline__ void raise_device_error(int32_t bit) { atomicO
 // With a block table (paged cache, bt != null) the index list holds physical
 // rows: position p of sequence b lives in row bt[b][p / bs] * bs + p % bs
 // (bs = 1 << log2_bs); a position past the table's max_blocks entries gives
-// -1 and MURMUR_DEVERR_BLOCK.
+// -1 and MURMUR_DEVERR_BLOCK, and so does one in a block whose entry is
+// negative (freed).
 static __device__ __forceinline__ int32_t paged_row(const int32_t *bt_row, int32_t max_blocks, int32_t log2_bs,
                                                     int32_t p, int &bad) {
     const int32_t blk = p >> log2_bs;
-    if (blk >= max_blocks) {
+    const int32_t entry = bt_row[blk < max_blocks ? blk : 0];  // the load stays inside the table
+    const int32_t phys = blk < max_blocks ? entry : -1;
+    if (phys < 0) {  // past the table, or a freed block
         bad = 1;
         return -1;
     }
-    return (bt_row[blk] << log2_bs) | (p & ((1 << log2_bs) - 1));
+    return (phys << log2_bs) | (p & ((1 << log2_bs) - 1));
 }
 
 __global__ __launch_bounds__(256) void evict_compact_kernel(const murmur_seg *__restrict__ seg,

@@ -154,4 +154,43 @@ MURMUR_HD inline int ring_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, int3
     return 0;
 }
 
+// Positions that no step from j on retains again, so their K/V can be freed
+// (Section 3.2: an evicted entry leaves the cache for good).  The speech
+// window's start l_j never decreases with j and the output window
+// [j - w, j) only moves forward, so these are, in global positions,
+//   speech:  [prompt_pre + min(n_sink, l_s), prompt_pre + l_j), the tokens
+//            behind the window that are not sinks (empty with speech
+//            eviction off);
+//   output:  [out0 + n_sink, out0 + j - w), the output tokens older than the
+//            window that are not sinks (empty with output eviction off).
+// Everything else -- prompts, sinks, the windows, speech ahead of the window
+// -- is retained now or at a later step.  Returns 0 and fills
+// {start, length} of both, or -1 for an invalid layout or policy (as
+// retained_pieces).
+MURMUR_HD inline int evicted_ranges(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s, int32_t d,
+                                    int32_t n_ss, int32_t w_o, int32_t n_so, int32_t speech[2], int32_t output[2]) {
+    Pieces pc;
+    if (retained_pieces(p_pre, l_s, p_mid, j, w_s, d, n_ss, w_o, n_so, &pc) != 0) return -1;
+    speech[0] = p_pre;
+    speech[1] = 0;
+    if (w_s != -1 && w_s < l_s) {
+        const int32_t first_move = d > 1 ? d : 1;
+        int32_t l = j >= first_move ? j - first_move + 1 : 0;
+        if (l > l_s - w_s) l = l_s - w_s;
+        const int32_t ns = n_ss < l_s ? n_ss : l_s;
+        if (l > ns) {
+            speech[0] = p_pre + ns;
+            speech[1] = l - ns;
+        }
+    }
+    const int32_t out0 = p_pre + l_s + p_mid;
+    output[0] = out0;
+    output[1] = 0;
+    if (w_o != -1 && j - w_o > n_so) {
+        output[0] = out0 + n_so;
+        output[1] = j - w_o - n_so;
+    }
+    return 0;
+}
+
 }  // namespace murmur

@@ -349,3 +349,109 @@ class PagedBatch:
     def step(self, i: int, replica: int = 0, stream=None) -> None:
         self.evict(i, stream)
         self.attend(i, replica, stream)
+
+
+class RecyclingPagedBatch:
+    """Consecutive decode steps on a paged cache whose blocks are recycled: before each step the blocks that
+    no later step retains (murmur_freeable_blocks_host) go back to a free list, and the blocks new positions
+    need are taken from it, so the pool holds O(prompt + speech + output window) rows per sequence however
+    long the decode runs.  A step is then murmur_evict_compact_paged + murmur_decode_attn (index list).
+
+    Host-side block manager and memory plumbing only: the pool [NL][n_blocks * block_size][Hkv][D] ("flash"
+    layout), the block table [B][max_blocks] (-1 = no block), the free list (a stack).  A block's rows are
+    written from the workload's cache when the block is taken, and overwritten with bf16 NaN when it is
+    freed (`poison`), so that a read of a freed block would show in the outputs."""
+
+    BF16_NAN = 0x7FC0
+
+    def __init__(self, wl: Workload, block_size: int, n_blocks: int, device: str = "cuda",
+                 out_dtype: int = M.MURMUR_DTYPE_F32, split_len: int = 0, poison: bool = True):
+        if np.ndim(wl.policy) == 3:
+            raise ValueError("paged steps take per-sequence policies")
+        self.wl = wl
+        self.bs = int(block_size)
+        self.n_blocks = int(n_blocks)
+        self.rows = self.n_blocks * self.bs
+        self.poison = poison
+        self.out_dtype = out_dtype
+        self.split_len = split_len
+        B, NL, Hq, Hkv, D = wl.batch, wl.n_layers, wl.hq, wl.hkv, wl.head_dim
+        self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
+        self.pol_np = np.ascontiguousarray(wl.policy, dtype=np.int32)
+        final = wl.seg(wl.steps - 1)
+        self.max_blocks = int((-(-final.sum(axis=1) // self.bs)).max())
+        self.max_keep = int(max(int(retained_counts(wl, s).max()) for s in range(wl.steps)))
+        self.table = np.full((B, self.max_blocks), -1, dtype=np.int32)
+        self.free = list(range(self.n_blocks - 1, -1, -1))
+        self.freed = np.zeros((B, self.max_blocks), dtype=bool)  # logical blocks already returned
+        self.peak_in_use = 0
+        dev = torch.device(device)
+        self.k = torch.zeros((NL, self.rows, Hkv, D), dtype=torch.bfloat16, device=dev)
+        self.v = torch.zeros_like(self.k)
+        self.kv = M.make_kv(self.k, self.v, NL, self.rows, (self.rows * Hkv * D, 0, D, Hkv * D))
+        self.bt = torch.from_numpy(self.table).to(dev)
+        self.pol = torch.from_numpy(self.pol_np).to(dev)
+        self.seg_dev = torch.zeros((B, 4), dtype=torch.int32, device=dev)
+        self.q = torch.zeros((NL, B, Hq, D), dtype=torch.bfloat16, device=dev)
+        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
+        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
+        odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
+        self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
+        self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
+        self.ws_bytes = M.murmur_decode_attn_workspace(NL, B, Hq, Hkv, self.max_keep, split_len)
+        self.ws = torch.zeros(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.int32, device=dev)
+
+    def in_use(self) -> int:
+        return self.n_blocks - len(self.free)
+
+    def _fill(self, b: int, blk: int, phys: int) -> None:
+        lo = blk * self.bs
+        hi = min(lo + self.bs, self.wl.max_len)
+        r0 = phys * self.bs
+        for dst, src in ((self.k, self.wl.k), (self.v, self.wl.v)):
+            rows = np.ascontiguousarray(src[:, b, :, lo:hi].transpose(0, 2, 1, 3))
+            dst[:, r0:r0 + hi - lo].copy_(torch.from_numpy(rows).view(torch.bfloat16))
+
+    def _release(self, b: int, blk: int) -> None:
+        phys = int(self.table[b, blk])
+        self.table[b, blk] = -1
+        self.freed[b, blk] = True
+        if phys < 0:  # freeable before it was ever needed: never allocated
+            return
+        if self.poison:
+            r0 = phys * self.bs
+            self.k[:, r0:r0 + self.bs].view(torch.int16).fill_(self.BF16_NAN)
+            self.v[:, r0:r0 + self.bs].view(torch.int16).fill_(self.BF16_NAN)
+        self.free.append(phys)
+
+    def prepare(self, step: int) -> np.ndarray:
+        """Frees what `step` and later steps never read, then takes blocks for every position up to the
+        current token.  Returns the freeable block ranges [B, 2, 2] of this step."""
+        seg = self.wl.seg(step)
+        blocks = M.murmur_freeable_blocks_host(seg, self.pol_np, self.bs, 1)
+        for b in range(self.B):
+            for first, n in blocks[b]:
+                for blk in range(int(first), int(first) + int(n)):
+                    if not self.freed[b, blk]:
+                        self._release(b, blk)
+        for b in range(self.B):
+            n_blk = -(-int(seg[b].sum()) // self.bs)
+            for blk in range(n_blk):
+                if self.table[b, blk] < 0 and not self.freed[b, blk]:
+                    if not self.free:
+                        raise MemoryError(f"block pool of {self.n_blocks} blocks exhausted at step {step}")
+                    phys = self.free.pop()
+                    self.table[b, blk] = phys
+                    self._fill(b, blk, phys)
+        self.peak_in_use = max(self.peak_in_use, self.in_use())
+        self.bt.copy_(torch.from_numpy(self.table))
+        self.seg_dev.copy_(torch.from_numpy(seg))
+        self.q.copy_(torch.from_numpy(self.wl.q(step)).view(torch.bfloat16))
+        return blocks
+
+    def step(self, step: int, stream=None) -> None:
+        M.murmur_evict_compact_paged(self.seg_dev, self.pol, 1, self.B, self.bt, self.max_blocks, self.bs, self.idx,
+                                     self.max_keep, self.count, None, stream)
+        M.murmur_decode_attn(self.q, self.kv, self.idx, None, self.count, self.max_keep, self.B, self.Hq, self.Hkv,
+                             self.D, self.wl.scale, self.split_len, self.out, self.out_dtype, self.lse, self.ws,
+                             self.ws_bytes, stream)

@@ -91,6 +91,9 @@ def _load():
     lib.murmur_ring_layout_host.restype = ctypes.c_int
     lib.murmur_ring_layout_host.argtypes = [ctypes.POINTER(murmur_seg), ctypes.POINTER(murmur_policy), i32, i32, i32,
                                             i32p, i32p]
+    lib.murmur_freeable_blocks_host.restype = ctypes.c_int
+    lib.murmur_freeable_blocks_host.argtypes = [ctypes.POINTER(murmur_seg), ctypes.POINTER(murmur_policy), i32, i32,
+                                                i32, i32p]
     lib.murmur_decode_step_ring.restype = ctypes.c_int
     lib.murmur_decode_step_ring.argtypes = [vp, vp, i32, ctypes.POINTER(murmur_ring), vp, ctypes.POINTER(murmur_kv),
                                             vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, i32, vp, i32, vp,
@@ -247,6 +250,20 @@ def murmur_ring_layout_host(seg, pol, out_capacity: int, pol_per_seq: int | None
     _check(_load().murmur_ring_layout_host(_segs(seg_np), _pols(pol_np), pol_per_seq, B, int(out_capacity),
                                            ranges.ctypes.data_as(i32p), cur.ctypes.data_as(i32p)))
     return ranges, cur
+
+
+def murmur_freeable_blocks_host(seg, pol, block_size: int, pol_per_seq: int | None = None) -> np.ndarray:
+    """Host-only: whole logical blocks no later step retains.  Returns int32 [B, 2, 2]: (first block, number of
+    blocks) of the speech part, then of the output part."""
+    seg_np = np.ascontiguousarray(seg, dtype=np.int32).reshape(-1, 4)
+    pol_np = np.ascontiguousarray(pol, dtype=np.int32)
+    if pol_per_seq is None:
+        pol_per_seq = 1 if pol_np.ndim == 2 and pol_np.shape[0] > 1 else 0
+    B = seg_np.shape[0]
+    blocks = np.zeros((B, 2, 2), dtype=np.int32)
+    _check(_load().murmur_freeable_blocks_host(_segs(seg_np), _pols(pol_np), pol_per_seq, B, int(block_size),
+                                               blocks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
+    return blocks
 
 
 def make_ring(out_capacity: int, k_new, v_new) -> murmur_ring:

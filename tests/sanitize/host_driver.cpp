@@ -54,6 +54,21 @@ int main() {
                 for (int k = 0; k < 6; ++k) total += ranges[b * 12 + 2 * k + 1];
                 CHECK(total == counts[b]);
             }
+        std::vector<int32_t> blocks(B * 4);
+        const int32_t bs = (int32_t)rnd(0, 64);
+        const int fr = murmur_freeable_blocks_host(seg.data(), pol.data(), 1, B, bs, blocks.data());
+        CHECK(fr == MURMUR_OK || fr == MURMUR_EINVAL);
+        if (fr == MURMUR_OK && rc == MURMUR_OK)
+            for (int b = 0; b < B; ++b) {  // freed blocks and retained positions never meet
+                const int64_t length = (int64_t)seg[b].prompt_pre + seg[b].speech_len + seg[b].prompt_mid + seg[b].out_len;
+                int64_t freed = 0;
+                for (int k = 0; k < 2; ++k) {
+                    CHECK(blocks[b * 4 + 2 * k] >= 0 && blocks[b * 4 + 2 * k + 1] >= 0);
+                    CHECK(((int64_t)blocks[b * 4 + 2 * k] + blocks[b * 4 + 2 * k + 1]) * bs <= length);
+                    freed += (int64_t)blocks[b * 4 + 2 * k + 1] * bs;
+                }
+                CHECK(freed + counts[b] <= length);
+            }
         size_t bytes = 0;
         const int32_t split = (int32_t)(rnd(0, 3) ? 32 * rnd(0, 40) : -1);
         const int wr = murmur_decode_attn_workspace((int32_t)rnd(1, 28), B, (int32_t)(4 * rnd(1, 7)), 4,

@@ -13,6 +13,7 @@ import pytest
 import torch
 
 import oracle
+from oracle import paged as OP
 from oracle import ring as OR
 from paper_2606_01483_amd import _build
 from paper_2606_01483_amd import murmur as M
@@ -38,14 +39,14 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 5
+    assert M.murmur_abi_version() == 6
 
 
 def test_retained_count_host_matches_oracle():
@@ -282,6 +283,40 @@ def test_ring_layout_host_matches_oracle_rows():
             out0 = int(seg_ok[b, 0] + seg_ok[b, 1] + seg_ok[b, 2])
             assert cur[b] == OR.ring_row(int(seg_ok[b, 3]) - 1, out0, int(pol_ok[b, 4]), cap)
             assert np.all(ranges[b, :, 1] >= 0)
+
+
+def expand_blocks(blocks_row):
+    out = []
+    for first, n in blocks_row:
+        out.extend(range(int(first), int(first) + int(n)))
+    return out
+
+
+def test_freeable_blocks_host_matches_oracle():
+    """The closed form's whole blocks equal the oracle's scan of later steps (300 random layouts, policies
+    and block sizes, sinks and windows on and off), the speech part first."""
+    rng = np.random.default_rng(31)
+    B = 300
+    seg = np.stack([rng.integers(0, 9, B), rng.integers(1, 90, B), rng.integers(0, 5, B), rng.integers(1, 80, B)],
+                   axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 40, B)), rng.integers(0, 20, B),
+                    rng.integers(0, 6, B), np.where(rng.random(B) < 0.2, OFF, rng.integers(1, 30, B)),
+                    rng.integers(0, 5, B)], axis=1).astype(np.int32)
+    for bs in (1, 3, 8):
+        got = M.murmur_freeable_blocks_host(seg, pol, bs)
+        for b in range(B):
+            want = OP.freeable_blocks(seg[b], pol[b], bs)
+            assert expand_blocks(got[b]) == want, (b, bs, seg[b], pol[b])
+
+
+def test_freeable_blocks_host_rejects():
+    seg = np.array([[32, 100, 0, 50]], dtype=np.int32)
+    with pytest.raises(M.MurmurError):
+        M.murmur_freeable_blocks_host(seg, np.array([0, 0, 0, -1, 0], dtype=np.int32), 16)  # window 0
+    with pytest.raises(M.MurmurError):
+        M.murmur_freeable_blocks_host(seg, np.array([-1, 0, 0, -1, 0], dtype=np.int32), 0)
+    lib = M.lib()
+    assert lib.murmur_freeable_blocks_host(None, None, 0, 1, 16, None) == M.MURMUR_EINVAL
 
 
 def test_ring_layout_host_rejects_rings_too_small():

@@ -13,7 +13,7 @@ import oracle
 from oracle import paged as OP
 from paper_2606_01483_amd import murmur as M
 from paper_2606_01483_amd import workloads as W
-from paper_2606_01483_amd.decode import PagedBatch
+from paper_2606_01483_amd.decode import PagedBatch, RecyclingPagedBatch
 from _tol import REL_TOL, LSE_TOL, lse_err, rel_err_fp32
 
 pytestmark = pytest.mark.gpu
@@ -95,3 +95,70 @@ def test_paged_block_table_too_short():
     torch.cuda.synchronize()
     assert M.murmur_device_error() & M.MURMUR_DEVERR_POSITION
     assert np.all(np.isnan(pb.out.float().cpu().numpy()))
+
+
+def recycling_workload(steps):
+    """Three sequences whose speech window (48 tokens, delay 20, 4 sinks) and output window (40, 2 sinks)
+    move over the whole decode; the third keeps everything (eviction off), so its blocks are never freed."""
+    seg0 = np.array([[16, 200, 4, 10], [30, 170, 0, 25], [8, 60, 2, 5]], dtype=np.int32)
+    pol = np.array([[48, 20, 4, 40, 2], [32, 5, 0, 24, 0], [-1, 0, 0, -1, 0]], dtype=np.int32)
+    return W.build("paged_recycle", 515, 2, seg0, pol, steps, planted=False, hq=8, hkv=2)
+
+
+@pytest.mark.parametrize("block_size", [16, 4])
+def test_paged_recycling_bounds_the_pool(block_size):
+    """A 200-step decode on a pool that cannot hold the whole cache: before each step the blocks that no
+    later step retains are freed (filled with NaN) and new positions reuse them.  Every step matches the
+    oracle's attention over the sequence-ordered cache with no device error (no freed block is read), and
+    the pool never needs more than prompt + speech + sinks + output window, plus two partial blocks per
+    freed range, per sequence."""
+    steps = 200
+    wl = recycling_workload(steps)
+    seg_last = wl.seg(steps - 1)
+    pol = wl.policy
+    # what each sequence may hold at once: prompts, speech, output sinks and window (the whole output when
+    # output eviction is off), rounded up to blocks, plus the blocks two freed ranges can leave partly used
+    cap = 0
+    for b in range(wl.batch):
+        p_pre, l_s, p_mid, j = (int(x) for x in seg_last[b])
+        outs = j if pol[b, 3] < 0 else int(pol[b, 4]) + int(pol[b, 3])
+        cap += -(-(p_pre + l_s + p_mid + outs) // block_size) + 4
+    without = int((-(-seg_last.sum(axis=1) // block_size)).sum())
+    assert cap < without
+    announce(f"paged recycling block {block_size}: pool {cap} blocks, {without} without freeing")
+    pb = RecyclingPagedBatch(wl, block_size, cap)
+    freed_total = 0
+    for s in range(steps):
+        blocks = pb.prepare(s)
+        freed_total = int(blocks[:, :, 1].sum())
+        pb.idx.fill_(-7)
+        pb.step(s)
+        torch.cuda.synchronize()
+        assert M.murmur_device_error() == 0, f"step {s}"
+        idx, cnt = oracle.retained(wl.seg(s), wl.policy, pb.max_keep)
+        assert np.array_equal(pb.count.cpu().numpy(), cnt)
+        assert np.array_equal(pb.idx.cpu().numpy(), OP.rows_of(idx, cnt, pb.table, block_size))
+        ref, ref_lse = oracle.attend(wl.q(s), wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=16)
+        assert rel_err_fp32(pb.out.float().cpu().numpy(), ref) <= REL_TOL, f"step {s}"
+        assert lse_err(pb.lse.cpu().numpy(), ref_lse) <= LSE_TOL, f"step {s}"
+    assert pb.peak_in_use <= cap
+    assert freed_total > 0 and pb.peak_in_use < without
+    assert not pb.freed[2].any()  # eviction off: nothing of the third sequence is freed
+
+
+def test_paged_freed_block_is_a_device_error():
+    """A retained position whose block the table marks freed (-1): the eviction reports
+    MURMUR_DEVERR_BLOCK and writes -1, the attention then gives NaN for that sequence only."""
+    wl = recycling_workload(4)
+    pb = RecyclingPagedBatch(wl, 16, 200)
+    pb.prepare(0)
+    pb.table[1, 0] = -1  # the prompt of sequence 1 is always retained
+    pb.bt.copy_(torch.from_numpy(pb.table))
+    announce("paged freed block read")
+    pb.step(0)
+    torch.cuda.synchronize()
+    code = M.murmur_device_error()
+    assert code & M.MURMUR_DEVERR_BLOCK and code & M.MURMUR_DEVERR_POSITION
+    assert np.all(pb.idx[1, :16].cpu().numpy() == -1)
+    y = pb.out.float().cpu().numpy()
+    assert np.all(np.isnan(y[:, 1])) and np.all(np.isfinite(y[:, 0])) and np.all(np.isfinite(y[:, 2]))
