@@ -970,11 +970,54 @@ static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, Sl
     }
 }
 
+// Up to kMergeBatch partials (every group of the 12 x 300 s workloads): one
+// batch, all loads of a thread in flight at once.  The loads are unconditional
+// (a branch around a load lets the compiler wait for it inside the branch):
+// one past the last partial gets an offset outside the buffer resource's
+// range, which the hardware answers with zero and no memory access, and a
+// select drops it.
+constexpr uint32_t kNoPartial = 0x80000000u;  // a byte offset past both partial arrays (each < 2^31 bytes)
+
+template <typename SlotOf>
+static __device__ __forceinline__ void merge_one_batch(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
+                                                       int64_t row0) {
+    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+    for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
+        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
+        float mm[kMergeBatch], ll[kMergeBatch];
+        f32x4 oo[kMergeBatch];
+#pragma unroll
+        for (int k = 0; k < kMergeBatch; ++k) {
+            const uint32_t prow = slot_of(k < n ? k : 0) * G + h;
+            mm[k] = load_coherent1(rml, k < n ? prow * 8 : kNoPartial);
+            ll[k] = load_coherent1(rml, k < n ? prow * 8 + 4 : kNoPartial);
+            oo[k] = load_coherent4(ro, k < n ? (prow * kHeadDim + d0) * 4 : kNoPartial);
+        }
+        float M = mm[0];
+#pragma unroll
+        for (int k = 1; k < kMergeBatch; ++k) M = k < n ? fmaxf(M, mm[k]) : M;
+        float L = 0.f;
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < kMergeBatch; ++k) {
+            const float f = (k >= n || mm[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mm[k] - M);
+            L += ll[k] * f;
+            O += oo[k] * f;
+        }
+        store_output(a, row0 + h, d0, O, M, L);
+    }
+}
+
 template <typename SlotOf>
 static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
                                                       int64_t row0, float *s_ml) {
     if (n > 2 * kMergeBatch) {
         merge_many(a, n, slot_of, G, tid, row0, s_ml);
+        return;
+    }
+    if (n <= kMergeBatch) {
+        merge_one_batch(a, n, slot_of, G, tid, row0);
         return;
     }
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
