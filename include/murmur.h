@@ -16,6 +16,12 @@
  *                            (and an equivalent table of contiguous ranges);
  *   murmur_decode_attn    -- split-K grouped-query attention over those
  *                            positions with a log-sum-exp merge of the splits.
+ * murmur_decode_step does both in one launch; murmur_decode_step_ring does it
+ * on physical eviction storage (an output ring) and appends the current
+ * token's K/V; murmur_evict_compact_paged emits the lists as rows of a paged
+ * pool.  Host-only helpers size the lists, lay out ring storage, name the
+ * paged blocks no later step reads, and plan the chunking of a long recording
+ * (Section 3.1, Equation 4).
  *
  * Conventions shared by every call:
  *   - Pointers named *_dev are device memory (HIP, the current device); all
