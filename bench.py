@@ -285,8 +285,54 @@ def paged_timing(wl, n_steps: int, steps: int, warmup: int, replicas: int, split
     attn_us = time_graph(graph) / steps
     if M.murmur_device_error() != 0:
         raise RuntimeError("device error during the timed paged steps")
-    return {"block_size": block_size, "pool_layout": "block, slot, kv head, head dim",
-            "step_two_launches_us": round(step_us, 3), "decode_attn_us": round(attn_us, 3)}
+    res = {"block_size": block_size, "pool_layout": "block, slot, kv head, head dim",
+           "step_two_launches_us": round(step_us, 3), "decode_attn_us": round(attn_us, 3)}
+    res.update(device_manager_timing(wl, n_steps, block_size, split_len))
+    return res
+
+
+def device_manager_timing(wl, n_steps: int, block_size: int, split_len: int) -> dict:
+    """The same decode on a paged cache whose block manager runs on the device: murmur_paged_step (free the
+    blocks no later step reads, take a block for the current token, write its K/V) alone, and the whole
+    three-launch step, each over all steps captured into one graph and replayed from the starting state.  One
+    copy of the cache (its state changes with every step), so the attention here reads warm data."""
+    import torch
+    from paper_2606_01483_amd import murmur as M
+    from paper_2606_01483_amd.decode import DevicePagedBatch
+    log("device block manager: graphs of paged steps")
+    lens = wl.seg(n_steps - 1).sum(axis=1)
+    dp = DevicePagedBatch(wl, block_size, int((-(-lens // block_size)).sum()) + wl.batch,
+                          out_dtype=M.MURMUR_DTYPE_BF16, split_len=split_len)
+    start = dp.state()
+    stream = torch.cuda.current_stream()
+
+    def per_step_us(fn) -> float:
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        dp.restore(start)
+        cap.wait_stream(stream)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            for i in range(n_steps):
+                fn(i)
+        best = None
+        for _ in range(3):  # the first replay warms up
+            dp.restore(start)
+            torch.cuda.synchronize()
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            graph.replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            us = t0.elapsed_time(t1) * 1e3 / n_steps
+            best = us if best is None else min(best, us)
+        return best
+
+    manager_us = per_step_us(dp.manage)
+    step_us = per_step_us(dp.step)
+    if M.murmur_device_error() != 0:
+        raise RuntimeError("device error during the device block manager timing")
+    return {"device_manager_us": round(manager_us, 3), "device_managed_step_us_warm": round(step_us, 3)}
 
 
 def recycled_blocks(seg0, policy, block_size: int = 16, n_outputs: int = 2700) -> dict:

@@ -82,6 +82,7 @@ enum {
     MURMUR_DEVERR_COUNT = 8,     /* decode_attn: count outside [1, max_keep] */
     MURMUR_DEVERR_CAPACITY = 16, /* decode_step_ring: the output ring cannot hold the retained outputs */
     MURMUR_DEVERR_BLOCK = 32,    /* evict_compact_paged: a retained position past the block table or in a freed block */
+    MURMUR_DEVERR_POOL = 64,     /* paged_step: the free stack ran out (or overflowed its capacity) */
 };
 
 /* One sequence (audio chunk) of the batch, Section 3.2's layout
@@ -135,7 +136,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 6
+#define MURMUR_ABI_VERSION 7
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -211,6 +212,46 @@ int murmur_evict_compact_paged(const murmur_seg *seg_dev, const murmur_policy *p
  * Errors: MURMUR_EINVAL as murmur_retained_count_host. */
 int murmur_freeable_blocks_host(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B,
                                 int32_t block_size, int32_t *blocks);
+
+/* One decode step of a paged cache's block manager, on the device, so that a
+ * whole decode loop -- paging included -- can be captured into one HIP graph
+ * (Section 3.2: evicted entries leave the KV cache).  For every sequence at
+ * step out_len, in one launch:
+ *   1. every block of block_table_dev that lies wholly inside the positions
+ *      no step from out_len on retains (the ranges murmur_freeable_blocks_host
+ *      names) and is still allocated (entry >= 0) is pushed onto the free
+ *      stack, and its entry becomes -1;
+ *   2. if the logical block of the current token (position
+ *      prompt_pre + speech_len + prompt_mid + out_len - 1) has no block, one
+ *      is popped for it (blocks freed in step 1 included);
+ * and, with a pool, in a second launch:
+ *   3. the current token's K and V are written into its pool row.
+ * Call it once per decode step, in order, before murmur_evict_compact_paged;
+ * every position before the current token must have a block (or have been
+ * freed).  Pushes and pops are placed by block-wide scans over the sequences
+ * in index order, so the result is deterministic.
+ *   full_scan:       1: step 1 looks at every block of the ranges (the first
+ *                    call after a prefill, or after steps were skipped);
+ *                    0: only at the blocks that became whole since step
+ *                    out_len - 1 (each later call: O(1) per sequence);
+ *   block_table_dev: device int32 [B][max_blocks], physical block numbers,
+ *                    -1 where there is none; updated in place;
+ *   free_stack_dev:  device int32 [capacity], free physical blocks in
+ *                    [0, *free_top_dev); capacity >= the pool's blocks;
+ *   free_top_dev:    device int32, the number of free blocks; updated;
+ *   pool:            nullable; the pool as murmur_decode_attn reads it in
+ *                    index mode (stride_b ignored, max_len = pool rows);
+ *   Hkv:             KV heads (with a pool);
+ *   k_new_dev, v_new_dev: bf16 [n_layers][B][Hkv][128], contiguous, 16-byte
+ *                    aligned (with a pool): the current token's K and V.
+ * Errors: MURMUR_EINVAL (argument checks), MURMUR_EHIP.  Device errors:
+ * MURMUR_DEVERR_POOL (the stack is empty: the entry stays -1, and so the
+ * attention reports the position), MURMUR_DEVERR_BLOCK (the current token
+ * lies past max_blocks), MURMUR_DEVERR_POLICY (that sequence is left as is). */
+int murmur_paged_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq, int32_t B,
+                      int32_t *block_table_dev, int32_t max_blocks, int32_t block_size, int32_t *free_stack_dev,
+                      int32_t *free_top_dev, int32_t capacity, int32_t full_scan, const murmur_kv *pool,
+                      int32_t Hkv, const void *k_new_dev, const void *v_new_dev, murmur_stream_t stream);
 
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
  * (0 = the automatic choice, MURMUR_SPLIT_STREAM, or positions per split).

@@ -333,6 +333,53 @@ MURMUR_EXPORT int murmur_freeable_blocks_host(const murmur_seg *seg, const murmu
     return ok();
 }
 
+MURMUR_EXPORT int murmur_paged_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                                    int32_t B, int32_t *block_table_dev, int32_t max_blocks, int32_t block_size,
+                                    int32_t *free_stack_dev, int32_t *free_top_dev, int32_t capacity,
+                                    int32_t full_scan, const murmur_kv *pool, int32_t Hkv, const void *k_new_dev,
+                                    const void *v_new_dev, murmur_stream_t stream) {
+    if (!seg_dev || !pol_dev || !block_table_dev || !free_stack_dev || !free_top_dev)
+        return fail(MURMUR_EINVAL, "seg_dev, pol_dev, block_table_dev, free_stack_dev and free_top_dev must not be NULL");
+    if (B < 1) return fail(MURMUR_EINVAL, "B must be >= 1 (got %d)", B);
+    if (max_blocks < 1) return fail(MURMUR_EINVAL, "max_blocks must be >= 1 (got %d)", max_blocks);
+    if (capacity < 1) return fail(MURMUR_EINVAL, "capacity must be >= 1 (got %d)", capacity);
+    if (pol_per_seq != 0 && pol_per_seq != 1) return fail(MURMUR_EINVAL, "pol_per_seq must be 0 or 1");
+    if (full_scan != 0 && full_scan != 1) return fail(MURMUR_EINVAL, "full_scan must be 0 or 1");
+    if (block_size < 1 || block_size > (1 << 20) || (block_size & (block_size - 1)) != 0)
+        return fail(MURMUR_EINVAL, "block_size must be a power of two in [1, 2^20] (got %d)", block_size);
+    if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(block_table_dev, 4) || !aligned(free_stack_dev, 4) ||
+        !aligned(free_top_dev, 4))
+        return fail(MURMUR_EINVAL, "device pointers must be 4-byte aligned");
+    if ((int64_t)B * max_blocks > ((int64_t)1 << 40)) return fail(MURMUR_EINVAL, "B * max_blocks too large");
+    if (pool) {
+        if (!pool->k || !pool->v || !k_new_dev || !v_new_dev)
+            return fail(MURMUR_EINVAL, "with a pool, pool->k, pool->v, k_new_dev and v_new_dev must not be NULL");
+        if (Hkv < 1 || pool->n_layers < 1 || pool->max_len < 1)
+            return fail(MURMUR_EINVAL, "Hkv, pool->n_layers and pool->max_len must be >= 1");
+        const int64_t strides[3] = {pool->stride_layer, pool->stride_h, pool->stride_pos};
+        for (int i = 0; i < 3; ++i)
+            if (strides[i] < 0 || strides[i] % 8 != 0)
+                return fail(MURMUR_EINVAL, "pool strides must be non-negative multiples of 8 elements");
+        if (pool->stride_pos < kHeadDim && pool->max_len > 1)
+            return fail(MURMUR_EINVAL, "pool->stride_pos (%lld) must be >= head_dim", (long long)pool->stride_pos);
+        if (!aligned(pool->k, 16) || !aligned(pool->v, 16) || !aligned(k_new_dev, 16) || !aligned(v_new_dev, 16))
+            return fail(MURMUR_EINVAL, "pool->k, pool->v, k_new_dev and v_new_dev must be 16-byte aligned");
+        if ((int64_t)B * pool->n_layers * Hkv > ((int64_t)1 << 36))
+            return fail(MURMUR_EINVAL, "B * n_layers * Hkv too large");
+    }
+    int log2_bs = 0;
+    while ((1 << log2_bs) < block_size) ++log2_bs;
+    int e = launch_paged_step(seg_dev, pol_dev, pol_per_seq, B, block_table_dev, max_blocks, log2_bs, free_stack_dev,
+                              free_top_dev, capacity, full_scan, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "paged_step launch failed: %s", hip_error_text(e));
+    if (pool) {
+        e = launch_paged_append(seg_dev, B, block_table_dev, max_blocks, log2_bs, *pool, Hkv, k_new_dev, v_new_dev,
+                                stream);
+        if (e != 0) return fail(MURMUR_EHIP, "paged_step append launch failed: %s", hip_error_text(e));
+    }
+    return ok();
+}
+
 MURMUR_EXPORT int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv,
                                                int32_t max_keep, int32_t split_len, size_t *bytes) {
     if (!bytes) return fail(MURMUR_EINVAL, "bytes must not be NULL");

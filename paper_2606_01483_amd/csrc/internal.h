@@ -93,6 +93,12 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream);
 int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream);
 int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, uint32_t *sink, murmur_stream_t stream);
+int launch_paged_step(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B, int32_t *bt,
+                      int32_t max_blocks, int32_t log2_bs, int32_t *stack, int32_t *top, int32_t capacity,
+                      int32_t full_scan, murmur_stream_t stream);
+int launch_paged_append(const murmur_seg *seg, int32_t B, const int32_t *bt, int32_t max_blocks, int32_t log2_bs,
+                        const murmur_kv &pool, int32_t Hkv, const void *k_new, const void *v_new,
+                        murmur_stream_t stream);
 int read_and_clear_device_error(murmur_stream_t stream, int32_t *code);
 const char *hip_error_text(int err);
 

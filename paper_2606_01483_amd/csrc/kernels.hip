@@ -105,6 +105,156 @@ __global__ __launch_bounds__(256) void evict_compact_kernel(const murmur_seg *__
 }
 
 // ---------------------------------------------------------------------------
+// paged_step: the block manager of a paged cache, one decode step, on the
+// device.  One workgroup handles every sequence, 256 at a time: it returns to
+// the free stack each still-allocated block that no step from out_len on
+// retains (evicted_ranges: the speech behind the window and the outputs older
+// than the window, minus sinks), then pops a block for the current token if
+// its logical block has none.  Pushes and pops are placed with block-wide
+// exclusive scans, so the stack stays dense and the result does not depend on
+// thread timing.  A full scan frees every allocated block inside the ranges;
+// otherwise only the blocks that became whole since step out_len - 1 are
+// looked at (one call per step, in order).
+// ---------------------------------------------------------------------------
+static __device__ __forceinline__ int block_exclusive_scan(int v, int *s, int tid, int &total) {
+    s[tid] = v;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const int t = tid >= off ? s[tid - off] : 0;
+        __syncthreads();
+        s[tid] += t;
+        __syncthreads();
+    }
+    total = s[255];
+    const int excl = s[tid] - v;
+    __syncthreads();
+    return excl;
+}
+
+__global__ __launch_bounds__(256) void paged_step_kernel(const murmur_seg *__restrict__ seg,
+                                                         const murmur_policy *__restrict__ pol, int32_t pol_per_seq,
+                                                         int32_t B, int32_t *__restrict__ bt, int32_t max_blocks,
+                                                         int32_t log2_bs, int32_t *__restrict__ stack,
+                                                         int32_t *__restrict__ top, int32_t capacity,
+                                                         int32_t full_scan) {
+    __shared__ int s_scan[256];
+    __shared__ int s_top;
+    const int tid = threadIdx.x;
+    if (tid == 0) s_top = *top;
+    __syncthreads();
+    int err = 0;
+    for (int b0 = 0; b0 < B; b0 += 256) {
+        const int b = b0 + tid;
+        int32_t ranges[2][2] = {{0, 0}, {0, 0}}, before[2][2] = {{0, 0}, {0, 0}};
+        int32_t cur = 0;  // logical block of the current token
+        bool valid = false;
+        if (b < B) {
+            const murmur_seg sq = seg[b];
+            const murmur_policy p = pol[pol_per_seq ? b : 0];
+            if (evicted_ranges(sq.prompt_pre, sq.speech_len, sq.prompt_mid, sq.out_len, p.speech_window,
+                               p.speech_delay, p.speech_sink, p.out_window, p.out_sink, ranges[0], ranges[1]) == 0) {
+                valid = true;
+                const int64_t len = (int64_t)sq.prompt_pre + sq.speech_len + sq.prompt_mid + sq.out_len;
+                cur = (int32_t)((len - 1) >> log2_bs);
+                // The ranges of the previous step (empty before the first): only blocks that became whole
+                // since then are new, unless the caller asks for a full scan.
+                if (!full_scan && sq.out_len > 1)
+                    evicted_ranges(sq.prompt_pre, sq.speech_len, sq.prompt_mid, sq.out_len - 1, p.speech_window,
+                                   p.speech_delay, p.speech_sink, p.out_window, p.out_sink, before[0], before[1]);
+            } else {
+                err |= MURMUR_DEVERR_POLICY;
+            }
+        }
+        int32_t *row = bt + (int64_t)(valid ? b : 0) * max_blocks;
+        // Whole logical blocks inside the two ranges, clipped to the table; without a full scan, from the
+        // previous step's last whole block on (each range's start stays put while it is not empty).
+        int32_t lo[2], hi[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int64_t a = ranges[k][0], e = (int64_t)ranges[k][0] + ranges[k][1];
+            int64_t first = (a + (1 << log2_bs) - 1) >> log2_bs;
+            const int64_t end = e >> log2_bs;
+            if (!full_scan && before[k][1] > 0) {
+                const int64_t end_before = ((int64_t)before[k][0] + before[k][1]) >> log2_bs;
+                if (end_before > first) first = end_before;
+            }
+            lo[k] = valid ? (int32_t)first : 0;
+            hi[k] = valid ? (int32_t)(end < max_blocks ? end : max_blocks) : 0;
+        }
+        int npush = 0;
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+            for (int32_t blk = lo[k]; blk < hi[k]; ++blk) npush += row[blk] >= 0;
+        int pushed;
+        const int off = block_exclusive_scan(npush, s_scan, tid, pushed);
+        int at = s_top + off;
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+            for (int32_t blk = lo[k]; blk < hi[k]; ++blk) {
+                const int32_t phys = row[blk];
+                if (phys < 0) continue;
+                if (at < capacity) stack[at] = phys;
+                else err |= MURMUR_DEVERR_POOL;
+                ++at;
+                row[blk] = -1;
+            }
+        __syncthreads();  // every thread has read s_top
+        if (tid == 0) s_top = s_top + pushed < capacity ? s_top + pushed : capacity;
+        __syncthreads();
+        if (valid && cur >= max_blocks) err |= MURMUR_DEVERR_BLOCK;
+        const int need = valid && cur < max_blocks && row[cur] < 0;
+        int taken;
+        const int off2 = block_exclusive_scan(need, s_scan, tid, taken);
+        if (need) {
+            const int from = s_top - 1 - off2;
+            if (from >= 0) row[cur] = stack[from];
+            else err |= MURMUR_DEVERR_POOL;
+        }
+        __syncthreads();  // every thread has read s_top and the stack
+        if (tid == 0) s_top = s_top - taken > 0 ? s_top - taken : 0;
+        __syncthreads();
+    }
+    if (tid == 0) *top = s_top;
+    if (err) raise_device_error(err);
+}
+
+// The current token's K and V rows (256 bytes each per layer and KV head) into
+// the pool row its block table gives; 16 bytes per thread.  A sequence whose
+// block is missing (an error paged_step has reported) or whose row lies
+// outside the pool is skipped.
+__global__ __launch_bounds__(256) void paged_append_kernel(const murmur_seg *__restrict__ seg, int32_t B,
+                                                           const int32_t *__restrict__ bt, int32_t max_blocks,
+                                                           int32_t log2_bs, uint16_t *__restrict__ k,
+                                                           uint16_t *__restrict__ v, int64_t s_layer, int64_t s_h,
+                                                           int64_t s_pos, int64_t rows,
+                                                           const uint16_t *__restrict__ k_new,
+                                                           const uint16_t *__restrict__ v_new, int32_t NL,
+                                                           int32_t Hkv) {
+    const int64_t items = (int64_t)B * NL * Hkv * 2 * 16;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < items; i += (int64_t)gridDim.x * blockDim.x) {
+        const int c = (int)(i & 15);
+        int64_t r = i >> 4;
+        const int is_v = (int)(r & 1);
+        r >>= 1;
+        const int h = (int)(r % Hkv);
+        r /= Hkv;
+        const int layer = (int)(r % NL);
+        const int b = (int)(r / NL);
+        const murmur_seg sq = seg[b];
+        const int64_t p = (int64_t)sq.prompt_pre + sq.speech_len + sq.prompt_mid + sq.out_len - 1;
+        const int64_t blk = p >> log2_bs;
+        if (p < 0 || blk >= max_blocks) continue;
+        const int32_t phys = bt[(int64_t)b * max_blocks + blk];
+        if (phys < 0) continue;
+        const int64_t prow = ((int64_t)phys << log2_bs) | (p & ((1 << log2_bs) - 1));
+        if (prow >= rows) continue;
+        const uint16_t *src = (is_v ? v_new : k_new) + (((int64_t)layer * B + b) * Hkv + h) * kHeadDim + 8 * c;
+        uint16_t *dst = (is_v ? v : k) + layer * s_layer + h * s_h + prow * s_pos + 8 * c;
+        *reinterpret_cast<u32x4 *>(dst) = *reinterpret_cast<const u32x4 *>(src);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // decode_attn helpers
 // ---------------------------------------------------------------------------
 static __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
@@ -1793,6 +1943,26 @@ int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream) {
         launch_decode_attn_mode<kSrcRanges>(a, (hipStream_t)stream);
     else
         launch_decode_attn_mode<kSrcIndex>(a, (hipStream_t)stream);
+    return (int)hipGetLastError();
+}
+
+int launch_paged_step(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B, int32_t *bt,
+                      int32_t max_blocks, int32_t log2_bs, int32_t *stack, int32_t *top, int32_t capacity,
+                      int32_t full_scan, murmur_stream_t stream) {
+    hipLaunchKernelGGL(paged_step_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, seg, pol, pol_per_seq, B, bt,
+                       max_blocks, log2_bs, stack, top, capacity, full_scan);
+    return (int)hipGetLastError();
+}
+
+int launch_paged_append(const murmur_seg *seg, int32_t B, const int32_t *bt, int32_t max_blocks, int32_t log2_bs,
+                        const murmur_kv &pool, int32_t Hkv, const void *k_new, const void *v_new,
+                        murmur_stream_t stream) {
+    const int64_t items = (int64_t)B * pool.n_layers * Hkv * 2 * 16;
+    const int64_t blocks = (items + 255) / 256 < 1024 ? (items + 255) / 256 : 1024;
+    hipLaunchKernelGGL(paged_append_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, seg, B, bt,
+                       max_blocks, log2_bs, (uint16_t *)pool.k, (uint16_t *)pool.v, pool.stride_layer, pool.stride_h,
+                       pool.stride_pos, (int64_t)pool.max_len, (const uint16_t *)k_new, (const uint16_t *)v_new,
+                       pool.n_layers, Hkv);
     return (int)hipGetLastError();
 }
 

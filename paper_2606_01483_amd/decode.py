@@ -455,3 +455,94 @@ class RecyclingPagedBatch:
         M.murmur_decode_attn(self.q, self.kv, self.idx, None, self.count, self.max_keep, self.B, self.Hq, self.Hkv,
                              self.D, self.wl.scale, self.split_len, self.out, self.out_dtype, self.lse, self.ws,
                              self.ws_bytes, stream)
+
+
+class DevicePagedBatch:
+    """Consecutive decode steps on a paged cache whose block manager runs on the device: per step,
+    murmur_paged_step (free the blocks no later step reads, take a block for the current token, write its
+    K/V), murmur_evict_compact_paged and murmur_decode_attn -- three launches and no host work, so a run of
+    steps can be captured into one HIP graph.
+
+    Memory plumbing only: the pool [NL][n_blocks * block_size][Hkv][D] ("flash" layout), the block table
+    [B][max_blocks], the free stack [n_blocks] and its top, per-step layouts, queries and current-token K/V
+    [steps][NL][B][Hkv][D].  The host prefill gives every position before step 0's current token a block
+    (taken from the top of the stack, as the device takes them) and writes its rows."""
+
+    def __init__(self, wl: Workload, block_size: int, n_blocks: int, device: str = "cuda",
+                 out_dtype: int = M.MURMUR_DTYPE_F32, split_len: int = 0):
+        if np.ndim(wl.policy) == 3:
+            raise ValueError("paged steps take per-sequence policies")
+        self.wl = wl
+        self.bs = int(block_size)
+        self.n_blocks = int(n_blocks)
+        self.rows = self.n_blocks * self.bs
+        self.out_dtype = out_dtype
+        self.split_len = split_len
+        B, NL, Hq, Hkv, D = wl.batch, wl.n_layers, wl.hq, wl.hkv, wl.head_dim
+        self.B, self.NL, self.Hq, self.Hkv, self.D = B, NL, Hq, Hkv, D
+        final = wl.seg(wl.steps - 1)
+        self.max_blocks = int((-(-final.sum(axis=1) // self.bs)).max())
+        self.max_keep = int(max(int(retained_counts(wl, s).max()) for s in range(wl.steps)))
+        dev = torch.device(device)
+        # host prefill: positions [0, len - 1) of step 0, blocks popped from the top of the stack
+        table = np.full((B, self.max_blocks), -1, dtype=np.int32)
+        stack = list(range(self.n_blocks))
+        k = np.zeros((NL, self.rows, Hkv, D), dtype=np.uint16)
+        v = np.zeros_like(k)
+        seg0 = wl.seg(0)
+        for b in range(B):
+            n = int(seg0[b].sum()) - 1
+            for blk in range(-(-n // self.bs)):
+                if not stack:
+                    raise MemoryError("the pool cannot hold the prefill")
+                phys = stack.pop()
+                table[b, blk] = phys
+                lo, hi = blk * self.bs, min((blk + 1) * self.bs, n)
+                r0 = phys * self.bs
+                k[:, r0:r0 + hi - lo] = wl.k[:, b, :, lo:hi].transpose(0, 2, 1, 3)
+                v[:, r0:r0 + hi - lo] = wl.v[:, b, :, lo:hi].transpose(0, 2, 1, 3)
+        self.k = torch.from_numpy(k).view(torch.bfloat16).to(dev)
+        self.v = torch.from_numpy(v).view(torch.bfloat16).to(dev)
+        self.kv = M.make_kv(self.k, self.v, NL, self.rows, (self.rows * Hkv * D, 0, D, Hkv * D))
+        self.bt = torch.from_numpy(table).to(dev)
+        self.stack = torch.zeros(self.n_blocks, dtype=torch.int32, device=dev)
+        self.stack[:len(stack)] = torch.tensor(stack, dtype=torch.int32, device=dev)
+        self.top = torch.tensor([len(stack)], dtype=torch.int32, device=dev)
+        self.pol = torch.from_numpy(np.ascontiguousarray(wl.policy, dtype=np.int32)).to(dev)
+        self.seg = torch.from_numpy(np.stack([wl.seg(s) for s in range(wl.steps)]).astype(np.int32)).to(dev)
+        self.q = torch.from_numpy(np.stack([wl.q(s) for s in range(wl.steps)])).view(torch.bfloat16).to(dev)
+        cur = []  # current token's K/V of every step: [steps][NL][B][Hkv][D]
+        for s in range(wl.steps):
+            p = wl.seg(s).sum(axis=1) - 1
+            cur.append((np.stack([wl.k[:, b, :, p[b]] for b in range(B)], axis=1),
+                        np.stack([wl.v[:, b, :, p[b]] for b in range(B)], axis=1)))
+        self.k_new = torch.from_numpy(np.stack([c[0] for c in cur])).view(torch.bfloat16).to(dev)
+        self.v_new = torch.from_numpy(np.stack([c[1] for c in cur])).view(torch.bfloat16).to(dev)
+        self.idx = torch.full((B, self.max_keep), -1, dtype=torch.int32, device=dev)
+        self.count = torch.zeros(B, dtype=torch.int32, device=dev)
+        odt = torch.bfloat16 if out_dtype == M.MURMUR_DTYPE_BF16 else torch.float32
+        self.out = torch.zeros((NL, B, Hq, D), dtype=odt, device=dev)
+        self.lse = torch.zeros((NL, B, Hq), dtype=torch.float32, device=dev)
+        self.ws_bytes = M.murmur_decode_attn_workspace(NL, B, Hq, Hkv, self.max_keep, split_len)
+        self.ws = torch.zeros(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.int32, device=dev)
+
+    def state(self) -> tuple:
+        """Copies of everything a step changes (pool, table, stack, top)."""
+        return tuple(t.clone() for t in (self.k, self.v, self.bt, self.stack, self.top))
+
+    def restore(self, st: tuple) -> None:
+        for t, s in zip((self.k, self.v, self.bt, self.stack, self.top), st):
+            t.copy_(s)
+
+    def manage(self, i: int, stream=None) -> None:
+        """murmur_paged_step of step i (a full scan at the first step, after the host prefill)."""
+        M.murmur_paged_step(self.seg[i], self.pol, 1, self.B, self.bt, self.max_blocks, self.bs, self.stack, self.top,
+                            self.n_blocks, i == 0, self.kv, self.Hkv, self.k_new[i], self.v_new[i], stream)
+
+    def step(self, i: int, stream=None) -> None:
+        self.manage(i, stream)
+        M.murmur_evict_compact_paged(self.seg[i], self.pol, 1, self.B, self.bt, self.max_blocks, self.bs, self.idx,
+                                     self.max_keep, self.count, None, stream)
+        M.murmur_decode_attn(self.q[i], self.kv, self.idx, None, self.count, self.max_keep, self.B, self.Hq, self.Hkv,
+                             self.D, self.wl.scale, self.split_len, self.out, self.out_dtype, self.lse, self.ws,
+                             self.ws_bytes, stream)

@@ -21,6 +21,7 @@ MURMUR_DEVERR_OVERFLOW, MURMUR_DEVERR_POLICY, MURMUR_DEVERR_POSITION, MURMUR_DEV
 MURMUR_DEVERR_CAPACITY = 16
 MURMUR_POL_PER_SEQ, MURMUR_POL_PER_LAYER = 1, 2
 MURMUR_DEVERR_BLOCK = 32
+MURMUR_DEVERR_POOL = 64
 N_PIECES = 6
 SPLIT_UNIT = 128
 MURMUR_SPLIT_STREAM = -1
@@ -94,6 +95,9 @@ def _load():
     lib.murmur_freeable_blocks_host.restype = ctypes.c_int
     lib.murmur_freeable_blocks_host.argtypes = [ctypes.POINTER(murmur_seg), ctypes.POINTER(murmur_policy), i32, i32,
                                                 i32, i32p]
+    lib.murmur_paged_step.restype = ctypes.c_int
+    lib.murmur_paged_step.argtypes = [vp, vp, i32, i32, vp, i32, i32, vp, vp, i32, i32, ctypes.POINTER(murmur_kv), i32,
+                                      vp, vp, vp]
     lib.murmur_decode_step_ring.restype = ctypes.c_int
     lib.murmur_decode_step_ring.argtypes = [vp, vp, i32, ctypes.POINTER(murmur_ring), vp, ctypes.POINTER(murmur_kv),
                                             vp, vp, vp, i32, i32, i32, i32, i32, ctypes.c_float, i32, vp, i32, vp,
@@ -264,6 +268,17 @@ def murmur_freeable_blocks_host(seg, pol, block_size: int, pol_per_seq: int | No
     _check(_load().murmur_freeable_blocks_host(_segs(seg_np), _pols(pol_np), pol_per_seq, B, int(block_size),
                                                blocks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
     return blocks
+
+
+def murmur_paged_step(seg_dev, pol_dev, pol_per_seq: int, B: int, block_table_dev, max_blocks: int, block_size: int,
+                      free_stack_dev, free_top_dev, capacity: int, full_scan: bool = False,
+                      pool: murmur_kv | None = None, Hkv: int = 0, k_new_dev=None, v_new_dev=None,
+                      stream=None) -> None:
+    """Device block manager of a paged cache for one decode step (free, allocate, append the current K/V)."""
+    _check(_load().murmur_paged_step(_addr(seg_dev), _addr(pol_dev), pol_per_seq, B, _addr(block_table_dev),
+                                     max_blocks, block_size, _addr(free_stack_dev), _addr(free_top_dev), capacity,
+                                     int(bool(full_scan)), ctypes.byref(pool) if pool is not None else None, Hkv,
+                                     _addr(k_new_dev), _addr(v_new_dev), _stream(stream)))
 
 
 def make_ring(out_capacity: int, k_new, v_new) -> murmur_ring:

@@ -124,6 +124,12 @@ int main() {
     CHECK(murmur_evict_compact(nullptr, fpol, 0, 12, fi, 10, fi, nullptr, nullptr) == MURMUR_EINVAL);
     CHECK(murmur_evict_compact_paged(fseg, fpol, 0, 12, fi, 8, 12, fi, 10, fi, nullptr, nullptr) == MURMUR_EINVAL);
     CHECK(murmur_read_probe(fake, 1000, 256, (uint32_t *)fake, nullptr) == MURMUR_EINVAL);
+    CHECK(murmur_paged_step(fseg, fpol, 0, 12, fi, 8, 12, fi, fi, 64, 0, nullptr, 0, nullptr, nullptr, nullptr) ==
+          MURMUR_EINVAL);  // block size not a power of two
+    CHECK(murmur_paged_step(fseg, fpol, 0, 12, fi, 8, 16, fi, fi, 0, 0, nullptr, 0, nullptr, nullptr, nullptr) ==
+          MURMUR_EINVAL);  // no capacity
+    CHECK(murmur_paged_step(fseg, fpol, 0, 12, fi, 8, 16, fi, fi, 64, 0, &kv, 4, nullptr, fake, nullptr) ==
+          MURMUR_EINVAL);  // a pool without the current K
     CHECK(murmur_last_error()[0] != '\0');
     printf("host driver: ok\n");
     return 0;

@@ -18,6 +18,14 @@ int launch_evict_compact(const murmur_seg *, const murmur_policy *, int32_t, int
 int launch_decode_attn(const AttnLaunch &, murmur_stream_t) { return reached("decode_attn"); }
 int launch_workspace_init(int32_t *, int64_t, murmur_stream_t) { return reached("workspace_init"); }
 int launch_read_probe(const void *, int64_t, int32_t, uint32_t *, murmur_stream_t) { return reached("read_probe"); }
+int launch_paged_step(const murmur_seg *, const murmur_policy *, int32_t, int32_t, int32_t *, int32_t, int32_t,
+                      int32_t *, int32_t *, int32_t, int32_t, murmur_stream_t) {
+    return reached("paged_step");
+}
+int launch_paged_append(const murmur_seg *, int32_t, const int32_t *, int32_t, int32_t, const murmur_kv &, int32_t,
+                        const void *, const void *, murmur_stream_t) {
+    return reached("paged_append");
+}
 int read_and_clear_device_error(murmur_stream_t, int32_t *) { return reached("device_error"); }
 const char *hip_error_text(int) { return "stub"; }
 }  // namespace murmur

@@ -39,14 +39,14 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 17
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 6
+    assert M.murmur_abi_version() == 7
 
 
 def test_retained_count_host_matches_oracle():
@@ -317,6 +317,28 @@ def test_freeable_blocks_host_rejects():
         M.murmur_freeable_blocks_host(seg, np.array([-1, 0, 0, -1, 0], dtype=np.int32), 0)
     lib = M.lib()
     assert lib.murmur_freeable_blocks_host(None, None, 0, 1, 16, None) == M.MURMUR_EINVAL
+
+
+def test_paged_step_argument_checks():
+    """murmur_paged_step rejects bad arguments before any launch; valid ones reach the launch (MURMUR_EHIP
+    without a GPU)."""
+    lib = M.lib()
+    kv = M.make_kv(FAKE, FAKE, 1, 4096, (4096 * 4 * 128, 0, 128, 4 * 128))
+
+    def call(seg=FAKE, pol=FAKE, per_seq=0, B=12, bt=FAKE, max_blocks=8, bs=16, stack=FAKE, top=FAKE, cap=64,
+             full=0, pool=None, hkv=4, kn=FAKE, vn=FAKE):
+        return lib.murmur_paged_step(seg, pol, per_seq, B, bt, max_blocks, bs, stack, top, cap, full,
+                                     ctypes.byref(pool) if pool is not None else None, hkv, kn, vn, None)
+
+    for over in (dict(seg=None), dict(bt=None), dict(stack=None), dict(top=None), dict(B=0), dict(max_blocks=0),
+                 dict(cap=0), dict(per_seq=2), dict(bs=12), dict(bs=0), dict(top=FAKE + 2), dict(full=2),
+                 dict(pool=kv, kn=None), dict(pool=kv, hkv=0), dict(pool=kv, vn=FAKE + 8)):
+        assert call(**over) == M.MURMUR_EINVAL, over
+        assert M.murmur_last_error() != ""
+    bad_kv = M.make_kv(FAKE, FAKE, 1, 4096, (4096 * 4 * 128, 0, 128, 100))
+    assert call(pool=bad_kv) == M.MURMUR_EINVAL
+    assert call() == M.MURMUR_EHIP
+    assert call(pool=kv) == M.MURMUR_EHIP
 
 
 def test_ring_layout_host_rejects_rings_too_small():

@@ -13,7 +13,7 @@ import oracle
 from oracle import paged as OP
 from paper_2606_01483_amd import murmur as M
 from paper_2606_01483_amd import workloads as W
-from paper_2606_01483_amd.decode import PagedBatch, RecyclingPagedBatch
+from paper_2606_01483_amd.decode import DevicePagedBatch, PagedBatch, RecyclingPagedBatch
 from _tol import REL_TOL, LSE_TOL, lse_err, rel_err_fp32
 
 pytestmark = pytest.mark.gpu
@@ -162,3 +162,116 @@ def test_paged_freed_block_is_a_device_error():
     assert np.all(pb.idx[1, :16].cpu().numpy() == -1)
     y = pb.out.float().cpu().numpy()
     assert np.all(np.isnan(y[:, 1])) and np.all(np.isfinite(y[:, 0])) and np.all(np.isfinite(y[:, 2]))
+
+
+def manager_model(seg, pol, bs, table, stack):
+    """The device block manager's step, written out: sequences in order push their still-allocated blocks
+    inside the freeable ranges (speech part, then output part, ascending), then those whose current token's
+    block is missing pop from the top of the stack in the same order."""
+    blocks = M.murmur_freeable_blocks_host(seg, pol, bs, 1)
+    for b in range(seg.shape[0]):
+        for first, n in blocks[b]:
+            for blk in range(int(first), int(first) + int(n)):
+                if blk < table.shape[1] and table[b, blk] >= 0:
+                    stack.append(int(table[b, blk]))
+                    table[b, blk] = -1
+    take = [b for b in range(seg.shape[0]) if table[b, (int(seg[b].sum()) - 1) // bs] < 0]
+    for i, b in enumerate(take):
+        table[b, (int(seg[b].sum()) - 1) // bs] = stack[len(stack) - 1 - i]
+    del stack[len(stack) - len(take):]
+
+
+def device_state(pb):
+    top = int(pb.top.item())
+    return pb.bt.cpu().numpy(), pb.stack[:top].cpu().numpy().tolist()
+
+
+@pytest.mark.parametrize("block_size", [16, 4])
+def test_device_block_manager_loop(block_size):
+    """200 steps with the block manager on the device (murmur_paged_step: free, allocate, append the current
+    K/V), on a pool smaller than the whole cache: every step's attention matches the oracle, the block table
+    and free stack equal the manager's rule written out on the host, and every block is either in use or on
+    the stack exactly once."""
+    steps = 200
+    wl = recycling_workload(steps)
+    seg_last = wl.seg(steps - 1)
+    cap = 0
+    for b in range(wl.batch):
+        p_pre, l_s, p_mid, j = (int(x) for x in seg_last[b])
+        outs = j if wl.policy[b, 3] < 0 else int(wl.policy[b, 4]) + int(wl.policy[b, 3])
+        cap += -(-(p_pre + l_s + p_mid + outs) // block_size) + 4
+    announce(f"device block manager, block {block_size}, pool {cap} blocks")
+    pb = DevicePagedBatch(wl, block_size, cap)
+    table, stack = device_state(pb)
+    table = table.copy()
+    for s in range(steps):
+        pb.step(s)
+        torch.cuda.synchronize()
+        assert M.murmur_device_error() == 0, f"step {s}"
+        manager_model(wl.seg(s), wl.policy, block_size, table, stack)
+        got_table, got_stack = device_state(pb)
+        assert np.array_equal(got_table, table), f"step {s}"
+        assert got_stack == stack, f"step {s}"
+        used = got_table[got_table >= 0].tolist()
+        assert sorted(used + got_stack) == list(range(cap)), f"step {s}"
+        idx, cnt = oracle.retained(wl.seg(s), wl.policy, pb.max_keep)
+        assert np.array_equal(pb.idx.cpu().numpy(), OP.rows_of(idx, cnt, got_table, block_size))
+        ref, ref_lse = oracle.attend(wl.q(s), wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=16)
+        assert rel_err_fp32(pb.out.float().cpu().numpy(), ref) <= REL_TOL, f"step {s}"
+        assert lse_err(pb.lse.cpu().numpy(), ref_lse) <= LSE_TOL, f"step {s}"
+
+
+def test_device_block_manager_graph_replays():
+    """Twelve steps (three launches each) captured into one HIP graph, replayed three times from the starting
+    state with eager work in between: outputs, pool, block table and free stack equal the eager run."""
+    wl = recycling_workload(12)
+    pb = DevicePagedBatch(wl, 8, 200)
+    start = pb.state()
+    for i in range(12):
+        pb.step(i)
+    torch.cuda.synchronize()
+    assert M.murmur_device_error() == 0
+    want = (pb.out.clone(), pb.lse.clone()) + pb.state()
+    announce("device block manager graph replays")
+    pb.restore(start)
+    graph = torch.cuda.CUDAGraph()
+    cap_stream = torch.cuda.Stream()
+    cap_stream.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=cap_stream):
+        for i in range(12):
+            pb.step(i)
+    for _ in range(3):
+        pb.restore(start)
+        pb.out.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = (pb.out, pb.lse) + (pb.k, pb.v, pb.bt, pb.stack, pb.top)
+        for g, w in zip(got, want):
+            assert torch.equal(g, w)
+    assert M.murmur_device_error() == 0
+
+
+def test_device_block_manager_pool_exhausted():
+    """A pool one block short: the sequence that finds the stack empty gets MURMUR_DEVERR_POOL, its table
+    entry stays -1 and its attention is NaN (reported as a bad position); the others are unaffected."""
+    wl = recycling_workload(40)
+    seg0 = wl.seg(0)
+    prefill = int(sum(-(-(int(seg0[b].sum()) - 1) // 16) for b in range(wl.batch)))
+    pb = DevicePagedBatch(wl, 16, prefill)  # no block left for a new one
+    announce("device block manager, pool exhausted")
+    hit = None
+    for s in range(40):
+        pb.step(s)
+        torch.cuda.synchronize()
+        code = M.murmur_device_error()
+        if code:
+            hit = (s, code)
+            break
+    assert hit is not None, "some sequence must need a new block within 40 steps"
+    s, code = hit
+    assert code & M.MURMUR_DEVERR_POOL
+    y = pb.out.float().cpu().numpy()
+    bad = [b for b in range(wl.batch) if np.isnan(y[:, b]).all()]
+    assert len(bad) >= 1 and all(np.isfinite(y[:, b]).all() for b in range(wl.batch) if b not in bad)
