@@ -228,8 +228,9 @@ int murmur_freeable_blocks_host(const murmur_seg *seg, const murmur_policy *pol,
  *   3. the current token's K and V are written into its pool row.
  * Call it once per decode step, in order, before murmur_evict_compact_paged;
  * every position before the current token must have a block (or have been
- * freed).  Pushes and pops are placed by block-wide scans over the sequences
- * in index order, so the result is deterministic.
+ * freed).  All pushes come before all pops, each in sequence order (placed by
+ * block-wide scans), so the result is deterministic and a step's allocations
+ * can use any block freed in that step.
  *   full_scan:       1: step 1 looks at every block of the ranges (the first
  *                    call after a prefill, or after steps were skipped);
  *                    0: only at the blocks that became whole since step

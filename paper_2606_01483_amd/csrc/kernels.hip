@@ -131,6 +131,54 @@ static __device__ __forceinline__ int block_exclusive_scan(int v, int *s, int ti
     return excl;
 }
 
+// One sequence's view for paged_step: whether its layout and policy are
+// valid, the logical block of its current token, and the logical blocks
+// [lo[k], hi[k]) to look at for freeing in the speech (k = 0) and output
+// (k = 1) ranges: the whole ranges with a full scan, else from the previous
+// step's last whole block on (a range's start stays put while it is not
+// empty, and its end only grows).  Blocks past the table are clipped.
+struct PagedSeq {
+    bool valid;
+    int32_t cur;
+    int32_t lo[2], hi[2];
+};
+
+static __device__ __forceinline__ PagedSeq paged_seq(const murmur_seg *seg, const murmur_policy *pol,
+                                                     int32_t pol_per_seq, int b, int B, int32_t max_blocks,
+                                                     int32_t log2_bs, int32_t full_scan, int &err) {
+    PagedSeq q{false, 0, {0, 0}, {0, 0}};
+    if (b >= B) return q;
+    const murmur_seg sq = seg[b];
+    const murmur_policy p = pol[pol_per_seq ? b : 0];
+    int32_t ranges[2][2], before[2][2] = {{0, 0}, {0, 0}};
+    if (evicted_ranges(sq.prompt_pre, sq.speech_len, sq.prompt_mid, sq.out_len, p.speech_window, p.speech_delay,
+                       p.speech_sink, p.out_window, p.out_sink, ranges[0], ranges[1]) != 0) {
+        err |= MURMUR_DEVERR_POLICY;
+        return q;
+    }
+    if (!full_scan && sq.out_len > 1)
+        evicted_ranges(sq.prompt_pre, sq.speech_len, sq.prompt_mid, sq.out_len - 1, p.speech_window, p.speech_delay,
+                       p.speech_sink, p.out_window, p.out_sink, before[0], before[1]);
+    q.valid = true;
+    const int64_t len = (int64_t)sq.prompt_pre + sq.speech_len + sq.prompt_mid + sq.out_len;
+    q.cur = (int32_t)((len - 1) >> log2_bs);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        int64_t first = ((int64_t)ranges[k][0] + (1 << log2_bs) - 1) >> log2_bs;
+        const int64_t end = ((int64_t)ranges[k][0] + ranges[k][1]) >> log2_bs;
+        if (!full_scan && before[k][1] > 0) {
+            const int64_t end_before = ((int64_t)before[k][0] + before[k][1]) >> log2_bs;
+            if (end_before > first) first = end_before;
+        }
+        q.lo[k] = (int32_t)first;
+        q.hi[k] = (int32_t)(end < max_blocks ? end : max_blocks);
+    }
+    return q;
+}
+
+// Two passes over the sequences, 256 at a time: every push first, then every
+// pop, both in sequence order, so a step's allocations can use any block freed
+// in that step.
 __global__ __launch_bounds__(256) void paged_step_kernel(const murmur_seg *__restrict__ seg,
                                                          const murmur_policy *__restrict__ pol, int32_t pol_per_seq,
                                                          int32_t B, int32_t *__restrict__ bt, int32_t max_blocks,
@@ -143,54 +191,19 @@ __global__ __launch_bounds__(256) void paged_step_kernel(const murmur_seg *__res
     if (tid == 0) s_top = *top;
     __syncthreads();
     int err = 0;
-    for (int b0 = 0; b0 < B; b0 += 256) {
+    for (int b0 = 0; b0 < B; b0 += 256) {  // frees
         const int b = b0 + tid;
-        int32_t ranges[2][2] = {{0, 0}, {0, 0}}, before[2][2] = {{0, 0}, {0, 0}};
-        int32_t cur = 0;  // logical block of the current token
-        bool valid = false;
-        if (b < B) {
-            const murmur_seg sq = seg[b];
-            const murmur_policy p = pol[pol_per_seq ? b : 0];
-            if (evicted_ranges(sq.prompt_pre, sq.speech_len, sq.prompt_mid, sq.out_len, p.speech_window,
-                               p.speech_delay, p.speech_sink, p.out_window, p.out_sink, ranges[0], ranges[1]) == 0) {
-                valid = true;
-                const int64_t len = (int64_t)sq.prompt_pre + sq.speech_len + sq.prompt_mid + sq.out_len;
-                cur = (int32_t)((len - 1) >> log2_bs);
-                // The ranges of the previous step (empty before the first): only blocks that became whole
-                // since then are new, unless the caller asks for a full scan.
-                if (!full_scan && sq.out_len > 1)
-                    evicted_ranges(sq.prompt_pre, sq.speech_len, sq.prompt_mid, sq.out_len - 1, p.speech_window,
-                                   p.speech_delay, p.speech_sink, p.out_window, p.out_sink, before[0], before[1]);
-            } else {
-                err |= MURMUR_DEVERR_POLICY;
-            }
-        }
-        int32_t *row = bt + (int64_t)(valid ? b : 0) * max_blocks;
-        // Whole logical blocks inside the two ranges, clipped to the table; without a full scan, from the
-        // previous step's last whole block on (each range's start stays put while it is not empty).
-        int32_t lo[2], hi[2];
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            const int64_t a = ranges[k][0], e = (int64_t)ranges[k][0] + ranges[k][1];
-            int64_t first = (a + (1 << log2_bs) - 1) >> log2_bs;
-            const int64_t end = e >> log2_bs;
-            if (!full_scan && before[k][1] > 0) {
-                const int64_t end_before = ((int64_t)before[k][0] + before[k][1]) >> log2_bs;
-                if (end_before > first) first = end_before;
-            }
-            lo[k] = valid ? (int32_t)first : 0;
-            hi[k] = valid ? (int32_t)(end < max_blocks ? end : max_blocks) : 0;
-        }
+        const PagedSeq q = paged_seq(seg, pol, pol_per_seq, b, B, max_blocks, log2_bs, full_scan, err);
+        int32_t *row = bt + (int64_t)(q.valid ? b : 0) * max_blocks;
         int npush = 0;
 #pragma unroll
         for (int k = 0; k < 2; ++k)
-            for (int32_t blk = lo[k]; blk < hi[k]; ++blk) npush += row[blk] >= 0;
+            for (int32_t blk = q.lo[k]; blk < q.hi[k]; ++blk) npush += row[blk] >= 0;
         int pushed;
-        const int off = block_exclusive_scan(npush, s_scan, tid, pushed);
-        int at = s_top + off;
+        int at = s_top + block_exclusive_scan(npush, s_scan, tid, pushed);
 #pragma unroll
         for (int k = 0; k < 2; ++k)
-            for (int32_t blk = lo[k]; blk < hi[k]; ++blk) {
+            for (int32_t blk = q.lo[k]; blk < q.hi[k]; ++blk) {
                 const int32_t phys = row[blk];
                 if (phys < 0) continue;
                 if (at < capacity) stack[at] = phys;
@@ -201,13 +214,19 @@ __global__ __launch_bounds__(256) void paged_step_kernel(const murmur_seg *__res
         __syncthreads();  // every thread has read s_top
         if (tid == 0) s_top = s_top + pushed < capacity ? s_top + pushed : capacity;
         __syncthreads();
-        if (valid && cur >= max_blocks) err |= MURMUR_DEVERR_BLOCK;
-        const int need = valid && cur < max_blocks && row[cur] < 0;
+    }
+    for (int b0 = 0; b0 < B; b0 += 256) {  // allocations
+        const int b = b0 + tid;
+        int no_err = 0;  // the first pass has reported invalid sequences
+        const PagedSeq q = paged_seq(seg, pol, pol_per_seq, b, B, max_blocks, log2_bs, 1, no_err);
+        int32_t *row = bt + (int64_t)(q.valid ? b : 0) * max_blocks;
+        if (q.valid && q.cur >= max_blocks) err |= MURMUR_DEVERR_BLOCK;
+        const int need = q.valid && q.cur < max_blocks && row[q.cur] < 0;
         int taken;
-        const int off2 = block_exclusive_scan(need, s_scan, tid, taken);
+        const int off = block_exclusive_scan(need, s_scan, tid, taken);
         if (need) {
-            const int from = s_top - 1 - off2;
-            if (from >= 0) row[cur] = stack[from];
+            const int from = s_top - 1 - off;
+            if (from >= 0) row[q.cur] = stack[from];
             else err |= MURMUR_DEVERR_POOL;
         }
         __syncthreads();  // every thread has read s_top and the stack

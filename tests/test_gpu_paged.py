@@ -275,3 +275,41 @@ def test_device_block_manager_pool_exhausted():
     y = pb.out.float().cpu().numpy()
     bad = [b for b in range(wl.batch) if np.isnan(y[:, b]).all()]
     assert len(bad) >= 1 and all(np.isfinite(y[:, b]).all() for b in range(wl.batch) if b not in bad)
+
+
+def test_device_block_manager_many_sequences():
+    """600 ragged sequences (three chunks of 256 in the manager's workgroup), 30 steps: the table and stack
+    equal the host rule at every step, with the K/V append (DevicePagedBatch) and, on a copy of the state,
+    without a pool (bookkeeping only); attention parity at the first and last step."""
+    rng = np.random.default_rng(606)
+    B, steps = 600, 30
+    seg0 = np.stack([rng.integers(0, 8, B), rng.integers(20, 90, B), rng.integers(0, 4, B), rng.integers(1, 30, B)],
+                    axis=1).astype(np.int32)
+    pol = np.stack([np.where(rng.random(B) < 0.2, OFF, rng.integers(4, 24, B)), rng.integers(0, 8, B),
+                    rng.integers(0, 4, B), np.where(rng.random(B) < 0.2, OFF, rng.integers(2, 16, B)),
+                    rng.integers(0, 3, B)], axis=1).astype(np.int32)
+    wl = W.build("paged_many", 607, 1, seg0, pol, steps, planted=False, hq=4, hkv=1)
+    bs = 8
+    last = wl.seg(steps - 1)
+    cap = int((-(-last.sum(axis=1) // bs)).sum())  # room for everything: exhaustion is not the point here
+    announce(f"device block manager, {B} sequences")
+    pb = DevicePagedBatch(wl, bs, cap)
+    table, stack = device_state(pb)
+    table = table.copy()
+    bt2, stack2, top2 = pb.bt.clone(), pb.stack.clone(), pb.top.clone()
+    for s in range(steps):
+        M.murmur_paged_step(pb.seg[s], pb.pol, 1, B, bt2, pb.max_blocks, bs, stack2, top2, pb.n_blocks, s == 0)
+        pb.step(s)
+        torch.cuda.synchronize()
+        assert M.murmur_device_error() == 0, f"step {s}"
+        manager_model(wl.seg(s), wl.policy, bs, table, stack)
+        got_table, got_stack = device_state(pb)
+        assert np.array_equal(got_table, table), f"step {s}"
+        assert got_stack == stack, f"step {s}"
+        assert np.array_equal(bt2.cpu().numpy(), table), f"step {s} (no pool)"
+        assert stack2[:int(top2.item())].cpu().numpy().tolist() == stack, f"step {s} (no pool)"
+        if s in (0, steps - 1):
+            idx, cnt = oracle.retained(wl.seg(s), wl.policy, pb.max_keep)
+            ref, ref_lse = oracle.attend(wl.q(s), wl.k, wl.v, idx, cnt, scale=wl.scale, n_threads=16)
+            assert rel_err_fp32(pb.out.float().cpu().numpy(), ref) <= REL_TOL, f"step {s}"
+            assert lse_err(pb.lse.cpu().numpy(), ref_lse) <= LSE_TOL, f"step {s}"
