@@ -969,19 +969,34 @@ static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b
     }
 }
 
-// Ring storage: copies the current token's K and V rows (256 bytes each) of
-// this (layer, sequence, KV head) into its ring row `cur`, unless the layout,
-// policy or ring is invalid or the row lies outside the cache.  No workgroup
-// of this launch reads that row (positions equal to cur read nr.k / nr.v).
-// Block-wide; threads 0-15 copy K, 16-31 copy V.
-static __device__ __forceinline__ void append_new_row(const AttnLaunch &a, const NewRows &nr, const uint16_t *kbase,
-                                                      const uint16_t *vbase, int policy_bad, int tid) {
-    if (policy_bad || (uint32_t)nr.cur >= (uint32_t)a.max_len || tid >= 32) return;
-    const int c = tid & 15;
-    const bool is_v = tid >= 16;
-    const u32x4 x = load16((is_v ? nr.v : nr.k) + 8 * c);
-    uint16_t *dst = const_cast<uint16_t *>(is_v ? vbase : kbase) + (int64_t)nr.cur * a.s_pos + 8 * c;
-    *reinterpret_cast<u32x4 *>(dst) = x;
+// Ring storage: the current token's K and V rows (256 bytes each) of this
+// (layer, sequence, KV head) go into its ring row `cur`, by split 0's first
+// wavefront (lanes 0-15 K, 16-31 V; lanes 32-63 load the same chunks and store
+// nothing), unless the layout, policy or ring is invalid or the row lies
+// outside the cache.  The rows are loaded when the kernel starts and stored
+// once the passes are done, so neither the load's round trip nor the store
+// lengthens the workgroup.  No workgroup of this launch reads row `cur`
+// (positions equal to cur read nr.k / nr.v) and the token it held is no longer
+// retained, so the store may land at any time.
+struct NewRowCopy {
+    u32x4 x;
+    bool on;
+};
+static __device__ __forceinline__ NewRowCopy load_new_row(const AttnLaunch &a, const NewRows &nr, int policy_bad,
+                                                          int lane, bool first_wave_of_split0) {
+    NewRowCopy c{{0u, 0u, 0u, 0u}, false};
+    if (first_wave_of_split0) {
+        const int l = lane & 31;
+        c.x = load16(((l >= 16) ? nr.v : nr.k) + 8 * (l & 15));
+        c.on = lane < 32 && !policy_bad && (uint32_t)nr.cur < (uint32_t)a.max_len;
+    }
+    return c;
+}
+static __device__ __forceinline__ void store_new_row(const AttnLaunch &a, const NewRowCopy &c, const NewRows &nr,
+                                                     const uint16_t *kbase, const uint16_t *vbase, int lane) {
+    if (!c.on) return;
+    uint16_t *dst = const_cast<uint16_t *>(lane >= 16 ? vbase : kbase) + (int64_t)nr.cur * a.s_pos + 8 * (lane & 15);
+    *reinterpret_cast<u32x4 *>(dst) = c.x;
 }
 
 // Combine of a workgroup's four wavefronts.  Each wavefront publishes its
@@ -1296,6 +1311,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
     int r = r_begin + wave * kWaveTile;
     materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
     if (kRing) materialize(nr.k, nr.v, nr.cur);
+    NewRowCopy app{};
+    if (kRing) app = load_new_row(a, nr, policy_bad, lane, split == 0 && wave == 0);
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
@@ -1322,6 +1339,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
                                c4);
     }
 
+    if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
     float *o_lds = reinterpret_cast<float *>(smem);  // each wavefront's O rows over its own V tile
     publish_wave(w, o_lds + wave * (kOWaveBytes / 4), cl, wave, n16, c4);
     const int wg_bad_pos = __syncthreads_or(w.bad_pos);
@@ -1332,7 +1350,6 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restr
         (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
         write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
                        max_keep, tid, r_begin, r_begin + a.split_len);
-    if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
@@ -1418,6 +1435,8 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     int r = r_begin + wave * kWaveTile;
     materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
     if (kRing) materialize(nr.k, nr.v, nr.cur);
+    NewRowCopy app{};
+    if (kRing) app = load_new_row(a, nr, policy_bad, lane, split == 0 && wave == 0);
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
@@ -1475,6 +1494,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
         }
     }
 
+    if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
     float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // each wavefront's O rows in its own stages
     constexpr int kStageWaveFloats = kStages * kStageBytes / 4;
     publish_wave(w, o_lds + wave * kStageWaveFloats, cl, wave, n16, c4);
@@ -1486,7 +1506,6 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
         (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
         write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
                        max_keep, tid, r_begin, r_begin + a.split_len);
-    if (kRing && split == 0) append_new_row(a, nr, kbase, vbase, policy_bad, tid);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
