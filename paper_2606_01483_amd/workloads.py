@@ -293,3 +293,19 @@ def with_policy(wl: Workload, policy) -> Workload:
     if pol.ndim == 1:
         pol = np.repeat(pol.reshape(1, 5), wl.batch, axis=0)
     return dataclasses.replace(wl, policy=pol)
+
+
+def large_cache(n_positions: int, seed: int, hkv: int = HKV, device: str = "cuda"):
+    """K and V of one sequence of n_positions (a long-context stand-in far beyond the paper's hour-long
+    recording, for tests at the largest sizes): N(0,1) rounded to bf16, drawn on the device from a seeded
+    torch generator one KV head at a time, since a host draw of this size takes minutes.  Returns torch bf16
+    tensors [1, 1, hkv, n_positions, 128]."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    k = torch.empty((1, 1, hkv, n_positions, HEAD_DIM), dtype=torch.bfloat16, device=device)
+    v = torch.empty_like(k)
+    for h in range(hkv):
+        for t in (k, v):
+            t[0, 0, h].copy_(torch.randn((n_positions, HEAD_DIM), generator=gen, device=device, dtype=torch.float32))
+    return k, v
