@@ -283,15 +283,6 @@ static __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) 
 
 static __device__ __forceinline__ u32x4 load16(const uint16_t *p) { return *reinterpret_cast<const u32x4 *>(p); }
 
-// fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
-static __device__ __forceinline__ uint32_t bf16_rne(float f) {
-    const uint32_t u = __builtin_bit_cast(uint32_t, f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
-static __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __builtin_bit_cast(float, bits16 << 16); }
-
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Two fp32 values -> packed bf16 pair (x in the low half), round to nearest
@@ -556,9 +547,6 @@ static __device__ __forceinline__ void materialize(const T &...x) {
     (materialize_one(x), ...);
 }
 
-// Keeps the instruction scheduler from moving anything across this point
-// (the consumer of one pass above the loads of the next, in particular).
-static __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Softmax update of one pass from its S^T tile (lane (head n16, c4), register
 // i of block blk: logit of rank 16*blk + 4*c4 + i of the pass): masks ranks
