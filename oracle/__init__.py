@@ -137,8 +137,3 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, idx: np.ndarray, count: 
     if rc != 0:
         raise ValueError("oracle_attn: invalid input")
     return out, lse
-
-
-def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
-    """Exact widening of bf16 bit patterns (uint16) to float64."""
-    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
