@@ -71,9 +71,6 @@ enum { MURMUR_DTYPE_BF16 = 1, MURMUR_DTYPE_F32 = 2 };
  * per layer too. */
 enum { MURMUR_POL_PER_SEQ = 1, MURMUR_POL_PER_LAYER = 2 };
 
-/* split_len value selecting the persistent stream schedule of murmur_decode_attn. */
-#define MURMUR_SPLIT_STREAM (-1)
-
 /* Device error word bits (murmur_device_error). */
 enum {
     MURMUR_DEVERR_OVERFLOW = 1,  /* evict_compact: retained count > max_keep */
@@ -136,7 +133,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 7
+#define MURMUR_ABI_VERSION 8
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -187,10 +184,11 @@ int murmur_evict_compact(const murmur_seg *seg_dev, const murmur_policy *pol_dev
  *   count_dev, ranges_dev: as murmur_evict_compact (ranges in sequence
  *               positions, not pool rows).
  * Errors as murmur_evict_compact; device error MURMUR_DEVERR_BLOCK (entry -1)
- * for a retained position past max_blocks blocks or in a block whose table
- * entry is negative (a freed block, see murmur_freeable_blocks_host).  Other
- * table entries are not range-checked here: a row outside the pool is
- * reported by murmur_decode_attn (MURMUR_DEVERR_POSITION, NaN outputs). */
+ * for a retained position past max_blocks blocks, in a block whose table
+ * entry is negative (a freed block, see murmur_freeable_blocks_host), or in a
+ * pool row beyond 2^31 - 1.  Other table entries are not range-checked here:
+ * a row outside the pool is reported by murmur_decode_attn
+ * (MURMUR_DEVERR_POSITION, NaN outputs). */
 int murmur_evict_compact_paged(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
                                int32_t B, const int32_t *block_table_dev, int32_t max_blocks, int32_t block_size,
                                int32_t *idx_dev, int32_t max_keep, int32_t *count_dev, int32_t *ranges_dev,
@@ -255,9 +253,9 @@ int murmur_paged_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, i
                       int32_t Hkv, const void *k_new_dev, const void *v_new_dev, murmur_stream_t stream);
 
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
- * (0 = the automatic choice, MURMUR_SPLIT_STREAM, or positions per split).
+ * (0 = the automatic choice, or positions per split).
  * The workspace holds ticket counters (one per (layer, sequence, kv-head)
- * group that is split, or two per stream workgroup) in a region at its start
+ * group that is split) in a region at its start
  * whose size depends on ws_bytes alone (4 bytes per KiB, rounded up to 256),
  * and the split partials after that region.  It must be zero-filled once
  * before its first use (or reset with murmur_decode_attn_workspace_init);
@@ -292,11 +290,9 @@ int murmur_decode_attn_workspace_init(void *ws_dev, size_t ws_bytes, murmur_stre
  *               sequence, KV head) is cut into splits of that many retained
  *               positions, one workgroup each (its four wavefronts take
  *               passes of 32 positions in turn), merged by log-sum-exp.
- *               MURMUR_SPLIT_STREAM: persistent workgroups, one per compute
- *               unit, stream balanced runs of 128-position units across all
- *               groups; only groups cut by a run boundary are merged (at most
- *               256 sequences).  0: automatic split length (about two
- *               workgroups per compute unit, at most 64 splits);
+ *               0: automatic split length (at most one dispatch round of
+ *               workgroups when the work is small, at most 64 splits per
+ *               group otherwise);
  *   out_dev:    [n_layers][B][Hq][D] of out_dtype, 16-byte aligned
  *               (MURMUR_DTYPE_BF16 rounds to nearest even, MURMUR_DTYPE_F32
  *               stores the fp32 accumulation);
@@ -325,8 +321,7 @@ int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, const int32_t *id
  *               murmur_evict_compact writes them (idx_dev [B][max_keep]),
  *               with MURMUR_POL_PER_LAYER one set per layer
  *               ([n_layers][B][max_keep], [n_layers][B], [n_layers][B][6][2]);
- *   split_len:  as murmur_decode_attn; MURMUR_SPLIT_STREAM takes per-sequence
- *               policies only (MURMUR_EUNSUPPORTED with MURMUR_POL_PER_LAYER);
+ *   split_len:  as murmur_decode_attn;
  *   every other argument: as murmur_decode_attn (same workspace size).
  * Device errors: MURMUR_DEVERR_POLICY and MURMUR_DEVERR_OVERFLOW as
  * murmur_evict_compact, MURMUR_DEVERR_COUNT for the same sequences (their
@@ -383,8 +378,7 @@ int murmur_ring_layout_host(const murmur_seg *seg, const murmur_policy *pol, int
  *               in storage rows (idx in piece order, not ascending);
  *   pol_per_seq: MURMUR_POL_* bits as murmur_decode_step (the ring must hold
  *               the retained outputs of every layer's policy);
- *   split_len:  as murmur_decode_attn, except MURMUR_SPLIT_STREAM
- *               (MURMUR_EUNSUPPORTED);
+ *   split_len:  as murmur_decode_attn;
  *   every other argument: as murmur_decode_step.
  * Device errors: those of murmur_decode_step, and MURMUR_DEVERR_CAPACITY for
  * a sequence whose ring cannot hold its retained outputs (count 0, NaN

@@ -68,9 +68,12 @@ def never_retained_again(seg_row, pol_row, horizon: int | None = None) -> np.nda
         horizon = default_horizon(seg_row, pol_row)
     length = p_pre + l_s + p_mid + j
     kept = np.zeros(length, dtype=bool)
-    for jj in range(j, j + horizon + 1):
-        idx, cnt = retained(np.array([[p_pre, l_s, p_mid, jj]], dtype=np.int32), pol_row)
-        rows = idx[0, :int(cnt[0])]
+    # the retained sets of steps j .. j + horizon, one row per step, from one call
+    steps = np.arange(j, j + horizon + 1, dtype=np.int32)
+    seg = np.stack([np.full_like(steps, p_pre), np.full_like(steps, l_s), np.full_like(steps, p_mid), steps], axis=1)
+    idx, cnt = retained(seg, pol_row)
+    for r in range(len(steps)):
+        rows = idx[r, :int(cnt[r])]
         kept[rows[rows < length]] = True
     return ~kept
 

@@ -48,69 +48,55 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     const int64_t groups = (int64_t)n_layers * B * Hkv;
     const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
     p.groups = groups;
-    const bool stream = split_len == MURMUR_SPLIT_STREAM;
-    if (stream) {
-        // Persistent workgroups, each leaving at most two partial segments; a
-        // group cut between workgroups takes the ticket of its first
-        // contributor's last slot.
-        const int64_t wg = groups * units < kStreamWorkgroups ? groups * units : kStreamWorkgroups;
-        p.stream_wg = (int32_t)(wg < 1 ? 1 : wg);
-        p.split_len = 0;
-        p.n_split = 0;
-        p.tickets = 2 * (int64_t)p.stream_wg;
-        p.ml_bytes = round_up((size_t)2 * p.stream_wg * G * 2 * sizeof(float), 256);
-        p.o_bytes = round_up((size_t)2 * p.stream_wg * G * kHeadDim * sizeof(float), 256);
-    } else {
-        if (split_len <= 0) {
-            // Few units (and no more splits than one merge combines): splits of
-            // one or two passes per wavefront from registers, as many as fill one
-            // dispatch round (kRoundWorkgroups) with equal shares, so no compute
-            // unit holds twice the work of another.  Otherwise the LDS-staged
-            // kernel, which takes a whole compute unit: as many splits as keep
-            // one dispatch round, fewer when there are more groups than that, at
-            // most kMaxAutoSplits.
-            int64_t per;
-            if (groups * units <= kSinglePassMaxUnits && units <= kMaxMergeSplits) {
-                // The split count that minimises an estimate of the launch time: each compute unit streams
-                // its split at kCuBytesPerUs, and more than one split adds the merge chain (store, ticket,
-                // loading the partials).  At most one dispatch round; splits of 1 or 2 passes.
-                const int64_t n_max = kRoundWorkgroups / groups < 1 ? 1 : kRoundWorkgroups / groups;
-                const double group_bytes = (double)max_keep * 4.0 * kHeadDim;  // K and V rows of one KV head
-                const double part_bytes = (double)G * (kHeadDim + 2) * 4.0;
-                int64_t best_len = 0;
-                double best = 0.0;
-                for (int64_t n = 1; n <= n_max; ++n) {
-                    int64_t len = (((int64_t)max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
-                    if (len < kSplitUnit) len = kSplitUnit;
-                    if (len > 2 * kSplitUnit) continue;  // more than two passes: the LDS-staged kernel's range
-                    const int64_t ns = ((int64_t)max_keep + len - 1) / len;
-                    const double t = group_bytes / ns / kCuBytesPerUs +
-                                     (ns > 1 ? kMergeChainUs + ns * part_bytes / kCuBytesPerUs : 0.0);
-                    if (best_len == 0 || t < best) {
-                        best = t;
-                        best_len = len;
-                    }
+    if (split_len <= 0) {
+        // Few units (and no more splits than one merge combines): splits of
+        // one or two passes per wavefront from registers, as many as fill one
+        // dispatch round (kRoundWorkgroups) with equal shares, so no compute
+        // unit holds twice the work of another.  Otherwise the LDS-staged
+        // kernel, which takes a whole compute unit: as many splits as keep
+        // one dispatch round, fewer when there are more groups than that, at
+        // most kMaxAutoSplits.
+        int64_t per;
+        if (groups * units <= kSinglePassMaxUnits && units <= kMaxMergeSplits) {
+            // The split count that minimises an estimate of the launch time: each compute unit streams
+            // its split at kCuBytesPerUs, and more than one split adds the merge chain (store, ticket,
+            // loading the partials).  At most one dispatch round; splits of 1 or 2 passes.
+            const int64_t n_max = kRoundWorkgroups / groups < 1 ? 1 : kRoundWorkgroups / groups;
+            const double group_bytes = (double)max_keep * 4.0 * kHeadDim;  // K and V rows of one KV head
+            const double part_bytes = (double)G * (kHeadDim + 2) * 4.0;
+            int64_t best_len = 0;
+            double best = 0.0;
+            for (int64_t n = 1; n <= n_max; ++n) {
+                int64_t len = (((int64_t)max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
+                if (len < kSplitUnit) len = kSplitUnit;
+                if (len > 2 * kSplitUnit) continue;  // more than two passes: the LDS-staged kernel's range
+                const int64_t ns = ((int64_t)max_keep + len - 1) / len;
+                const double t = group_bytes / ns / kCuBytesPerUs +
+                                 (ns > 1 ? kMergeChainUs + ns * part_bytes / kCuBytesPerUs : 0.0);
+                if (best_len == 0 || t < best) {
+                    best = t;
+                    best_len = len;
                 }
-                if (best_len == 0) best_len = 2 * kSplitUnit;
-                split_len = (int32_t)best_len;
-                per = 0;
-            } else {
-                int64_t want = kRoundWorkgroups / groups;
-                if (want > kMaxAutoSplits) want = kMaxAutoSplits;
-                if (want > units) want = units;
-                if (want < 1) want = 1;
-                per = (units + want - 1) / want;
-                if (per < 2) per = 2;
             }
-            if (per > 0) split_len = (int32_t)(per * kSplitUnit);
+            if (best_len == 0) best_len = 2 * kSplitUnit;
+            split_len = (int32_t)best_len;
+            per = 0;
+        } else {
+            int64_t want = kRoundWorkgroups / groups;
+            if (want > kMaxAutoSplits) want = kMaxAutoSplits;
+            if (want > units) want = units;
+            if (want < 1) want = 1;
+            per = (units + want - 1) / want;
+            if (per < 2) per = 2;
         }
-        p.split_len = split_len;
-        p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
-        if (p.n_split > 1) {
-            p.tickets = groups;
-            p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
-            p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
-        }
+        if (per > 0) split_len = (int32_t)(per * kSplitUnit);
+    }
+    p.split_len = split_len;
+    p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
+    if (p.n_split > 1) {
+        p.tickets = groups;
+        p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
+        p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
     }
     // The smallest size whose ticket region holds the tickets and leaves room
     // for the partials, with 256 bytes to spare so that any larger size does
@@ -175,11 +161,8 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     if (out_dtype != MURMUR_DTYPE_BF16 && out_dtype != MURMUR_DTYPE_F32)
         return fail(MURMUR_EINVAL, "out_dtype must be MURMUR_DTYPE_BF16 or MURMUR_DTYPE_F32 (got %d)", out_dtype);
     if (!isfinite(scale)) return fail(MURMUR_EINVAL, "scale must be finite");
-    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kWaveTile != 0))
-        return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
-                    kWaveTile, split_len);
-    if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
-        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
+    if (split_len < 0 || split_len % kWaveTile != 0)
+        return fail(MURMUR_EINVAL, "split_len must be 0 or a positive multiple of %d (got %d)", kWaveTile, split_len);
     const int64_t strides[4] = {kv->stride_layer, kv->stride_b, kv->stride_h, kv->stride_pos};
     for (int i = 0; i < 4; ++i)
         if (strides[i] < 0 || strides[i] % 8 != 0)
@@ -195,7 +178,7 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
     if (ws_bytes < plan.total)
         return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
-    if (!plan.stream_wg && plan.n_split > kMaxMergeSplits)
+    if (plan.n_split > kMaxMergeSplits)
         return fail(MURMUR_EINVAL, "split_len %d gives %d splits for max_keep %d; at most %d are supported",
                     plan.split_len, plan.n_split, max_keep, kMaxMergeSplits);
     if (plan.o_bytes >= ((size_t)1 << 31))
@@ -220,9 +203,9 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     // depends only on ws_bytes (see murmur_decode_attn_workspace).
     const size_t region = ticket_region(ws_bytes);
     a.ticket = (int32_t *)ws;
-    // Partials exist for split schedules of more than one split and for the stream schedule.
+    // Partials exist when a group has more than one split.
     const bool partials = plan.ml_bytes > 0;
-    if (partials != (plan.stream_wg > 0 || plan.n_split > 1) || region < (size_t)plan.tickets * 4 ||
+    if (partials != (plan.n_split > 1) || region < (size_t)plan.tickets * 4 ||
         region + plan.ml_bytes + plan.o_bytes > ws_bytes)
         return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
     a.part_ml = partials ? (float *)(ws + region) : nullptr;
@@ -238,7 +221,6 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     a.NL = kv->n_layers;
     a.split_len = plan.split_len;
     a.n_split = plan.n_split;
-    a.stream_wg = plan.stream_wg;
     a.out_f32 = out_dtype == MURMUR_DTYPE_F32;
     a.scale_log2 = scale * 1.4426950408889634f;
     return ok();
@@ -386,11 +368,8 @@ MURMUR_EXPORT int murmur_decode_attn_workspace(int32_t n_layers, int32_t B, int3
     if (n_layers < 1 || B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1)
         return fail(MURMUR_EINVAL, "n_layers, B, Hq, Hkv and max_keep must be >= 1");
     if (Hq % Hkv != 0) return fail(MURMUR_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
-    if (split_len != MURMUR_SPLIT_STREAM && (split_len < 0 || split_len % kWaveTile != 0))
-        return fail(MURMUR_EINVAL, "split_len must be 0, MURMUR_SPLIT_STREAM or a positive multiple of %d (got %d)",
-                    kWaveTile, split_len);
-    if (split_len == MURMUR_SPLIT_STREAM && B > kStreamMaxB)
-        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes at most %d sequences (got %d)", kStreamMaxB, B);
+    if (split_len < 0 || split_len % kWaveTile != 0)
+        return fail(MURMUR_EINVAL, "split_len must be 0 or a positive multiple of %d (got %d)", kWaveTile, split_len);
     *bytes = plan_workspace(n_layers, B, Hq, Hkv, max_keep, split_len).total;
     return ok();
 }
@@ -434,8 +413,6 @@ MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_pol
     if (!seg_dev || !pol_dev) return fail(MURMUR_EINVAL, "seg_dev and pol_dev must not be NULL");
     if (pol_per_seq < 0 || pol_per_seq > (MURMUR_POL_PER_SEQ | MURMUR_POL_PER_LAYER))
         return fail(MURMUR_EINVAL, "pol_per_seq must be a set of MURMUR_POL_* bits (0..3, got %d)", pol_per_seq);
-    if ((pol_per_seq & MURMUR_POL_PER_LAYER) && split_len == MURMUR_SPLIT_STREAM)
-        return fail(MURMUR_EUNSUPPORTED, "the stream schedule takes per-sequence policies only");
     if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
         !aligned(ranges_dev, 4))
         return fail(MURMUR_EINVAL, "seg/pol/idx/count/ranges pointers must be 4-byte aligned");
@@ -501,9 +478,6 @@ MURMUR_EXPORT int murmur_decode_step_ring(const murmur_seg *seg_dev, const murmu
         return fail(MURMUR_EINVAL, "ring->k_new and ring->v_new must be 16-byte aligned");
     if (ring->out_capacity < 1)
         return fail(MURMUR_EINVAL, "ring->out_capacity must be >= 1 (got %d)", ring->out_capacity);
-    if (split_len == MURMUR_SPLIT_STREAM)
-        return fail(MURMUR_EUNSUPPORTED, "ring storage runs on the split schedules (split_len 0 or a multiple of %d)",
-                    kWaveTile);
     if (!aligned(seg_dev, 4) || !aligned(pol_dev, 4) || !aligned(idx_dev, 4) || !aligned(count_dev, 4) ||
         !aligned(ranges_dev, 4))
         return fail(MURMUR_EINVAL, "seg/pol/idx/count/ranges pointers must be 4-byte aligned");

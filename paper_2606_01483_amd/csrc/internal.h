@@ -17,11 +17,6 @@ constexpr int kSplitUnit = kWaveTile * kWavesPerWg;  // 128 positions: one pass 
 constexpr int kMaxAutoSplits = 64;
 constexpr int kRoundWorkgroups = 256;     // one workgroup per compute unit
 constexpr int kSinglePassMaxUnits = 512;  // below this many units the automatic split is one pass
-// Stream schedule: one persistent workgroup per compute unit of the 256,
-// chosen automatically once there are at least kStreamMinUnits units of 128
-// positions; sequences' tables live in LDS, so at most kStreamMaxB sequences.
-constexpr int kStreamWorkgroups = 256;
-constexpr int kStreamMaxB = 256;
 // Splits one merge can combine: it stages 2 * n_split * G + 2 * G floats in
 // the workgroup's 32 KiB of V-tile LDS.
 constexpr int kMaxMergeSplits = 240;
@@ -57,20 +52,18 @@ struct AttnLaunch {
     const int32_t *idx;
     void *out;
     float *lse;
-    int32_t *ticket;   // split schedule: [groups]; stream schedule: [2 * workgroups]
+    int32_t *ticket;   // [groups]: one counter per (layer, sequence, KV head) that is split
     float *part_ml;    // [groups][n_split][G][2]  (running max in log2 units, sum)
     float *part_o;     // [groups][n_split][G][128]
     uint32_t part_ml_bytes, part_o_bytes;  // extents of the two partial arrays (< 2^31)
     int32_t max_len, max_keep, B, Hq, Hkv, G, NL;
     int32_t split_len, n_split, out_f32;
-    int32_t stream_wg;  // > 0: stream schedule with this many workgroups
     float scale_log2;  // logit scale times log2(e)
 };
 
 struct WorkspacePlan {
     int32_t split_len;
     int32_t n_split;
-    int32_t stream_wg;  // > 0: stream schedule
     int64_t groups;
     int64_t tickets;  // ticket counters the launch uses
     size_t ml_bytes, o_bytes, total;

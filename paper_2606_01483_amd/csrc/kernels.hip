@@ -38,21 +38,15 @@ static __device__ __forceinline__ void raise_device_error(int32_t bit) { atomicO
 // ---------------------------------------------------------------------------
 // evict_compact: one workgroup per sequence.
 // ---------------------------------------------------------------------------
-// With a block table (paged cache, bt != null) the index list holds physical
-// rows: position p of sequence b lives in row bt[b][p / bs] * bs + p % bs
-// (bs = 1 << log2_bs); a position past the table's max_blocks entries gives
-// -1 and MURMUR_DEVERR_BLOCK, and so does one in a block whose entry is
-// negative (freed).
+// With a block table (paged cache, bt != null) the index list holds pool rows
+// (paged_pool_row): a position past the table's max_blocks entries, in a freed
+// block (negative entry) or in a row beyond 2^31 - 1 gives -1 and
+// MURMUR_DEVERR_BLOCK.
 static __device__ __forceinline__ int32_t paged_row(const int32_t *bt_row, int32_t max_blocks, int32_t log2_bs,
                                                     int32_t p, int &bad) {
-    const int32_t blk = p >> log2_bs;
-    const int32_t entry = bt_row[blk < max_blocks ? blk : 0];  // the load stays inside the table
-    const int32_t phys = blk < max_blocks ? entry : -1;
-    if (phys < 0) {  // past the table, or a freed block
-        bad = 1;
-        return -1;
-    }
-    return (phys << log2_bs) | (p & ((1 << log2_bs) - 1));
+    const int32_t row = paged_pool_row(bt_row, max_blocks, log2_bs, p);
+    bad |= row < 0;
+    return row;
 }
 
 __global__ __launch_bounds__(256) void evict_compact_kernel(const murmur_seg *__restrict__ seg,
@@ -1503,396 +1497,6 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
                    reinterpret_cast<float *>(&stages[0][0][0]));
 }
 
-// ---------------------------------------------------------------------------
-// decode_attn, stream schedule: a persistent grid of P workgroups.  The work
-// is the sequence of 128-position units of every (layer, sequence, KV head)
-// group in (layer, sequence, KV head) order; workgroup p takes the contiguous
-// units [p*U/P, (p+1)*U/P).  Every wavefront streams its 32-position share of
-// each unit through two LDS stages with direct-to-LDS loads, the next unit's
-// K/V rows and its group's query rows in flight while the current unit is
-// computed, across group boundaries.  A group the workgroup covers whole is
-// written directly; a group cut by a range boundary leaves a partial in slot
-// 2p (its first segment) or 2p+1 (its last), and the tickets of those (at most
-// two) are taken once the stream is done, the last contributor merging.
-// Per-sequence counts, range tables and unit offsets are staged in LDS.
-// Every wavefront issues the same number of direct-to-LDS loads per unit, so
-// the hand-placed waits stay exact; the accesses to the stage and query
-// buffers themselves are inline assembly (see the LDS-staged passes).
-// ---------------------------------------------------------------------------
-struct UnitPos {
-    int layer, b, g, k;  // k: unit index within the group
-};
-
-constexpr int kQSlotBytes = kMaxGroup * kHeadDim * 2;  // 4 KiB: the query rows of one group
-constexpr int kQLoads = kQSlotBytes / 1024;            // direct-to-LDS loads of a group's query rows
-constexpr int kUnitLoads = kStageLoads + kQLoads;      // per wavefront and unit (index entries aside)
-
-// A wavefront's unscaled O rows into its region at `base` (row-major, rows
-// kOStride floats apart): lane (n16, c4) holds rows 4*c4 + i, head dims
-// 16*db + n16.
-static __device__ __forceinline__ void publish_rows_lds(uint32_t base, const WaveAcc &w, int n16, int c4) {
-    const uint32_t addr = base + (uint32_t)((4 * c4 * kOStride + n16) * 4);
-#define MURMUR_W(i, db) "ds_write_b32 %0, %" #i " offset:" #db "\n\t"
-    asm volatile(
-        MURMUR_W(1, 0) MURMUR_W(2, 64) MURMUR_W(3, 128) MURMUR_W(4, 192) MURMUR_W(5, 256) MURMUR_W(6, 320)
-        MURMUR_W(7, 384) MURMUR_W(8, 448)
-        MURMUR_W(9, 528) MURMUR_W(10, 592) MURMUR_W(11, 656) MURMUR_W(12, 720) MURMUR_W(13, 784) MURMUR_W(14, 848)
-        MURMUR_W(15, 912) MURMUR_W(16, 976)
-        MURMUR_W(17, 1056) MURMUR_W(18, 1120) MURMUR_W(19, 1184) MURMUR_W(20, 1248) MURMUR_W(21, 1312)
-        MURMUR_W(22, 1376) MURMUR_W(23, 1440) MURMUR_W(24, 1504)
-        MURMUR_W(25, 1584) MURMUR_W(26, 1648) MURMUR_W(27, 1712) MURMUR_W(28, 1776) MURMUR_W(29, 1840)
-        MURMUR_W(30, 1904) MURMUR_W(31, 1968) MURMUR_W(32, 2032)
-        "s_waitcnt lgkmcnt(0)"
-        ::"v"(addr),
-        "v"(w.acc[0][0]), "v"(w.acc[1][0]), "v"(w.acc[2][0]), "v"(w.acc[3][0]), "v"(w.acc[4][0]), "v"(w.acc[5][0]),
-        "v"(w.acc[6][0]), "v"(w.acc[7][0]),
-        "v"(w.acc[0][1]), "v"(w.acc[1][1]), "v"(w.acc[2][1]), "v"(w.acc[3][1]), "v"(w.acc[4][1]), "v"(w.acc[5][1]),
-        "v"(w.acc[6][1]), "v"(w.acc[7][1]),
-        "v"(w.acc[0][2]), "v"(w.acc[1][2]), "v"(w.acc[2][2]), "v"(w.acc[3][2]), "v"(w.acc[4][2]), "v"(w.acc[5][2]),
-        "v"(w.acc[6][2]), "v"(w.acc[7][2]),
-        "v"(w.acc[0][3]), "v"(w.acc[1][3]), "v"(w.acc[2][3]), "v"(w.acc[3][3]), "v"(w.acc[4][3]), "v"(w.acc[5][3]),
-        "v"(w.acc[6][3]), "v"(w.acc[7][3])
-        : "memory");
-#undef MURMUR_W
-}
-
-// The four wavefronts' published O values of head h, dims d0 .. d0+3, from
-// regions 32 KiB apart starting at `base`.
-static __device__ __forceinline__ void gather_rows_lds(uint32_t base, int h, int d0, f32x4 (&o)[kWavesPerWg]) {
-    const uint32_t a0 = base + (uint32_t)((h * kOStride + d0) * 4), a2 = a0 + 65536u;
-    asm volatile(
-        "ds_read_b128 %0, %4\n\t"
-        "ds_read_b128 %1, %4 offset:32768\n\t"
-        "ds_read_b128 %2, %5\n\t"
-        "ds_read_b128 %3, %5 offset:32768\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
-        : "v"(a0), "v"(a2)
-        : "memory");
-}
-
-// Query rows of a group (G rows of 128 bf16 at q_rows) into a query slot:
-// load j, lane l copies 16-byte chunk j*64 + l (chunks past the group repeat
-// its last one, so every lane loads).
-static __device__ __forceinline__ void dma_query(uint8_t *slot, const uint16_t *q_rows, int G, int lane) {
-#pragma unroll
-    for (int j = 0; j < kQLoads; ++j) {
-        const int chunk = min(j * 64 + lane, G * (kHeadDim / 8) - 1);
-        __builtin_amdgcn_global_load_lds(q_rows + chunk * 8, (lds_void_t *)(slot + j * 1024), 16, 0, 0);
-    }
-}
-
-// Q^T operand (as load_q) from a query slot.
-static __device__ __forceinline__ void read_query(const uint8_t *slot, int G, int n16, int c4, u32x4 (&qf)[4]) {
-    const int hq = n16 < G ? n16 : G - 1;
-    const uint32_t addr = lds_addr(slot) + (uint32_t)(hq * kHeadDim * 2 + c4 * 16);
-    asm volatile(
-        "ds_read_b128 %0, %4\n\t"
-        "ds_read_b128 %1, %4 offset:64\n\t"
-        "ds_read_b128 %2, %4 offset:128\n\t"
-        "ds_read_b128 %3, %4 offset:192\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(qf[0]), "=&v"(qf[1]), "=&v"(qf[2]), "=&v"(qf[3])
-        : "v"(addr)
-        : "memory");
-}
-
-// Workgroup barrier for LDS traffic only: waits for this wavefront's LDS
-// accesses, not for its global loads.  (__syncthreads() also orders global
-// memory, so it waits for every direct-to-LDS load in flight and would drain
-// the stream's prefetch at every group boundary.)
-static __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-template <int kSrc>
-__global__ __launch_bounds__(256) void decode_attn_stream_kernel(const int32_t *__restrict__ src0,
-                                                                 const int32_t *__restrict__ src1,
-                                                                 const int32_t *__restrict__ idx,
-                                                                 const uint16_t *__restrict__ q, int32_t max_keep,
-                                                                 int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
-                                                                 const AttnLaunch a) {
-    __shared__ __attribute__((aligned(16))) uint8_t stages[kWavesPerWg][2][kStageBytes];
-    __shared__ __attribute__((aligned(16))) uint8_t q_slot[2][kQSlotBytes];
-    __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kSrc != kSrcIndex ? 1 : kWavesPerWg][2][kIdxSlotBytes];
-    __shared__ CombineLds cl;
-    __shared__ int s_last;
-    __shared__ int32_t s_cnt[kStreamMaxB];      // counts clamped to [0, max_keep]
-    __shared__ int32_t s_pre[kStreamMaxB + 1];  // Hkv * (units of the sequences before b), b = 0..B
-    __shared__ int32_t s_rg[kSrc != kSrcIndex ? kStreamMaxB : 1][2 * kPieces];
-    __shared__ uint32_t s_bad[kStreamMaxB / 32];  // sequences with an invalid count
-    __shared__ int s_wave_bad[kWavesPerWg];       // per wavefront: an invalid position in this segment
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int n16 = lane & 15;
-    const int c4 = lane >> 4;
-    const int Hq = Hkv * G;
-
-    // ---- per-sequence tables -------------------------------------------------
-    if (tid < kStreamMaxB / 32) s_bad[tid] = 0;
-    __syncthreads();
-    for (int t = tid; t < B; t += blockDim.x) {
-        int32_t rg[2 * kPieces];
-        int policy_bad = 0;
-        int32_t unused_cur;
-        const int c = seq_count<kSrc>(src0, src1, t, pol_per_seq, 0, B, 0, rg, policy_bad, unused_cur);
-        const bool badc = c < 1 || c > max_keep;
-        const int cc = c < 0 ? 0 : (c > max_keep ? max_keep : c);
-        s_cnt[t] = cc;
-        s_pre[t + 1] = cc > kSplitUnit ? (cc + kSplitUnit - 1) / kSplitUnit : 1;  // units, at least one
-        if (badc) atomicOr(&s_bad[t >> 5], 1u << (t & 31));
-        if (kSrc != kSrcIndex) {
-#pragma unroll
-            for (int k = 0; k < 2 * kPieces; ++k) s_rg[t][k] = rg[k];
-        }
-    }
-    __syncthreads();
-    if (wave == 0) {  // exclusive prefix sum of the unit counts by one wavefront, a chunk per lane
-        constexpr int kPer = kStreamMaxB / 64;
-        const int per = (B + 63) / 64;
-        int units[kPer];
-        int local = 0;
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {  // read every count before any prefix overwrites it
-            const int t = lane * per + i;
-            units[i] = (i < per && t < B) ? s_pre[t + 1] : 0;
-            local += units[i];
-        }
-        int incl = local;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int v = __shfl_up(incl, off);
-            if (lane >= off) incl += v;
-        }
-        int run = incl - local;
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            const int t = lane * per + i;
-            if (i < per && t < B) s_pre[t] = run * Hkv;
-            run += units[i];
-        }
-        if (lane == 63) s_pre[B] = incl * Hkv;
-    }
-    __syncthreads();
-
-    const int64_t U_layer = s_pre[B];
-    const int64_t U = (int64_t)a.NL * U_layer;
-    // Counts below max_keep can leave fewer units than workgroups: only the
-    // first P = min(grid, U) take part, so that every one of them has work and
-    // the contributor count of a group is the number of its owners.
-    const int64_t P = U < (int64_t)gridDim.x ? U : (int64_t)gridDim.x, p = blockIdx.x;
-    if (p >= P) return;
-    int64_t u = p * U / P;
-    const int64_t u_end = (p + 1) * U / P;
-    const int64_t u_begin = u;
-    auto owner = [&](int64_t unit) { return ((unit + 1) * P - 1) / U; };
-    auto units_of = [&](int b) { return (s_pre[b + 1] - s_pre[b]) / Hkv; };
-
-    UnitPos cur;
-    {
-        cur.layer = (int)(u / U_layer);
-        const int r = (int)(u - cur.layer * U_layer);
-        int lo = 0, hi = B - 1;  // last b with s_pre[b] <= r
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (s_pre[mid] <= r) lo = mid; else hi = mid - 1;
-        }
-        cur.b = lo;
-        const int off = r - s_pre[lo], ub = units_of(lo);
-        cur.g = off / ub;
-        cur.k = off - cur.g * ub;
-    }
-    auto advance = [&](UnitPos x) {
-        if (++x.k == units_of(x.b)) {
-            x.k = 0;
-            if (++x.g == Hkv) {
-                x.g = 0;
-                if (++x.b == B) {
-                    x.b = 0;
-                    ++x.layer;
-                }
-            }
-        }
-        return x;
-    };
-    auto same_group = [](const UnitPos &x, const UnitPos &y) { return x.layer == y.layer && x.b == y.b && x.g == y.g; };
-    auto first_rank = [&](const UnitPos &x) { return x.k * kSplitUnit + wave * kWaveTile; };
-    auto row_of = [&](const UnitPos &x) { return ((int64_t)x.layer * B + x.b) * Hq + x.g * G; };
-    // Index-list row of unit x; a unit that does not exist reads nothing.
-    auto irow_of = [&](const UnitPos &x, bool exists) {
-        return raw_buffer(idx + (int64_t)x.b * max_keep, exists ? (uint32_t)max_keep * 4u : 0u);
-    };
-    uint8_t *st[2] = {&stages[wave][0][0], &stages[wave][1][0]};
-    uint8_t *ring[2] = {&idx_ring[kSrc != kSrcIndex ? 0 : wave][0][0], &idx_ring[kSrc != kSrcIndex ? 0 : wave][1][0]};
-    // Issues every load of unit x into stage `stage` and query slot `qs`: the
-    // group's query rows, then the K/V rows of this wavefront's share.
-    // kSrcIndex: the unit's index entries are in `entries`.
-    auto issue = [&](const UnitPos &x, uint8_t *stage, int qs, const uint8_t *entries, int &bad) {
-        const int cnt = s_cnt[x.b];
-        const int r0 = first_rank(x);
-        int32_t pos[8];
-        if (kSrc != kSrcIndex) {
-            int32_t rg[2 * kPieces];
-#pragma unroll
-            for (int k = 0; k < 2 * kPieces; ++k) rg[k] = s_rg[x.b][k];
-            dma_pos_ranges(make_tab(rg), r0, cnt, a.max_len, c4, pos, bad);
-        } else {
-            dma_pos_index(entries, r0, cnt, a.max_len, c4, pos, bad);
-        }
-        dma_query(&q_slot[qs][0], q + row_of(x) * kHeadDim, G, lane);
-        const int64_t off = x.layer * a.s_layer + x.b * a.s_b + x.g * a.s_h;
-        dma_pass(stage, a.k + off, a.v + off, a.s_pos, pos, lane, false, NewRows{-1, nullptr, nullptr});
-    };
-
-    WaveAcc w;
-    wave_acc_reset(w);
-    int seg_k0 = cur.k;  // first unit of the current segment within its group
-    // Tickets of the cut groups, taken after the stream.
-    int n_pending = 0;
-    int64_t pend_sg[2] = {0, 0}, pend_row0[2] = {0, 0};
-    int pend_ub[2] = {0, 0};
-
-    // The segment of group x in this workgroup ends with unit x, computed from stage `stg`.
-    auto seg_end = [&](const UnitPos &x, int stg) {
-        const bool bad_count = (s_bad[x.b >> 5] >> (x.b & 31)) & 1u;
-        if (c4 == 0) {
-            cl.ml[n16][wave][0] = w.m_run;
-            cl.ml[n16][wave][1] = w.l_run;
-        }
-        publish_rows_lds(lds_addr(st[stg]), w, n16, c4);
-        const bool wave_bad = __ballot(w.bad_pos != 0) != 0;
-        if (lane == 0) s_wave_bad[wave] = wave_bad;
-        lds_barrier();
-        const int wg_bad_pos = s_wave_bad[0] | s_wave_bad[1] | s_wave_bad[2] | s_wave_bad[3];
-        const bool bad = wg_bad_pos || bad_count;
-        const int ub = units_of(x.b);
-        const bool whole = seg_k0 == 0 && x.k == ub - 1;
-        const int64_t s_g = x.layer * U_layer + s_pre[x.b] + (int64_t)x.g * ub;  // group's first unit
-        const uint32_t slot = (uint32_t)(2 * p + (u_begin < s_g ? 1 : 0));
-        const int64_t row0 = row_of(x);
-        const uint32_t obase = lds_addr(&stages[0][stg][0]);
-        for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
-            const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-            f32x4 ow[kWavesPerWg];
-            gather_rows_lds(obase, h, d0, ow);
-            const f32x4 a01 = *reinterpret_cast<const f32x4 *>(&cl.ml[h][0][0]);
-            const f32x4 a23 = *reinterpret_cast<const f32x4 *>(&cl.ml[h][2][0]);
-            const float m[kWavesPerWg] = {a01[0], a01[2], a23[0], a23[2]};
-            const float l[kWavesPerWg] = {a01[1], a01[3], a23[1], a23[3]};
-            const float M = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
-            float L = 0.f;
-            f32x4 O = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int wv = 0; wv < kWavesPerWg; ++wv) {
-                const float f = m[wv] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[wv] - M);
-                L += l[wv] * f;
-                O += f * ow[wv];
-            }
-            if (bad) L = __builtin_nanf("");
-            if (whole) {
-                store_output(a, row0 + h, d0, O, M, L);
-            } else {
-                const uint32_t prow = slot * G + h;
-                store_coherent4(raw_buffer(a.part_o, a.part_o_bytes), (prow * kHeadDim + d0) * 4, O);
-                if (d0 == 0) {
-                    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-                    store_coherent1(rml, prow * 8, M);
-                    store_coherent1(rml, prow * 8 + 4, L);
-                }
-            }
-        }
-        if (bad && tid == 0)
-            raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
-        if (!whole) {
-            pend_sg[n_pending] = s_g;
-            pend_row0[n_pending] = row0;
-            pend_ub[n_pending] = ub;
-            ++n_pending;
-        }
-        lds_barrier();  // every read of this stage's published rows (and of the flags) is done before reuse
-        wave_acc_reset(w);
-        seg_k0 = 0;
-    };
-
-    // Prologue: the first unit's loads (and, for index lists, the entries of
-    // the first two units).
-    int qpar = 0;
-    if (kSrc == kSrcIndex) {
-        dma_idx(ring[0], irow_of(cur, true), first_rank(cur), lane);
-        const UnitPos n1 = advance(cur);
-        dma_idx(ring[1], irow_of(n1, u + 1 < u_end), first_rank(n1), lane);
-        wait_vm<1>();
-    }
-    issue(cur, st[0], 0, ring[0], w.bad_pos);
-    for (int n = 0;; ++n, ++u) {
-        const int sp = n & 1;
-        const bool more = u + 1 < u_end;
-        const UnitPos nxt = advance(cur);
-        const bool new_group = !same_group(nxt, cur);
-        const int qnext = new_group ? qpar ^ 1 : qpar;
-        int next_bad = 0;  // invalid positions met while resolving the next unit
-        if (more) {
-            if (kSrc == kSrcIndex) {
-                // Entries of the next unit: issued just before this unit's loads,
-                // so only those kUnitLoads loads may still be in flight.
-                wait_vm<kUnitLoads>();
-                const UnitPos nn = advance(nxt);
-                // The unit after next's entries go first (into the slot this unit's
-                // entries used), then the next unit's loads: the wait above stays
-                // exact at the next iteration.
-                dma_idx(ring[sp], irow_of(nn, u + 2 < u_end), first_rank(nn), lane);
-                issue(nxt, st[sp ^ 1], qnext, ring[sp ^ 1], next_bad);
-                wait_vm<kUnitLoads + 1>();  // this unit's loads; the next unit's stay in flight
-            } else {
-                issue(nxt, st[sp ^ 1], qnext, nullptr, next_bad);
-                wait_vm<kUnitLoads>();
-            }
-        } else {
-            wait_vm<0>();
-        }
-        {
-            const int valid = s_cnt[cur.b] - first_rank(cur);
-            if (valid > 0) {
-                u32x4 qf[4];
-                read_query(&q_slot[qpar][0], G, n16, c4, qf);
-                compute_pass_lds<true>(st[sp], qf, min(kWaveTile, valid), a.scale_log2, w, n16, c4);
-            }
-        }
-        if (!more || new_group) seg_end(cur, sp);
-        w.bad_pos |= next_bad;
-        if (!more) break;
-        cur = nxt;
-        qpar = qnext;
-    }
-
-    // Tickets of the cut groups; the last contributor of each merges.
-    for (int i = 0; i < n_pending; ++i) {
-        const int64_t s_g = pend_sg[i];
-        const int64_t first = owner(s_g), last = owner(s_g + pend_ub[i] - 1);
-        // The group's ticket is that of its first contributor's last segment
-        // (slot 2 * first + 1): one per cut group, at most 2P tickets.
-        if (take_ticket(a, (int)(2 * first + 1), (int)(last - first + 1), tid, s_last)) {
-            merge_partials(
-                a, (int)(last - first + 1),
-                [&](int j) {
-                    const int64_t pp = first + j;
-                    return (uint32_t)(2 * pp + ((pp * U / P) < s_g ? 1 : 0));
-                },
-                G, tid, pend_row0[i], reinterpret_cast<float *>(&stages[0][0][0]));
-        }
-    }
-
-    if (kSrc == kSrcLayout) {  // the evict_compact outputs, sequences spread over the workgroups
-        for (int bb = (int)p; bb < B; bb += (int)P) {
-            int32_t rg[2 * kPieces];
-            int policy_bad = 0;
-            int32_t unused_cur;
-            const int c = seq_count<kSrc>(src0, src1, bb, pol_per_seq, 0, B, 0, rg, policy_bad, unused_cur);
-            write_retained(a, bb, c, policy_bad, rg, max_keep, tid, 0, max_keep);
-        }
-    }
-}
-
 // Read-only streaming probe (measurement): workgroup w reads the 16-byte
 // units [w * per, (w + 1) * per) of the buffer, eight loads per thread in
 // flight (indexes clamped into the share, so every load is unconditional).
@@ -1934,13 +1538,6 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 
 template <int kSrc>
 static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
-    if constexpr (kSrc != kSrcRing) {  // ring storage runs on the split schedules only
-        if (a.stream_wg > 0) {
-            hipLaunchKernelGGL(decode_attn_stream_kernel<kSrc>, dim3((unsigned)a.stream_wg), dim3(kWavesPerWg * 64),
-                               0, stream, a.src0, a.src1, a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
-            return;
-        }
-    }
     const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
     // Splits of up to two passes run from registers; longer splits stage their
     // passes in LDS, double-buffered within one dispatch round, else one stage

@@ -31,6 +31,20 @@ namespace murmur {
 
 constexpr int kPieces = 6;
 
+// Row of position p (>= 0) of one sequence in a paged pool: block table row
+// bt_row of max_blocks physical block numbers, blocks of 1 << log2_bs rows
+// (log2_bs <= 20), row = bt_row[p >> log2_bs] * block size + p mod block size.
+// -1 when p lies past the table, in a block whose entry is negative (a freed
+// block), or in a row beyond 2^31 - 1.  The table is read inside its bounds only.
+MURMUR_HD inline int32_t paged_pool_row(const int32_t *bt_row, int32_t max_blocks, int32_t log2_bs, int32_t p) {
+    const int32_t blk = p >> log2_bs;
+    const int32_t entry = bt_row[blk < max_blocks ? blk : 0];
+    const int32_t phys = blk < max_blocks ? entry : -1;
+    if (phys < 0) return -1;
+    const int64_t row = ((int64_t)phys << log2_bs) | (int64_t)(p & ((1 << log2_bs) - 1));
+    return row > (int64_t)0x7fffffff ? -1 : (int32_t)row;
+}
+
 struct Pieces {
     int32_t start[kPieces];
     int32_t len[kPieces];

@@ -24,7 +24,6 @@ MURMUR_DEVERR_BLOCK = 32
 MURMUR_DEVERR_POOL = 64
 N_PIECES = 6
 SPLIT_UNIT = 128
-MURMUR_SPLIT_STREAM = -1
 
 _ERROR_NAMES = {MURMUR_EINVAL: "EINVAL", MURMUR_EUNSUPPORTED: "EUNSUPPORTED", MURMUR_ENOSPACE: "ENOSPACE",
                 MURMUR_EHIP: "EHIP"}

@@ -46,7 +46,7 @@ def test_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 7
+    assert M.murmur_abi_version() == 8
 
 
 def test_retained_count_host_matches_oracle():
@@ -115,7 +115,7 @@ def call_attn(a):
     (dict(split_len=-128), M.MURMUR_EINVAL),
     (dict(split_len=-2), M.MURMUR_EINVAL),
     (dict(max_keep=(1 << 28) + 1), M.MURMUR_EUNSUPPORTED),
-    (dict(split_len=M.MURMUR_SPLIT_STREAM, B=300), M.MURMUR_EUNSUPPORTED),
+    (dict(split_len=-1), M.MURMUR_EINVAL),
     (dict(q=FAKE + 8), M.MURMUR_EINVAL),
     (dict(ws=FAKE + 64), M.MURMUR_EINVAL),
     (dict(lse=FAKE + 2), M.MURMUR_EINVAL),
@@ -185,17 +185,6 @@ def test_workspace_sizing():
     # many groups of two splits
     ws = M.murmur_decode_attn_workspace(28, 256, 4, 4, 512, 256)
     check_plan(ws, split_partials(28 * 256 * 4, 2, 1), 28 * 256 * 4)
-    # the stream schedule with one head per group: the tickets set the size
-    ws = M.murmur_decode_attn_workspace(1, 12, 4, 4, 35160, M.MURMUR_SPLIT_STREAM)
-    check_plan(ws, rnd(2 * 256 * 1 * 2 * 4) + rnd(2 * 256 * 1 * 128 * 4), 512)
-    assert ws == rnd(512 * 1024)
-    # the stream schedule: 256 workgroups with two partial slots and two tickets each
-    ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, M.MURMUR_SPLIT_STREAM)
-    stream = rnd(2 * 256 * 7 * 2 * 4) + rnd(2 * 256 * 7 * 128 * 4)
-    check_plan(ws, stream, 512)
-    # forced stream on a tiny problem: as many workgroups as units (4 groups x 2 units)
-    ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 192, M.MURMUR_SPLIT_STREAM)
-    check_plan(ws, rnd(2 * 8 * 7 * 2 * 4) + rnd(2 * 8 * 7 * 128 * 4), 16)
     with pytest.raises(M.MurmurError):
         M.murmur_decode_attn_workspace(1, 12, 28, 5, 850)
     with pytest.raises(M.MurmurError):
@@ -204,14 +193,14 @@ def test_workspace_sizing():
     check_plan(M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 64), split_partials(48, 14, 7), 48)
     check_plan(M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 192), split_partials(48, 5, 7), 48)
     with pytest.raises(M.MurmurError) as e:
-        M.murmur_decode_attn_workspace(1, 300, 28, 4, 850, M.MURMUR_SPLIT_STREAM)
-    assert e.value.code == M.MURMUR_EUNSUPPORTED
+        M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, -1)  # negative split lengths are rejected
+    assert e.value.code == M.MURMUR_EINVAL
 
 
 def test_decode_attn_accepts_any_larger_workspace():
     """Host validation (the workspace plan included) passes for the exact size and for larger ones; with no
     GPU the launch itself then fails with MURMUR_EHIP."""
-    for split_len in (0, 256, M.MURMUR_SPLIT_STREAM):
+    for split_len in (0, 256):
         ws = M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, split_len)
         for w in (ws, ws + 1, ws + 65536 + 13, 4 * ws):
             assert call_attn(attn_args(split_len=split_len, ws_bytes=w)) == M.MURMUR_EHIP, (split_len, w)
@@ -236,7 +225,7 @@ def call_step(a, seg=FAKE, pol=FAKE, pol_per_seq=0):
     ({}, dict(pol=None), M.MURMUR_EINVAL),
     ({}, dict(pol_per_seq=4), M.MURMUR_EINVAL),
     ({}, dict(pol_per_seq=-1), M.MURMUR_EINVAL),
-    (dict(split_len=M.MURMUR_SPLIT_STREAM), dict(pol_per_seq=M.MURMUR_POL_PER_LAYER), M.MURMUR_EUNSUPPORTED),
+    (dict(split_len=-1), dict(pol_per_seq=M.MURMUR_POL_PER_LAYER), M.MURMUR_EINVAL),
     ({}, dict(seg=FAKE + 2), M.MURMUR_EINVAL),
     (dict(idx=FAKE + 1), {}, M.MURMUR_EINVAL),
     (dict(q=None), {}, M.MURMUR_EINVAL),
@@ -364,7 +353,7 @@ def call_ring_step(a, ring, seg=FAKE, pol=FAKE):
     ({}, M.murmur_ring(0, FAKE, FAKE), M.MURMUR_EINVAL),
     ({}, M.murmur_ring(256, None, FAKE), M.MURMUR_EINVAL),
     ({}, M.murmur_ring(256, FAKE + 8, FAKE), M.MURMUR_EINVAL),
-    (dict(split_len=M.MURMUR_SPLIT_STREAM), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_EUNSUPPORTED),
+    (dict(split_len=-1), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_EINVAL),
     (dict(D=64), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_EUNSUPPORTED),
     (dict(ws_bytes=1000), M.murmur_ring(256, FAKE, FAKE), M.MURMUR_ENOSPACE),
 ])

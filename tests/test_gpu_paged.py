@@ -67,14 +67,14 @@ def test_paged_300s_chunks_with_eviction(split_len):
 
 
 def test_paged_28_layers():
-    """Several layers in one pool per layer (layer stride), ragged sequences, per-sequence policies."""
+    """28 layers, one pool per layer (layer stride), ragged sequences, per-sequence policies."""
     rng = np.random.default_rng(3)
     B = 5
     seg0 = np.stack([rng.integers(0, 40, B), rng.integers(100, 700, B), rng.integers(0, 9, B),
                      rng.integers(1, 300, B)], axis=1).astype(np.int32)
     pol = np.stack([np.array([64, OFF, 200, 33, OFF]), rng.integers(0, 50, B), rng.integers(0, 6, B),
                     np.array([40, 100, OFF, 7, 256]), rng.integers(0, 4, B)], axis=1).astype(np.int32)
-    wl = W.build("paged_ragged", 99, 6, seg0, pol, 3, planted=False)
+    wl = W.build("paged_ragged", 99, 28, seg0, pol, 3, planted=False)
     check_paged(wl, [0, 2], 32, "flash")
 
 
@@ -94,6 +94,24 @@ def test_paged_block_table_too_short():
     pb.attend(0)
     torch.cuda.synchronize()
     assert M.murmur_device_error() & M.MURMUR_DEVERR_POSITION
+    assert np.all(np.isnan(pb.out.float().cpu().numpy()))
+
+
+def test_paged_row_beyond_int32_is_a_device_error():
+    """A block-table entry whose pool row does not fit in 32 bits (block number 2^27 with blocks of 16): the
+    eviction writes -1 and reports MURMUR_DEVERR_BLOCK instead of wrapping into the pool, and the attention
+    reports the position (NaN outputs for that sequence)."""
+    announce("paged row beyond 2^31")
+    wl = W.make("c1")
+    pb = PagedBatch(wl, 16, out_dtype=M.MURMUR_DTYPE_F32, steps=[0])
+    bt = pb.block_table.copy()
+    bt[0, 0] = 1 << 27  # the prompt's first block: always retained; 2^27 * 16 = 2^31
+    pb.bt.copy_(torch.from_numpy(bt))
+    pb.step(0)
+    torch.cuda.synchronize()
+    code = M.murmur_device_error()
+    assert code & M.MURMUR_DEVERR_BLOCK and code & M.MURMUR_DEVERR_POSITION
+    assert np.all(pb.idx.cpu().numpy()[0, :16] == -1)
     assert np.all(np.isnan(pb.out.float().cpu().numpy()))
 
 
@@ -166,15 +184,14 @@ def test_paged_freed_block_is_a_device_error():
 
 def manager_model(seg, pol, bs, table, stack):
     """The device block manager's step, written out: sequences in order push their still-allocated blocks
-    inside the freeable ranges (speech part, then output part, ascending), then those whose current token's
-    block is missing pop from the top of the stack in the same order."""
-    blocks = M.murmur_freeable_blocks_host(seg, pol, bs, 1)
+    that the oracle finds freeable (blocks holding only positions no later step retains, from the oracle's
+    literal Algorithm 1/2 loops, ascending: speech blocks before output blocks), then those whose current
+    token's block is missing pop from the top of the stack in the same order."""
     for b in range(seg.shape[0]):
-        for first, n in blocks[b]:
-            for blk in range(int(first), int(first) + int(n)):
-                if blk < table.shape[1] and table[b, blk] >= 0:
-                    stack.append(int(table[b, blk]))
-                    table[b, blk] = -1
+        for blk in OP.freeable_blocks(seg[b], pol[b], bs):
+            if blk < table.shape[1] and table[b, blk] >= 0:
+                stack.append(int(table[b, blk]))
+                table[b, blk] = -1
     take = [b for b in range(seg.shape[0]) if table[b, (int(seg[b].sum()) - 1) // bs] < 0]
     for i, b in enumerate(take):
         table[b, (int(seg[b].sum()) - 1) // bs] = stack[len(stack) - 1 - i]

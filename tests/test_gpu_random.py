@@ -1,7 +1,7 @@
 """Seeded random configurations through every entry point, against the fp64 oracle (GPU).
 
 Each case draws a batch size, layer count, GQA shape, sequence layouts, per-sequence policies, a split length
-(or the stream schedule) and an entry point -- index list, range table, fused step, ring storage or paged
+and an entry point -- index list, range table, fused step, ring storage or paged
 pool -- and checks two decode steps: the attention to the fp32 bar and, where the entry point writes them,
 the retained sets bit for bit.  The case is printed before it touches the GPU.
 """
@@ -49,7 +49,7 @@ def draw_case(k):
     mode = MODES[k % len(MODES)]
     choices = [0, 32, 64, 96, 128, 192, 256, 384, 640, 1024]
     if mode != "ring":
-        choices.append(M.MURMUR_SPLIT_STREAM)
+        choices.append(512)
     split_len = int(rng.choice(choices))
     unscaled = bool(rng.random() < 0.5)  # queries N(0,1) with scale 1/sqrt(D), else pre-scaled with scale 1
     return dict(B=B, NL=NL, hkv=hkv, group=group, seg0=seg0, pol=pol, mode=mode, split_len=split_len,
