@@ -16,7 +16,8 @@
  *                            (and an equivalent table of contiguous ranges);
  *   murmur_decode_attn    -- split-K grouped-query attention over those
  *                            positions with a log-sum-exp merge of the splits.
- * murmur_decode_step does both in one launch; murmur_decode_step_ring does it
+ * murmur_decode_step does both in one launch (murmur_decode_step_static too,
+ * without a workspace argument); murmur_decode_step_ring does it
  * on physical eviction storage (an output ring) and appends the current
  * token's K/V; murmur_evict_compact_paged emits the lists as rows of a paged
  * pool.  Host-only helpers size the lists, lay out ring storage, name the
@@ -26,7 +27,9 @@
  * Conventions shared by every call:
  *   - Pointers named *_dev are device memory (HIP, the current device); all
  *     other pointers are host memory.  Every buffer is owned by the caller;
- *     the library keeps no pointer after a call returns and allocates nothing.
+ *     the library keeps no pointer after a call returns and allocates nothing
+ *     (murmur_decode_step_static uses a scratch array of the library's own,
+ *     see there).
  *   - Hot calls are asynchronous on `stream` (NULL = the null stream), never
  *     synchronise the host, issue only kernel launches, and may be captured
  *     into a HIP graph.
@@ -133,7 +136,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 8
+#define MURMUR_ABI_VERSION 9
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -331,6 +334,29 @@ int murmur_decode_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, 
                        int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
                        float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
                        void *ws_dev, size_t ws_bytes, murmur_stream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * one-launch decode step of murmur_decode_step without a workspace argument.
+ * Its tickets and split partials live in a scratch array of
+ * MURMUR_STATIC_SCRATCH_BYTES that the library holds in device memory, one
+ * copy per device, from the first call on that device until the process
+ * ends; the call itself allocates and frees nothing.  On the first call on a
+ * device the scratch's tickets are zeroed by a small kernel on `stream`;
+ * every completed call leaves them at zero.  All calls on one device share
+ * that device's scratch: calls that overlap in time on one device (other
+ * streams, concurrent host threads) race and must not be issued.
+ * Arguments, outputs and device errors: as murmur_decode_step.  Errors as
+ * murmur_decode_step, plus MURMUR_ENOSPACE when the call's tickets and
+ * partials (murmur_decode_attn_workspace for the same sizes and split_len)
+ * exceed MURMUR_STATIC_SCRATCH_BYTES, and MURMUR_EHIP when the scratch's
+ * address cannot be looked up. */
+#define MURMUR_STATIC_SCRATCH_BYTES (4u << 20)
+int murmur_decode_step_static(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                              const void *q_dev, const murmur_kv *kv, int32_t *idx_dev, int32_t *count_dev,
+                              int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                              float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                              murmur_stream_t stream);
 
 /* Physical eviction storage (Section 3.2: evicted entries leave the cache).
  * The output region of each sequence's cache holds its out_sink output sinks

@@ -141,12 +141,24 @@ int check_host_policy(const murmur_seg *seg, const murmur_policy *pol, int32_t p
 namespace murmur {
 namespace {
 
-// Validation and launch description shared by murmur_decode_attn and
-// murmur_decode_step (everything but where the retained sets come from).
+// Tickets in the ticket region at the start of the workspace, partials after
+// it; the region depends only on ws_bytes (see murmur_decode_attn_workspace).
+void bind_workspace(AttnLaunch &a, void *ws_dev, size_t ws_bytes) {
+    uint8_t *ws = (uint8_t *)ws_dev;
+    const size_t region = ticket_region(ws_bytes);
+    a.ticket = (int32_t *)ws;
+    a.part_ml = a.part_ml_bytes ? (float *)(ws + region) : nullptr;
+    a.part_o = a.part_ml_bytes ? (float *)(ws + region + a.part_ml_bytes) : nullptr;
+}
+
+// Validation and launch description shared by murmur_decode_attn and the
+// decode steps (everything but where the retained sets come from).  With
+// ws_dev NULL and static_ws set, the workspace is the library's scratch array
+// of ws_bytes (bound by the caller after these checks); otherwise ws_dev.
 int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv,
                  int32_t D, float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
-                 void *ws_dev, size_t ws_bytes, AttnLaunch &a) {
-    if (!q_dev || !kv || !out_dev || !ws_dev)
+                 void *ws_dev, size_t ws_bytes, AttnLaunch &a, bool static_ws = false) {
+    if (!q_dev || !kv || !out_dev || (!ws_dev && !static_ws))
         return fail(MURMUR_EINVAL, "q_dev, kv, out_dev and ws_dev must not be NULL");
     if (!kv->k || !kv->v) return fail(MURMUR_EINVAL, "kv->k and kv->v must not be NULL");
     if (B < 1 || Hq < 1 || Hkv < 1 || max_keep < 1 || kv->n_layers < 1 || kv->max_len < 1)
@@ -176,6 +188,9 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     if (!aligned(ws_dev, 256)) return fail(MURMUR_EINVAL, "ws_dev must be 256-byte aligned");
 
     const WorkspacePlan plan = plan_workspace(kv->n_layers, B, Hq, Hkv, max_keep, split_len);
+    if (ws_bytes < plan.total && static_ws)
+        return fail(MURMUR_ENOSPACE, "this call needs %zu bytes of scratch; the allocation-free step has %zu "
+                    "(use murmur_decode_step with a workspace)", plan.total, ws_bytes);
     if (ws_bytes < plan.total)
         return fail(MURMUR_ENOSPACE, "workspace of %zu bytes is too small (%zu needed)", ws_bytes, plan.total);
     if (plan.n_split > kMaxMergeSplits)
@@ -198,20 +213,15 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     a.s_pos = kv->stride_pos;
     a.out = out_dev;
     a.lse = lse_dev;
-    uint8_t *ws = (uint8_t *)ws_dev;
-    // Tickets in the ticket region at the start, partials after it; the split
-    // depends only on ws_bytes (see murmur_decode_attn_workspace).
-    const size_t region = ticket_region(ws_bytes);
-    a.ticket = (int32_t *)ws;
     // Partials exist when a group has more than one split.
+    const size_t region = ticket_region(ws_bytes);
     const bool partials = plan.ml_bytes > 0;
     if (partials != (plan.n_split > 1) || region < (size_t)plan.tickets * 4 ||
         region + plan.ml_bytes + plan.o_bytes > ws_bytes)
         return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
-    a.part_ml = partials ? (float *)(ws + region) : nullptr;
-    a.part_o = partials ? (float *)(ws + region + plan.ml_bytes) : nullptr;
     a.part_ml_bytes = (uint32_t)plan.ml_bytes;
     a.part_o_bytes = (uint32_t)plan.o_bytes;
+    if (!static_ws) bind_workspace(a, ws_dev, ws_bytes);
     a.max_len = kv->max_len;
     a.max_keep = max_keep;
     a.B = B;
@@ -405,11 +415,14 @@ MURMUR_EXPORT int murmur_decode_attn(const void *q_dev, const murmur_kv *kv, con
     return ok();
 }
 
-MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
-                                     const void *q_dev, const murmur_kv *kv, int32_t *idx_dev, int32_t *count_dev,
-                                     int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
-                                     float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
-                                     void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
+namespace {
+
+// Checks and launch description of murmur_decode_step and its allocation-free
+// variant (static_ws: the workspace is bound by the caller).
+int prepare_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq, const void *q_dev,
+                 const murmur_kv *kv, int32_t *idx_dev, int32_t *count_dev, int32_t *ranges_dev, int32_t max_keep,
+                 int32_t B, int32_t Hq, int32_t Hkv, int32_t D, float scale, int32_t split_len, void *out_dev,
+                 int32_t out_dtype, float *lse_dev, void *ws_dev, size_t ws_bytes, bool static_ws, AttnLaunch &a) {
     if (!seg_dev || !pol_dev) return fail(MURMUR_EINVAL, "seg_dev and pol_dev must not be NULL");
     if (pol_per_seq < 0 || pol_per_seq > (MURMUR_POL_PER_SEQ | MURMUR_POL_PER_LAYER))
         return fail(MURMUR_EINVAL, "pol_per_seq must be a set of MURMUR_POL_* bits (0..3, got %d)", pol_per_seq);
@@ -417,9 +430,8 @@ MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_pol
         !aligned(ranges_dev, 4))
         return fail(MURMUR_EINVAL, "seg/pol/idx/count/ranges pointers must be 4-byte aligned");
     if ((int64_t)B * max_keep > ((int64_t)1 << 40)) return fail(MURMUR_EINVAL, "B * max_keep too large");
-    AttnLaunch a;
     const int rc = prepare_attn(q_dev, kv, max_keep, B, Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev,
-                                ws_dev, ws_bytes, a);
+                                ws_dev, ws_bytes, a, static_ws);
     if (rc != MURMUR_OK) return rc;
     a.src0 = reinterpret_cast<const int32_t *>(seg_dev);
     a.src1 = reinterpret_cast<const int32_t *>(pol_dev);
@@ -428,8 +440,48 @@ MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_pol
     a.idx_out = idx_dev;
     a.count_out = count_dev;
     a.ranges_out = ranges_dev;
+    return ok();
+}
+
+}  // namespace
+
+MURMUR_EXPORT int murmur_decode_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, int32_t pol_per_seq,
+                                     const void *q_dev, const murmur_kv *kv, int32_t *idx_dev, int32_t *count_dev,
+                                     int32_t *ranges_dev, int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                     float scale, int32_t split_len, void *out_dev, int32_t out_dtype, float *lse_dev,
+                                     void *ws_dev, size_t ws_bytes, murmur_stream_t stream) {
+    AttnLaunch a;
+    const int rc = prepare_step(seg_dev, pol_dev, pol_per_seq, q_dev, kv, idx_dev, count_dev, ranges_dev, max_keep, B,
+                                Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev, ws_dev, ws_bytes, false, a);
+    if (rc != MURMUR_OK) return rc;
     const int e = launch_decode_attn(a, stream);
     if (e != 0) return fail(MURMUR_EHIP, "decode_step launch failed: %s", hip_error_text(e));
+    return ok();
+}
+
+MURMUR_EXPORT int murmur_decode_step_static(const murmur_seg *seg_dev, const murmur_policy *pol_dev,
+                                            int32_t pol_per_seq, const void *q_dev, const murmur_kv *kv,
+                                            int32_t *idx_dev, int32_t *count_dev, int32_t *ranges_dev,
+                                            int32_t max_keep, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                            float scale, int32_t split_len, void *out_dev, int32_t out_dtype,
+                                            float *lse_dev, murmur_stream_t stream) {
+    AttnLaunch a;
+    const int rc = prepare_step(seg_dev, pol_dev, pol_per_seq, q_dev, kv, idx_dev, count_dev, ranges_dev, max_keep, B,
+                                Hq, Hkv, D, scale, split_len, out_dev, out_dtype, lse_dev, nullptr,
+                                MURMUR_STATIC_SCRATCH_BYTES, true, a);
+    if (rc != MURMUR_OK) return rc;
+    void *scratch = nullptr;
+    bool fresh = false;
+    int e = static_scratch(&scratch, &fresh);
+    if (e != 0) return fail(MURMUR_EHIP, "looking up the scratch array failed: %s", hip_error_text(e));
+    if (fresh) {  // first call on this device: the tickets start at zero (later calls leave them at zero)
+        e = launch_workspace_init((int32_t *)scratch, (int64_t)(ticket_region(MURMUR_STATIC_SCRATCH_BYTES) / 4),
+                                  stream);
+        if (e != 0) return fail(MURMUR_EHIP, "scratch ticket reset failed: %s", hip_error_text(e));
+    }
+    bind_workspace(a, scratch, MURMUR_STATIC_SCRATCH_BYTES);
+    e = launch_decode_attn(a, stream);
+    if (e != 0) return fail(MURMUR_EHIP, "decode_step_static launch failed: %s", hip_error_text(e));
     return ok();
 }
 

@@ -85,6 +85,10 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
                          int32_t max_blocks, int32_t log2_bs, murmur_stream_t stream);
 int launch_decode_attn(const AttnLaunch &a, murmur_stream_t stream);
 int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream);
+// Device address of the current device's scratch array (MURMUR_STATIC_SCRATCH_BYTES,
+// 256-byte aligned), looked up once per device; *fresh is true on that first
+// lookup, when the caller must zero the ticket region.  Returns a hipError_t value.
+int static_scratch(void **ptr, bool *fresh);
 int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, uint32_t *sink, murmur_stream_t stream);
 int launch_paged_step(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B, int32_t *bt,
                       int32_t max_blocks, int32_t log2_bs, int32_t *stack, int32_t *top, int32_t capacity,

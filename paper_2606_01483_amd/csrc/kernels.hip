@@ -20,6 +20,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "internal.h"
 #include "policy.h"
 
@@ -1599,6 +1601,34 @@ int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream) {
     const int64_t blocks = n / 256 + 1 < 1024 ? n / 256 + 1 : 1024;
     hipLaunchKernelGGL(workspace_init_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, ticket, n);
     return (int)hipGetLastError();
+}
+
+// Scratch of murmur_decode_step_static (tickets, then split partials, laid out
+// as a workspace of MURMUR_STATIC_SCRATCH_BYTES): one copy per device, held
+// until the process ends.  Host code never uses the array's name as an
+// address: static_scratch() looks the device address up once per device.
+static __device__ __align__(256) uint8_t scratch[MURMUR_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mutex;
+static void *g_scratch_ptr[kMaxDevices];
+
+int static_scratch(void **ptr, bool *fresh) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return (int)e;
+    if (dev < 0 || dev >= kMaxDevices) return (int)hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    *fresh = g_scratch_ptr[dev] == nullptr;
+    if (*fresh) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return (int)e;
+        if (p == nullptr || (uintptr_t)p % 256 != 0) return (int)hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return 0;
 }
 
 int read_and_clear_device_error(murmur_stream_t stream, int32_t *code) {

@@ -88,6 +88,9 @@ def _load():
     lib.murmur_decode_step.restype = ctypes.c_int
     lib.murmur_decode_step.argtypes = [vp, vp, i32, vp, ctypes.POINTER(murmur_kv), vp, vp, vp, i32, i32, i32, i32, i32,
                                        ctypes.c_float, i32, vp, i32, vp, vp, sz, vp]
+    lib.murmur_decode_step_static.restype = ctypes.c_int
+    lib.murmur_decode_step_static.argtypes = [vp, vp, i32, vp, ctypes.POINTER(murmur_kv), vp, vp, vp, i32, i32, i32,
+                                              i32, i32, ctypes.c_float, i32, vp, i32, vp, vp]
     lib.murmur_ring_layout_host.restype = ctypes.c_int
     lib.murmur_ring_layout_host.argtypes = [ctypes.POINTER(murmur_seg), ctypes.POINTER(murmur_policy), i32, i32, i32,
                                             i32p, i32p]
@@ -238,6 +241,19 @@ def murmur_decode_step(seg_dev, pol_dev, pol_per_seq: int, q_dev, kv: murmur_kv,
                                       _addr(idx_dev), _addr(count_dev), _addr(ranges_dev), max_keep, B, Hq, Hkv, D,
                                       float(scale), split_len, _addr(out_dev), out_dtype, _addr(lse_dev),
                                       _addr(ws_dev), ws_bytes, _stream(stream)))
+
+
+def murmur_decode_step_static(seg_dev, pol_dev, pol_per_seq: int, q_dev, kv: murmur_kv, idx_dev, count_dev,
+                              ranges_dev, max_keep: int, B: int, Hq: int, Hkv: int, D: int, scale: float,
+                              split_len: int, out_dev, out_dtype: int, lse_dev, stream=None) -> None:
+    """murmur_decode_step without a workspace: tickets and partials in the library's per-device scratch."""
+    _check(_load().murmur_decode_step_static(_addr(seg_dev), _addr(pol_dev), pol_per_seq, _addr(q_dev),
+                                             ctypes.byref(kv), _addr(idx_dev), _addr(count_dev), _addr(ranges_dev),
+                                             max_keep, B, Hq, Hkv, D, float(scale), split_len, _addr(out_dev),
+                                             out_dtype, _addr(lse_dev), _stream(stream)))
+
+
+MURMUR_STATIC_SCRATCH_BYTES = 4 << 20
 
 
 def murmur_ring_layout_host(seg, pol, out_capacity: int, pol_per_seq: int | None = None):

@@ -118,6 +118,10 @@ int main() {
                              nullptr, fake, 1 << 30, nullptr) == MURMUR_EINVAL);
     CHECK(murmur_decode_step(fseg, fpol, 4, fake, &kv, nullptr, nullptr, nullptr, 850, 12, 28, 4, 128, 1.f, 0, fake,
                              MURMUR_DTYPE_BF16, nullptr, fake, 1 << 30, nullptr) == MURMUR_EINVAL);
+    CHECK(murmur_decode_step_static(fseg, fpol, 4, fake, &kv, nullptr, nullptr, nullptr, 850, 12, 28, 4, 128, 1.f,
+                                    0, fake, MURMUR_DTYPE_BF16, nullptr, nullptr) == MURMUR_EINVAL);
+    CHECK(murmur_decode_step_static(fseg, fpol, 0, fake, &kv, nullptr, nullptr, nullptr, 850, 12, 28, 4, 128, 1.f,
+                                    32, fake, MURMUR_DTYPE_BF16, nullptr, nullptr) == MURMUR_ENOSPACE);
     murmur_ring ring{0, fake, fake};
     CHECK(murmur_decode_step_ring(fseg, fpol, 1, &ring, fake, &kv, nullptr, nullptr, nullptr, 850, 12, 28, 4, 128,
                                   1.f, 0, fake, MURMUR_DTYPE_BF16, nullptr, fake, 1 << 30, nullptr) == MURMUR_EINVAL);

@@ -26,6 +26,7 @@ int launch_paged_append(const murmur_seg *, int32_t, const int32_t *, int32_t, i
                         const void *, const void *, murmur_stream_t) {
     return reached("paged_append");
 }
+int static_scratch(void **, bool *) { return reached("static_scratch"); }
 int read_and_clear_device_error(murmur_stream_t, int32_t *) { return reached("device_error"); }
 const char *hip_error_text(int) { return "stub"; }
 }  // namespace murmur

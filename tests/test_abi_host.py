@@ -39,14 +39,14 @@ def declared_functions():
 
 def test_exports_every_declared_function():
     names = declared_functions()
-    assert len(names) == 17
+    assert len(names) == 18
     lib = ctypes.CDLL(M.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 8
+    assert M.murmur_abi_version() == 9
 
 
 def test_retained_count_host_matches_oracle():
@@ -237,6 +237,42 @@ def call_step(a, seg=FAKE, pol=FAKE, pol_per_seq=0):
 def test_decode_step_rejects(over, step_kw, code):
     assert call_step(attn_args(**over), **step_kw) == code
     assert M.murmur_last_error() != ""
+
+
+def call_step_static(a, seg=FAKE, pol=FAKE, pol_per_seq=0):
+    return M.lib().murmur_decode_step_static(seg, pol, pol_per_seq, a["q"], ctypes.byref(a["kv"]), a["idx"],
+                                             a["count"], a["ranges"], a["max_keep"], a["B"], a["Hq"], a["Hkv"],
+                                             a["D"], a["scale"], a["split_len"], a["out"], a["out_dtype"], a["lse"], 0)
+
+
+@pytest.mark.parametrize("over,step_kw,code", [
+    ({}, dict(seg=None), M.MURMUR_EINVAL),
+    ({}, dict(pol_per_seq=4), M.MURMUR_EINVAL),
+    (dict(q=None), {}, M.MURMUR_EINVAL),
+    (dict(D=64), {}, M.MURMUR_EUNSUPPORTED),
+    (dict(split_len=100), {}, M.MURMUR_EINVAL),
+    # 48 groups cut into 27 splits of 32 positions: 4.7 MiB of partials, beyond the 4 MiB scratch
+    (dict(split_len=32), {}, M.MURMUR_ENOSPACE),
+    # 28 layers x 12 sequences x 4 KV heads = 1344 split groups need more tickets than the scratch holds
+    (dict(kv=M.murmur_kv(FAKE, FAKE, 28, 4096, 0, 0, 0, 128), split_len=512, max_keep=1024), {},
+     M.MURMUR_ENOSPACE),
+])
+def test_decode_step_static_rejects(over, step_kw, code):
+    """The allocation-free step runs every check before any HIP call, including the scratch limit."""
+    assert call_step_static(attn_args(**over), **step_kw) == code
+    assert M.murmur_last_error() != ""
+
+
+def test_decode_step_static_scratch_limit():
+    """What fits: the calls whose workspace (same sizes and split_len) is at most MURMUR_STATIC_SCRATCH_BYTES."""
+    limit = M.MURMUR_STATIC_SCRATCH_BYTES
+    assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 0) <= limit        # 12 x 300 s chunks, eviction
+    assert M.murmur_decode_attn_workspace(28, 12, 28, 4, 850, 0) <= limit       # 28 layers
+    assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, 0) <= limit       # the hour-long single pass
+    assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 32) > limit
+    assert M.murmur_decode_attn_workspace(28, 12, 28, 4, 1024, 512) > limit
+    # without a GPU a call that passes the checks fails at the first HIP call
+    assert call_step_static(attn_args()) == M.MURMUR_EHIP
 
 
 # ---- ring storage (host layout and argument checks) ----------------------------------------------
