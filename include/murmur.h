@@ -259,7 +259,7 @@ int murmur_paged_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, i
  * (0 = the automatic choice, or positions per split).
  * The workspace holds ticket counters (one per (layer, sequence, kv-head)
  * group that is split) in a region at its start
- * whose size depends on ws_bytes alone (4 bytes per KiB, rounded up to 256),
+ * whose size depends on ws_bytes alone (128 bytes per KiB, rounded up to 256),
  * and the split partials after that region.  It must be zero-filled once
  * before its first use (or reset with murmur_decode_attn_workspace_init);
  * every completed call leaves the tickets at zero again.  Calls of any shapes

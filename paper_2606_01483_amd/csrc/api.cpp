@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "internal.h"
 #include "murmur.h"
 #include "policy.h"
@@ -39,7 +41,26 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
 
-size_t ticket_region(size_t ws_bytes) { return round_up(4 * ((ws_bytes + 1023) / 1024), 256); }
+size_t ticket_region(size_t ws_bytes) { return round_up(4 * kTicketStride * ((ws_bytes + 1023) / 1024), 256); }
+
+namespace {
+
+// ceil(2^32 / d): multiply-high by it divides values below 2^16 exactly.  0
+// for d = 1, whose value does not fit (the kernel then divides by one), and
+// for d = 0 (an unused divisor).
+uint32_t magic16(uint32_t d) { return d <= 1 ? 0u : (uint32_t)((((uint64_t)1 << 32) + d - 1) / d); }
+
+// Estimated launch time (us) of a one-round split with at most len positions per
+// workgroup and at most n splits per group (the model behind the automatic choice,
+// with constants measured on MI355X): each compute unit streams its share at
+// kCuBytesPerUs, and more than one split adds the merge chain and the merging
+// workgroup's loads of n partials.
+double wide_cost(int64_t len, int64_t n, int64_t G) {
+    const double part_bytes = (double)G * (kHeadDim + 2) * 4.0;
+    return (double)len * 4.0 * kHeadDim / kCuBytesPerUs + (n > 1 ? kMergeChainUs + n * part_bytes / kCuBytesPerUs : 0.0);
+}
+
+}  // namespace
 
 WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
                              int32_t split_len) {
@@ -48,55 +69,83 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     const int64_t groups = (int64_t)n_layers * B * Hkv;
     const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
     p.groups = groups;
-    if (split_len <= 0) {
-        // Few units (and no more splits than one merge combines): splits of
-        // one or two passes per wavefront from registers, as many as fill one
-        // dispatch round (kRoundWorkgroups) with equal shares, so no compute
-        // unit holds twice the work of another.  Otherwise the LDS-staged
-        // kernel, which takes a whole compute unit: as many splits as keep
-        // one dispatch round, fewer when there are more groups than that, at
-        // most kMaxAutoSplits.
-        int64_t per;
-        if (groups * units <= kSinglePassMaxUnits && units <= kMaxMergeSplits) {
-            // The split count that minimises an estimate of the launch time: each compute unit streams
-            // its split at kCuBytesPerUs, and more than one split adds the merge chain (store, ticket,
-            // loading the partials).  At most one dispatch round; splits of 1 or 2 passes.
-            const int64_t n_max = kRoundWorkgroups / groups < 1 ? 1 : kRoundWorkgroups / groups;
-            const double group_bytes = (double)max_keep * 4.0 * kHeadDim;  // K and V rows of one KV head
-            const double part_bytes = (double)G * (kHeadDim + 2) * 4.0;
-            int64_t best_len = 0;
-            double best = 0.0;
-            for (int64_t n = 1; n <= n_max; ++n) {
-                int64_t len = (((int64_t)max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
-                if (len < kSplitUnit) len = kSplitUnit;
-                if (len > 2 * kSplitUnit) continue;  // more than two passes: the LDS-staged kernel's range
-                const int64_t ns = ((int64_t)max_keep + len - 1) / len;
-                const double t = group_bytes / ns / kCuBytesPerUs +
-                                 (ns > 1 ? kMergeChainUs + ns * part_bytes / kCuBytesPerUs : 0.0);
-                if (best_len == 0 || t < best) {
+    // The wide schedule (splits of at most kWideSplit positions, a wavefront per
+    // pass) needs its work indices below 2^16.
+    const bool wide_ok = groups < 65536 && Hkv < 65536 && B < 65536;
+    int64_t n_hi = 0, n_lo = 0, len_hi = 0, len_lo = 0, groups_hi = 0;
+    if (split_len == 0 && wide_ok && groups <= kRoundWorkgroups) {
+        // One dispatch round: n_lo splits per group, and one more for the first
+        // groups_hi groups when that fills the round; the candidate with the
+        // lowest estimate (fewer workgroups on a tie).
+        double best = 0.0;
+        for (int64_t n = 1; n * groups <= kRoundWorkgroups; ++n) {
+            const int64_t len = ((int64_t)max_keep + n - 1) / n;
+            if (len > kWideSplit) continue;
+            for (int fill = 0; fill < 2; ++fill) {
+                const int64_t gh = fill ? std::min(groups, kRoundWorkgroups - n * groups) : 0;
+                if (fill && gh == 0) continue;
+                const int64_t lh = ((int64_t)max_keep + n) / (n + 1);
+                const double t = wide_cost(len, gh > 0 ? n + 1 : n, G);
+                if (n_lo == 0 || t < best - 1e-9) {
                     best = t;
-                    best_len = len;
+                    n_lo = n;
+                    len_lo = len;
+                    groups_hi = gh;
+                    n_hi = gh > 0 ? n + 1 : 0;
+                    len_hi = gh > 0 ? lh : 0;
                 }
             }
-            if (best_len == 0) best_len = 2 * kSplitUnit;
-            split_len = (int32_t)best_len;
-            per = 0;
-        } else {
+        }
+    } else if (split_len > 0 && split_len <= kWideSplit && wide_ok) {
+        n_lo = ((int64_t)max_keep + split_len - 1) / split_len;
+        len_lo = split_len;
+    }
+    if (split_len == 0 && n_lo > 0) {
+        // The LDS-staged kernel's automatic split (below) when the model expects it to be faster.
+        int64_t want = std::min<int64_t>(std::min<int64_t>(kRoundWorkgroups / groups, kMaxAutoSplits), units);
+        if (want < 1) want = 1;
+        const int64_t per = std::max<int64_t>((units + want - 1) / want, 2);
+        const int64_t n_lds = ((int64_t)max_keep + per * kSplitUnit - 1) / (per * kSplitUnit);
+        const double t_wide = wide_cost(len_lo, groups_hi > 0 ? n_hi : n_lo, G);
+        if (wide_cost(std::min<int64_t>(per * kSplitUnit, max_keep), n_lds, G) < t_wide) n_lo = 0;
+    }
+    if (n_lo > 0 && n_lo < 65536 && groups * n_lo + groups_hi < 65536) {
+        p.wide_wg = (int32_t)(groups * n_lo + groups_hi);
+        p.sched.groups_hi = (uint32_t)groups_hi;
+        p.sched.n_split = (uint32_t)n_hi | (uint32_t)n_lo << 16;
+        p.sched.magic_hi = magic16((uint32_t)n_hi);
+        p.sched.magic_lo = magic16((uint32_t)n_lo);
+        p.sched.len = (uint32_t)len_hi | (uint32_t)len_lo << 16;
+        p.sched.hkv_b = (uint32_t)Hkv | (uint32_t)B << 16;
+        p.sched.magic_hkv = magic16((uint32_t)Hkv);
+        p.sched.magic_b = magic16((uint32_t)B);
+        p.n_split = (int32_t)(n_hi > n_lo ? n_hi : n_lo);
+        p.split_len = (int32_t)len_lo;
+        if (p.n_split > 1) {
+            p.tickets = groups;
+            p.ml_bytes = round_up((size_t)p.wide_wg * G * 2 * sizeof(float), 256);
+            p.o_bytes = round_up((size_t)p.wide_wg * G * kHeadDim * sizeof(float), 256);
+        }
+    } else {
+        if (split_len <= 0) {
+            // The LDS-staged kernel, which takes a whole compute unit: as many
+            // splits as keep one dispatch round, fewer when there are more groups
+            // than that, at most kMaxAutoSplits.
             int64_t want = kRoundWorkgroups / groups;
             if (want > kMaxAutoSplits) want = kMaxAutoSplits;
             if (want > units) want = units;
             if (want < 1) want = 1;
-            per = (units + want - 1) / want;
+            int64_t per = (units + want - 1) / want;
             if (per < 2) per = 2;
+            split_len = (int32_t)(per * kSplitUnit);
         }
-        if (per > 0) split_len = (int32_t)(per * kSplitUnit);
-    }
-    p.split_len = split_len;
-    p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
-    if (p.n_split > 1) {
-        p.tickets = groups;
-        p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
-        p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
+        p.split_len = split_len;
+        p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
+        if (p.n_split > 1) {
+            p.tickets = groups;
+            p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
+            p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
+        }
     }
     // The smallest size whose ticket region holds the tickets and leaves room
     // for the partials, with 256 bytes to spare so that any larger size does
@@ -216,7 +265,7 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     // Partials exist when a group has more than one split.
     const size_t region = ticket_region(ws_bytes);
     const bool partials = plan.ml_bytes > 0;
-    if (partials != (plan.n_split > 1) || region < (size_t)plan.tickets * 4 ||
+    if (partials != (plan.n_split > 1) || region < (size_t)plan.tickets * 4 * kTicketStride ||
         region + plan.ml_bytes + plan.o_bytes > ws_bytes)
         return fail(MURMUR_EINVAL, "internal: inconsistent workspace plan");
     a.part_ml_bytes = (uint32_t)plan.ml_bytes;
@@ -231,6 +280,8 @@ int prepare_attn(const void *q_dev, const murmur_kv *kv, int32_t max_keep, int32
     a.NL = kv->n_layers;
     a.split_len = plan.split_len;
     a.n_split = plan.n_split;
+    a.wide_wg = plan.wide_wg;
+    a.sched = plan.sched;
     a.out_f32 = out_dtype == MURMUR_DTYPE_F32;
     a.scale_log2 = scale * 1.4426950408889634f;
     return ok();

@@ -16,7 +16,6 @@ constexpr int kWavesPerWg = 4;
 constexpr int kSplitUnit = kWaveTile * kWavesPerWg;  // 128 positions: one pass of a workgroup
 constexpr int kMaxAutoSplits = 64;
 constexpr int kRoundWorkgroups = 256;     // one workgroup per compute unit
-constexpr int kSinglePassMaxUnits = 512;  // below this many units the automatic split is one pass
 // Splits one merge can combine: it stages 2 * n_split * G + 2 * G floats in
 // the workgroup's 32 KiB of V-tile LDS.
 constexpr int kMaxMergeSplits = 240;
@@ -27,6 +26,29 @@ constexpr int kMergeBatch = 8;  // splits whose partials one merging thread load
 // about 2.3 us on top of the data phase.
 constexpr double kCuBytesPerUs = 40e3;
 constexpr double kMergeChainUs = 2.3;
+
+// Wide schedule: workgroups of kWideWaves wavefronts, each wavefront one pass
+// of kWaveTile retained positions, so a split holds at most kWideSplit.
+constexpr int kWideWaves = 8;
+constexpr int kWideSplit = kWideWaves * kWaveTile;  // 256
+
+// Work of the wide schedule's workgroups, decoded on the device with exact
+// multiply-high divisions (values below 2^16, multipliers ceil(2^32 / d), 0
+// for d = 1): the
+// first groups_hi (layer, sequence, KV head) groups are cut into n_hi splits
+// of len_hi positions, the others into n_lo of len_lo; workgroup w takes the
+// w-th (group, split) in that order and, when its group has more than one
+// split, leaves its partial in slot w.
+struct WideSched {
+    uint32_t groups_hi;
+    uint32_t n_split;   // n_hi | n_lo << 16
+    uint32_t magic_hi;  // ceil(2^32 / n_hi)
+    uint32_t magic_lo;  // ceil(2^32 / n_lo)
+    uint32_t len;       // len_hi | len_lo << 16
+    uint32_t hkv_b;     // Hkv | B << 16
+    uint32_t magic_hkv;
+    uint32_t magic_b;
+};
 
 // Launch description of one decode_attn call, fully validated by the caller.
 // Where the attention takes the retained sets from (see AttnLaunch::src0/src1).
@@ -52,27 +74,35 @@ struct AttnLaunch {
     const int32_t *idx;
     void *out;
     float *lse;
-    int32_t *ticket;   // [groups]: one counter per (layer, sequence, KV head) that is split
+    int32_t *ticket;   // [groups][kTicketStride]: one counter per split (layer, sequence, KV head)
     float *part_ml;    // [groups][n_split][G][2]  (running max in log2 units, sum)
     float *part_o;     // [groups][n_split][G][128]
     uint32_t part_ml_bytes, part_o_bytes;  // extents of the two partial arrays (< 2^31)
     int32_t max_len, max_keep, B, Hq, Hkv, G, NL;
     int32_t split_len, n_split, out_f32;
     float scale_log2;  // logit scale times log2(e)
+    int32_t wide_wg;   // > 0: the wide schedule with this many workgroups (sched)
+    WideSched sched;
 };
 
 struct WorkspacePlan {
     int32_t split_len;
-    int32_t n_split;
+    int32_t n_split;  // splits per group (the wide schedule: of the groups with the most)
+    int32_t wide_wg;  // > 0: the wide schedule's workgroups
+    WideSched sched;
     int64_t groups;
     int64_t tickets;  // ticket counters the launch uses
     size_t ml_bytes, o_bytes, total;
 };
 
+// Ticket counters sit kTicketStride int32 apart (one 128-byte cache line
+// each), so that the atomics of different groups do not queue on one line.
+constexpr int kTicketStride = 32;
 // Bytes at the start of a workspace of ws_bytes that hold the tickets (the
-// partials follow).  Depends on the size alone, so calls of different shapes
-// that share a workspace place their tickets alike, and never where another
-// call left partials.
+// partials follow): 128 bytes per KiB, rounded up to 256, room for a ticket
+// per KiB.  Depends on the size alone, so calls of different shapes that share
+// a workspace place their tickets alike, and never where another call left
+// partials.
 size_t ticket_region(size_t ws_bytes);
 
 // Split choice and workspace layout; deterministic in its arguments.

@@ -288,17 +288,6 @@ static __device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-// LDS tile of one wavefront: V^T for 128 head dims x 32 positions, in 16-byte
-// units (one head dim, eight positions).  Unit (d, q) -- q = position octet --
-// sits at q*128 + swz(d); the XOR swizzle and the half swap for odd d make both
-// the transposing ds_write_b128 and the operand ds_read_b64 bank-conflict free
-// for 32- and 64-bank LDS models.
-static __device__ __forceinline__ int vt_unit(int d, int q) {
-    const int dp = d ^ ((d >> 3) & 7) ^ (((d >> 6) & 1) << 3);
-    return q * 128 + dp;
-}
-
-constexpr int kVtBytesPerWave = 4 * 128 * 16;  // 8 KiB
 constexpr float kNegInf = -__builtin_huge_valf();
 
 // Device-coherent accesses for the split partials: raw buffer loads and stores
@@ -322,6 +311,14 @@ static __device__ __forceinline__ f32x4 load_coherent4(__amdgpu_buffer_rsrc_t r,
 }
 static __device__ __forceinline__ float load_coherent1(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCoherent));
+}
+// The same with a scalar byte offset added to the vector one (the split slot
+// of a partial, so that the loads of all slots share one vector offset).
+static __device__ __forceinline__ f32x4 load_coherent4_s(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t soff) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, kCoherent));
+}
+static __device__ __forceinline__ float load_coherent1_s(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t soff) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, soff, kCoherent));
 }
 // Wait until every vector-memory access of this wavefront has completed; also a
 // compiler barrier, so no store is moved past it.
@@ -358,12 +355,6 @@ static __device__ __forceinline__ float sum_over_c4(float x) {
     swap32(a, b);
     return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
-
-// K and V fragments of one pass of kWaveTile retained positions.
-struct PassRegs {
-    u32x4 kf[2][4];  // MFMA A operands: position 16*blk + n16, head dims kc*32 + 8*c4 .. +8
-    u32x4 vf[8];     // position 8*c4 + t, head dims 8*n16 .. +8
-};
 
 // Running softmax state of one wavefront for one (layer, sequence, KV head):
 // lane (head n16, c4) holds the max (log2 units) and sum of head n16; acc holds
@@ -427,76 +418,6 @@ static __device__ __forceinline__ int tab_pos(const RangeTab &t, int r, int &pie
     return p;
 }
 
-// Positions of the rows one lane loads in a pass of 32 ranks from r0: K rows
-// of ranks r0 + 16*blk + n16 (blk = 0, 1) and V rows of ranks r0 + 8*c4 + t
-// (t = 0..7).  Every lane loads, so ranks at or past the count, and positions
-// outside [0, max_len), read row 0 instead: their logits and V rows are masked
-// when the pass is computed.  A retained rank whose position is outside the
-// cache sets `bad` (the K ranks of the 64 lanes cover all 32 ranks).
-struct PassPos {
-    int32_t k[2];
-    int32_t v[8];
-};
-
-static __device__ __forceinline__ int keep_pos(int r, int p, int cnt, int max_len, int &bad) {
-    const bool live = r < cnt;
-    const bool inb = (uint32_t)p < (uint32_t)max_len;
-    bad |= live && !inb;
-    return live && inb ? p : 0;
-}
-
-static __device__ __forceinline__ void pass_pos_ranges(const RangeTab &t, int r0, int cnt, int max_len, int n16,
-                                                       int c4, PassPos &pp, int &bad) {
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        const int r = r0 + 16 * blk + n16;
-        int pc;
-        pp.k[blk] = keep_pos(r, tab_pos(t, r, pc), cnt, max_len, bad);
-    }
-    // The eight V ranks of a lane are consecutive: one piece -> consecutive rows.
-    const int rv = r0 + 8 * c4;
-    int pc0, pc7;
-    const int p0 = tab_pos(t, rv, pc0);
-    const int p7 = tab_pos(t, rv + 7, pc7);
-    if (pc0 == pc7 && rv + 7 < cnt && p0 >= 0 && p7 < max_len) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pp.v[i] = p0 + i;
-    } else {
-        int unused = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            int pc;
-            pp.v[i] = keep_pos(rv + i, tab_pos(t, rv + i, pc), cnt, max_len, unused);
-        }
-    }
-}
-
-// Index-list entries of the same ranks, loaded ahead of the pass that uses
-// them.  The buffer resource spans the row's count, so ranks past it read 0
-// without a memory access (and a resource of 0 bytes reads nothing at all).
-struct IdxRegs {
-    int32_t k[2];
-    int32_t v[8];
-};
-
-static __device__ __forceinline__ void load_idx(IdxRegs &I, __amdgpu_buffer_rsrc_t row, int r0, int n16, int c4) {
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-        I.k[blk] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(row, (uint32_t)(r0 + 16 * blk + n16) * 4u, 0, 0);
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        I.v[i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(row, (uint32_t)(r0 + 8 * c4 + i) * 4u, 0, 0);
-}
-
-static __device__ __forceinline__ void pass_pos_index(const IdxRegs &I, int r0, int cnt, int max_len, int n16,
-                                                      int c4, PassPos &pp, int &bad) {
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) pp.k[blk] = keep_pos(r0 + 16 * blk + n16, I.k[blk], cnt, max_len, bad);
-    int unused = 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) pp.v[i] = keep_pos(r0 + 8 * c4 + i, I.v[i], cnt, max_len, unused);
-}
-
 // The current token in ring storage: rows at position `cur` are read from
 // the K/V passed with the call instead of the cache, whose row `cur` this
 // launch overwrites (kRing only; otherwise cur is never compared).
@@ -505,31 +426,6 @@ struct NewRows {
     const uint16_t *k;
     const uint16_t *v;
 };
-
-template <bool kRing>
-static __device__ __forceinline__ const uint16_t *row_ptr(const uint16_t *base, int p, int64_t s_pos,
-                                                          const NewRows &nr, const uint16_t *fresh) {
-    const uint16_t *row = base + (int64_t)p * s_pos;
-    return kRing && p == nr.cur ? fresh : row;
-}
-
-// K and V fragments of one pass, all loads issued unconditionally.  Keeping
-// every load outside control flow lets the compiler's wait counting stay
-// exact across the software pipeline: the wait before a pass's compute
-// covers that pass's loads only, never the loads issued after them.
-template <bool kRing>
-static __device__ __forceinline__ void issue_kv(PassRegs &R, const uint16_t *kbase, const uint16_t *vbase,
-                                                int64_t s_pos, const PassPos &pp, int n16, int c4,
-                                                const NewRows &nr) {
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        const uint16_t *row = row_ptr<kRing>(kbase, pp.k[blk], s_pos, nr, nr.k) + 8 * c4;
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) R.kf[blk][kc] = load16(row + kc * 32);
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) R.vf[i] = load16(row_ptr<kRing>(vbase, pp.v[i], s_pos, nr, nr.v) + 8 * n16);
-}
 
 // Forces uniform values into scalar registers at this point: the scalar loads
 // they come from are then issued together, ahead of one wait, instead of
@@ -600,64 +496,6 @@ static __device__ __forceinline__ void softmax_step(const f32x4 (&s)[2], int val
         p_hi[wd] = hi;
         p_lo[wd] = pack_bf16(e0 - __builtin_bit_cast(float, hi << 16), e1 - __builtin_bit_cast(float, hi & 0xffff0000u));
     }
-}
-
-// One pass from registers: S^T = K Q^T, softmax update, O += P V.  `valid` =
-// number of valid ranks of the pass (1..32).
-template <bool kOnline>
-static __device__ __forceinline__ void compute_pass(PassRegs &R, const u32x4 (&qf)[4], int valid,
-                                                    float scale_log2, uint8_t *vt, WaveAcc &w, int n16, int c4) {
-    f32x4 s[2];
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        s[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < 4; ++kc) s[blk] = mfma16x16x32(R.kf[blk][kc], qf[kc], s[blk]);
-    }
-    const bool partial = valid < kWaveTile;
-    u32x4 p_hi, p_lo;
-    softmax_step<kOnline>(s, valid, scale_log2, w, c4, p_hi, p_lo);
-
-    // V rows of masked ranks were read from row 0: zero them so that 0 * V
-    // stays 0 whatever that row holds.
-    if (partial) {
-#pragma unroll
-        for (int t = 0; t < 8; ++t)
-            if (8 * c4 + t >= valid) R.vf[t] = u32x4{0, 0, 0, 0};
-    }
-
-    // V^T through LDS.  Lane (e = n16, octet c4) holds positions 8*c4 + t
-    // (t = 0..7) of head dims 8e .. 8e+7; one v_perm_b32 per output word
-    // gathers a head dim's values of two positions, then one 16-byte unit per
-    // head dim is stored (halves swapped for odd head dims).
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int wd = i >> 1;
-        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;  // high or low halves of both words
-        uint32_t o[4];
-#pragma unroll
-        for (int pp = 0; pp < 4; ++pp) o[pp] = __builtin_amdgcn_perm(R.vf[2 * pp + 1][wd], R.vf[2 * pp][wd], sel);
-        const u32x4 unit = (i & 1) ? u32x4{o[2], o[3], o[0], o[1]} : u32x4{o[0], o[1], o[2], o[3]};
-        *reinterpret_cast<u32x4 *>(vt + vt_unit(8 * n16 + i, c4) * 16) = unit;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    // O += P V for each block of 16 head dims.  B operand lane (dim n16, c4)
-    // needs positions 4*c4 .. +3 and 16 + 4*c4 .. +3 of head dim d.
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-        const int d = 16 * db + n16;
-        const int hsw = ((c4 & 1) ^ (d & 1)) * 8;
-        const u32x2 lo = *reinterpret_cast<const u32x2 *>(vt + vt_unit(d, c4 >> 1) * 16 + hsw);
-        const u32x2 hi = *reinterpret_cast<const u32x2 *>(vt + vt_unit(d, 2 + (c4 >> 1)) * 16 + hsw);
-        const u32x4 bv = u32x4{lo[0], lo[1], hi[0], hi[1]};
-        w.acc[db] = mfma16x16x32(p_hi, bv, w.acc[db]);
-        w.acc[db] = mfma16x16x32(p_lo, bv, w.acc[db]);
-    }
-    // The next pass overwrites this wave's tile only after these reads have
-    // returned (their results feed the MFMAs above).
 }
 
 // ---------------------------------------------------------------------------
@@ -924,6 +762,7 @@ static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t
 // index-list entries of ranks [r_lo, r_hi) (the splits of a sequence share
 // the list between them); the one with r_lo == 0 also writes the count, the
 // table and the errors.  Block-wide.
+template <int kThreads>
 static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b, int cnt, int policy_bad,
                                                       const int32_t (&rg)[2 * kPieces], int max_keep, int tid,
                                                       int r_lo, int r_hi) {
@@ -946,10 +785,10 @@ static __device__ __forceinline__ void write_retained(const AttnLaunch &a, int b
         for (int k = 0; k < kPieces; ++k) {
             const int n = rg[2 * k + 1] < max_keep - off ? rg[2 * k + 1] : max_keep - off;
             const int lo = off > r_lo ? off : r_lo, e = off + n < hi ? off + n : hi;
-            for (int r = lo + tid; r < e; r += kWavesPerWg * 64) row[r] = rg[2 * k] + (r - off);
+            for (int r = lo + tid; r < e; r += kThreads) row[r] = rg[2 * k] + (r - off);
             off += n;
         }
-        for (int r = (off > r_lo ? off : r_lo) + tid; r < hi; r += kWavesPerWg * 64) row[r] = -1;
+        for (int r = (off > r_lo ? off : r_lo) + tid; r < hi; r += kThreads) row[r] = -1;
     }
 }
 
@@ -983,21 +822,38 @@ static __device__ __forceinline__ void store_new_row(const AttnLaunch &a, const 
     *reinterpret_cast<u32x4 *>(dst) = c.x;
 }
 
+// Workgroup barrier that also ORs a per-thread flag over the workgroup: each
+// wavefront writes whether any of its lanes holds the flag into its own LDS
+// slot before the barrier.  (__syncthreads_or would load the block size from
+// the kernel arguments at this point: a scalar memory round trip in front of
+// the barrier.)
+template <int kWaves>
+static __device__ __forceinline__ int barrier_or(int flag, int *s_wave_flag, int wave, int lane) {
+    const int any = __ballot(flag != 0) != 0;
+    if (lane == 0) s_wave_flag[wave] = any;
+    __syncthreads();
+    int r = 0;
+#pragma unroll
+    for (int wv = 0; wv < kWaves; ++wv) r |= s_wave_flag[wv];
+    return r;
+}
+
 // Combine of a workgroup's four wavefronts.  Each wavefront publishes its
 // state -- (max, sum) per head and its unscaled O rows -- into LDS regions no
 // other wavefront touches before the workgroup barrier that follows; after
 // the barrier the threads writing the result rescale and add the four states
 // as they read them.  One barrier and no dependent LDS round trip between.
-struct __attribute__((aligned(16))) CombineLds {
-    float ml[kMaxGroup][kWavesPerWg][2];  // per head and wavefront: max (log2 units), sum
+template <int kWaves>
+struct __attribute__((aligned(16))) CombineLdsT {
+    float ml[kMaxGroup][kWaves][2];  // per head and wavefront: max (log2 units), sum
 };
+using CombineLds = CombineLdsT<kWavesPerWg>;
 constexpr int kOStride = kHeadDim + 4;                  // floats per published O row (padded: conflict-free stores)
 constexpr int kOWaveBytes = kMaxGroup * kOStride * 4;   // 8448: a wavefront's published rows
-static_assert(kOWaveBytes >= kVtBytesPerWave && kOWaveBytes % 16 == 0,
-              "a wavefront's LDS slot holds its V tile, then its published rows");
 
-static __device__ __forceinline__ void publish_wave(const WaveAcc &w, float *o_w, CombineLds &cl, int wave, int n16,
-                                                    int c4) {
+template <int kWaves>
+static __device__ __forceinline__ void publish_wave(const WaveAcc &w, float *o_w, CombineLdsT<kWaves> &cl, int wave,
+                                                    int n16, int c4) {
     if (c4 == 0) {
         cl.ml[n16][wave][0] = w.m_run;
         cl.ml[n16][wave][1] = w.l_run;
@@ -1011,17 +867,25 @@ static __device__ __forceinline__ void publish_wave(const WaveAcc &w, float *o_w
 // The workgroup's state of head h, head dims d0 .. d0+3, from the published
 // states: M = max over the wavefronts, L and O rescaled to M.  wave_stride:
 // floats between consecutive wavefronts' regions.
-static __device__ __forceinline__ void gather_head(const float *o_lds, int wave_stride, const CombineLds &cl, int h,
-                                                   int d0, float &M, float &L, f32x4 &O) {
-    const f32x4 a01 = *reinterpret_cast<const f32x4 *>(&cl.ml[h][0][0]);
-    const f32x4 a23 = *reinterpret_cast<const f32x4 *>(&cl.ml[h][2][0]);
-    const float m[kWavesPerWg] = {a01[0], a01[2], a23[0], a23[2]};
-    const float l[kWavesPerWg] = {a01[1], a01[3], a23[1], a23[3]};
-    M = fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3]));
+template <int kWaves>
+static __device__ __forceinline__ void gather_head(const float *o_lds, int wave_stride, const CombineLdsT<kWaves> &cl,
+                                                   int h, int d0, float &M, float &L, f32x4 &O) {
+    float m[kWaves], l[kWaves];
+#pragma unroll
+    for (int p = 0; p < kWaves / 2; ++p) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(&cl.ml[h][2 * p][0]);
+        m[2 * p] = v[0];
+        l[2 * p] = v[1];
+        m[2 * p + 1] = v[2];
+        l[2 * p + 1] = v[3];
+    }
+    M = m[0];
+#pragma unroll
+    for (int wv = 1; wv < kWaves; ++wv) M = fmaxf(M, m[wv]);
     L = 0.f;
     O = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int wv = 0; wv < kWavesPerWg; ++wv) {
+    for (int wv = 0; wv < kWaves; ++wv) {
         const float f = m[wv] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[wv] - M);
         L += l[wv] * f;
         O += f * *reinterpret_cast<const f32x4 *>(&o_lds[wv * wave_stride + h * kOStride + d0]);
@@ -1043,10 +907,11 @@ static __device__ __forceinline__ void store_output(const AttnLaunch &a, int64_t
 // Writes the workgroup's combined result: the output itself when it covered
 // the whole (layer, sequence, KV head), else a partial in slot `slot`.  bad:
 // the sum becomes NaN (and so do the outputs).
+template <int kWaves>
 static __device__ __forceinline__ void write_result(const AttnLaunch &a, const float *o_lds, int wave_stride,
-                                                    const CombineLds &cl, bool bad, int G, int tid, int64_t row0,
-                                                    bool whole, uint32_t slot) {
-    for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
+                                                    const CombineLdsT<kWaves> &cl, bool bad, int G, int tid,
+                                                    int64_t row0, bool whole, uint32_t slot) {
+    for (int c = tid; c < G * (kHeadDim / 4); c += kWaves * 64) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
         float mx, L;
         f32x4 O;
@@ -1073,9 +938,9 @@ static __device__ __forceinline__ bool take_ticket(const AttnLaunch &a, int grp,
     wait_vmem();
     __syncthreads();
     if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&a.ticket[grp], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int prev = __hip_atomic_fetch_add(&a.ticket[grp * kTicketStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = prev == n - 1;
-        if (s_last) __hip_atomic_store(&a.ticket[grp], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (s_last) __hip_atomic_store(&a.ticket[grp * kTicketStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
     return s_last != 0;
@@ -1092,12 +957,11 @@ static __device__ __forceinline__ bool take_ticket(const AttnLaunch &a, int grp,
 // loads in flight while the current one is accumulated (loads past the last
 // partial re-read it with a zero weight, so every load is unconditional).
 // s_ml: LDS scratch of n * G * 2 floats, free by the time the merge runs.
-template <typename SlotOf>
+template <int kThreads, typename SlotOf>
 static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
                                                int64_t row0, float *s_ml) {
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-    constexpr int kThreads = kWavesPerWg * 64;
     for (int e = tid; e < n * G; e += kThreads) {
         const int i = e / G, h = e - i * G;
         const uint32_t prow = slot_of(i) * G + h;
@@ -1146,12 +1010,12 @@ static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, Sl
 // select drops it.
 constexpr uint32_t kNoPartial = 0x80000000u;  // a byte offset past both partial arrays (each < 2^31 bytes)
 
-template <typename SlotOf>
+template <int kThreads, typename SlotOf>
 static __device__ __forceinline__ void merge_one_batch(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
                                                        int64_t row0) {
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-    for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
+    for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
         float mm[kMergeBatch], ll[kMergeBatch];
         f32x4 oo[kMergeBatch];
@@ -1177,20 +1041,20 @@ static __device__ __forceinline__ void merge_one_batch(const AttnLaunch &a, int 
     }
 }
 
-template <typename SlotOf>
+template <int kThreads, typename SlotOf>
 static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
                                                       int64_t row0, float *s_ml) {
     if (n > 2 * kMergeBatch) {
-        merge_many(a, n, slot_of, G, tid, row0, s_ml);
+        merge_many<kThreads>(a, n, slot_of, G, tid, row0, s_ml);
         return;
     }
     if (n <= kMergeBatch) {
-        merge_one_batch(a, n, slot_of, G, tid, row0);
+        merge_one_batch<kThreads>(a, n, slot_of, G, tid, row0);
         return;
     }
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-    for (int c = tid; c < G * (kHeadDim / 4); c += kWavesPerWg * 64) {
+    for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
         float M = kNegInf, L = 0.f;
         f32x4 O = {0.f, 0.f, 0.f, 0.f};
@@ -1224,126 +1088,6 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
 }
 
 // ---------------------------------------------------------------------------
-// decode_attn, split schedule, splits of up to kPasses workgroup passes (128
-// retained positions each): one workgroup per (split, layer and KV head,
-// sequence); wavefront w takes the passes of 32 positions at w*32 and, with
-// two passes, w*32 + 128, all their loads issued up front into registers, so
-// the compute unit's whole share is in flight at once.  kSrc: where the
-// retained set comes from.  The last workgroup of each group merges the
-// splits.  The leading scalar arguments are the ones the first memory
-// accesses need; the build preloads them into SGPRs so no kernel-argument load
-// precedes the range-table load.
-// ---------------------------------------------------------------------------
-template <int kSrc, int kPasses>
-__global__ __launch_bounds__(256) void decode_attn_kernel(const int32_t *__restrict__ src0,
-                                                          const int32_t *__restrict__ src1,
-                                                          const int32_t *__restrict__ idx,
-                                                          const uint16_t *__restrict__ q, int32_t max_keep,
-                                                          int32_t B, int32_t pol_per_seq, int32_t Hkv, int32_t G,
-                                                          const AttnLaunch a) {
-    __shared__ __attribute__((aligned(16))) uint8_t smem[kWavesPerWg * kOWaveBytes];  // V tiles, then O rows
-    static_assert(kMaxMergeSplits * kMaxGroup * 2 * 4 <= sizeof(smem), "merge scratch fits the tile LDS");
-    __shared__ CombineLds cl;
-    __shared__ int s_last;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int n16 = lane & 15;
-    const int c4 = lane >> 4;
-
-    // Grid: x = split, y = layer * Hkv + KV head, z = sequence.  The
-    // sequence's retained-set description is loaded first: the first K/V loads
-    // wait for it and for nothing else.
-    const int split = blockIdx.x;
-    const int b = blockIdx.z;
-    int32_t rg[2 * kPieces];
-    int policy_bad = 0;
-    int32_t cur_row = -1;  // ring storage: the current token's row
-    const int layer = (int)blockIdx.y / Hkv;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
-    const int g = (int)blockIdx.y - layer * Hkv;
-    const int lb = layer * B + b;
-    const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
-    const int Hq = Hkv * G;
-    const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
-    const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
-    const int r_begin = split * a.split_len;
-    const int r_end = min(r_begin + a.split_len, cnt);
-
-    RangeTab tab;
-    __amdgpu_buffer_rsrc_t irow;
-    if (kSrc != kSrcIndex) tab = make_tab(rg);
-    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)max_keep * 4u);  // ranks past the count are masked
-
-    const int64_t row0 = (int64_t)lb * Hq + g * G;  // first output row of the group
-    u32x4 qf[4];
-    load_q(qf, q, row0, G, n16, c4);
-    const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
-    const uint16_t *kbase = a.k + kv_off;
-    const uint16_t *vbase = a.v + kv_off;
-    constexpr bool kRing = kSrc == kSrcRing;
-    NewRows nr{cur_row, nullptr, nullptr};
-    if (kRing) {
-        nr.k = a.k_new + (int64_t)grp * kHeadDim;
-        nr.v = a.v_new + (int64_t)grp * kHeadDim;
-    }
-    uint8_t *vt = smem + wave * kOWaveBytes;  // this wavefront's V tile, later its O rows
-
-    WaveAcc w;
-    wave_acc_reset(w);
-    int r = r_begin + wave * kWaveTile;
-    materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
-    if (kRing) materialize(nr.k, nr.v, nr.cur);
-    NewRowCopy app{};
-    if (kRing) app = load_new_row(a, nr, policy_bad, lane, split == 0 && wave == 0);
-    if (kSrc != kSrcIndex)
-        materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
-                    tab.off[3], tab.off[4], tab.off[5]);
-    // Ranks past the split's end load row 0 (the same row in every lane).
-    auto positions = [&](const IdxRegs &I, int r0, PassPos &pp) {
-        if (kSrc != kSrcIndex) pass_pos_ranges(tab, r0, r_end, a.max_len, n16, c4, pp, w.bad_pos);
-        else pass_pos_index(I, r0, r_end, a.max_len, n16, c4, pp, w.bad_pos);
-    };
-    if (r < r_end) {
-        PassRegs R[kPasses];
-        IdxRegs I[kPasses];
-        PassPos pp;
-        if (kSrc == kSrcIndex)
-#pragma unroll
-            for (int p = 0; p < kPasses; ++p) load_idx(I[p], irow, r + p * kSplitUnit, n16, c4);
-#pragma unroll
-        for (int p = 0; p < kPasses; ++p) {
-            positions(I[p], r + p * kSplitUnit, pp);
-            issue_kv<kRing>(R[p], kbase, vbase, a.s_pos, pp, n16, c4, nr);
-        }
-        compute_pass<false>(R[0], qf, min(kWaveTile, r_end - r), a.scale_log2, vt, w, n16, c4);
-        if (kPasses > 1 && r + kSplitUnit < r_end)
-            compute_pass<true>(R[kPasses - 1], qf, min(kWaveTile, r_end - r - kSplitUnit), a.scale_log2, vt, w, n16,
-                               c4);
-    }
-
-    if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
-    float *o_lds = reinterpret_cast<float *>(smem);  // each wavefront's O rows over its own V tile
-    publish_wave(w, o_lds + wave * (kOWaveBytes / 4), cl, wave, n16, c4);
-    const int wg_bad_pos = __syncthreads_or(w.bad_pos);
-    const bool bad = wg_bad_pos || bad_count;
-    write_result(a, o_lds, kOWaveBytes / 4, cl, bad, G, tid, row0, a.n_split == 1,
-                 (uint32_t)grp * a.n_split + split);
-    if ((kSrc == kSrcLayout || kRing) && g == 0 &&
-        (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
-        write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
-                       max_keep, tid, r_begin, r_begin + a.split_len);
-    if (bad && tid == 0)
-        raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
-    if (a.n_split == 1) return;
-    if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
-    const uint32_t pbase = (uint32_t)grp * a.n_split;
-    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0,
-                   reinterpret_cast<float *>(smem));
-}
-
-// ---------------------------------------------------------------------------
 // decode_attn, split schedule with LDS-staged passes, for splits of more than
 // two workgroup passes: grid and split layout as decode_attn_kernel.  With
 // kStages = 2 each wavefront double-buffers its passes in two LDS stages (K
@@ -1366,6 +1110,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     __shared__ __attribute__((aligned(16))) uint8_t idx_ring[kSrc != kSrcIndex ? 1 : kWavesPerWg][2][kIdxSlotBytes];
     __shared__ CombineLds cl;
     __shared__ int s_last;
+    __shared__ int s_wave_flag[kWavesPerWg];
     static_assert(kMaxMergeSplits * kMaxGroup * 2 * 4 <= sizeof(stages) && kOWaveBytes <= kStages * kStageBytes,
                   "merge scratch and published rows fit the stages");
 
@@ -1482,21 +1227,300 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     float *o_lds = reinterpret_cast<float *>(&stages[0][0][0]);  // each wavefront's O rows in its own stages
     constexpr int kStageWaveFloats = kStages * kStageBytes / 4;
     publish_wave(w, o_lds + wave * kStageWaveFloats, cl, wave, n16, c4);
-    const int wg_bad_pos = __syncthreads_or(w.bad_pos);
+    const int wg_bad_pos = barrier_or<kWavesPerWg>(w.bad_pos, s_wave_flag, wave, lane);
     const bool bad = wg_bad_pos || bad_count;
     write_result(a, o_lds, kStageWaveFloats, cl, bad, G, tid, row0, a.n_split == 1,
                  (uint32_t)grp * a.n_split + split);
     if ((kSrc == kSrcLayout || kRing) && g == 0 &&
         (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
-        write_retained(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq, policy_bad, rg,
+        write_retained<kWavesPerWg * 64>(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq,
+                                         policy_bad, rg,
                        max_keep, tid, r_begin, r_begin + a.split_len);
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
     if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
     const uint32_t pbase = (uint32_t)grp * a.n_split;
-    merge_partials(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0,
+    merge_partials<kWavesPerWg * 64>(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0,
                    reinterpret_cast<float *>(&stages[0][0][0]));
+}
+
+// ---------------------------------------------------------------------------
+// decode_attn, wide schedule: workgroups of kWideWaves wavefronts in a 1-D
+// grid, one (layer, sequence, KV head) split each (WideSched decodes which),
+// and every wavefront exactly one pass of 32 retained positions: it issues
+// the direct-to-LDS loads of its K and V rows into its own 16 KiB stage and its
+// query rows into registers, waits for them and computes.  A wavefront thus
+// never stalls on issuing a later pass's loads before computing an earlier
+// one, needs no online rescale (its state is one pass), and the workgroup's
+// eight states are combined through LDS.  Splits hold at most 256 positions;
+// the schedule spreads the groups' splits over one dispatch round with as
+// equal shares as the group count allows.  Split partials sit in the slot of
+// the workgroup's index; the last workgroup of a group merges them.
+// ---------------------------------------------------------------------------
+constexpr int kWideThreads = kWideWaves * 64;
+
+// The workgroup's state of head h, head dims d0 .. d0+3, from the eight
+// published wavefront states (as gather_head, with every LDS read issued
+// before the first is used).
+static __device__ __forceinline__ void gather_wide(const float *o_lds, int wave_stride,
+                                                   const CombineLdsT<kWideWaves> &cl, int h, int d0, float &M, float &L,
+                                                   f32x4 &O) {
+    f32x4 ml[kWideWaves / 2], o[kWideWaves];
+#pragma unroll
+    for (int p = 0; p < kWideWaves / 2; ++p) ml[p] = *reinterpret_cast<const f32x4 *>(&cl.ml[h][2 * p][0]);
+#pragma unroll
+    for (int wv = 0; wv < kWideWaves; ++wv)
+        o[wv] = *reinterpret_cast<const f32x4 *>(&o_lds[wv * wave_stride + h * kOStride + d0]);
+    M = kNegInf;
+#pragma unroll
+    for (int p = 0; p < kWideWaves / 2; ++p) M = fmaxf(M, fmaxf(ml[p][0], ml[p][2]));
+    L = 0.f;
+    O = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int wv = 0; wv < kWideWaves; ++wv) {
+        const float m = ml[wv / 2][(wv & 1) * 2], l = ml[wv / 2][(wv & 1) * 2 + 1];
+        const float f = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - M);
+        L += l * f;
+        O += f * o[wv];
+    }
+}
+
+// Log-sum-exp merge of the n partials of a group (slots slot0 .. slot0+n-1),
+// head h, head dims d0 .. d0+3, by one thread of a wavefront whose two halves
+// hold two heads (32 threads each).  The (max, sum) pairs come in chunks of 32
+// slots with one load per chunk: lane j loads the pair of slot j of its half's
+// head, and the others take them by lane shuffle.  The O values of all slots
+// share one vector offset; each load adds its slot's distance as a scalar
+// offset (inside the partial arrays: the slots are the group's own).  A load
+// past the last slot takes a vector offset outside the buffer instead (the
+// hardware's range check covers the vector offset, not the scalar one) and
+// scalar offset 0, which the hardware answers with zero without a memory
+// access.  Batches of kMergeBatch slots, the next batch's loads in flight
+// while the current one is folded in.  Few load instructions matter: the
+// compute unit's address unit takes them one by one for all wavefronts.
+static __device__ __forceinline__ void merge_o_load(f32x4 (&o)[kMergeBatch], __amdgpu_buffer_rsrc_t ro, uint32_t vo,
+                                                    uint32_t so, int base, int n) {
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) {
+        const bool in = base + k < n;
+        o[k] = load_coherent4_s(ro, in ? vo : kNoPartial, in ? (uint32_t)(base + k) * so : 0u);
+    }
+}
+
+// Folds slots base .. base+kMergeBatch-1 into (M, L, O); pair j of the current
+// chunk of pairs (pm, pl) sits in lane (lane & 32) + j, for j = base - cb + k.
+static __device__ __forceinline__ void merge_fold(const f32x4 (&o)[kMergeBatch], float pm, float pl, int cb,
+                                                  int base, int n, int lane, float &M, float &L, f32x4 &O) {
+    float m[kMergeBatch], l[kMergeBatch];
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) {
+        const int src = (lane & 32) + ((base - cb + k) & 31);
+        m[k] = __shfl(pm, src);
+        l[k] = __shfl(pl, src);
+    }
+    float mx = M;
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) mx = base + k < n ? fmaxf(mx, m[k]) : mx;
+    const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - mx);
+    L *= sc;
+    O *= sc;
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) {
+        const float f = (base + k >= n || m[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m[k] - mx);
+        L += l[k] * f;
+        O += o[k] * f;
+    }
+    M = mx;
+}
+
+static_assert(32 % kMergeBatch == 0, "a batch of slots lies in one chunk of pairs");
+
+static __device__ __forceinline__ void merge_wide(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
+                                                  __amdgpu_buffer_rsrc_t rml, int n, uint32_t slot0, int G, int h,
+                                                  int d0, int lane, int64_t row0) {
+    const uint32_t vo = ((slot0 * (uint32_t)G + (uint32_t)h) * kHeadDim + d0) * 4;
+    const uint32_t so = (uint32_t)G * kHeadDim * 4;  // bytes from one slot's rows to the next
+    float M = kNegInf, L = 0.f;
+    f32x4 O = {0.f, 0.f, 0.f, 0.f};
+    f32x4 b0[kMergeBatch], b1[kMergeBatch];
+    for (int cb = 0; cb < n; cb += 32) {
+        const int j = cb + (lane & 31);
+        const uint32_t vml = ((slot0 + (uint32_t)j) * (uint32_t)G + (uint32_t)h) * 8;
+        const float pm = load_coherent1(rml, j < n ? vml : kNoPartial);
+        const float pl = load_coherent1(rml, j < n ? vml + 4 : kNoPartial);
+        const int ce = min(cb + 32, n);
+        merge_o_load(b0, ro, vo, so, cb, n);
+        for (int base = cb; base < ce; base += 2 * kMergeBatch) {
+            if (base + kMergeBatch < ce) merge_o_load(b1, ro, vo, so, base + kMergeBatch, n);
+            merge_fold(b0, pm, pl, cb, base, n, lane, M, L, O);
+            if (base + kMergeBatch >= ce) break;
+            if (base + 2 * kMergeBatch < ce) merge_o_load(b0, ro, vo, so, base + 2 * kMergeBatch, n);
+            merge_fold(b1, pm, pl, cb, base + kMergeBatch, n, lane, M, L, O);
+        }
+    }
+    store_output(a, row0 + h, d0, O, M, L);
+}
+
+// x / d for x < 2^16 from magic = ceil(2^32 / d); magic 0 stands for d = 1
+// (whose ceil(2^32 / d) does not fit in 32 bits).
+static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) { return magic ? __umulhi(x, magic) : x; }
+
+// The WideSched fields are separate scalar arguments (with the pointers, the
+// first 16 dwords, which the build preloads into SGPRs; a struct argument
+// would be loaded from memory first).
+template <int kSrc>
+__global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
+    const int32_t *__restrict__ src0, const int32_t *__restrict__ src1, uint32_t groups_hi, uint32_t n_split,
+    uint32_t magic_hi, uint32_t magic_lo, uint32_t len_hi_lo, uint32_t hkv_b, uint32_t magic_hkv, uint32_t magic_b,
+    const int32_t *__restrict__ idx, int32_t max_keep, int32_t pol_per_seq, const uint16_t *__restrict__ q,
+    const AttnLaunch a) {
+    const WideSched ws{groups_hi, n_split, magic_hi, magic_lo, len_hi_lo, hkv_b, magic_hkv, magic_b};
+    __shared__ __attribute__((aligned(16))) uint8_t stages[kWideWaves][kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t idx_slot[kSrc != kSrcIndex ? 1 : kWideWaves][kIdxSlotBytes];
+    __shared__ CombineLdsT<kWideWaves> cl;
+    __shared__ int s_last;
+    __shared__ int s_wave_flag[kWideWaves];
+    static_assert(kMaxMergeSplits * kMaxGroup * 2 * 4 <= sizeof(stages) && kMaxGroup * kOStride * 4 <= kStageBytes,
+                  "merge scratch and published rows fit the stages");
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int n16 = lane & 15;
+    const int c4 = lane >> 4;
+
+    // Which split of which group: scalar arithmetic on preloaded arguments,
+    // so the retained-set description is the first memory access.
+    const uint32_t wg = blockIdx.x;
+    const uint32_t n_hi = ws.n_split & 0xffffu, n_lo = ws.n_split >> 16;
+    const uint32_t hi_wg = ws.groups_hi * n_hi;
+    uint32_t grp, split, n, len, slot0;
+    if (wg < hi_wg) {
+        grp = div16(wg, ws.magic_hi);
+        split = wg - grp * n_hi;
+        n = n_hi;
+        len = ws.len & 0xffffu;
+        slot0 = grp * n_hi;
+    } else {
+        const uint32_t w2 = wg - hi_wg;
+        const uint32_t gl = div16(w2, ws.magic_lo);
+        split = w2 - gl * n_lo;
+        grp = ws.groups_hi + gl;
+        n = n_lo;
+        len = ws.len >> 16;
+        slot0 = hi_wg + gl * n_lo;
+    }
+    const int Hkv = (int)(ws.hkv_b & 0xffffu), B = (int)(ws.hkv_b >> 16);
+    const uint32_t lb = div16(grp, ws.magic_hkv);
+    const int g = (int)(grp - lb * (uint32_t)Hkv);
+    const int layer = (int)div16(lb, ws.magic_b);
+    const int b = (int)lb - layer * B;
+    int32_t rg[2 * kPieces];
+    int policy_bad = 0;
+    int32_t cur_row = -1;  // ring storage: the current token's row
+    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
+    const int G = a.G;
+    const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
+    const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
+    const int r_begin = (int)(split * len);
+    const int r_end = min(r_begin + (int)len, cnt);
+
+    RangeTab tab;
+    __amdgpu_buffer_rsrc_t irow;
+    if (kSrc != kSrcIndex) tab = make_tab(rg);
+    else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)max_keep * 4u);  // ranks past the count are masked
+
+    const int64_t row0 = (int64_t)lb * (Hkv * G) + g * G;  // first output row of the group
+    const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
+    const uint16_t *kbase = a.k + kv_off;
+    const uint16_t *vbase = a.v + kv_off;
+    constexpr bool kRing = kSrc == kSrcRing;
+    NewRows nr{cur_row, nullptr, nullptr};
+    if (kRing) {
+        nr.k = a.k_new + (int64_t)grp * kHeadDim;
+        nr.v = a.v_new + (int64_t)grp * kHeadDim;
+    }
+    uint8_t *stage = &stages[wave][0];
+
+    WaveAcc w;
+    wave_acc_reset(w);
+    const int r0 = r_begin + wave * kWaveTile;
+    materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
+    if (kRing) materialize(nr.k, nr.v, nr.cur);
+    NewRowCopy app{};
+    if (kRing) app = load_new_row(a, nr, policy_bad, lane, split == 0 && wave == 0);
+    if (kSrc != kSrcIndex)
+        materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
+                    tab.off[3], tab.off[4], tab.off[5]);
+    if (r0 < r_end) {
+        int32_t pos[8];
+        if (kSrc != kSrcIndex) {
+            dma_pos_ranges(tab, r0, r_end, a.max_len, c4, pos, w.bad_pos);
+        } else {
+            dma_idx(&idx_slot[wave][0], irow, r0, lane);
+            wait_vm<0>();
+            dma_pos_index(&idx_slot[wave][0], r0, r_end, a.max_len, c4, pos, w.bad_pos);
+        }
+        u32x4 qf[4];
+        load_q(qf, q, row0, G, n16, c4);
+        dma_pass(stage, kbase, vbase, a.s_pos, pos, lane, kRing, nr);
+        wait_vm<0>();
+        compute_pass_lds<false>(stage, qf, min(kWaveTile, r_end - r0), a.scale_log2, w, n16, c4);
+    }
+
+    if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
+    float *o_lds = reinterpret_cast<float *>(&stages[0][0]);  // each wavefront's O rows in its own stage
+    constexpr int kStageFloats = kStageBytes / 4;
+    publish_wave(w, o_lds + wave * kStageFloats, cl, wave, n16, c4);
+    const int wg_bad_pos = barrier_or<kWideWaves>(w.bad_pos, s_wave_flag, wave, lane);
+    const bool bad = wg_bad_pos || bad_count;
+    // The workgroup's state of head h, head dims d0 .. d0+3, per writer thread:
+    // the output itself for a group of one split, else the partial in slot wg.
+    const bool writer = tid < G * (kHeadDim / 4);
+    const int h = tid >> 5, d0 = (tid & 31) * 4;
+    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+    if (writer) {
+        float M, L;
+        f32x4 O;
+        gather_wide(o_lds, kStageFloats, cl, h, d0, M, L, O);
+        if (bad) L = __builtin_nanf("");
+        if (n == 1) {
+            store_output(a, row0 + h, d0, O, M, L);
+        } else {
+            const uint32_t prow = wg * (uint32_t)G + (uint32_t)h;
+            store_coherent4(ro, (prow * kHeadDim + d0) * 4, O);
+            if (d0 == 0) {
+                store_coherent1(rml, prow * 8, M);
+                store_coherent1(rml, prow * 8 + 4, L);
+            }
+        }
+    }
+    if ((kSrc == kSrcLayout || kRing) && g == 0 &&
+        (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
+        write_retained<kWideThreads>(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq,
+                                     policy_bad, rg, max_keep, tid, r_begin,
+                                     split == n - 1 ? max_keep : r_begin + (int)len);
+    if (bad && tid == 0)
+        raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
+    if (n == 1) return;
+    // Tickets: every writer wavefront takes one once its own partial stores
+    // have completed; the group is complete when all n * writer_waves are
+    // taken, and the workgroup whose wavefront took the last one merges.
+    const int writer_waves = (G * (kHeadDim / 4) + 63) / 64;
+    const int total = (int)n * writer_waves;
+    int last = 0;
+    if (wave < writer_waves) {
+        wait_vmem();
+        if (lane == 0) {
+            const int prev = __hip_atomic_fetch_add(&a.ticket[grp * kTicketStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            last = prev == total - 1;
+            if (last) __hip_atomic_store(&a.ticket[grp * kTicketStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    if (!barrier_or<kWideWaves>(last, s_wave_flag, wave, lane)) return;
+    if (writer) merge_wide(a, ro, rml, (int)n, slot0, G, h, d0, lane, row0);
 }
 
 // Read-only streaming probe (measurement): workgroup w reads the 16-byte
@@ -1540,22 +1564,23 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
 
 template <int kSrc>
 static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
+    if (a.wide_wg > 0) {
+        const WideSched &w = a.sched;
+        hipLaunchKernelGGL(decode_attn_wide_kernel<kSrc>, dim3((unsigned)a.wide_wg), dim3(kWideThreads), 0, stream,
+                           a.src0, a.src1, w.groups_hi, w.n_split, w.magic_hi, w.magic_lo, w.len, w.hkv_b, w.magic_hkv,
+                           w.magic_b, a.idx, a.max_keep, a.pol_per_seq, a.q, a);
+        return;
+    }
     const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
-    // Splits of up to two passes run from registers; longer splits stage their
-    // passes in LDS, double-buffered within one dispatch round, else one stage
-    // per wavefront and two workgroups per compute unit.
+    // Longer splits stage their passes in LDS, double-buffered within one
+    // dispatch round, else one stage per wavefront and two workgroups per
+    // compute unit.
     const bool one_round = (int64_t)a.n_split * a.NL * a.Hkv * a.B <= kRoundWorkgroups;
-    if (a.split_len > 2 * kSplitUnit && one_round)
+    if (one_round)
         hipLaunchKernelGGL((decode_attn_lds_kernel<kSrc, 2>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
                            a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
-    else if (a.split_len > 2 * kSplitUnit)
-        hipLaunchKernelGGL((decode_attn_lds_kernel<kSrc, 1>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
-                           a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
-    else if (a.split_len > kSplitUnit)
-        hipLaunchKernelGGL((decode_attn_kernel<kSrc, 2>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
-                           a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
     else
-        hipLaunchKernelGGL((decode_attn_kernel<kSrc, 1>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
+        hipLaunchKernelGGL((decode_attn_lds_kernel<kSrc, 1>), grid, dim3(kWavesPerWg * 64), 0, stream, a.src0, a.src1,
                            a.idx, a.q, a.max_keep, a.B, a.pol_per_seq, a.Hkv, a.G, a);
 }
 

@@ -139,8 +139,8 @@ _cache = {}
 
 
 def tickets_clear(ws, ws_bytes):
-    """The ticket region at the start of the workspace (4 bytes per KiB, rounded up to 256) is all zero."""
-    region = (4 * -(-ws_bytes // 1024) + 255) // 256 * 256
+    """The ticket region at the start of the workspace (128 bytes per KiB, rounded up to 256) is all zero."""
+    region = (128 * -(-ws_bytes // 1024) + 255) // 256 * 256
     return int(torch.count_nonzero(ws[: region // 4]).item()) == 0
 
 
