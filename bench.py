@@ -84,16 +84,27 @@ def committed_traffic(config: str) -> float | None:
 
 
 def summarize_trace(directory: str, top: int = 8) -> str:
-    """Markdown table of a rocprofv3 --kernel-trace --stats run (its *kernel_stats.csv)."""
+    """Markdown tables of a rocprofv3 --kernel-trace --stats run: its *kernel_stats.csv, then the median
+    and p90 of each kernel's dispatch durations from its *kernel_trace.csv."""
     import csv
     import glob
     path = sorted(glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True))[0]
     rows = list(csv.DictReader(open(path)))
+    short = lambda n: n if len(n) <= 72 else n[:69] + "..."
     out = ["| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns | Std dev |", "|---|---|---|---|---|---|---|---|"]
     for r in rows[:top]:
-        name = r["Name"] if len(r["Name"]) <= 72 else r["Name"][:69] + "..."
-        out.append(f"| {name} | {r['Calls']} | {r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | {r['Percentage']} | "
-                   f"{r['MinNs']} | {r['MaxNs']} | {float(r['StdDev']):.0f} |")
+        out.append(f"| {short(r['Name'])} | {r['Calls']} | {r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | "
+                   f"{r['Percentage']} | {r['MinNs']} | {r['MaxNs']} | {float(r['StdDev']):.0f} |")
+    traces = sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True))
+    if traces:
+        dur: dict[str, list[int]] = {}
+        for r in csv.DictReader(open(traces[0])):
+            dur.setdefault(r["Kernel_Name"], []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        out += ["", "| Kernel | Dispatches | Mean ns | Median ns | p90 ns |", "|---|---|---|---|---|"]
+        for r in rows[:top]:
+            d = np.array(dur.get(r["Name"], [0]), dtype=np.float64)
+            out.append(f"| {short(r['Name'])} | {len(d)} | {d.mean():.0f} | {np.median(d):.0f} | "
+                       f"{np.percentile(d, 90):.0f} |")
     return "\n".join(out)
 
 
@@ -168,29 +179,82 @@ def cpu_baseline(wl, budget_s: float, threads: int) -> dict:
                       f"{wl.hq} heads), retained set + fp64 attention, {threads} threads, {dt:.1f} s wall"}
 
 
-def read_ceiling(nbytes: int, steps: int, capture, time_graph, workgroups: int = 256) -> dict:
-    """The practical read ceiling: murmur_read_probe (a plain read-only streaming kernel, one workgroup
-    per compute unit) over the same byte count as one attention launch, each launch of a replayed graph
-    reading the next of enough regions to defeat the Infinity Cache; and over 1 GiB."""
+PROBE_WORKGROUPS = (256, 512, 1024, 2048, 4096)
+PROBE_THREADS = (256, 512, 1024)
+PROBE_DEPTHS = (2, 4, 8, 16)
+
+
+def probe_configs() -> list[tuple[str, int, int, int]]:
+    """(load type, workgroups, threads, loads in flight per thread) of the read-ceiling sweep; the
+    direct-to-LDS probe is limited to 64 KiB of LDS per workgroup."""
+    out = []
+    for mode in ("registers", "lds"):
+        for wg in PROBE_WORKGROUPS:
+            for t in PROBE_THREADS:
+                for d in PROBE_DEPTHS:
+                    if mode == "lds" and (t // 64) * d > 64:
+                        continue
+                    out.append((mode, wg, t, d))
+    return out
+
+
+def read_sweep(nbytes: int, steps: int, capture, time_graph, configs=None) -> list[dict]:
+    """murmur_read_probe (a plain read-only streaming kernel) over every configuration of the sweep:
+    per configuration, a replayed graph of `steps` launches over nbytes each, every launch reading the
+    next of enough regions to defeat the 256 MB Infinity Cache; and a graph of 8 launches over 1 GiB
+    (two alternating regions)."""
     import torch
     from paper_2606_01483_amd import murmur as M
     nbytes = max(16, nbytes // 16 * 16)
     regions = max(2, math.ceil(2.2 * MALL_BYTES / nbytes))
+    configs = configs or probe_configs()
+    sink = torch.zeros(max(PROBE_WORKGROUPS), dtype=torch.int32, device="cuda")
+    modes = {"registers": M.MURMUR_PROBE_REGISTERS, "lds": M.MURMUR_PROBE_LDS}
+    log(f"read-ceiling sweep: {len(configs)} configurations, {nbytes / 1e6:.1f} MB x {regions} regions and 1 GiB")
+    out = []
     buf = torch.empty(regions * nbytes, dtype=torch.uint8, device="cuda")
-    sink = torch.zeros(workgroups, dtype=torch.int32, device="cuda")
-    log(f"read ceiling: {nbytes / 1e6:.1f} MB x {regions} regions")
-    graph = capture(lambda: [M.murmur_read_probe(buf[(i % regions) * nbytes:], nbytes, workgroups, sink)
-                             for i in range(steps)])
-    us = time_graph(graph) / steps
-    del graph, buf
+    for mode, wg, t, d in configs:
+        graph = capture(lambda: [M.murmur_read_probe(buf[(i % regions) * nbytes:], nbytes, wg, sink, t, d, modes[mode])
+                                 for i in range(steps)])
+        us = time_graph(graph) / steps
+        out.append({"mode": mode, "workgroups": wg, "threads": t, "depth": d, "bytes": nbytes, "us": round(us, 3),
+                    "GBps": round(nbytes / us / 1e3, 1)})
+        del graph
+    del buf
     gib = 1 << 30
     big = torch.empty(2 * gib, dtype=torch.uint8, device="cuda")
-    graph = capture(lambda: [M.murmur_read_probe(big[(i % 2) * gib:], gib, workgroups, sink) for i in range(8)])
-    us_gib = time_graph(graph) / 8
-    del graph, big
+    for r, (mode, wg, t, d) in zip(out, configs):
+        graph = capture(lambda: [M.murmur_read_probe(big[(i % 2) * gib:], gib, wg, sink, t, d, modes[mode])
+                                 for i in range(8)])
+        us = time_graph(graph) / 8
+        r["us_1GiB"], r["GBps_1GiB"] = round(us, 3), round(gib / us / 1e3, 1)
+        del graph
+    del big
     torch.cuda.empty_cache()
-    return {"bytes": nbytes, "workgroups": workgroups, "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1),
-            "us_1GiB": round(us_gib, 3), "GBps_1GiB": round(gib / us_gib / 1e3, 1)}
+    return out
+
+
+def read_ceiling(nbytes: int, steps: int, capture, time_graph) -> dict:
+    """The practical read ceiling: the fastest configuration of the read_sweep at the attention launch's
+    byte count, and the fastest at 1 GiB."""
+    sweep = read_sweep(nbytes, steps, capture, time_graph)
+    best = max(sweep, key=lambda r: r["GBps"])
+    best_gib = max(sweep, key=lambda r: r["GBps_1GiB"])
+    key = lambda r: f"{r['mode']}, {r['workgroups']} workgroups x {r['threads']} threads, depth {r['depth']}"
+    return {"bytes": best["bytes"], "us": best["us"], "GBps": best["GBps"], "config": key(best),
+            "us_1GiB": best_gib["us_1GiB"], "GBps_1GiB": best_gib["GBps_1GiB"], "config_1GiB": key(best_gib),
+            "configurations": len(sweep),
+            "GBps_default_probe": next(r["GBps"] for r in sweep if (r["mode"], r["workgroups"], r["threads"],
+                                                                    r["depth"]) == ("registers", 256, 256, 8))}
+
+
+def sweep_table(rows: list[dict]) -> str:
+    out = ["| Load type | Workgroups | Threads | Depth | µs (attention bytes) | GB/s | µs (1 GiB) | GB/s (1 GiB) |",
+           "|---|---|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -r["GBps"]):
+        out.append(f"| {r['mode']} | {r['workgroups']} | {r['threads']} | {r['depth']} | {r['us']:.3f} | "
+                   f"{r['GBps']:.0f} | {r['us_1GiB']:.1f} | {r['GBps_1GiB']:.0f} |")
+    return "\n".join(out)
 
 
 def oracle_parity(wl, db, i: int) -> dict:
@@ -356,6 +420,53 @@ def recycled_blocks(seg0, policy, block_size: int = 16, n_outputs: int = 2700) -
             "blocks_without_freeing": int((-(-seg.sum(axis=1) // block_size)).sum())}
 
 
+def graph_tools(stream):
+    """capture(fn): fn's launches captured into a HIP graph on a side stream, replayed once to warm up;
+    time_graph(graph): µs of one replay, between HIP events recorded on `stream` around it."""
+    import torch
+
+    def capture(fn):
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            fn()
+        torch.cuda.synchronize()
+        graph.replay()  # warm replay
+        torch.cuda.synchronize()
+        return graph
+
+    def time_graph(graph) -> float:
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        graph.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) * 1e3
+
+    return capture, time_graph
+
+
+def per_step_attn(db, steps: list[int], replicas: int, capture, time_graph) -> dict:
+    """decode_attn duration step by step: per distinct step, its retained set, then a replayed graph of
+    max(replicas, 4) back-to-back launches over it, each on the next KV replica (the replicas together
+    hold more than twice the Infinity Cache), mean per launch; the median, p90, mean, min and max over
+    the steps."""
+    per = []
+    n = max(replicas, 4)
+    for s in sorted(set(steps)):
+        db.evict(s)
+        graph = capture(lambda: [db.attend(s, r % replicas) for r in range(n)])
+        per.append(time_graph(graph) / n)
+        del graph
+    a = np.array(per)
+    return {"steps": len(per), "launches_per_step": n, "median": round(float(np.median(a)), 3),
+            "p90": round(float(np.percentile(a, 90)), 3), "mean": round(float(a.mean()), 3),
+            "min": round(float(a.min()), 3), "max": round(float(a.max()), 3)}
+
+
 def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, cpu_budget: float,
         split_len: int, use_ranges: bool, with_ring: bool = True) -> dict:
     import torch
@@ -404,26 +515,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         torch.cuda.synchronize()
         bracket_us = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
 
-    def capture(fn):
-        graph = torch.cuda.CUDAGraph()
-        cap = torch.cuda.Stream()
-        cap.wait_stream(stream)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(graph, stream=cap):
-            fn()
-        torch.cuda.synchronize()
-        graph.replay()  # warm replay
-        torch.cuda.synchronize()
-        return graph
-
-    def time_graph(graph) -> float:
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0.record(stream)
-        graph.replay()
-        t1.record(stream)
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) * 1e3
+    capture, time_graph = graph_tools(stream)
 
     # Whole steps, captured once into a graph and replayed: the single-launch murmur_decode_step (the
     # step's value, retained-set outputs written), and murmur_evict_compact + murmur_decode_attn.
@@ -449,9 +541,14 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
         if M.murmur_device_error() != 0:
             raise RuntimeError("device error during the timed decode_attn launches")
         alg_bytes = float(kv_step[order[0]] + io)  # every launch of the decode_attn graph reads this set
+        log("timing decode_attn step by step")
+        attn_per_step = per_step_attn(db, order, replicas, capture, time_graph)
+        if M.murmur_device_error() != 0:
+            raise RuntimeError("device error during the per-step decode_attn launches")
     else:
         two_launch_us = None
         attn_us = step_us
+        attn_per_step = None
         alg_bytes = float(np.mean([kv_step[o] for o in order]) + io)
 
     ceiling = read_ceiling(int(alg_bytes), steps, capture, time_graph)
@@ -484,6 +581,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
                    "split_len": db.split_len or "auto"},
         "step_two_launches_us": round(two_launch_us, 3) if two_launch else None,
         "decode_attn_us": round(attn_us, 3),
+        "decode_attn_per_step_us": attn_per_step,
         "decode_attn_event_bracket_us": None if bracket_us is None else {
             "mean": round(float(bracket_us.mean()), 3), "median": round(float(np.median(bracket_us)), 3),
             "p90": round(float(np.percentile(bracket_us, 90)), 3)},
@@ -603,6 +701,8 @@ def main() -> int:
     ap.add_argument("--pmc-kernel", default="decode_attn_kernel<1, 2>", help="kernel name part for --summarize-pmc")
     ap.add_argument("--copy-mib", type=int, default=256, help="copy size of the --copy-reference runs")
     ap.add_argument("--alg-bytes", type=int, default=0, help="algorithmic bytes per launch (bench JSON)")
+    ap.add_argument("--read-sweep", type=int, default=0, metavar="BYTES",
+                    help="only run the read-ceiling sweep at this byte count (and 1 GiB), print a markdown table")
     args = ap.parse_args()
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
@@ -619,6 +719,15 @@ def main() -> int:
         return 0
     if args.copy_reference:
         print(json.dumps(copy_reference(args.copy_reference, 8)), flush=True)
+        return 0
+    if args.read_sweep:
+        import torch
+        from paper_2606_01483_amd import murmur as M
+        torch.cuda.init()
+        M.lib()
+        rows = read_sweep(args.read_sweep, args.steps, *graph_tools(torch.cuda.current_stream()))
+        print(sweep_table(rows), flush=True)
+        print(json.dumps(rows), flush=True)
         return 0
     if args.all:
         from paper_2606_01483_amd import workloads as W

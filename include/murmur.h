@@ -136,7 +136,7 @@ typedef struct murmur_kv {
 } murmur_kv;
 
 /* ABI version of this header (bumped on any signature change). */
-#define MURMUR_ABI_VERSION 9
+#define MURMUR_ABI_VERSION 10
 int murmur_abi_version(void);
 
 /* Text of the last failure on the calling thread; valid until the next call
@@ -454,15 +454,21 @@ int murmur_chunk_timestamps(const double *t_local, const int32_t *chunk, int32_t
 
 /* Measurement only (not part of the method): a plain read-only streaming
  * kernel, the practical ceiling the attention's achieved HBM bandwidth is
- * compared with.  n_workgroups workgroups of 256 threads each read a
- * contiguous share of buf_dev[0, bytes) with 16-byte loads, eight per
- * thread in flight, and keep an XOR of what they read; sink_dev
- * [n_workgroups] (4-byte aligned) is written only if that XOR equals a fixed
- * pattern, so the loads are not optimised away and nearly nothing is
- * written.  buf_dev 16-byte aligned, bytes a positive multiple of 16,
- * n_workgroups in [1, 65535].  Errors: MURMUR_EINVAL, MURMUR_EHIP. */
-int murmur_read_probe(const void *buf_dev, size_t bytes, int32_t n_workgroups, uint32_t *sink_dev,
-                      murmur_stream_t stream);
+ * compared with.  n_workgroups workgroups of `threads` threads each read a
+ * contiguous share of buf_dev[0, bytes) with 16-byte loads and keep an XOR of
+ * what they read; sink_dev [n_workgroups] (4-byte aligned) is written only
+ * if that XOR equals a fixed pattern, so the loads are not optimised away and
+ * nearly nothing is written.  mode MURMUR_PROBE_REGISTERS: each thread issues
+ * `depth` loads into registers, then waits for them; MURMUR_PROBE_LDS: the
+ * loads go straight to LDS (the load type of the attention kernels), `depth`
+ * per thread in flight at any time, using (threads / 64) * depth KiB of LDS.
+ * buf_dev 16-byte aligned, bytes a positive multiple of 16, n_workgroups in
+ * [1, 65535], threads a multiple of 64 in [64, 1024], depth 1, 2, 4, 8 or 16,
+ * at most 64 KiB of LDS.  Errors: MURMUR_EINVAL, MURMUR_EHIP. */
+#define MURMUR_PROBE_REGISTERS 0
+#define MURMUR_PROBE_LDS 1
+int murmur_read_probe(const void *buf_dev, size_t bytes, int32_t n_workgroups, int32_t threads, int32_t depth,
+                      int32_t mode, uint32_t *sink_dev, murmur_stream_t stream);
 
 /* Synchronises `stream`, returns the device error word of the current device
  * in *code (0 = none) and clears it.  Not for use inside a captured graph. */

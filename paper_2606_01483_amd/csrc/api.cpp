@@ -111,7 +111,7 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     }
     if (n_lo > 0 && n_lo < 65536 && groups * n_lo + groups_hi < 65536) {
         p.wide_wg = (int32_t)(groups * n_lo + groups_hi);
-        p.sched.groups_hi = (uint32_t)groups_hi;
+        p.sched.groups_hi = (uint32_t)groups_hi | (uint32_t)p.wide_wg << 16;
         p.sched.n_split = (uint32_t)n_hi | (uint32_t)n_lo << 16;
         p.sched.magic_hi = magic16((uint32_t)n_hi);
         p.sched.magic_lo = magic16((uint32_t)n_lo);
@@ -687,14 +687,23 @@ MURMUR_EXPORT int murmur_chunk_timestamps(const double *t_local, const int32_t *
     return ok();
 }
 
-MURMUR_EXPORT int murmur_read_probe(const void *buf_dev, size_t bytes, int32_t n_workgroups, uint32_t *sink_dev,
-                                    murmur_stream_t stream) {
+MURMUR_EXPORT int murmur_read_probe(const void *buf_dev, size_t bytes, int32_t n_workgroups, int32_t threads,
+                                    int32_t depth, int32_t mode, uint32_t *sink_dev, murmur_stream_t stream) {
     if (!buf_dev || !sink_dev) return fail(MURMUR_EINVAL, "buf_dev and sink_dev must not be NULL");
     if (!aligned(buf_dev, 16) || !aligned(sink_dev, 4))
         return fail(MURMUR_EINVAL, "buf_dev must be 16-byte and sink_dev 4-byte aligned");
     if (bytes == 0 || bytes % 16 != 0) return fail(MURMUR_EINVAL, "bytes must be a positive multiple of 16");
     if (n_workgroups < 1 || n_workgroups > 65535) return fail(MURMUR_EINVAL, "n_workgroups must be in [1, 65535]");
-    const int e = launch_read_probe(buf_dev, (int64_t)(bytes / 16), n_workgroups, sink_dev, stream);
+    if (threads < 64 || threads > 1024 || threads % 64 != 0)
+        return fail(MURMUR_EINVAL, "threads must be a multiple of 64 in [64, 1024]");
+    if (depth != 1 && depth != 2 && depth != 4 && depth != 8 && depth != 16)
+        return fail(MURMUR_EINVAL, "depth must be 1, 2, 4, 8 or 16");
+    if (mode != MURMUR_PROBE_REGISTERS && mode != MURMUR_PROBE_LDS)
+        return fail(MURMUR_EINVAL, "mode must be MURMUR_PROBE_REGISTERS or MURMUR_PROBE_LDS");
+    if (mode == MURMUR_PROBE_LDS && (threads / 64) * depth > 64)
+        return fail(MURMUR_EINVAL, "MURMUR_PROBE_LDS needs (threads / 64) * depth KiB of LDS, at most 64");
+    const int e = launch_read_probe(buf_dev, (int64_t)(bytes / 16), n_workgroups, threads, depth,
+                                    mode == MURMUR_PROBE_LDS, sink_dev, stream);
     if (e != 0) return fail(MURMUR_EHIP, "read_probe launch failed: %s", hip_error_text(e));
     return ok();
 }

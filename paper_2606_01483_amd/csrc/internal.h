@@ -36,11 +36,11 @@ constexpr int kWideSplit = kWideWaves * kWaveTile;  // 256
 // multiply-high divisions (values below 2^16, multipliers ceil(2^32 / d), 0
 // for d = 1): the
 // first groups_hi (layer, sequence, KV head) groups are cut into n_hi splits
-// of len_hi positions, the others into n_lo of len_lo; workgroup w takes the
-// w-th (group, split) in that order and, when its group has more than one
-// split, leaves its partial in slot w.
+// of len_hi positions, the others into n_lo of len_lo; the w-th (group,
+// split) in that order goes to the workgroup that xcd_order maps to w and,
+// when its group has more than one split, leaves its partial in slot w.
 struct WideSched {
-    uint32_t groups_hi;
+    uint32_t groups_hi;  // groups_hi | W << 16, W the number of workgroups
     uint32_t n_split;   // n_hi | n_lo << 16
     uint32_t magic_hi;  // ceil(2^32 / n_hi)
     uint32_t magic_lo;  // ceil(2^32 / n_lo)
@@ -119,7 +119,8 @@ int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream);
 // 256-byte aligned), looked up once per device; *fresh is true on that first
 // lookup, when the caller must zero the ticket region.  Returns a hipError_t value.
 int static_scratch(void **ptr, bool *fresh);
-int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, uint32_t *sink, murmur_stream_t stream);
+int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, int32_t threads, int32_t depth, bool lds,
+                      uint32_t *sink, murmur_stream_t stream);
 int launch_paged_step(const murmur_seg *seg, const murmur_policy *pol, int32_t pol_per_seq, int32_t B, int32_t *bt,
                       int32_t max_blocks, int32_t log2_bs, int32_t *stack, int32_t *top, int32_t capacity,
                       int32_t full_scan, murmur_stream_t stream);

@@ -1362,6 +1362,17 @@ static __device__ __forceinline__ void merge_wide(const AttnLaunch &a, __amdgpu_
     store_output(a, row0 + h, d0, O, M, L);
 }
 
+// The hardware hands workgroup w of a launch to XCD w mod 8.  The work items
+// (in the order the schedule lists them) are dealt out XCD by XCD instead:
+// XCD x takes a contiguous run of them, so the splits of a group, which trade
+// partials, share one L2 where the counts allow.  A bijection of [0, W).
+static __device__ __forceinline__ uint32_t xcd_order(uint32_t wg, uint32_t W) {
+    const uint32_t per = (W + 7) >> 3;        // work items of the first XCDs
+    const uint32_t tall = W - 8 * (per - 1);  // XCDs that take `per` (the others per - 1)
+    const uint32_t x = wg & 7, local = wg >> 3;
+    return x < tall ? x * per + local : tall * per + (x - tall) * (per - 1) + local;
+}
+
 // x / d for x < 2^16 from magic = ceil(2^32 / d); magic 0 stands for d = 1
 // (whose ceil(2^32 / d) does not fit in 32 bits).
 static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) { return magic ? __umulhi(x, magic) : x; }
@@ -1392,9 +1403,10 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
 
     // Which split of which group: scalar arithmetic on preloaded arguments,
     // so the retained-set description is the first memory access.
-    const uint32_t wg = blockIdx.x;
+    const uint32_t wg = xcd_order(blockIdx.x, ws.groups_hi >> 16);
+    const uint32_t gh = ws.groups_hi & 0xffffu;
     const uint32_t n_hi = ws.n_split & 0xffffu, n_lo = ws.n_split >> 16;
-    const uint32_t hi_wg = ws.groups_hi * n_hi;
+    const uint32_t hi_wg = gh * n_hi;
     uint32_t grp, split, n, len, slot0;
     if (wg < hi_wg) {
         grp = div16(wg, ws.magic_hi);
@@ -1406,7 +1418,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
         const uint32_t w2 = wg - hi_wg;
         const uint32_t gl = div16(w2, ws.magic_lo);
         split = w2 - gl * n_lo;
-        grp = ws.groups_hi + gl;
+        grp = gh + gl;
         n = n_lo;
         len = ws.len >> 16;
         slot0 = hi_wg + gl * n_lo;
@@ -1524,23 +1536,46 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
 }
 
 // Read-only streaming probe (measurement): workgroup w reads the 16-byte
-// units [w * per, (w + 1) * per) of the buffer, eight loads per thread in
-// flight (indexes clamped into the share, so every load is unconditional).
-__global__ __launch_bounds__(256) void read_probe_kernel(const u32x4 *__restrict__ p, int64_t n16,
-                                                         uint32_t *__restrict__ sink) {
+// units [w * per, (w + 1) * per) of the buffer.  kLds false: each thread
+// issues kDepth loads into registers (indexes clamped into the share, so every
+// load is unconditional), then folds them into an XOR.  kLds true: the loads
+// go straight to LDS (the attention kernels' load type), wavefront by
+// wavefront, each into the next of kDepth 1 KiB slots of the wavefront's own
+// ring, kDepth of them in flight at any time; the XOR is then taken over the
+// last ring.  Block size: any multiple of 64 up to 1024.
+template <int kDepth, bool kLds>
+__global__ __launch_bounds__(1024) void read_probe_kernel(const u32x4 *__restrict__ p, int64_t n16,
+                                                          uint32_t *__restrict__ sink) {
+    extern __shared__ __align__(16) uint8_t probe_ring[];
     const int64_t per = (n16 + gridDim.x - 1) / gridDim.x;
     const int64_t lo = (int64_t)blockIdx.x * per;
     const int64_t hi = lo + per < n16 ? lo + per : n16;
+    const int T = blockDim.x;
     u32x4 acc = {0, 0, 0, 0};
-    for (int64_t i = lo + threadIdx.x; i < hi; i += 8 * 256) {
-        u32x4 v[8];
+    if constexpr (!kLds) {
+        for (int64_t i = lo + threadIdx.x; i < hi; i += (int64_t)kDepth * T) {
+            u32x4 v[kDepth];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int64_t j = i + k * 256;
-            v[k] = p[j < hi ? j : hi - 1];
+            for (int k = 0; k < kDepth; ++k) {
+                const int64_t j = i + (int64_t)k * T;
+                v[k] = p[j < hi ? j : hi - 1];
+            }
+#pragma unroll
+            for (int k = 0; k < kDepth; ++k) acc ^= v[k];
         }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) acc ^= v[k];
+    } else {
+        const int lane = threadIdx.x & 63;
+        uint8_t *ring = probe_ring + (threadIdx.x >> 6) * kDepth * 1024;
+        int slot = 0;
+        // wavefront-uniform trip count: the last units of a share are clamped
+        for (int64_t b = lo + (threadIdx.x & ~63); b < hi; b += T) {
+            const int64_t j = b + lane < hi ? b + lane : hi - 1;
+            __builtin_amdgcn_global_load_lds(p + j, (lds_void_t *)(ring + slot * 1024), 16, 0, 0);
+            slot = slot + 1 == kDepth ? 0 : slot + 1;
+            wait_vm<kDepth - 1>();
+        }
+        wait_vm<0>();
+        acc = *(const u32x4 *)(ring + lane * 16);
     }
     const uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
     if (x == 0x9E3779B9u) sink[blockIdx.x] = x;
@@ -1616,10 +1651,29 @@ int launch_paged_append(const murmur_seg *seg, int32_t B, const int32_t *bt, int
     return (int)hipGetLastError();
 }
 
-int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, uint32_t *sink, murmur_stream_t stream) {
-    hipLaunchKernelGGL(read_probe_kernel, dim3((unsigned)n_workgroups), dim3(256), 0, (hipStream_t)stream,
-                       (const u32x4 *)buf, n16, sink);
+template <int kDepth>
+static int launch_read_probe_depth(const void *buf, int64_t n16, int32_t n_workgroups, int32_t threads, bool lds,
+                                   uint32_t *sink, murmur_stream_t stream) {
+    const size_t lds_bytes = lds ? (size_t)(threads / 64) * kDepth * 1024 : 0;
+    if (lds)
+        hipLaunchKernelGGL((read_probe_kernel<kDepth, true>), dim3((unsigned)n_workgroups), dim3((unsigned)threads),
+                           lds_bytes, (hipStream_t)stream, (const u32x4 *)buf, n16, sink);
+    else
+        hipLaunchKernelGGL((read_probe_kernel<kDepth, false>), dim3((unsigned)n_workgroups), dim3((unsigned)threads),
+                           0, (hipStream_t)stream, (const u32x4 *)buf, n16, sink);
     return (int)hipGetLastError();
+}
+
+int launch_read_probe(const void *buf, int64_t n16, int32_t n_workgroups, int32_t threads, int32_t depth, bool lds,
+                      uint32_t *sink, murmur_stream_t stream) {
+    switch (depth) {
+    case 1: return launch_read_probe_depth<1>(buf, n16, n_workgroups, threads, lds, sink, stream);
+    case 2: return launch_read_probe_depth<2>(buf, n16, n_workgroups, threads, lds, sink, stream);
+    case 4: return launch_read_probe_depth<4>(buf, n16, n_workgroups, threads, lds, sink, stream);
+    case 8: return launch_read_probe_depth<8>(buf, n16, n_workgroups, threads, lds, sink, stream);
+    case 16: return launch_read_probe_depth<16>(buf, n16, n_workgroups, threads, lds, sink, stream);
+    default: return (int)hipErrorInvalidValue;
+    }
 }
 
 int launch_workspace_init(int32_t *ticket, int64_t n, murmur_stream_t stream) {

@@ -111,7 +111,7 @@ def _load():
     lib.murmur_chunk_timestamps.restype = ctypes.c_int
     lib.murmur_chunk_timestamps.argtypes = [f64p, i32p, i32, f64p, i32, f64p]
     lib.murmur_read_probe.restype = ctypes.c_int
-    lib.murmur_read_probe.argtypes = [vp, sz, i32, vp, vp]
+    lib.murmur_read_probe.argtypes = [vp, sz, i32, i32, i32, i32, vp, vp]
     lib.murmur_device_error.restype = ctypes.c_int
     lib.murmur_device_error.argtypes = [vp, i32p]
     _lib = lib
@@ -349,10 +349,17 @@ def murmur_chunk_timestamps(t_local, chunk, chunk_len):
     return out
 
 
-def murmur_read_probe(buf_dev, nbytes: int, n_workgroups: int, sink_dev, stream=None) -> None:
-    """Read-only streaming probe over buf_dev[0, nbytes) (measurement of the practical read ceiling)."""
-    _check(_load().murmur_read_probe(_addr(buf_dev), int(nbytes), int(n_workgroups), _addr(sink_dev),
-                                     _stream(stream)))
+MURMUR_PROBE_REGISTERS = 0
+MURMUR_PROBE_LDS = 1
+
+
+def murmur_read_probe(buf_dev, nbytes: int, n_workgroups: int, sink_dev, threads: int = 256, depth: int = 8,
+                      mode: int = MURMUR_PROBE_REGISTERS, stream=None) -> None:
+    """Read-only streaming probe over buf_dev[0, nbytes) (measurement of the practical read ceiling):
+    n_workgroups workgroups of `threads` threads, `depth` 16-byte loads per thread in flight, into
+    registers (MURMUR_PROBE_REGISTERS) or straight to LDS (MURMUR_PROBE_LDS)."""
+    _check(_load().murmur_read_probe(_addr(buf_dev), int(nbytes), int(n_workgroups), int(threads), int(depth),
+                                     int(mode), _addr(sink_dev), _stream(stream)))
 
 
 def murmur_device_error(stream=None) -> int:

@@ -127,7 +127,8 @@ int main() {
                                   1.f, 0, fake, MURMUR_DTYPE_BF16, nullptr, fake, 1 << 30, nullptr) == MURMUR_EINVAL);
     CHECK(murmur_evict_compact(nullptr, fpol, 0, 12, fi, 10, fi, nullptr, nullptr) == MURMUR_EINVAL);
     CHECK(murmur_evict_compact_paged(fseg, fpol, 0, 12, fi, 8, 12, fi, 10, fi, nullptr, nullptr) == MURMUR_EINVAL);
-    CHECK(murmur_read_probe(fake, 1000, 256, (uint32_t *)fake, nullptr) == MURMUR_EINVAL);
+    CHECK(murmur_read_probe(fake, 1000, 256, 256, 8, MURMUR_PROBE_REGISTERS, (uint32_t *)fake, nullptr) == MURMUR_EINVAL);
+    CHECK(murmur_read_probe(fake, 1024, 256, 1024, 8, MURMUR_PROBE_LDS, (uint32_t *)fake, nullptr) == MURMUR_EINVAL);
     CHECK(murmur_paged_step(fseg, fpol, 0, 12, fi, 8, 12, fi, fi, 64, 0, nullptr, 0, nullptr, nullptr, nullptr) ==
           MURMUR_EINVAL);  // block size not a power of two
     CHECK(murmur_paged_step(fseg, fpol, 0, 12, fi, 8, 16, fi, fi, 0, 0, nullptr, 0, nullptr, nullptr, nullptr) ==

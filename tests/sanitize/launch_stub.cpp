@@ -17,7 +17,9 @@ int launch_evict_compact(const murmur_seg *, const murmur_policy *, int32_t, int
 }
 int launch_decode_attn(const AttnLaunch &, murmur_stream_t) { return reached("decode_attn"); }
 int launch_workspace_init(int32_t *, int64_t, murmur_stream_t) { return reached("workspace_init"); }
-int launch_read_probe(const void *, int64_t, int32_t, uint32_t *, murmur_stream_t) { return reached("read_probe"); }
+int launch_read_probe(const void *, int64_t, int32_t, int32_t, int32_t, bool, uint32_t *, murmur_stream_t) {
+    return reached("read_probe");
+}
 int launch_paged_step(const murmur_seg *, const murmur_policy *, int32_t, int32_t, int32_t *, int32_t, int32_t,
                       int32_t *, int32_t *, int32_t, int32_t, murmur_stream_t) {
     return reached("paged_step");

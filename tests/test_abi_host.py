@@ -46,7 +46,7 @@ def test_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert M.murmur_abi_version() == 9
+    assert M.murmur_abi_version() == 10
 
 
 def test_retained_count_host_matches_oracle():
@@ -420,11 +420,20 @@ def test_ring_prefill_matches_the_oracle_appends():
 
 def test_read_probe_rejects():
     lib = M.lib()
-    assert lib.murmur_read_probe(None, 1024, 256, FAKE, 0) == M.MURMUR_EINVAL
-    assert lib.murmur_read_probe(FAKE, 1000, 256, FAKE, 0) == M.MURMUR_EINVAL
-    assert lib.murmur_read_probe(FAKE, 0, 256, FAKE, 0) == M.MURMUR_EINVAL
-    assert lib.murmur_read_probe(FAKE, 1024, 0, FAKE, 0) == M.MURMUR_EINVAL
-    assert lib.murmur_read_probe(FAKE + 8, 1024, 256, FAKE, 0) == M.MURMUR_EINVAL
+    R, L = M.MURMUR_PROBE_REGISTERS, M.MURMUR_PROBE_LDS
+    assert lib.murmur_read_probe(None, 1024, 256, 256, 8, R, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 1000, 256, 256, 8, R, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 0, 256, 256, 8, R, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 1024, 0, 256, 8, R, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE + 8, 1024, 256, 256, 8, R, FAKE, 0) == M.MURMUR_EINVAL
+    for threads in (0, 32, 100, 1088):
+        assert lib.murmur_read_probe(FAKE, 1024, 256, threads, 8, R, FAKE, 0) == M.MURMUR_EINVAL
+    for depth in (0, 3, 32):
+        assert lib.murmur_read_probe(FAKE, 1024, 256, 256, depth, R, FAKE, 0) == M.MURMUR_EINVAL
+    assert lib.murmur_read_probe(FAKE, 1024, 256, 256, 8, 2, FAKE, 0) == M.MURMUR_EINVAL
+    # direct-to-LDS: (threads / 64) * depth KiB of LDS, at most 64
+    assert lib.murmur_read_probe(FAKE, 1024, 256, 1024, 8, L, FAKE, 0) == M.MURMUR_EINVAL
+    assert b"LDS" in lib.murmur_last_error()
 
 
 def test_evict_compact_paged_rejects():
