@@ -83,28 +83,28 @@ def committed_traffic(config: str) -> float | None:
         return None
 
 
-def summarize_trace(directory: str, top: int = 8) -> str:
-    """Markdown tables of a rocprofv3 --kernel-trace --stats run: its *kernel_stats.csv, then the median
-    and p90 of each kernel's dispatch durations from its *kernel_trace.csv."""
+def summarize_trace(directory: str, top: int = 10) -> str:
+    """Markdown tables of a rocprofv3 --kernel-trace --stats run: per kernel, calls and durations (the
+    instantiations of the read probe folded into one row), then the median and p90 of each kernel's
+    dispatch durations, from the run's *kernel_trace.csv."""
     import csv
     import glob
-    path = sorted(glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True))[0]
-    rows = list(csv.DictReader(open(path)))
+    path = sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True))[0]
+    dur: dict[str, list[int]] = {}
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"]
+        if "read_probe_kernel<" in name:
+            name = "murmur::read_probe_kernel (every configuration of the sweep)"
+        dur.setdefault(name, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    total = sum(sum(d) for d in dur.values())
+    rows = sorted(dur.items(), key=lambda kv: -sum(kv[1]))[:top]
     short = lambda n: n if len(n) <= 72 else n[:69] + "..."
-    out = ["| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns | Std dev |", "|---|---|---|---|---|---|---|---|"]
-    for r in rows[:top]:
-        out.append(f"| {short(r['Name'])} | {r['Calls']} | {r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | "
-                   f"{r['Percentage']} | {r['MinNs']} | {r['MaxNs']} | {float(r['StdDev']):.0f} |")
-    traces = sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True))
-    if traces:
-        dur: dict[str, list[int]] = {}
-        for r in csv.DictReader(open(traces[0])):
-            dur.setdefault(r["Kernel_Name"], []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
-        out += ["", "| Kernel | Dispatches | Mean ns | Median ns | p90 ns |", "|---|---|---|---|---|"]
-        for r in rows[:top]:
-            d = np.array(dur.get(r["Name"], [0]), dtype=np.float64)
-            out.append(f"| {short(r['Name'])} | {len(d)} | {d.mean():.0f} | {np.median(d):.0f} | "
-                       f"{np.percentile(d, 90):.0f} |")
+    out = ["| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns | Median ns | p90 ns |",
+           "|---|---|---|---|---|---|---|---|---|"]
+    for name, d in rows:
+        a = np.array(d, dtype=np.float64)
+        out.append(f"| {short(name)} | {len(a)} | {int(a.sum())} | {a.mean():.0f} | {100 * a.sum() / total:.2f} | "
+                   f"{int(a.min())} | {int(a.max())} | {np.median(a):.0f} | {np.percentile(a, 90):.0f} |")
     return "\n".join(out)
 
 
