@@ -15,11 +15,17 @@ Timing:
     bracketed by device synchronisation and HIP events on the replay stream;
   * roofline.achieved: algorithmic bytes of one decode_attn launch divided by
     its mean duration: K decode_attn launches captured into a graph, replayed
-    between two HIP events on the stream they are launched on, divided by K
-    (per-launch event brackets, which also count each launch's dispatch
-    latency, are reported alongside);
-  * every step reads a different replica of the KV cache (rotation over more
-    than 2 x 256 MB), so reads come from HBM, not the 256 MB Infinity Cache.
+    between two HIP events on the stream they are launched on, divided by K;
+    decode_attn_per_step_us: the same per timed step (a graph of launches over
+    that step's retained set), median and p90 over the steps; per-launch event
+    brackets, which also count each launch's dispatch latency, are reported
+    alongside;
+  * cold reads: every launch reads the next replica of the KV cache (the
+    replicas hold more than 2 x 256 MB), and an untimed 512 MB read before
+    each timed replay evicts what the warm-up replay left in the 256 MB
+    Infinity Cache, so K/V come from HBM;
+  * read_ceiling: the fastest of 105 configurations of a plain streaming read
+    (murmur_read_probe) over the same byte count, timed the same way.
 cpu_baseline: the fp64 oracle timed on this host's cores on a bounded number
 of steps of the same workload.
 """
@@ -59,9 +65,18 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_code_text(source: str) -> str:
+    """The kernel source without its comments, whitespace runs collapsed: what the counters depend on."""
+    import re
+    source = re.sub(r"/\*.*?\*/", " ", source, flags=re.S)
+    source = re.sub(r"//[^\n]*", " ", source)
+    return " ".join(source.split())
+
+
+def kernel_source_hash(path: str = KERNEL_SOURCE) -> str:
+    """First 16 hex digits of the sha256 of the kernel code (comments and whitespace do not count)."""
     import hashlib
-    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+    return hashlib.sha256(kernel_code_text(open(path).read()).encode()).hexdigest()[:16]
 
 
 def committed_traffic(config: str) -> float | None:
@@ -422,8 +437,14 @@ def recycled_blocks(seg0, policy, block_size: int = 16, n_outputs: int = 2700) -
 
 def graph_tools(stream):
     """capture(fn): fn's launches captured into a HIP graph on a side stream, replayed once to warm up;
-    time_graph(graph): µs of one replay, between HIP events recorded on `stream` around it."""
+    time_graph(graph): µs of one replay, between HIP events recorded on `stream` around it.  Before the timed
+    replay a plain read of 512 MB (twice the Infinity Cache) runs untimed, so that no data of the warm-up
+    replay is still cached when the timed one starts."""
     import torch
+    from paper_2606_01483_amd import murmur as M
+    flush_bytes = 2 * MALL_BYTES
+    flush_buf = torch.empty(flush_bytes, dtype=torch.uint8, device="cuda")
+    flush_sink = torch.zeros(1024, dtype=torch.int32, device="cuda")
 
     def capture(fn):
         graph = torch.cuda.CUDAGraph()
@@ -439,6 +460,7 @@ def graph_tools(stream):
 
     def time_graph(graph) -> float:
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        M.murmur_read_probe(flush_buf, flush_bytes, 1024, flush_sink, 256, 8, M.MURMUR_PROBE_REGISTERS, stream)
         torch.cuda.synchronize()
         t0.record(stream)
         graph.replay()
@@ -451,11 +473,11 @@ def graph_tools(stream):
 
 def per_step_attn(db, steps: list[int], replicas: int, capture, time_graph) -> dict:
     """decode_attn duration step by step: per distinct step, its retained set, then a replayed graph of
-    max(replicas, 4) back-to-back launches over it, each on the next KV replica (the replicas together
+    max(replicas, 32) back-to-back launches over it, each on the next KV replica (the replicas together
     hold more than twice the Infinity Cache), mean per launch; the median, p90, mean, min and max over
     the steps."""
     per = []
-    n = max(replicas, 4)
+    n = max(replicas, 32)
     for s in sorted(set(steps)):
         db.evict(s)
         graph = capture(lambda: [db.attend(s, r % replicas) for r in range(n)])
@@ -698,7 +720,7 @@ def main() -> int:
     ap.add_argument("--summarize-trace", metavar="DIR", help="print the kernel table of a rocprofv3 --stats run")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="print the traffic summary from four rocprofv3 --pmc runs")
-    ap.add_argument("--pmc-kernel", default="decode_attn_kernel<1, 2>", help="kernel name part for --summarize-pmc")
+    ap.add_argument("--pmc-kernel", default="decode_attn_wide_kernel<1>", help="kernel name part for --summarize-pmc")
     ap.add_argument("--copy-mib", type=int, default=256, help="copy size of the --copy-reference runs")
     ap.add_argument("--alg-bytes", type=int, default=0, help="algorithmic bytes per launch (bench JSON)")
     ap.add_argument("--read-sweep", type=int, default=0, metavar="BYTES",

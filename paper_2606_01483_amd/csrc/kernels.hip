@@ -1,18 +1,23 @@
 // gfx950 (MI355X, CDNA4) kernels of libmurmur.
 //
-//   evict_compact_kernel  Section 3.2, Algorithms 1-2 and Equation 2: the
-//                         retained set of every sequence as an ascending index
-//                         list, a count and a six-piece range table.
-//   decode_attn_kernel    Section 3.2, Equation 1: split-K grouped-query decode
-//                         attention over the retained positions, fp32
-//                         accumulation, with the log-sum-exp merge of the
-//                         splits fused into the last workgroup of each
-//                         (layer, sequence, KV head).
+//   evict_compact_kernel     Section 3.2, Algorithms 1-2 and Equation 2: the
+//                            retained set of every sequence as an ascending
+//                            index list, a count and a six-piece range table.
+//   decode_attn_wide_kernel  Section 3.2, Equation 1: split-K grouped-query
+//                            decode attention over the retained positions,
+//                            splits of up to 256 positions, eight wavefronts
+//                            per workgroup, one 32-position pass each.
+//   decode_attn_lds_kernel   the same for longer splits: each wavefront
+//                            streams its passes through LDS stages.
+//   Both accumulate in fp32 and fuse the log-sum-exp merge of the splits into
+//   the last workgroup of each (layer, sequence, KV head).
+//   paged_step_kernel, paged_append_kernel: the device block manager of the
+//   paged cache (freeing behind the windows, appending the current token).
 //
 // Attention data flow per 64-wide wavefront and pass of 32 retained positions:
-//   K rows  --global 16 B loads-->  MFMA A operands   S^T = K Q^T (16x16x32 bf16)
-//   V rows  --global 16 B loads-->  8x8 bf16 transpose in registers
-//           --ds_write_b128 (swizzled)--> LDS --ds_read_b64--> MFMA B operands
+//   K, V rows --global_load_lds_dwordx4--> LDS stage (XOR-swizzled 16 B chunks)
+//   K: ds_read_b128 --> MFMA A operands      S^T = K Q^T (16x16x32 bf16)
+//   V: ds_read_b64_tr_b16 (transposing) --> MFMA B operands
 //   P = exp2(S - m) stays in registers: the S^T accumulator layout is already
 //   the A-operand layout of O = P V, split into bf16 hi + lo parts so the
 //   product keeps ~16 mantissa bits.
@@ -1088,8 +1093,9 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
 }
 
 // ---------------------------------------------------------------------------
-// decode_attn, split schedule with LDS-staged passes, for splits of more than
-// two workgroup passes: grid and split layout as decode_attn_kernel.  With
+// decode_attn, split schedule with LDS-staged passes, for splits longer than
+// the wide schedule's: one workgroup of four wavefronts per (split, layer and
+// KV head, sequence), wavefront w taking passes w, w + 4, ...  With
 // kStages = 2 each wavefront double-buffers its passes in two LDS stages (K
 // and V, 16 KiB per stage), issuing the next pass's direct-to-LDS loads before
 // computing the current one; the workgroup takes 128 KiB of LDS, a compute

@@ -35,7 +35,7 @@ def write_counters(path, rows):
 def test_traffic_summary_arithmetic(tmp_path):
     """FETCH_SIZE and WRITE_SIZE per dispatch of the named kernel (mean over its dispatches, others ignored),
     each scaled so that a plain copy of known size reads its true bytes."""
-    k = "decode_attn_kernel<1, 2>"
+    k = "decode_attn_wide_kernel<1>"
     write_counters(tmp_path / "f", [(k, 100.0), (k, 300.0), ("other", 9e9)])
     write_counters(tmp_path / "w", [(k, 40.0), ("other", 1.0)])
     write_counters(tmp_path / "cf", [("__amd_rocclr_copyBuffer", 512.0)])  # a 1 MiB copy: fetch under-reads 2x
@@ -80,3 +80,12 @@ def test_recycled_block_count_matches_the_oracle():
         peak = max(peak, held)
     assert got["peak_blocks"] == peak
     assert got["blocks_without_freeing"] == sum(-(-(int(seg0[b, :3].sum()) + 60) // 4) for b in range(2))
+
+
+def test_kernel_hash_ignores_comments_only():
+    """The traffic gate's hash changes with the kernel code, not with its comments or layout."""
+    a = "int f(int x) { return x + 1; } // one\n/* two\n lines */ int g;"
+    b = "int f(int x)  {\n  return x + 1;\n}\n// other words\nint g;"
+    c = "int f(int x) { return x + 2; } int g;"
+    assert bench.kernel_code_text(a) == bench.kernel_code_text(b)
+    assert bench.kernel_code_text(a) != bench.kernel_code_text(c)

@@ -274,7 +274,7 @@ def test_index_mode_matches_range_mode_and_is_deterministic():
 
 def test_workspace_shared_across_shapes():
     """One workspace, zeroed once, serves calls of different shapes and kernels in turn (4, 48 and 384
-    (layer, sequence, KV head) groups; 2 to 21 splits per group; register and LDS-staged splits), all
+    (layer, sequence, KV head) groups; 2 to 21 splits per group; wide-schedule and LDS-staged splits), all
     passing the same ws_bytes: a call with more groups than the one before never finds its tickets on
     partials that call left behind."""
     announce("attn workspace shared across shapes and schedules")
@@ -432,7 +432,8 @@ def test_graph_replays_match_eager_and_pipelined_schedule():
 
 def test_many_ragged_sequences_both_modes():
     """130 ragged sequences over 2 layers with per-sequence policies (empty speech and outputs included), index-list
-    and range modes, the automatic split and fixed splits of one pass, two passes and LDS-staged passes."""
+    and range modes, the automatic split, fixed splits on the wide schedule (96 and 256 positions) and on the
+    LDS-staged kernel (512)."""
     announce("attn 130 ragged sequences")
     rng = np.random.default_rng(99)
     B = 130

@@ -126,7 +126,7 @@ def ragged_workload(n_layers, steps, seed=77):
 @pytest.mark.parametrize("n_layers,split_len", [(2, 0), (2, 64), (2, 512), (12, 512)])
 def test_ring_ragged_policies_with_sinks(n_layers, split_len):
     """Six sequences with different layouts, windows (1 .. 60, and off) and sinks, a ring of 64 rows:
-    register splits (automatic and 64 positions), the LDS-staged kernel in one dispatch round and, with
+    wide-schedule splits (automatic and 64 positions), the LDS-staged kernel in one dispatch round and, with
     12 layers, over more than one round."""
     announce(f"ring ragged NL={n_layers} split_len={split_len}")
     wl = ragged_workload(n_layers, steps=40)
