@@ -26,6 +26,10 @@ constexpr int kMergeBatch = 8;  // splits whose partials one merging thread load
 // about 2.3 us on top of the data phase.
 constexpr double kCuBytesPerUs = 40e3;
 constexpr double kMergeChainUs = 2.3;
+// The wide schedule's merge keeps two batches of kMergeBatch partials in flight: every further
+// 2 * kMergeBatch partials of a group add one serial load round trip (measured: 14 splits of 192
+// positions 8.5 us, 17 of 160 9.0 us on 4 groups of 2592).
+constexpr double kMergeRoundTripUs = 0.5;
 
 // Wide schedule: workgroups of kWideWaves wavefronts, each wavefront one pass
 // of kWaveTile retained positions, so a split holds at most kWideSplit.

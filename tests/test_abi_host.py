@@ -168,10 +168,11 @@ def test_workspace_sizing():
     # 48 groups of 850 positions: 5 splits of 170 positions each, 240 workgroups in one round
     check_plan(ws, split_partials(48, 5, 7), 48)
     assert ws - ticket_region(ws) < split_partials(48, 6, 7)
-    # 4 groups of 2592: the estimate balances the per-unit share against merging many partials: 18 splits
-    check_plan(M.murmur_decode_attn_workspace(1, 1, 28, 4, 2592), split_partials(4, 18, 7), 4)
+    # 4 groups of 2592: the estimate balances the per-unit share against merging many partials; past 16
+    # partials (two load batches) a merge takes another round trip, so 16 splits
+    check_plan(M.murmur_decode_attn_workspace(1, 1, 28, 4, 2592), split_partials(4, 16, 7), 4)
     ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 2592)
-    assert ws - ticket_region(ws) < split_partials(4, 19, 7)
+    assert ws - ticket_region(ws) < split_partials(4, 17, 7)
     assert M.murmur_decode_attn_workspace(1, 1, 28, 4, 100) == 256  # one split: nothing to merge
     assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 1024) == 256
     # an explicit split length on a long list
