@@ -58,7 +58,10 @@ DESCRIPTIONS = {
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_01483_amd", "csrc", "kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2606_01483_amd", "csrc")
+# The device code and the host code that plans its launches (split counts, workspace layout): what the
+# committed traffic figures depend on.
+KERNEL_SOURCES = tuple(os.path.join(CSRC, f) for f in ("kernels.hip", "api.cpp", "internal.h", "policy.h"))
 
 
 def log(msg: str) -> None:
@@ -73,15 +76,20 @@ def kernel_code_text(source: str) -> str:
     return " ".join(source.split())
 
 
-def kernel_source_hash(path: str = KERNEL_SOURCE) -> str:
-    """First 16 hex digits of the sha256 of the kernel code (comments and whitespace do not count)."""
+def kernel_source_hash(paths=KERNEL_SOURCES) -> str:
+    """First 16 hex digits of the sha256 of the kernel and launch-planning code (comments and whitespace do
+    not count)."""
     import hashlib
-    return hashlib.sha256(kernel_code_text(open(path).read()).encode()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in paths:
+        h.update(kernel_code_text(open(path).read()).encode())
+        h.update(b"\0")
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(config: str) -> float | None:
     """HBM bytes per decode_attn launch from the committed rocprofv3 counter summary of this workload,
-    or None if there is none or the kernel source has changed since the counters were taken."""
+    or None if there is none or the kernel or launch-planning code has changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"decode_attn_{config}_traffic.txt")
     if not os.path.exists(path):
         return None
