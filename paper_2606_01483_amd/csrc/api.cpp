@@ -118,7 +118,7 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
         p.sched.n_split = (uint32_t)n_hi | (uint32_t)n_lo << 16;
         p.sched.magic_hi = magic16((uint32_t)n_hi);
         p.sched.magic_lo = magic16((uint32_t)n_lo);
-        p.sched.len = (uint32_t)len_hi | (uint32_t)len_lo << 16;
+        p.sched.len = (uint32_t)len_hi | (uint32_t)len_lo << 9 | (uint32_t)G << 18;
         p.sched.hkv_b = (uint32_t)Hkv | (uint32_t)B << 16;
         p.sched.magic_hkv = magic16((uint32_t)Hkv);
         p.sched.magic_b = magic16((uint32_t)B);

@@ -48,7 +48,8 @@ struct WideSched {
     uint32_t n_split;   // n_hi | n_lo << 16
     uint32_t magic_hi;  // ceil(2^32 / n_hi)
     uint32_t magic_lo;  // ceil(2^32 / n_lo)
-    uint32_t len;       // len_hi | len_lo << 16
+    uint32_t len;       // len_hi | len_lo << 9 | G << 18 (split lengths <= 256, G query heads per KV head);
+                        // the launch adds the policy mode (MURMUR_POL_* bits) << 23
     uint32_t hkv_b;     // Hkv | B << 16
     uint32_t magic_hkv;
     uint32_t magic_b;

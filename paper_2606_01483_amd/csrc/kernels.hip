@@ -720,8 +720,90 @@ static __device__ __forceinline__ int policy_row(int32_t pol_mode, int layer, in
 // of ring_cap output slots and the row of the current token in `cur`.  An
 // invalid layout or policy gives count 0 and sets policy_bad to 1 (2: the
 // ring cannot hold the retained outputs).
+// The few words a workgroup needs to find its sequence's retained set are
+// fetched with one vector load (lane k reads the word at its own address) and
+// made wavefront-uniform with readlane.  Scalar loads would share their wait
+// counter with the scalar loads of the launch description, and a scalar wait
+// cannot be partial: the compiler's first wait for a launch field would then
+// put a second memory round trip in front of the first K/V loads.  Vector
+// loads have a counter of their own, so both round trips overlap.  seq_words
+// issues the load, seq_count_from uses its result: in between, the caller pins
+// the launch fields it needs.
+static __device__ __forceinline__ int32_t word_of_lane(const int32_t *addr) { return *addr; }
+
+// 0 in a vector register the compiler cannot see through: an address offset by
+// it stays a per-lane address, so its load stays a vector load.
+static __device__ __forceinline__ int opaque_lane_zero() {
+    int z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    return z;
+}
+
+// Words of sequence b (see seq_count_from): kSrcLayout / kSrcRing: lanes 0-3
+// its layout, lanes 4-8 its policy; kSrcRanges: lanes 0-11 its range table;
+// kSrcIndex: its count.
 template <int kSrc>
-static __device__ __forceinline__ int seq_count(const int32_t *p0, const int32_t *p1, int b, int32_t pol_mode,
+static __device__ __forceinline__ int32_t seq_words(const int32_t *p0, const int32_t *p1, int b, int32_t pol_mode,
+                                                    int layer, int B) {
+    const int lane = threadIdx.x & 63;
+    if (kSrc == kSrcLayout || kSrc == kSrcRing) {
+        const int32_t *sg = p0 + 4 * b;
+        const int32_t *pl = p1 + 5 * policy_row(pol_mode, layer, b, B);
+        return word_of_lane(lane < 4 ? sg + lane : (lane < 9 ? pl + (lane - 4) : sg));
+    }
+    if (kSrc == kSrcRanges) return word_of_lane(p1 + b * 2 * kPieces + (lane < 2 * kPieces ? lane : 0));
+    return word_of_lane(p0 + b + opaque_lane_zero());
+}
+
+// Count of sequence b and, unless kSrcIndex, its range table, from the words
+// seq_words loaded.  Their sources: counts (kSrcIndex) or range tables
+// (kSrcRanges, the count being the table's total length), or (kSrcLayout,
+// kSrcRing) layouts (murmur_seg [B]) and policies (murmur_policy rows, see
+// policy_row).  kSrcRing gives the pieces in ring-storage rows of ring_cap
+// output slots and the row of the current token in `cur`.  An invalid layout
+// or policy gives count 0 and sets policy_bad to 1 (2: the ring cannot hold
+// the retained outputs).
+template <int kSrc>
+static __device__ __forceinline__ int seq_count_from(int32_t x, int32_t ring_cap, int32_t (&rg)[2 * kPieces],
+                                                     int &policy_bad, int32_t &cur) {
+    if (kSrc == kSrcLayout || kSrc == kSrcRing) {
+        const int32_t s0 = __builtin_amdgcn_readlane(x, 0), s1 = __builtin_amdgcn_readlane(x, 1),
+                      s2 = __builtin_amdgcn_readlane(x, 2), s3 = __builtin_amdgcn_readlane(x, 3);
+        const int32_t w0 = __builtin_amdgcn_readlane(x, 4), w1 = __builtin_amdgcn_readlane(x, 5),
+                      w2 = __builtin_amdgcn_readlane(x, 6), w3 = __builtin_amdgcn_readlane(x, 7),
+                      w4 = __builtin_amdgcn_readlane(x, 8);
+        Pieces pc;
+        const int rc = kSrc == kSrcRing ? ring_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, ring_cap, &pc, &cur)
+                                        : retained_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, &pc);
+        if (rc != 0) {
+            policy_bad = rc == -2 ? 2 : 1;
+#pragma unroll
+            for (int k = 0; k < 2 * kPieces; ++k) rg[k] = 0;
+            return 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) {
+            rg[2 * k] = pc.start[k];
+            rg[2 * k + 1] = pc.len[k];
+        }
+        return pc.count;
+    }
+    if (kSrc == kSrcRanges) {  // the count is the table's total length
+        int c = 0;
+#pragma unroll
+        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = __builtin_amdgcn_readlane(x, k);
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) c += rg[2 * k + 1];
+        return c;
+    }
+    return __builtin_amdgcn_readfirstlane(x);
+}
+
+// Count of sequence b and, unless kSrcIndex, its range table, read with
+// scalar loads (the LDS-staged kernel, whose other scalar loads go out in the
+// same batch).  Sources as for seq_count_from.
+template <int kSrc>
+static __device__ __forceinline__ int seq_count_scalar(const int32_t *p0, const int32_t *p1, int b, int32_t pol_mode,
                                                 int layer, int B, int32_t ring_cap, int32_t (&rg)[2 * kPieces],
                                                 int &policy_bad, int32_t &cur) {
     if (kSrc == kSrcLayout || kSrc == kSrcRing) {
@@ -1135,7 +1217,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     int policy_bad = 0;
     int32_t cur_row = -1;  // ring storage: the current token's row
     const int layer = (int)blockIdx.y / Hkv;
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
+    const int cnt_seq = seq_count_scalar<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
     const int g = (int)blockIdx.y - layer * Hkv;
     const int lb = layer * B + b;
     const int grp = lb * Hkv + g;  // ((layer * B) + b) * Hkv + g
@@ -1314,30 +1396,49 @@ static __device__ __forceinline__ void merge_o_load(f32x4 (&o)[kMergeBatch], __a
     }
 }
 
-// Folds slots base .. base+kMergeBatch-1 into (M, L, O); pair j of the current
-// chunk of pairs (pm, pl) sits in lane (lane & 32) + j, for j = base - cb + k.
-static __device__ __forceinline__ void merge_fold(const f32x4 (&o)[kMergeBatch], float pm, float pl, int cb,
-                                                  int base, int n, int lane, float &M, float &L, f32x4 &O) {
-    float m[kMergeBatch], l[kMergeBatch];
+// Folds the kCnt slots base .. base+kCnt-1 into (M, L, O); pair j of the
+// current chunk of pairs (pm, pl) sits in lane (lane & 32) + j, for
+// j = base - cb + k.
+template <int kCnt>
+static __device__ __forceinline__ void merge_fold_n(const f32x4 (&o)[kMergeBatch], float pm, float pl, int cb,
+                                                    int base, int lane, float &M, float &L, f32x4 &O) {
+    float m[kCnt], l[kCnt];
 #pragma unroll
-    for (int k = 0; k < kMergeBatch; ++k) {
+    for (int k = 0; k < kCnt; ++k) {
         const int src = (lane & 32) + ((base - cb + k) & 31);
         m[k] = __shfl(pm, src);
         l[k] = __shfl(pl, src);
     }
     float mx = M;
 #pragma unroll
-    for (int k = 0; k < kMergeBatch; ++k) mx = base + k < n ? fmaxf(mx, m[k]) : mx;
+    for (int k = 0; k < kCnt; ++k) mx = fmaxf(mx, m[k]);
     const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - mx);
     L *= sc;
     O *= sc;
 #pragma unroll
-    for (int k = 0; k < kMergeBatch; ++k) {
-        const float f = (base + k >= n || m[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m[k] - mx);
+    for (int k = 0; k < kCnt; ++k) {
+        const float f = m[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[k] - mx);
         L += l[k] * f;
         O += o[k] * f;
     }
     M = mx;
+}
+
+// Folds the slots of the batch at `base` that exist (fewer than kMergeBatch
+// when it is the group's last): the work of absent slots is not done at all.
+static __device__ __forceinline__ void merge_fold(const f32x4 (&o)[kMergeBatch], float pm, float pl, int cb,
+                                                  int base, int n, int lane, float &M, float &L, f32x4 &O) {
+    static_assert(kMergeBatch == 8, "one case per batch size");
+    switch (min(n - base, kMergeBatch)) {
+    case 1: merge_fold_n<1>(o, pm, pl, cb, base, lane, M, L, O); break;
+    case 2: merge_fold_n<2>(o, pm, pl, cb, base, lane, M, L, O); break;
+    case 3: merge_fold_n<3>(o, pm, pl, cb, base, lane, M, L, O); break;
+    case 4: merge_fold_n<4>(o, pm, pl, cb, base, lane, M, L, O); break;
+    case 5: merge_fold_n<5>(o, pm, pl, cb, base, lane, M, L, O); break;
+    case 6: merge_fold_n<6>(o, pm, pl, cb, base, lane, M, L, O); break;
+    case 7: merge_fold_n<7>(o, pm, pl, cb, base, lane, M, L, O); break;
+    default: merge_fold_n<8>(o, pm, pl, cb, base, lane, M, L, O); break;
+    }
 }
 
 static_assert(32 % kMergeBatch == 0, "a batch of slots lies in one chunk of pairs");
@@ -1376,12 +1477,15 @@ static __device__ __forceinline__ uint32_t xcd_order(uint32_t wg, uint32_t W) {
     const uint32_t per = (W + 7) >> 3;        // work items of the first XCDs
     const uint32_t tall = W - 8 * (per - 1);  // XCDs that take `per` (the others per - 1)
     const uint32_t x = wg & 7, local = wg >> 3;
-    return x < tall ? x * per + local : tall * per + (x - tall) * (per - 1) + local;
+    const uint32_t first = x * per + local, rest = tall * per + (x - tall) * (per - 1) + local;
+    return x < tall ? first : rest;
 }
 
 // x / d for x < 2^16 from magic = ceil(2^32 / d); magic 0 stands for d = 1
 // (whose ceil(2^32 / d) does not fit in 32 bits).
-static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) { return magic ? __umulhi(x, magic) : x; }
+static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) {
+    return __umulhi(x, magic) + (x & (0u - (uint32_t)(magic == 0u)));  // no branch: umulhi(x, 0) = 0
+}
 
 // The WideSched fields are separate scalar arguments (with the pointers, the
 // first 16 dwords, which the build preloads into SGPRs; a struct argument
@@ -1390,9 +1494,15 @@ template <int kSrc>
 __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     const int32_t *__restrict__ src0, const int32_t *__restrict__ src1, uint32_t groups_hi, uint32_t n_split,
     uint32_t magic_hi, uint32_t magic_lo, uint32_t len_hi_lo, uint32_t hkv_b, uint32_t magic_hkv, uint32_t magic_b,
-    const int32_t *__restrict__ idx, int32_t max_keep, int32_t pol_per_seq, const uint16_t *__restrict__ q,
-    const AttnLaunch a) {
+    const int32_t *__restrict__ idx, const uint16_t *__restrict__ q, const AttnLaunch a) {
     const WideSched ws{groups_hi, n_split, magic_hi, magic_lo, len_hi_lo, hkv_b, magic_hkv, magic_b};
+    // G and the policy mode from a preloaded argument: loading them from memory
+    // put a second round trip in front of the first K/V loads
+    const int G = (int)((ws.len >> 18) & 0x1fu);
+    const int32_t pol_per_seq = (int32_t)(ws.len >> 23) & 3;
+    // from the launch description: every dword of the loads it takes is then in use, so no
+    // scratch value lands in a register a scalar load is still filling (which forces a wait)
+    const int32_t max_keep = a.max_keep;
     __shared__ __attribute__((aligned(16))) uint8_t stages[kWideWaves][kStageBytes];
     __shared__ __attribute__((aligned(16))) uint8_t idx_slot[kSrc != kSrcIndex ? 1 : kWideWaves][kIdxSlotBytes];
     __shared__ CombineLdsT<kWideWaves> cl;
@@ -1413,22 +1523,15 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     const uint32_t gh = ws.groups_hi & 0xffffu;
     const uint32_t n_hi = ws.n_split & 0xffffu, n_lo = ws.n_split >> 16;
     const uint32_t hi_wg = gh * n_hi;
-    uint32_t grp, split, n, len, slot0;
-    if (wg < hi_wg) {
-        grp = div16(wg, ws.magic_hi);
-        split = wg - grp * n_hi;
-        n = n_hi;
-        len = ws.len & 0xffffu;
-        slot0 = grp * n_hi;
-    } else {
-        const uint32_t w2 = wg - hi_wg;
-        const uint32_t gl = div16(w2, ws.magic_lo);
-        split = w2 - gl * n_lo;
-        grp = gh + gl;
-        n = n_lo;
-        len = ws.len >> 16;
-        slot0 = hi_wg + gl * n_lo;
-    }
+    // selects, not branches: straight-line scalar code up to the first loads
+    const bool in_hi = wg < hi_wg;
+    const uint32_t w2 = in_hi ? wg : wg - hi_wg;
+    const uint32_t n = in_hi ? n_hi : n_lo;
+    const uint32_t gq = div16(w2, in_hi ? ws.magic_hi : ws.magic_lo);
+    const uint32_t grp = in_hi ? gq : gh + gq;
+    const uint32_t split = w2 - gq * n;
+    const uint32_t len = in_hi ? (ws.len & 0x1ffu) : ((ws.len >> 9) & 0x1ffu);
+    const uint32_t slot0 = (in_hi ? 0u : hi_wg) + gq * n;
     const int Hkv = (int)(ws.hkv_b & 0xffffu), B = (int)(ws.hkv_b >> 16);
     const uint32_t lb = div16(grp, ws.magic_hkv);
     const int g = (int)(grp - lb * (uint32_t)Hkv);
@@ -1437,8 +1540,16 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     int32_t rg[2 * kPieces];
     int policy_bad = 0;
     int32_t cur_row = -1;  // ring storage: the current token's row
-    const int cnt_seq = seq_count<kSrc>(src0, src1, b, pol_per_seq, layer, B, a.ring_cap, rg, policy_bad, cur_row);
-    const int G = a.G;
+    const int32_t seq_w = seq_words<kSrc>(src0, src1, b, pol_per_seq, layer, B);
+    // Every launch field the kernel reads, pinned in scalar registers here: their
+    // loads go out in one batch ahead of one wait, which the vector load above
+    // overlaps, instead of later batches whose waits would each add a round trip
+    // before the first K/V loads.
+    materialize(a.k, a.v, a.s_layer, a.s_b, a.s_h, a.s_pos, a.max_len, a.scale_log2, a.max_keep, q, a.out, a.lse,
+                a.ticket, a.part_ml, a.part_o, a.part_ml_bytes, a.part_o_bytes, a.out_f32);
+    if (kSrc == kSrcLayout || kSrc == kSrcRing) materialize(a.idx_out, a.count_out, a.ranges_out);
+    if (kSrc == kSrcRing) materialize(a.ring_cap, a.k_new, a.v_new);
+    const int cnt_seq = seq_count_from<kSrc>(seq_w, a.ring_cap, rg, policy_bad, cur_row);
     const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
     const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
     const int r_begin = (int)(split * len);
@@ -1608,8 +1719,9 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.wide_wg > 0) {
         const WideSched &w = a.sched;
         hipLaunchKernelGGL(decode_attn_wide_kernel<kSrc>, dim3((unsigned)a.wide_wg), dim3(kWideThreads), 0, stream,
-                           a.src0, a.src1, w.groups_hi, w.n_split, w.magic_hi, w.magic_lo, w.len, w.hkv_b, w.magic_hkv,
-                           w.magic_b, a.idx, a.max_keep, a.pol_per_seq, a.q, a);
+                           a.src0, a.src1, w.groups_hi, w.n_split, w.magic_hi, w.magic_lo,
+                           w.len | (uint32_t)(a.pol_per_seq & 3) << 23, w.hkv_b, w.magic_hkv, w.magic_b, a.idx,
+                           a.q, a);
         return;
     }
     const dim3 grid((unsigned)a.n_split, (unsigned)(a.NL * a.Hkv), (unsigned)a.B);
