@@ -34,17 +34,21 @@ def _run(cmd: list[str]) -> None:
         raise RuntimeError(f"build step failed ({res.returncode}): {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
 
 
+COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall"]
+# Device code: packed-fp32 instruction selection off; the first 16 kernel-argument dwords preloaded into SGPRs.
+KERNEL_FLAGS = [f"--offload-arch={ARCH}", *COMMON_FLAGS, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-kernarg-preload-count=16"]
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source and link libmurmur.so (always rebuilds)."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     hipcc = _hipcc()
-    common = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall"]
     k_obj = os.path.join(BUILD_DIR, "kernels.o")
     a_obj = os.path.join(BUILD_DIR, "api.o")
     steps = [
-        [hipcc, f"--offload-arch={ARCH}", *common, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-mllvm", "-amdgpu-kernarg-preload-count=16", "-c", os.path.join(CSRC, "kernels.hip"), "-o", k_obj],
-        ["g++", *common, "-Wextra", "-c", os.path.join(CSRC, "api.cpp"), "-o", a_obj],
+        [hipcc, *KERNEL_FLAGS, "-c", os.path.join(CSRC, "kernels.hip"), "-o", k_obj],
+        ["g++", *COMMON_FLAGS, "-Wextra", "-c", os.path.join(CSRC, "api.cpp"), "-o", a_obj],
     ]
     for cmd in steps:
         if verbose:
