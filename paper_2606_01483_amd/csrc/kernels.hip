@@ -627,8 +627,11 @@ static __device__ __forceinline__ void dma_pos_index(const uint8_t *slot, int r0
 }
 
 // One pass from an LDS stage: operand reads, S^T = K Q^T, softmax update,
-// O += P V.
-template <bool kOnline>
+// O += P V.  kWaitDma: the stage's direct-to-LDS loads (dma_pass: the K tile's,
+// then the V tile's, the last loads this wavefront issued) may still be in
+// flight; the K operands are read once the K loads are in, and S^T and the
+// softmax are computed while the V loads land.
+template <bool kOnline, bool kWaitDma = false>
 static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, const u32x4 (&qf)[4], int valid,
                                                         float scale_log2, WaveAcc &w, int n16, int c4) {
     const uint32_t kt = lds_addr(stage), vt = kt + kTileBytes;
@@ -647,39 +650,57 @@ static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, co
         va[db] = vt + vr * kTileRowBytes + (((2 * db + ((n16 & 3) >> 1)) ^ vr) << 4) + (n16 & 1) * 8;
     u32x4 kf[8];
     u32x2 vf[16];
-    asm volatile(
-        "ds_read_b128 %0, %24\n\t"
-        "ds_read_b128 %1, %25\n\t"
-        "ds_read_b128 %2, %26\n\t"
-        "ds_read_b128 %3, %27\n\t"
-        "ds_read_b128 %4, %24 offset:4096\n\t"
-        "ds_read_b128 %5, %25 offset:4096\n\t"
-        "ds_read_b128 %6, %26 offset:4096\n\t"
-        "ds_read_b128 %7, %27 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %8, %28\n\t"
-        "ds_read_b64_tr_b16 %9, %28 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %10, %29\n\t"
-        "ds_read_b64_tr_b16 %11, %29 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %12, %30\n\t"
-        "ds_read_b64_tr_b16 %13, %30 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %14, %31\n\t"
-        "ds_read_b64_tr_b16 %15, %31 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %16, %32\n\t"
-        "ds_read_b64_tr_b16 %17, %32 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %18, %33\n\t"
-        "ds_read_b64_tr_b16 %19, %33 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %20, %34\n\t"
-        "ds_read_b64_tr_b16 %21, %34 offset:4096\n\t"
-        "ds_read_b64_tr_b16 %22, %35\n\t"
-        "ds_read_b64_tr_b16 %23, %35 offset:4096\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(kf[0]), "=&v"(kf[1]), "=&v"(kf[2]), "=&v"(kf[3]), "=&v"(kf[4]), "=&v"(kf[5]), "=&v"(kf[6]), "=&v"(kf[7]),
-          "=&v"(vf[0]), "=&v"(vf[1]), "=&v"(vf[2]), "=&v"(vf[3]), "=&v"(vf[4]), "=&v"(vf[5]), "=&v"(vf[6]), "=&v"(vf[7]),
-          "=&v"(vf[8]), "=&v"(vf[9]), "=&v"(vf[10]), "=&v"(vf[11]), "=&v"(vf[12]), "=&v"(vf[13]), "=&v"(vf[14]),
-          "=&v"(vf[15])
-        : "v"(ka[0]), "v"(ka[1]), "v"(ka[2]), "v"(ka[3]), "v"(va[0]), "v"(va[1]), "v"(va[2]), "v"(va[3]), "v"(va[4]),
-          "v"(va[5]), "v"(va[6]), "v"(va[7])
-        : "memory");
+    if constexpr (!kWaitDma) {
+        asm volatile(
+            "ds_read_b128 %0, %24\n\t"
+            "ds_read_b128 %1, %25\n\t"
+            "ds_read_b128 %2, %26\n\t"
+            "ds_read_b128 %3, %27\n\t"
+            "ds_read_b128 %4, %24 offset:4096\n\t"
+            "ds_read_b128 %5, %25 offset:4096\n\t"
+            "ds_read_b128 %6, %26 offset:4096\n\t"
+            "ds_read_b128 %7, %27 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %8, %28\n\t"
+            "ds_read_b64_tr_b16 %9, %28 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %10, %29\n\t"
+            "ds_read_b64_tr_b16 %11, %29 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %12, %30\n\t"
+            "ds_read_b64_tr_b16 %13, %30 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %14, %31\n\t"
+            "ds_read_b64_tr_b16 %15, %31 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %16, %32\n\t"
+            "ds_read_b64_tr_b16 %17, %32 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %18, %33\n\t"
+            "ds_read_b64_tr_b16 %19, %33 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %20, %34\n\t"
+            "ds_read_b64_tr_b16 %21, %34 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %22, %35\n\t"
+            "ds_read_b64_tr_b16 %23, %35 offset:4096\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(kf[0]), "=&v"(kf[1]), "=&v"(kf[2]), "=&v"(kf[3]), "=&v"(kf[4]), "=&v"(kf[5]), "=&v"(kf[6]), "=&v"(kf[7]),
+              "=&v"(vf[0]), "=&v"(vf[1]), "=&v"(vf[2]), "=&v"(vf[3]), "=&v"(vf[4]), "=&v"(vf[5]), "=&v"(vf[6]), "=&v"(vf[7]),
+              "=&v"(vf[8]), "=&v"(vf[9]), "=&v"(vf[10]), "=&v"(vf[11]), "=&v"(vf[12]), "=&v"(vf[13]), "=&v"(vf[14]),
+              "=&v"(vf[15])
+            : "v"(ka[0]), "v"(ka[1]), "v"(ka[2]), "v"(ka[3]), "v"(va[0]), "v"(va[1]), "v"(va[2]), "v"(va[3]), "v"(va[4]),
+              "v"(va[5]), "v"(va[6]), "v"(va[7])
+            : "memory");
+    } else {
+        wait_vm<kStageLoads / 2>();  // the K tile's loads (issued before the V tile's)
+        asm volatile(
+            "ds_read_b128 %0, %8\n\t"
+            "ds_read_b128 %1, %9\n\t"
+            "ds_read_b128 %2, %10\n\t"
+            "ds_read_b128 %3, %11\n\t"
+            "ds_read_b128 %4, %8 offset:4096\n\t"
+            "ds_read_b128 %5, %9 offset:4096\n\t"
+            "ds_read_b128 %6, %10 offset:4096\n\t"
+            "ds_read_b128 %7, %11 offset:4096\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(kf[0]), "=&v"(kf[1]), "=&v"(kf[2]), "=&v"(kf[3]), "=&v"(kf[4]), "=&v"(kf[5]), "=&v"(kf[6]),
+              "=&v"(kf[7])
+            : "v"(ka[0]), "v"(ka[1]), "v"(ka[2]), "v"(ka[3])
+            : "memory");
+    }
     f32x4 s[2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
@@ -689,6 +710,32 @@ static __device__ __forceinline__ void compute_pass_lds(const uint8_t *stage, co
     }
     u32x4 p_hi, p_lo;
     softmax_step<kOnline>(s, valid, scale_log2, w, c4, p_hi, p_lo);
+    if constexpr (kWaitDma) {
+        wait_vm<0>();  // the V tile's loads
+        asm volatile(
+            "ds_read_b64_tr_b16 %0, %16\n\t"
+            "ds_read_b64_tr_b16 %1, %16 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %2, %17\n\t"
+            "ds_read_b64_tr_b16 %3, %17 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %4, %18\n\t"
+            "ds_read_b64_tr_b16 %5, %18 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %6, %19\n\t"
+            "ds_read_b64_tr_b16 %7, %19 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %8, %20\n\t"
+            "ds_read_b64_tr_b16 %9, %20 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %10, %21\n\t"
+            "ds_read_b64_tr_b16 %11, %21 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %12, %22\n\t"
+            "ds_read_b64_tr_b16 %13, %22 offset:4096\n\t"
+            "ds_read_b64_tr_b16 %14, %23\n\t"
+            "ds_read_b64_tr_b16 %15, %23 offset:4096\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(vf[0]), "=&v"(vf[1]), "=&v"(vf[2]), "=&v"(vf[3]), "=&v"(vf[4]), "=&v"(vf[5]), "=&v"(vf[6]),
+              "=&v"(vf[7]), "=&v"(vf[8]), "=&v"(vf[9]), "=&v"(vf[10]), "=&v"(vf[11]), "=&v"(vf[12]), "=&v"(vf[13]),
+              "=&v"(vf[14]), "=&v"(vf[15])
+            : "v"(va[0]), "v"(va[1]), "v"(va[2]), "v"(va[3]), "v"(va[4]), "v"(va[5]), "v"(va[6]), "v"(va[7])
+            : "memory");
+    }
     // B operand of head dims 16*db .. +15: positions 4*c4 .. +3 (h = 0) and
     // 16 + 4*c4 .. +3 (h = 1), the k order of P.
 #pragma unroll
@@ -1594,8 +1641,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
         u32x4 qf[4];
         load_q(qf, q, row0, G, n16, c4);
         dma_pass(stage, kbase, vbase, a.s_pos, pos, lane, kRing, nr);
-        wait_vm<0>();
-        compute_pass_lds<false>(stage, qf, min(kWaveTile, r_end - r0), a.scale_log2, w, n16, c4);
+        compute_pass_lds<false, true>(stage, qf, min(kWaveTile, r_end - r0), a.scale_log2, w, n16, c4);
     }
 
     if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
