@@ -1410,15 +1410,29 @@ static __device__ __forceinline__ void gather_wide(const float *o_lds, int wave_
     M = kNegInf;
 #pragma unroll
     for (int p = 0; p < kWideWaves / 2; ++p) M = fmaxf(M, fmaxf(ml[p][0], ml[p][2]));
-    L = 0.f;
-    O = f32x4{0.f, 0.f, 0.f, 0.f};
+    // every factor first (independent exp2s), then sums in a tree: no chain of
+    // dependent exp2 and multiply-add through the eight states
+    float f[kWideWaves], lf[kWideWaves];
+    f32x4 of[kWideWaves];
 #pragma unroll
     for (int wv = 0; wv < kWideWaves; ++wv) {
-        const float m = ml[wv / 2][(wv & 1) * 2], l = ml[wv / 2][(wv & 1) * 2 + 1];
-        const float f = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - M);
-        L += l * f;
-        O += f * o[wv];
+        const float m = ml[wv / 2][(wv & 1) * 2];
+        f[wv] = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - M);
     }
+#pragma unroll
+    for (int wv = 0; wv < kWideWaves; ++wv) {
+        lf[wv] = ml[wv / 2][(wv & 1) * 2 + 1] * f[wv];
+        of[wv] = o[wv] * f[wv];
+    }
+#pragma unroll
+    for (int w2 = kWideWaves / 2; w2 >= 1; w2 /= 2)
+#pragma unroll
+        for (int wv = 0; wv < w2; ++wv) {
+            lf[wv] += lf[wv + w2];
+            of[wv] += of[wv + w2];
+        }
+    L = lf[0];
+    O = of[0];
 }
 
 // Log-sum-exp merge of the n partials of a group (slots slot0 .. slot0+n-1),
@@ -1459,15 +1473,27 @@ static __device__ __forceinline__ void merge_fold_n(const f32x4 (&o)[kMergeBatch
     float mx = M;
 #pragma unroll
     for (int k = 0; k < kCnt; ++k) mx = fmaxf(mx, m[k]);
+    // every factor first (independent exp2s), then sums in a tree
+    float lf[kCnt + 1];
+    f32x4 of[kCnt + 1];
     const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - mx);
-    L *= sc;
-    O *= sc;
 #pragma unroll
     for (int k = 0; k < kCnt; ++k) {
         const float f = m[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[k] - mx);
-        L += l[k] * f;
-        O += o[k] * f;
+        lf[k] = l[k] * f;
+        of[k] = o[k] * f;
     }
+    lf[kCnt] = L * sc;
+    of[kCnt] = O * sc;
+#pragma unroll
+    for (int w = 1; w < kCnt + 1; w *= 2)
+#pragma unroll
+        for (int k = 0; k + w < kCnt + 1; k += 2 * w) {
+            lf[k] += lf[k + w];
+            of[k] += of[k + w];
+        }
+    L = lf[0];
+    O = of[0];
     M = mx;
 }
 
