@@ -14,8 +14,11 @@ Timing:
   * value / ms_per_step: K steps captured once into a HIP graph and replayed,
     bracketed by device synchronisation and HIP events on the replay stream;
   * roofline.achieved: algorithmic bytes of one decode_attn launch divided by
-    its mean duration: K decode_attn launches captured into a graph, replayed
-    between two HIP events on the stream they are launched on, divided by K;
+    its duration: the marginal cost of a launch in a replayed graph of
+    back-to-back launches (graphs of N and 2N launches between HIP events on
+    the stream they are launched on, the difference over N), which leaves out
+    the graph's fixed start; the plain mean over K launches is reported as
+    decode_attn_graph_mean_us;
     decode_attn_per_step_us: the same per timed step (a graph of launches over
     that step's retained set), median and p90 over the steps; per-launch event
     brackets, which also count each launch's dispatch latency, are reported
@@ -223,9 +226,10 @@ def probe_configs() -> list[tuple[str, int, int, int]]:
 
 def read_sweep(nbytes: int, steps: int, capture, time_graph, configs=None) -> list[dict]:
     """murmur_read_probe (a plain read-only streaming kernel) over every configuration of the sweep:
-    per configuration, a replayed graph of `steps` launches over nbytes each, every launch reading the
-    next of enough regions to defeat the 256 MB Infinity Cache; and a graph of 8 launches over 1 GiB
-    (two alternating regions)."""
+    per configuration, the marginal per-launch time (marginal_us, n = max(steps, 64)) of launches over
+    nbytes each, every launch reading the next of enough regions to defeat the 256 MB Infinity Cache;
+    and a graph of 8 launches over 1 GiB (two alternating regions; a replay's fixed start is negligible
+    beside them)."""
     import torch
     from paper_2606_01483_amd import murmur as M
     nbytes = max(16, nbytes // 16 * 16)
@@ -236,13 +240,12 @@ def read_sweep(nbytes: int, steps: int, capture, time_graph, configs=None) -> li
     log(f"read-ceiling sweep: {len(configs)} configurations, {nbytes / 1e6:.1f} MB x {regions} regions and 1 GiB")
     out = []
     buf = torch.empty(regions * nbytes, dtype=torch.uint8, device="cuda")
+    n = max(steps, 64)
     for mode, wg, t, d in configs:
-        graph = capture(lambda: [M.murmur_read_probe(buf[(i % regions) * nbytes:], nbytes, wg, sink, t, d, modes[mode])
-                                 for i in range(steps)])
-        us = time_graph(graph) / steps
+        us, _ = marginal_us(lambda i: M.murmur_read_probe(buf[(i % regions) * nbytes:], nbytes, wg, sink, t, d,
+                                                          modes[mode]), n, capture, time_graph)
         out.append({"mode": mode, "workgroups": wg, "threads": t, "depth": d, "bytes": nbytes, "us": round(us, 3),
                     "GBps": round(nbytes / us / 1e3, 1)})
-        del graph
     del buf
     gib = 1 << 30
     big = torch.empty(2 * gib, dtype=torch.uint8, device="cuda")
@@ -446,8 +449,9 @@ def recycled_blocks(seg0, policy, block_size: int = 16, n_outputs: int = 2700) -
 def graph_tools(stream):
     """capture(fn): fn's launches captured into a HIP graph on a side stream, replayed once to warm up;
     time_graph(graph): µs of one replay, between HIP events recorded on `stream` around it.  Before the timed
-    replay a plain read of 512 MB (twice the Infinity Cache) runs untimed, so that no data of the warm-up
-    replay is still cached when the timed one starts."""
+    replay two plain reads of 512 MB (twice the Infinity Cache) run untimed, so that no data of the warm-up
+    replay is still cached when the timed one starts; they are queued with the replay, so the GPU is busy
+    while the host submits it and the start event is followed by the replay's first kernel at once."""
     import torch
     from paper_2606_01483_amd import murmur as M
     flush_bytes = 2 * MALL_BYTES
@@ -468,8 +472,11 @@ def graph_tools(stream):
 
     def time_graph(graph) -> float:
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        M.murmur_read_probe(flush_buf, flush_bytes, 1024, flush_sink, 256, 8, M.MURMUR_PROBE_REGISTERS, stream)
         torch.cuda.synchronize()
+        # The flush reads run while the host submits the replay (no synchronisation in between), so the
+        # replay's kernels follow the start event at once: the host's submission latency stays outside.
+        for _ in range(2):
+            M.murmur_read_probe(flush_buf, flush_bytes, 1024, flush_sink, 256, 8, M.MURMUR_PROBE_REGISTERS, stream)
         t0.record(stream)
         graph.replay()
         t1.record(stream)
@@ -479,18 +486,28 @@ def graph_tools(stream):
     return capture, time_graph
 
 
+def marginal_us(launch, n: int, capture, time_graph) -> tuple[float, float]:
+    """Per-launch time of back-to-back launches without the graph's fixed start cost: replayed graphs of n and
+    of 2n launches (launch(i) issues the i-th), (t(2n) - t(n)) / n; and the plain mean t(n) / n beside it."""
+    g1 = capture(lambda: [launch(i) for i in range(n)])
+    t1 = time_graph(g1)
+    del g1
+    g2 = capture(lambda: [launch(i) for i in range(2 * n)])
+    t2 = time_graph(g2)
+    del g2
+    return (t2 - t1) / n, t1 / n
+
+
 def per_step_attn(db, steps: list[int], replicas: int, capture, time_graph) -> dict:
-    """decode_attn duration step by step: per distinct step, its retained set, then a replayed graph of
-    max(replicas, 32) back-to-back launches over it, each on the next KV replica (the replicas together
-    hold more than twice the Infinity Cache), mean per launch; the median, p90, mean, min and max over
+    """decode_attn duration step by step: per distinct step, its retained set, then the marginal per-launch
+    time (marginal_us) of back-to-back launches over it, each on the next KV replica (the replicas together
+    hold more than twice the Infinity Cache), n = max(replicas, 32); the median, p90, mean, min and max over
     the steps."""
     per = []
     n = max(replicas, 32)
     for s in sorted(set(steps)):
         db.evict(s)
-        graph = capture(lambda: [db.attend(s, r % replicas) for r in range(n)])
-        per.append(time_graph(graph) / n)
-        del graph
+        per.append(marginal_us(lambda r: db.attend(s, r % replicas), n, capture, time_graph)[0])
     a = np.array(per)
     return {"steps": len(per), "launches_per_step": n, "median": round(float(np.median(a)), 3),
             "p90": round(float(np.percentile(a, 90)), 3), "mean": round(float(a.mean()), 3),
@@ -563,11 +580,16 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
             raise RuntimeError("device error during the timed steps")
 
         # decode_attn alone: the same launches back to back (retained set of the first timed step, each
-        # launch reading the next KV replica), so the mean is the kernel's own duration.
-        log("timing decode_attn launches as a replayed HIP graph")
+        # launch reading the next KV replica).  The kernel's duration is the marginal cost of a launch in
+        # such a graph (graphs of n and 2n launches, n = max(steps, 64)): a replay also pays a fixed start
+        # (about 10 us here), which the mean over the K timed launches carries divided by K.
+        log("timing decode_attn launches as replayed HIP graphs")
         db.evict(order[0])
+        n_attn = max(steps, 64)
+        attn_us, _ = marginal_us(lambda i: db.attend(order[i % steps], i % replicas), n_attn, capture, time_graph)
         attn_graph = capture(lambda: [db.attend(order[i], rep[i]) for i in range(steps)])
-        attn_us = time_graph(attn_graph) / steps
+        attn_graph_mean_us = time_graph(attn_graph) / steps
+        del attn_graph
         if M.murmur_device_error() != 0:
             raise RuntimeError("device error during the timed decode_attn launches")
         alg_bytes = float(kv_step[order[0]] + io)  # every launch of the decode_attn graph reads this set
@@ -578,6 +600,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
     else:
         two_launch_us = None
         attn_us = step_us
+        attn_graph_mean_us = step_us
         attn_per_step = None
         alg_bytes = float(np.mean([kv_step[o] for o in order]) + io)
 
@@ -611,6 +634,7 @@ def run(config: str, steps: int, warmup: int, replicas: int | None, cpu: bool, c
                    "split_len": db.split_len or "auto"},
         "step_two_launches_us": round(two_launch_us, 3) if two_launch else None,
         "decode_attn_us": round(attn_us, 3),
+        "decode_attn_graph_mean_us": round(attn_graph_mean_us, 3),
         "decode_attn_per_step_us": attn_per_step,
         "decode_attn_event_bracket_us": None if bracket_us is None else {
             "mean": round(float(bracket_us.mean()), 3), "median": round(float(np.median(bracket_us)), 3),
