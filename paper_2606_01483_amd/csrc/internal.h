@@ -49,11 +49,16 @@ struct WideSched {
     uint32_t magic_hi;  // ceil(2^32 / n_hi)
     uint32_t magic_lo;  // ceil(2^32 / n_lo)
     uint32_t len;       // len_hi | len_lo << 9 | G << 18 (split lengths <= 256, G query heads per KV head);
-                        // the launch adds the policy mode (MURMUR_POL_* bits) << 23
+                        // the launch adds the policy mode (MURMUR_POL_* bits) << 23 and, at bit 25,
+                        // whether stride_pos < kRunRowLimit
     uint32_t hkv_b;     // Hkv | B << 16
     uint32_t magic_hkv;
     uint32_t magic_b;
 };
+
+// Row strides (elements) below this let a pass of kWaveTile consecutive rows
+// address its K/V rows with 32-bit byte offsets from its first row.
+constexpr int64_t kRunRowLimit = (int64_t)1 << 23;
 
 // Launch description of one decode_attn call, fully validated by the caller.
 // Where the attention takes the retained sets from (see AttnLaunch::src0/src1).

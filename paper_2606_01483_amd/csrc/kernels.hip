@@ -597,6 +597,58 @@ static __device__ __forceinline__ void dma_pos_ranges(const RangeTab &t, int r0,
     }
 }
 
+// Whether the ranks r0 .. r0+valid-1 of a pass lie in one piece of the range
+// table, and if so the position p0 of rank r0: the pass then reads the
+// consecutive rows p0 .. p0+valid-1, all inside [0, max_len).  One piece: no piece starts at a rank in
+// (r0, r0+valid-1], so every rank of the pass has the piece of r0 (the last k
+// with rank >= lo[k]), whatever the table.  Every argument is uniform over the
+// wavefront, so the test is scalar code.
+static __device__ __forceinline__ bool tab_run(const RangeTab &t, int r0, int valid, int max_len, int &p0) {
+    // (readfirstlane: the entries stay separate scalars; a select chain over the
+    // table's fields could otherwise become an indexed load of a copy of it)
+    int p = r0 + __builtin_amdgcn_readfirstlane(t.off[0]);
+    uint32_t first_in = 0xffffffffu;  // min over pieces k >= 1 of lo[k] - r0 - 1 (unsigned)
+#pragma unroll
+    for (int k = 1; k < kPieces; ++k) {
+        const int lo = __builtin_amdgcn_readfirstlane(t.lo[k]), off = __builtin_amdgcn_readfirstlane(t.off[k]);
+        p = r0 >= lo ? r0 + off : p;
+        first_in = min(first_in, (uint32_t)(lo - r0 - 1));
+    }
+    p0 = p;
+    // lo[k] in (r0, r0 + valid - 1] exactly when lo[k] - r0 - 1 < valid - 1 unsigned
+    return first_in >= (uint32_t)(valid - 1) && p >= 0 && p <= max_len - valid;
+}
+
+// dma_pass for a pass whose rows are consecutive (tab_run): the loads take the
+// wavefront's first K (V) row as a scalar base and a 32-bit offset per lane,
+// one offset per row shared by K and V, so issuing them costs one vector add
+// each instead of a 64-bit address computation.  Ranks at or past `valid`
+// read row p0, as in dma_pos_ranges.  Lane (q, sl) of load j reads chunk
+// sl ^ ((4j + q) & 15) of row 4j + q, as in dma_pass; that chunk's byte
+// offset 16 * (sl ^ q) ^ 64 * (j & 3) repeats with period 4 in j.
+template <bool kFull>
+static __device__ __forceinline__ void dma_pass_run(uint8_t *stage, const uint16_t *kbase, const uint16_t *vbase,
+                                                    int64_t s_pos, int p0, int valid, int lane) {
+    const int q = lane >> 4, sl = lane & 15;
+    const uint32_t row_bytes = (uint32_t)s_pos * 2u;
+    const uint8_t *kb = reinterpret_cast<const uint8_t *>(kbase + (int64_t)p0 * s_pos);
+    const uint8_t *vb = reinterpret_cast<const uint8_t *>(vbase + (int64_t)p0 * s_pos);
+    const uint32_t qrow = (uint32_t)q * row_bytes, chunk = (uint32_t)(sl ^ q) * 16u;
+    uint32_t voff[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t row = qrow + (uint32_t)(4 * j) * row_bytes;
+        const uint32_t c = chunk ^ (64u * (uint32_t)(j & 3));
+        voff[j] = (kFull || 4 * j + q < valid ? row : 0u) + c;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        __builtin_amdgcn_global_load_lds(kb + voff[j], (lds_void_t *)(stage + j * 1024), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        __builtin_amdgcn_global_load_lds(vb + voff[j], (lds_void_t *)(stage + kTileBytes + j * 1024), 16, 0, 0);
+}
+
 // Index entries of one pass into an LDS slot with one direct-to-LDS load:
 // word 8q + j holds the entry of rank r0 + 4j + q (q = 0..3, j = 0..7), so a
 // lane reads its eight entries as two 16-byte words.  The buffer resource
@@ -1573,6 +1625,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     // put a second round trip in front of the first K/V loads
     const int G = (int)((ws.len >> 18) & 0x1fu);
     const int32_t pol_per_seq = (int32_t)(ws.len >> 23) & 3;
+    const bool short_rows = (ws.len >> 25) & 1u;  // a K/V row is under kRunRowLimit elements
     // from the launch description: every dword of the loads it takes is then in use, so no
     // scratch value lands in a register a scalar load is still filling (which forces a wait)
     const int32_t max_keep = a.max_keep;
@@ -1586,7 +1639,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: the pass's rank arithmetic is scalar
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
 
@@ -1656,18 +1709,27 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
     if (r0 < r_end) {
-        int32_t pos[8];
-        if (kSrc != kSrcIndex) {
-            dma_pos_ranges(tab, r0, r_end, a.max_len, c4, pos, w.bad_pos);
-        } else {
-            dma_idx(&idx_slot[wave][0], irow, r0, lane);
-            wait_vm<0>();
-            dma_pos_index(&idx_slot[wave][0], r0, r_end, a.max_len, c4, pos, w.bad_pos);
-        }
+        const int valid = min(kWaveTile, r_end - r0);
         u32x4 qf[4];
         load_q(qf, q, row0, G, n16, c4);
-        dma_pass(stage, kbase, vbase, a.s_pos, pos, lane, kRing, nr);
-        compute_pass_lds<false, true>(stage, qf, min(kWaveTile, r_end - r0), a.scale_log2, w, n16, c4);
+        int p0;
+        if (kSrc != kSrcIndex && !kRing && short_rows && tab_run(tab, r0, valid, a.max_len, p0)) {
+            if (valid == kWaveTile)
+                dma_pass_run<true>(stage, kbase, vbase, a.s_pos, p0, valid, lane);
+            else
+                dma_pass_run<false>(stage, kbase, vbase, a.s_pos, p0, valid, lane);
+        } else {
+            int32_t pos[8];
+            if (kSrc != kSrcIndex) {
+                dma_pos_ranges(tab, r0, r_end, a.max_len, c4, pos, w.bad_pos);
+            } else {
+                dma_idx(&idx_slot[wave][0], irow, r0, lane);
+                wait_vm<0>();
+                dma_pos_index(&idx_slot[wave][0], r0, r_end, a.max_len, c4, pos, w.bad_pos);
+            }
+            dma_pass(stage, kbase, vbase, a.s_pos, pos, lane, kRing, nr);
+        }
+        compute_pass_lds<false, true>(stage, qf, valid, a.scale_log2, w, n16, c4);
     }
 
     if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
@@ -1792,7 +1854,8 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
         const WideSched &w = a.sched;
         hipLaunchKernelGGL(decode_attn_wide_kernel<kSrc>, dim3((unsigned)a.wide_wg), dim3(kWideThreads), 0, stream,
                            a.src0, a.src1, w.groups_hi, w.n_split, w.magic_hi, w.magic_lo,
-                           w.len | (uint32_t)(a.pol_per_seq & 3) << 23, w.hkv_b, w.magic_hkv, w.magic_b, a.idx,
+                           w.len | (uint32_t)(a.pol_per_seq & 3) << 23 | (uint32_t)(a.s_pos < kRunRowLimit) << 25,
+                           w.hkv_b, w.magic_hkv, w.magic_b, a.idx,
                            a.q, a);
         return;
     }
