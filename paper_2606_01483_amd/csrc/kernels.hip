@@ -1760,18 +1760,28 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
             }
         }
     }
+    // Wavefronts whose threads hold the workgroup's state (and take tickets below).
+    const int writer_waves = (G * (kHeadDim / 4) + 63) / 64;
     if ((kSrc == kSrcLayout || kRing) && g == 0 &&
-        (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER)))  // per-layer policies: one set per layer
-        write_retained<kWideThreads>(a, (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b, cnt_seq,
-                                     policy_bad, rg, max_keep, tid, r_begin,
-                                     split == n - 1 ? max_keep : r_begin + (int)len);
+        (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER))) {  // per-layer policies: one set per layer
+        const int b_out = (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b;
+        const int r_hi = split == n - 1 ? max_keep : r_begin + (int)len;
+        // By the wavefronts that take no ticket when they are half of them: a
+        // ticket then waits for the partial stores only, not for these.
+        if (writer_waves <= kWideWaves / 2) {
+            if (wave >= kWideWaves / 2)
+                write_retained<kWideThreads / 2>(a, b_out, cnt_seq, policy_bad, rg, max_keep, tid - kWideThreads / 2,
+                                                 r_begin, r_hi);
+        } else {
+            write_retained<kWideThreads>(a, b_out, cnt_seq, policy_bad, rg, max_keep, tid, r_begin, r_hi);
+        }
+    }
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (n == 1) return;
     // Tickets: every writer wavefront takes one once its own partial stores
     // have completed; the group is complete when all n * writer_waves are
     // taken, and the workgroup whose wavefront took the last one merges.
-    const int writer_waves = (G * (kHeadDim / 4) + 63) / 64;
     const int total = (int)n * writer_waves;
     int last = 0;
     if (wave < writer_waves) {
