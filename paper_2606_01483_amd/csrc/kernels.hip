@@ -647,6 +647,33 @@ static __device__ __forceinline__ void dma_pass_run(uint8_t *stage, const uint16
 #pragma unroll
     for (int j = 0; j < 8; ++j)
         __builtin_amdgcn_global_load_lds(vb + voff[j], (lds_void_t *)(stage + kTileBytes + j * 1024), 16, 0, 0);
+    // Ends the path with a statement of its own: the compiler would otherwise
+    // sink the last load of this and dma_pass's path into one shared block,
+    // which takes a 64-bit address.
+    asm volatile("" ::: "memory");
+}
+
+// The 16 K/V loads of the pass at ranks r0 .. min(r0 + kWaveTile, r_end) - 1
+// from the range table: consecutive rows through dma_pass_run (tab_run; not
+// for ring storage, whose current row comes from another buffer), else
+// per-row positions through dma_pass.  short_rows: stride_pos < kRunRowLimit.
+template <bool kRing>
+static __device__ __forceinline__ void dma_pass_ranges(uint8_t *stage, const RangeTab &tab, int r0, int r_end,
+                                                       int max_len, bool short_rows, const uint16_t *kbase,
+                                                       const uint16_t *vbase, int64_t s_pos, int lane, int c4,
+                                                       int &bad, const NewRows &nr) {
+    const int valid = min(kWaveTile, r_end - r0);
+    int p0;
+    if (!kRing && short_rows && tab_run(tab, r0, valid, max_len, p0)) {
+        if (valid == kWaveTile)
+            dma_pass_run<true>(stage, kbase, vbase, s_pos, p0, valid, lane);
+        else
+            dma_pass_run<false>(stage, kbase, vbase, s_pos, p0, valid, lane);
+    } else {
+        int32_t pos[8];
+        dma_pos_ranges(tab, r0, r_end, max_len, c4, pos, bad);
+        dma_pass(stage, kbase, vbase, s_pos, pos, lane, kRing, nr);
+    }
 }
 
 // Index entries of one pass into an LDS slot with one direct-to-LDS load:
@@ -1303,7 +1330,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: the passes' rank arithmetic is scalar
     const int n16 = lane & 15;
     const int c4 = lane >> 4;
 
@@ -1356,6 +1383,7 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     if (kSrc != kSrcIndex)
         materialize(tab.lo[1], tab.lo[2], tab.lo[3], tab.lo[4], tab.lo[5], tab.off[0], tab.off[1], tab.off[2],
                     tab.off[3], tab.off[4], tab.off[5]);
+    const bool short_rows = a.s_pos < kRunRowLimit;
     if (r < r_end && kStages == 1) {
         int32_t pos[8];
         if (kSrc == kSrcIndex) {
@@ -1364,12 +1392,13 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
         }
         for (int k = 0;; r += kSplitUnit, ++k) {
             if (kSrc != kSrcIndex) {
-                dma_pos_ranges(tab, r, r_end, a.max_len, c4, pos, w.bad_pos);
+                dma_pass_ranges<kRing>(st[0], tab, r, r_end, a.max_len, short_rows, kbase, vbase, a.s_pos, lane, c4,
+                                       w.bad_pos, nr);
             } else {
                 wait_vm<1>();  // this pass's entries; the next pass's may stay in flight
                 dma_pos_index(ring[k & 1], r, r_end, a.max_len, c4, pos, w.bad_pos);
+                dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
             }
-            dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
             wait_vm<0>();
             compute_pass_lds<true>(st[0], qf, min(kWaveTile, r_end - r), a.scale_log2, w, n16, c4);
             if (r + kSplitUnit >= r_end) break;
@@ -1378,25 +1407,27 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     } else if (r < r_end) {
         int32_t pos[8];
         if (kSrc != kSrcIndex) {
-            dma_pos_ranges(tab, r, r_end, a.max_len, c4, pos, w.bad_pos);
+            dma_pass_ranges<kRing>(st[0], tab, r, r_end, a.max_len, short_rows, kbase, vbase, a.s_pos, lane, c4,
+                                   w.bad_pos, nr);
         } else {
             dma_idx(ring[0], irow, r, lane);
             dma_idx(ring[1], irow, r + kSplitUnit, lane);
             wait_vm<1>();
             dma_pos_index(ring[0], r, r_end, a.max_len, c4, pos, w.bad_pos);
+            dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
         }
-        dma_pass(st[0], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
         for (int k = 0;; r += kSplitUnit, ++k) {
             const uint8_t *cur = st[k & 1];
             if (r + kSplitUnit < r_end) {
                 if (kSrc != kSrcIndex) {
-                    dma_pos_ranges(tab, r + kSplitUnit, r_end, a.max_len, c4, pos, w.bad_pos);
+                    dma_pass_ranges<kRing>(st[(k + 1) & 1], tab, r + kSplitUnit, r_end, a.max_len, short_rows, kbase,
+                                           vbase, a.s_pos, lane, c4, w.bad_pos, nr);
                 } else {
                     wait_vm<kStageLoads>();  // entries of the next pass (issued before this pass's rows)
                     dma_pos_index(ring[(k + 1) & 1], r + kSplitUnit, r_end, a.max_len, c4, pos, w.bad_pos);
                     dma_idx(ring[k & 1], irow, r + 2 * kSplitUnit, lane);
+                    dma_pass(st[(k + 1) & 1], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
                 }
-                dma_pass(st[(k + 1) & 1], kbase, vbase, a.s_pos, pos, lane, kRing, nr);
                 if (kSrc != kSrcIndex)
                     wait_vm<kStageLoads>();  // this pass's rows; the next pass's stay in flight
                 else
@@ -1712,21 +1743,14 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
         const int valid = min(kWaveTile, r_end - r0);
         u32x4 qf[4];
         load_q(qf, q, row0, G, n16, c4);
-        int p0;
-        if (kSrc != kSrcIndex && !kRing && short_rows && tab_run(tab, r0, valid, a.max_len, p0)) {
-            if (valid == kWaveTile)
-                dma_pass_run<true>(stage, kbase, vbase, a.s_pos, p0, valid, lane);
-            else
-                dma_pass_run<false>(stage, kbase, vbase, a.s_pos, p0, valid, lane);
+        if (kSrc != kSrcIndex) {
+            dma_pass_ranges<kRing>(stage, tab, r0, r_end, a.max_len, short_rows, kbase, vbase, a.s_pos, lane, c4,
+                                   w.bad_pos, nr);
         } else {
             int32_t pos[8];
-            if (kSrc != kSrcIndex) {
-                dma_pos_ranges(tab, r0, r_end, a.max_len, c4, pos, w.bad_pos);
-            } else {
-                dma_idx(&idx_slot[wave][0], irow, r0, lane);
-                wait_vm<0>();
-                dma_pos_index(&idx_slot[wave][0], r0, r_end, a.max_len, c4, pos, w.bad_pos);
-            }
+            dma_idx(&idx_slot[wave][0], irow, r0, lane);
+            wait_vm<0>();
+            dma_pos_index(&idx_slot[wave][0], r0, r_end, a.max_len, c4, pos, w.bad_pos);
             dma_pass(stage, kbase, vbase, a.s_pos, pos, lane, kRing, nr);
         }
         compute_pass_lds<false, true>(stage, qf, valid, a.scale_log2, w, n16, c4);
