@@ -1784,14 +1784,14 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
             }
         }
     }
-    // Wavefronts whose threads hold the workgroup's state (and take tickets below).
+    // Wavefronts whose threads hold the workgroup's state (and store the partial).
     const int writer_waves = (G * (kHeadDim / 4) + 63) / 64;
     if ((kSrc == kSrcLayout || kRing) && g == 0 &&
         (layer == 0 || (pol_per_seq & MURMUR_POL_PER_LAYER))) {  // per-layer policies: one set per layer
         const int b_out = (pol_per_seq & MURMUR_POL_PER_LAYER) ? layer * B + b : b;
         const int r_hi = split == n - 1 ? max_keep : r_begin + (int)len;
-        // By the wavefronts that take no ticket when they are half of them: a
-        // ticket then waits for the partial stores only, not for these.
+        // By the wavefronts that store no partial when they are half of them:
+        // the ticket then waits for the partial stores only, not for these.
         if (writer_waves <= kWideWaves / 2) {
             if (wave >= kWideWaves / 2)
                 write_retained<kWideThreads / 2>(a, b_out, cnt_seq, policy_bad, rg, max_keep, tid - kWideThreads / 2,
@@ -1803,20 +1803,21 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (n == 1) return;
-    // Tickets: every writer wavefront takes one once its own partial stores
-    // have completed; the group is complete when all n * writer_waves are
-    // taken, and the workgroup whose wavefront took the last one merges.
-    const int total = (int)n * writer_waves;
-    int last = 0;
-    if (wave < writer_waves) {
-        wait_vmem();
-        if (lane == 0) {
-            const int prev = __hip_atomic_fetch_add(&a.ticket[grp * kTicketStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            last = prev == total - 1;
-            if (last) __hip_atomic_store(&a.ticket[grp * kTicketStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+    // Ticket: one per workgroup, once every writer wavefront's partial stores
+    // have completed (each waits for its own, then the barrier); the workgroup
+    // that takes the group's n-th merges.  (A ticket per writer wavefront saves
+    // the barrier but queues four times the atomics on the group's counter,
+    // which costs more.)  The other wavefronts' stores (the retained set) are
+    // not waited for.
+    if (wave < writer_waves) wait_vmem();
+    __syncthreads();
+    if (tid == 0) {
+        const int prev = __hip_atomic_fetch_add(&a.ticket[grp * kTicketStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = prev == (int)n - 1;
+        if (s_last) __hip_atomic_store(&a.ticket[grp * kTicketStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (!barrier_or<kWideWaves>(last, s_wave_flag, wave, lane)) return;
+    __syncthreads();
+    if (!s_last) return;
     if (writer) merge_wide(a, ro, rml, (int)n, slot0, G, h, d0, lane, row0);
 }
 
