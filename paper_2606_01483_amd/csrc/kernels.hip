@@ -1599,6 +1599,51 @@ static __device__ __forceinline__ void merge_fold(const f32x4 (&o)[kMergeBatch],
 
 static_assert(32 % kMergeBatch == 0, "a batch of slots lies in one chunk of pairs");
 
+// The merge's load offsets for a group of at most kMergeBatch splits (all its
+// pairs and O values in one batch): the (max, sum) pair of slot lane & 31 of
+// the thread's head, and per slot k the O values' vector and scalar offsets
+// (out of the buffer for absent slots, as merge_o_load).  Computed before the
+// ticket, while its atomic is in flight, so that the merging workgroup issues
+// its loads right after the ticket.
+struct MergeOffsets {
+    uint32_t vml;
+    uint32_t vo[kMergeBatch];
+    uint32_t so[kMergeBatch];
+};
+static __device__ __forceinline__ MergeOffsets merge_offsets(int n, uint32_t slot0, int G, int h, int d0, int lane) {
+    MergeOffsets m;
+    const uint32_t j = (uint32_t)(lane & 31);
+    m.vml = j < (uint32_t)n ? ((slot0 + j) * (uint32_t)G + (uint32_t)h) * 8 : kNoPartial;
+    const uint32_t vo = ((slot0 * (uint32_t)G + (uint32_t)h) * kHeadDim + d0) * 4;
+    const uint32_t so = (uint32_t)G * kHeadDim * 4;
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) {
+        m.vo[k] = k < n ? vo : kNoPartial;
+        m.so[k] = k < n ? (uint32_t)k * so : 0u;
+    }
+    // opaque from here on: neither moved past the ticket nor computed again there
+    asm volatile(""
+                 : "+v"(m.vml), "+v"(m.vo[0]), "+v"(m.vo[1]), "+v"(m.vo[2]), "+v"(m.vo[3]), "+v"(m.vo[4]),
+                   "+v"(m.vo[5]), "+v"(m.vo[6]), "+v"(m.vo[7]), "+s"(m.so[0]), "+s"(m.so[1]), "+s"(m.so[2]),
+                   "+s"(m.so[3]), "+s"(m.so[4]), "+s"(m.so[5]), "+s"(m.so[6]), "+s"(m.so[7]));
+    return m;
+}
+
+// merge_wide for a group of at most kMergeBatch splits, from merge_offsets.
+static __device__ __forceinline__ void merge_wide_one_batch(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
+                                                            __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo, int n,
+                                                            int h, int d0, int lane, int64_t row0) {
+    const float pm = load_coherent1(rml, mo.vml);
+    const float pl = load_coherent1(rml, mo.vml + 4);
+    f32x4 o[kMergeBatch];
+#pragma unroll
+    for (int k = 0; k < kMergeBatch; ++k) o[k] = load_coherent4_s(ro, mo.vo[k], mo.so[k]);
+    float M = kNegInf, L = 0.f;
+    f32x4 O = {0.f, 0.f, 0.f, 0.f};
+    merge_fold(o, pm, pl, 0, 0, n, lane, M, L, O);
+    store_output(a, row0 + h, d0, O, M, L);
+}
+
 static __device__ __forceinline__ void merge_wide(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
                                                   __amdgpu_buffer_rsrc_t rml, int n, uint32_t slot0, int G, int h,
                                                   int d0, int lane, int64_t row0) {
@@ -1803,6 +1848,8 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (n == 1) return;
+    MergeOffsets mo;
+    if (n <= (uint32_t)kMergeBatch) mo = merge_offsets((int)n, slot0, G, h, d0, lane);
     // Ticket: one per workgroup, once every writer wavefront's partial stores
     // have completed (each waits for its own, then the barrier); the workgroup
     // that takes the group's n-th merges.  (A ticket per writer wavefront saves
@@ -1818,7 +1865,12 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     }
     __syncthreads();
     if (!s_last) return;
-    if (writer) merge_wide(a, ro, rml, (int)n, slot0, G, h, d0, lane, row0);
+    if (writer) {
+        if (n <= (uint32_t)kMergeBatch)
+            merge_wide_one_batch(a, ro, rml, mo, (int)n, h, d0, lane, row0);
+        else
+            merge_wide(a, ro, rml, (int)n, slot0, G, h, d0, lane, row0);
+    }
 }
 
 // Read-only streaming probe (measurement): workgroup w reads the 16-byte
