@@ -100,3 +100,55 @@ def test_attn_many_short_sequences():
     assert lse_err(db.lse.cpu().numpy(), ref_lse) <= LSE_TOL
     g_idx, g_cnt, _ = (t.cpu().numpy() for t in db.sets[0])
     assert np.array_equal(g_cnt, cnt) and np.array_equal(g_idx, idx)
+
+
+@pytest.mark.parametrize("s_pos", [(1 << 23) - 8, 1 << 23])
+def test_attn_long_row_strides(s_pos):
+    """K/V rows 2^23 - 8 and 2^23 elements apart (16 MiB per position; the head rows at the start of each).
+    Below 2^23 a pass of 32 consecutive rows addresses them from its first row with 32-bit offsets (up to 31
+    rows, about 2^29 bytes); at 2^23 the launch takes 64-bit addresses per row instead.  One sequence of 65
+    positions, eviction off, 32-position splits (the last a one-position pass), through the fused step and the
+    range-table attention, against the fp64 oracle."""
+    L, hq, hkv, D = 65, W.HQ, W.HKV, W.HEAD_DIM
+    announce(f"row stride {s_pos} elements, {L} positions")
+    rng = np.random.default_rng(4300 + (s_pos & 15))
+    k_bits = W.f32_to_bf16_bits(rng.standard_normal((1, 1, hkv, L, D), dtype=np.float32))
+    v_bits = W.f32_to_bf16_bits(rng.standard_normal((1, 1, hkv, L, D), dtype=np.float32))
+    q_bits = W.f32_to_bf16_bits(rng.standard_normal((1, 1, hq, D), dtype=np.float32))
+    scale = 1.0 / math.sqrt(D)
+    dev = torch.device("cuda")
+    span = (L - 1) * s_pos + hkv * D  # elements from the first row to the end of the last one's head rows
+    kv_dev = []
+    for bits in (k_bits, v_bits):
+        buf = torch.empty(span, dtype=torch.bfloat16, device=dev)  # only the head rows are written and read
+        rows = torch.from_numpy(bits[0, 0].transpose(1, 0, 2).copy()).view(torch.bfloat16).to(dev)  # [L, hkv, D]
+        buf.as_strided((L, hkv, D), (s_pos, D, 1)).copy_(rows)
+        kv_dev.append(buf)
+    kv = M.make_kv(kv_dev[0], kv_dev[1], 1, L, (0, 0, D, s_pos))
+    seg_d = torch.tensor([[0, L - 1, 0, 1]], dtype=torch.int32, device=dev)  # speech 0..63, output token 64
+    pol_d = torch.tensor([OFF, 0, 0, OFF, 0], dtype=torch.int32, device=dev)
+    q = torch.from_numpy(q_bits).view(torch.bfloat16).to(dev)
+    count = torch.zeros(1, dtype=torch.int32, device=dev)
+    ranges = torch.zeros((1, M.N_PIECES, 2), dtype=torch.int32, device=dev)
+    ws_bytes = M.murmur_decode_attn_workspace(1, 1, hq, hkv, L, 32)
+    ws = torch.zeros(ws_bytes // 4 + 64, dtype=torch.int32, device=dev)
+    outs = []
+    for path in ("fused", "ranges"):
+        out = torch.full((1, 1, hq, D), float("nan"), dtype=torch.float32, device=dev)
+        lse = torch.zeros((1, 1, hq), dtype=torch.float32, device=dev)
+        if path == "fused":
+            M.murmur_decode_step(seg_d, pol_d, 0, q, kv, None, count, ranges, L, 1, hq, hkv, D, scale, 32, out,
+                                 M.MURMUR_DTYPE_F32, lse, ws, ws_bytes)
+        else:
+            M.murmur_decode_attn(q, kv, None, ranges, count, L, 1, hq, hkv, D, scale, 32, out, M.MURMUR_DTYPE_F32,
+                                 lse, ws, ws_bytes)
+        torch.cuda.synchronize()
+        assert M.murmur_device_error() == 0, path
+        assert int(count.item()) == L
+        outs.append((out.cpu().numpy(), lse.cpu().numpy()))
+    del kv_dev
+    ref, ref_lse = oracle.attend(q_bits, k_bits, v_bits, np.arange(L, dtype=np.int32)[None],
+                                 np.array([L], dtype=np.int32), scale=scale, n_threads=16)
+    for (out, lse), path in zip(outs, ("fused", "ranges")):
+        assert rel_err_fp32(out, ref) <= REL_TOL, path
+        assert lse_err(lse, ref_lse) <= LSE_TOL, path
