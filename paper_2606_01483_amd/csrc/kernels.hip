@@ -886,12 +886,14 @@ static __device__ __forceinline__ int32_t seq_words(const int32_t *p0, const int
 // (kSrcRanges, the count being the table's total length), or (kSrcLayout,
 // kSrcRing) layouts (murmur_seg [B]) and policies (murmur_policy rows, see
 // policy_row).  kSrcRing gives the pieces in ring-storage rows of ring_cap
-// output slots and the row of the current token in `cur`.  An invalid layout
-// or policy gives count 0 and sets policy_bad to 1 (2: the ring cannot hold
-// the retained outputs).
+// output slots and the row of the current token in `cur`; an invalid layout or
+// policy gives count 0 and sets policy_bad to 1 (2: the ring cannot hold the
+// retained outputs).  kSrcLayout gives the pieces without the validity test,
+// whose nine input words it leaves in lw for layout_valid once the first loads
+// are out (the positions read are bounded whatever the table says).
 template <int kSrc>
 static __device__ __forceinline__ int seq_count_from(int32_t x, int32_t ring_cap, int32_t (&rg)[2 * kPieces],
-                                                     int &policy_bad, int32_t &cur) {
+                                                     int &policy_bad, int32_t &cur, int32_t (&lw)[9]) {
     if (kSrc == kSrcLayout || kSrc == kSrcRing) {
         const int32_t s0 = __builtin_amdgcn_readlane(x, 0), s1 = __builtin_amdgcn_readlane(x, 1),
                       s2 = __builtin_amdgcn_readlane(x, 2), s3 = __builtin_amdgcn_readlane(x, 3);
@@ -899,8 +901,19 @@ static __device__ __forceinline__ int seq_count_from(int32_t x, int32_t ring_cap
                       w2 = __builtin_amdgcn_readlane(x, 6), w3 = __builtin_amdgcn_readlane(x, 7),
                       w4 = __builtin_amdgcn_readlane(x, 8);
         Pieces pc;
-        const int rc = kSrc == kSrcRing ? ring_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, ring_cap, &pc, &cur)
-                                        : retained_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, &pc);
+        if (kSrc == kSrcLayout) {
+            retained_pieces_unchecked(s0, s1, s2, s3, w0, w1, w2, w3, w4, &pc);
+            const int32_t words[9] = {s0, s1, s2, s3, w0, w1, w2, w3, w4};
+#pragma unroll
+            for (int k = 0; k < 9; ++k) lw[k] = words[k];
+#pragma unroll
+            for (int k = 0; k < kPieces; ++k) {
+                rg[2 * k] = pc.start[k];
+                rg[2 * k + 1] = pc.len[k];
+            }
+            return pc.count;
+        }
+        const int rc = ring_pieces(s0, s1, s2, s3, w0, w1, w2, w3, w4, ring_cap, &pc, &cur);
         if (rc != 0) {
             policy_bad = rc == -2 ? 2 : 1;
 #pragma unroll
@@ -923,6 +936,16 @@ static __device__ __forceinline__ int seq_count_from(int32_t x, int32_t ring_cap
         return c;
     }
     return __builtin_amdgcn_readfirstlane(x);
+}
+
+// layout_valid of the words seq_count_from left, evaluated where it is called:
+// the words pass through an opaque statement that also orders memory, so the
+// compiler neither hoists the test in front of the loads issued before it nor
+// reuses earlier work.
+static __device__ __forceinline__ bool layout_valid_late(const int32_t (&lw)[9]) {
+    int32_t v0 = lw[0], v1 = lw[1], v2 = lw[2], v3 = lw[3], v4 = lw[4], v5 = lw[5], v6 = lw[6], v7 = lw[7], v8 = lw[8];
+    asm volatile("" : "+s"(v0), "+s"(v1), "+s"(v2), "+s"(v3), "+s"(v4), "+s"(v5), "+s"(v6), "+s"(v7), "+s"(v8)::"memory");
+    return layout_valid(v0, v1, v2, v3, v4, v5, v6, v7, v8);
 }
 
 // Count of sequence b and, unless kSrcIndex, its range table, read with
@@ -1751,8 +1774,8 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
                 a.ticket, a.part_ml, a.part_o, a.part_ml_bytes, a.part_o_bytes, a.out_f32);
     if (kSrc == kSrcLayout || kSrc == kSrcRing) materialize(a.idx_out, a.count_out, a.ranges_out);
     if (kSrc == kSrcRing) materialize(a.ring_cap, a.k_new, a.v_new);
-    const int cnt_seq = seq_count_from<kSrc>(seq_w, a.ring_cap, rg, policy_bad, cur_row);
-    const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
+    int32_t lw[9];  // kSrcLayout: the layout and policy words, tested once the first loads are out
+    int cnt_seq = seq_count_from<kSrc>(seq_w, a.ring_cap, rg, policy_bad, cur_row, lw);
     const int cnt = cnt_seq < 0 ? 0 : (cnt_seq > max_keep ? max_keep : cnt_seq);
     const int r_begin = (int)(split * len);
     const int r_end = min(r_begin + (int)len, cnt);
@@ -1777,6 +1800,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     WaveAcc w;
     wave_acc_reset(w);
     const int r0 = r_begin + wave * kWaveTile;
+    bool layout_ok = true;
     materialize(kbase, vbase, a.s_pos, a.max_len, a.scale_log2, cnt);
     if (kRing) materialize(nr.k, nr.v, nr.cur);
     NewRowCopy app{};
@@ -1798,8 +1822,19 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
             dma_pos_index(&idx_slot[wave][0], r0, r_end, a.max_len, c4, pos, w.bad_pos);
             dma_pass(stage, kbase, vbase, a.s_pos, pos, lane, kRing, nr);
         }
+        if (kSrc == kSrcLayout) layout_ok = layout_valid_late(lw);  // while this pass's rows are on their way
         compute_pass_lds<false, true>(stage, qf, valid, a.scale_log2, w, n16, c4);
+    } else if (kSrc == kSrcLayout) {
+        layout_ok = layout_valid_late(lw);
     }
+    if (kSrc == kSrcLayout && !layout_ok) {  // as an invalid layout gives it: count 0, empty table, no positions
+        policy_bad = 1;
+        cnt_seq = 0;
+#pragma unroll
+        for (int k = 0; k < 2 * kPieces; ++k) rg[k] = 0;
+        w.bad_pos = 0;
+    }
+    const bool bad_count = cnt_seq < 1 || cnt_seq > max_keep;
 
     if (kRing) store_new_row(a, app, nr, kbase, vbase, lane);
     float *o_lds = reinterpret_cast<float *>(&stages[0][0]);  // each wavefront's O rows in its own stage

@@ -51,17 +51,29 @@ struct Pieces {
     int32_t count;
 };
 
-// Returns 0 and fills *out, or -1 if the layout or policy is invalid (negative
-// lengths, j < 1, a window of 0 or below -1, a negative delay or sink count,
-// or a sequence longer than 2^31 - 1 positions).
-MURMUR_HD inline int retained_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s, int32_t d,
-                                     int32_t n_ss, int32_t w_o, int32_t n_so, Pieces *out) {
-    if (p_pre < 0 || l_s < 0 || p_mid < 0 || j < 1) return -1;
-    if (!(w_s == -1 || w_s >= 1) || d < 0 || n_ss < 0) return -1;
-    if (!(w_o == -1 || w_o >= 1) || n_so < 0) return -1;
-    const int64_t total = (int64_t)p_pre + l_s + p_mid + j;
-    if (total > 0x7fffffffLL) return -1;
-    const int32_t speech0 = p_pre, mid0 = p_pre + l_s, out0 = p_pre + l_s + p_mid;
+// Whether a layout and policy are valid: no negative length, j >= 1, windows
+// -1 or >= 1, no negative delay or sink count, and a sequence of at most
+// 2^31 - 1 positions.
+MURMUR_HD inline bool layout_valid(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s, int32_t d,
+                                   int32_t n_ss, int32_t w_o, int32_t n_so) {
+    if (p_pre < 0 || l_s < 0 || p_mid < 0 || j < 1) return false;
+    if (!(w_s == -1 || w_s >= 1) || d < 0 || n_ss < 0) return false;
+    if (!(w_o == -1 || w_o >= 1) || n_so < 0) return false;
+    return (int64_t)p_pre + l_s + p_mid + j <= 0x7fffffffLL;
+}
+
+// 32-bit sums and differences that wrap instead of overflowing: for a valid
+// layout every intermediate value fits, so they are exact there.
+MURMUR_HD inline int32_t wrap_add(int32_t a, int32_t b) { return (int32_t)((uint32_t)a + (uint32_t)b); }
+MURMUR_HD inline int32_t wrap_sub(int32_t a, int32_t b) { return (int32_t)((uint32_t)a - (uint32_t)b); }
+
+// The pieces of the retained set without the validity test: for a valid layout
+// and policy the same as retained_pieces; for an invalid one some well-defined
+// but meaningless table (a caller that uses it must bound every position it
+// reads and discard the result once layout_valid says no).
+MURMUR_HD inline void retained_pieces_unchecked(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s,
+                                                int32_t d, int32_t n_ss, int32_t w_o, int32_t n_so, Pieces *out) {
+    const int32_t speech0 = p_pre, mid0 = wrap_add(p_pre, l_s), out0 = wrap_add(mid0, p_mid);
 
     out->start[0] = 0;
     out->len[0] = p_pre;
@@ -70,23 +82,25 @@ MURMUR_HD inline int retained_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, 
     if (w_s == -1 || w_s >= l_s) {
         out->start[1] = speech0;
         out->len[1] = l_s;
-        out->start[2] = speech0 + l_s;
+        out->start[2] = mid0;
         out->len[2] = 0;
     } else {
         const int32_t first_move = d > 1 ? d : 1;
-        int32_t l = j >= first_move ? j - first_move + 1 : 0;
-        if (l > l_s - w_s) l = l_s - w_s;
+        int32_t l = j >= first_move ? wrap_add(wrap_sub(j, first_move), 1) : 0;
+        const int32_t room = wrap_sub(l_s, w_s);
+        if (l > room) l = room;
         const int32_t ns = n_ss < l_s ? n_ss : l_s;
+        const int32_t win_end = wrap_add(l, w_s);
         if (l <= ns) {  // the window touches or overlaps the sinks: one piece
-            const int32_t end = ns > l + w_s ? ns : l + w_s;
+            const int32_t end = ns > win_end ? ns : win_end;
             out->start[1] = speech0;
             out->len[1] = end;
-            out->start[2] = speech0 + end;
+            out->start[2] = wrap_add(speech0, end);
             out->len[2] = 0;
         } else {
             out->start[1] = speech0;
             out->len[1] = ns;
-            out->start[2] = speech0 + l;
+            out->start[2] = wrap_add(speech0, l);
             out->len[2] = w_s;
         }
     }
@@ -95,29 +109,30 @@ MURMUR_HD inline int retained_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, 
     out->len[3] = p_mid;
 
     // Output: 0-based sinks [0, so) united with the window [j - w, j).
-    if (w_o == -1 || w_o >= j) {
+    const int32_t w0 = wrap_sub(j, w_o);
+    const int32_t so = n_so < j ? n_so : j;
+    if (w_o == -1 || w_o >= j || w0 <= so) {
         out->start[4] = out0;
         out->len[4] = j;
-        out->start[5] = out0 + j;
+        out->start[5] = wrap_add(out0, j);
         out->len[5] = 0;
     } else {
-        const int32_t so = n_so < j ? n_so : j;
-        const int32_t w0 = j - w_o;
-        if (w0 <= so) {
-            out->start[4] = out0;
-            out->len[4] = j;
-            out->start[5] = out0 + j;
-            out->len[5] = 0;
-        } else {
-            out->start[4] = out0;
-            out->len[4] = so;
-            out->start[5] = out0 + w0;
-            out->len[5] = w_o;
-        }
+        out->start[4] = out0;
+        out->len[4] = so;
+        out->start[5] = wrap_add(out0, w0);
+        out->len[5] = w_o;
     }
     int32_t c = 0;
-    for (int k = 0; k < kPieces; ++k) c += out->len[k];
+    for (int k = 0; k < kPieces; ++k) c = wrap_add(c, out->len[k]);
     out->count = c;
+}
+
+// Returns 0 and fills *out, or -1 if the layout or policy is invalid (see
+// layout_valid).
+MURMUR_HD inline int retained_pieces(int32_t p_pre, int32_t l_s, int32_t p_mid, int32_t j, int32_t w_s, int32_t d,
+                                     int32_t n_ss, int32_t w_o, int32_t n_so, Pieces *out) {
+    if (!layout_valid(p_pre, l_s, p_mid, j, w_s, d, n_ss, w_o, n_so)) return -1;
+    retained_pieces_unchecked(p_pre, l_s, p_mid, j, w_s, d, n_ss, w_o, n_so, out);
     return 0;
 }
 
