@@ -1652,19 +1652,36 @@ static __device__ __forceinline__ MergeOffsets merge_offsets(int n, uint32_t slo
     return m;
 }
 
-// merge_wide for a group of at most kMergeBatch splits, from merge_offsets.
-static __device__ __forceinline__ void merge_wide_one_batch(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
-                                                            __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo, int n,
+// Exactly kCnt loads of O: a load past the last slot would be answered with
+// zeros without a memory access, but it still passes through the compute
+// unit's address unit, on the merging workgroup's critical path (three such
+// loads per thread cost c3 0.2 us).
+template <int kCnt>
+static __device__ __forceinline__ void merge_wide_one_batch_n(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
+                                                            __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo,
                                                             int h, int d0, int lane, int64_t row0) {
     const float pm = load_coherent1(rml, mo.vml);
     const float pl = load_coherent1(rml, mo.vml + 4);
     f32x4 o[kMergeBatch];
 #pragma unroll
-    for (int k = 0; k < kMergeBatch; ++k) o[k] = load_coherent4_s(ro, mo.vo[k], mo.so[k]);
+    for (int k = 0; k < kCnt; ++k) o[k] = load_coherent4_s(ro, mo.vo[k], mo.so[k]);
     float M = kNegInf, L = 0.f;
     f32x4 O = {0.f, 0.f, 0.f, 0.f};
-    merge_fold(o, pm, pl, 0, 0, n, lane, M, L, O);
+    merge_fold_n<kCnt>(o, pm, pl, 0, 0, lane, M, L, O);
     store_output(a, row0 + h, d0, O, M, L);
+}
+static __device__ __forceinline__ void merge_wide_one_batch(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
+                                                            __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo, int n,
+                                                            int h, int d0, int lane, int64_t row0) {
+    switch (n) {
+    case 2: merge_wide_one_batch_n<2>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 3: merge_wide_one_batch_n<3>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 4: merge_wide_one_batch_n<4>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 5: merge_wide_one_batch_n<5>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 6: merge_wide_one_batch_n<6>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 7: merge_wide_one_batch_n<7>(a, ro, rml, mo, h, d0, lane, row0); break;
+    default: merge_wide_one_batch_n<8>(a, ro, rml, mo, h, d0, lane, row0); break;
+    }
 }
 
 static __device__ __forceinline__ void merge_wide(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
