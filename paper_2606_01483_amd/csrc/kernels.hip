@@ -1238,42 +1238,62 @@ static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, Sl
     }
 }
 
-// Up to kMergeBatch partials (every group of the 12 x 300 s workloads): one
-// batch, all loads of a thread in flight at once.  The loads are unconditional
-// (a branch around a load lets the compiler wait for it inside the branch):
-// one past the last partial gets an offset outside the buffer resource's
-// range, which the hardware answers with zero and no memory access, and a
-// select drops it.
+// Where a load past the last partial must stay unconditional (a branch around a
+// load lets the compiler wait for it inside the branch), it gets this offset,
+// outside the buffer resource's range, which the hardware answers with zero
+// and no memory access; a select or a zero weight drops it.
 constexpr uint32_t kNoPartial = 0x80000000u;  // a byte offset past both partial arrays (each < 2^31 bytes)
 
-template <int kThreads, typename SlotOf>
-static __device__ __forceinline__ void merge_one_batch(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
-                                                       int64_t row0) {
+// Up to kMergeBatch partials (every group of the 12 x 300 s workloads): one
+// batch, all loads of a thread in flight at once.
+
+template <int kThreads, int kCnt, typename SlotOf>
+static __device__ __forceinline__ void merge_one_batch_n(const AttnLaunch &a, SlotOf slot_of, int G, int tid,
+                                                         int64_t row0) {
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
     for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        float mm[kMergeBatch], ll[kMergeBatch];
-        f32x4 oo[kMergeBatch];
+        float mm[kCnt], ll[kCnt];
+        f32x4 oo[kCnt];
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; ++k) {
-            const uint32_t prow = slot_of(k < n ? k : 0) * G + h;
-            mm[k] = load_coherent1(rml, k < n ? prow * 8 : kNoPartial);
-            ll[k] = load_coherent1(rml, k < n ? prow * 8 + 4 : kNoPartial);
-            oo[k] = load_coherent4(ro, k < n ? (prow * kHeadDim + d0) * 4 : kNoPartial);
+        for (int k = 0; k < kCnt; ++k) {
+            const uint32_t prow = slot_of(k) * G + h;
+            mm[k] = load_coherent1(rml, prow * 8);
+            ll[k] = load_coherent1(rml, prow * 8 + 4);
+            oo[k] = load_coherent4(ro, (prow * kHeadDim + d0) * 4);
         }
         float M = mm[0];
 #pragma unroll
-        for (int k = 1; k < kMergeBatch; ++k) M = k < n ? fmaxf(M, mm[k]) : M;
+        for (int k = 1; k < kCnt; ++k) M = fmaxf(M, mm[k]);
         float L = 0.f;
         f32x4 O = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; ++k) {
-            const float f = (k >= n || mm[k] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mm[k] - M);
+        for (int k = 0; k < kCnt; ++k) {
+            const float f = mm[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mm[k] - M);
             L += ll[k] * f;
             O += oo[k] * f;
         }
         store_output(a, row0 + h, d0, O, M, L);
+    }
+}
+
+// Up to kMergeBatch partials in one batch of loads, specialised on the count:
+// exactly n loads of each kind (a load past the last partial, even one the
+// hardware answers with zeros, still passes through the address unit).
+template <int kThreads, typename SlotOf>
+static __device__ __forceinline__ void merge_one_batch(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
+                                                       int64_t row0) {
+    static_assert(kMergeBatch == 8, "one case per batch size");
+    switch (n) {
+    case 1: merge_one_batch_n<kThreads, 1>(a, slot_of, G, tid, row0); break;
+    case 2: merge_one_batch_n<kThreads, 2>(a, slot_of, G, tid, row0); break;
+    case 3: merge_one_batch_n<kThreads, 3>(a, slot_of, G, tid, row0); break;
+    case 4: merge_one_batch_n<kThreads, 4>(a, slot_of, G, tid, row0); break;
+    case 5: merge_one_batch_n<kThreads, 5>(a, slot_of, G, tid, row0); break;
+    case 6: merge_one_batch_n<kThreads, 6>(a, slot_of, G, tid, row0); break;
+    case 7: merge_one_batch_n<kThreads, 7>(a, slot_of, G, tid, row0); break;
+    default: merge_one_batch_n<kThreads, 8>(a, slot_of, G, tid, row0); break;
     }
 }
 
