@@ -1586,9 +1586,10 @@ static __device__ __forceinline__ void merge_o_load(f32x4 (&o)[kMergeBatch], __a
 // Folds the kCnt slots base .. base+kCnt-1 into (M, L, O); pair j of the
 // current chunk of pairs (pm, pl) sits in lane (lane & 32) + j, for
 // j = base - cb + k.
-template <int kCnt>
-static __device__ __forceinline__ void merge_fold_n(const f32x4 (&o)[kMergeBatch], float pm, float pl, int cb,
-                                                    int base, int lane, float &M, float &L, f32x4 &O) {
+template <int kCnt, int kLen>
+static __device__ __forceinline__ void merge_fold_n(const f32x4 (&o)[kLen], float pm, float pl, int cb, int base,
+                                                    int lane, float &M, float &L, f32x4 &O) {
+    static_assert(kCnt <= kLen && kCnt <= 32, "the slots lie in the array and in one chunk of pairs");
     float m[kCnt], l[kCnt];
 #pragma unroll
     for (int k = 0; k < kCnt; ++k) {
@@ -1642,65 +1643,80 @@ static __device__ __forceinline__ void merge_fold(const f32x4 (&o)[kMergeBatch],
 
 static_assert(32 % kMergeBatch == 0, "a batch of slots lies in one chunk of pairs");
 
-// The merge's load offsets for a group of at most kMergeBatch splits (all its
-// pairs and O values in one batch): the (max, sum) pair of slot lane & 31 of
-// the thread's head, and per slot k the O values' vector and scalar offsets
-// (out of the buffer for absent slots, as merge_o_load).  Computed before the
-// ticket, while its atomic is in flight, so that the merging workgroup issues
-// its loads right after the ticket.
+// The merge's load offsets for a group of at most kMergeDirect splits (all
+// its pairs and O values loaded at once): the (max, sum) pair of slot lane & 31
+// of the thread's head (out of the buffer past the last slot), the O values'
+// vector offset, which every slot shares, and per slot its scalar distance.
+// Computed before the ticket, while its atomic is in flight, so that the
+// merging workgroup issues its loads right after the ticket.
+constexpr int kMergeDirect = 2 * kMergeBatch;
 struct MergeOffsets {
     uint32_t vml;
-    uint32_t vo[kMergeBatch];
-    uint32_t so[kMergeBatch];
+    uint32_t vo;
+    uint32_t so[kMergeDirect];  // so[0] = 0
 };
 static __device__ __forceinline__ MergeOffsets merge_offsets(int n, uint32_t slot0, int G, int h, int d0, int lane) {
     MergeOffsets m;
     const uint32_t j = (uint32_t)(lane & 31);
     m.vml = j < (uint32_t)n ? ((slot0 + j) * (uint32_t)G + (uint32_t)h) * 8 : kNoPartial;
-    const uint32_t vo = ((slot0 * (uint32_t)G + (uint32_t)h) * kHeadDim + d0) * 4;
-    const uint32_t so = (uint32_t)G * kHeadDim * 4;
+    m.vo = ((slot0 * (uint32_t)G + (uint32_t)h) * kHeadDim + d0) * 4;
+    const uint32_t so = (uint32_t)G * kHeadDim * 4;  // bytes from one slot's rows to the next
 #pragma unroll
-    for (int k = 0; k < kMergeBatch; ++k) {
-        m.vo[k] = k < n ? vo : kNoPartial;
-        m.so[k] = k < n ? (uint32_t)k * so : 0u;
-    }
+    for (int k = 0; k < kMergeDirect; ++k) m.so[k] = (uint32_t)k * so;
     // opaque from here on: neither moved past the ticket nor computed again there
     asm volatile(""
-                 : "+v"(m.vml), "+v"(m.vo[0]), "+v"(m.vo[1]), "+v"(m.vo[2]), "+v"(m.vo[3]), "+v"(m.vo[4]),
-                   "+v"(m.vo[5]), "+v"(m.vo[6]), "+v"(m.vo[7]), "+s"(m.so[0]), "+s"(m.so[1]), "+s"(m.so[2]),
-                   "+s"(m.so[3]), "+s"(m.so[4]), "+s"(m.so[5]), "+s"(m.so[6]), "+s"(m.so[7]));
+                 : "+v"(m.vml), "+v"(m.vo), "+s"(m.so[1]), "+s"(m.so[2]), "+s"(m.so[3]), "+s"(m.so[4]),
+                   "+s"(m.so[5]), "+s"(m.so[6]), "+s"(m.so[7]), "+s"(m.so[8]), "+s"(m.so[9]), "+s"(m.so[10]),
+                   "+s"(m.so[11]), "+s"(m.so[12]), "+s"(m.so[13]), "+s"(m.so[14]), "+s"(m.so[15]));
     return m;
 }
 
-// Exactly kCnt loads of O: a load past the last slot would be answered with
-// zeros without a memory access, but it still passes through the compute
-// unit's address unit, on the merging workgroup's critical path (three such
-// loads per thread cost c3 0.2 us).
+// Exactly kCnt loads of O, all in flight before the fold: a load past the last
+// slot would be answered with zeros without a memory access, but it still
+// passes through the compute unit's address unit, on the merging workgroup's
+// critical path (three such loads per thread cost c3 0.2 us).
 template <int kCnt>
-static __device__ __forceinline__ void merge_wide_one_batch_n(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
-                                                            __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo,
-                                                            int h, int d0, int lane, int64_t row0) {
+static __device__ __forceinline__ void merge_wide_direct_n(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
+                                                         __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo, int h,
+                                                         int d0, int lane, int64_t row0) {
+    static_assert(kCnt <= kMergeDirect, "offsets for every slot");
     const float pm = load_coherent1(rml, mo.vml);
     const float pl = load_coherent1(rml, mo.vml + 4);
-    f32x4 o[kMergeBatch];
+    f32x4 o[kCnt];
 #pragma unroll
-    for (int k = 0; k < kCnt; ++k) o[k] = load_coherent4_s(ro, mo.vo[k], mo.so[k]);
+    for (int k = 0; k < kCnt; ++k) o[k] = load_coherent4_s(ro, mo.vo, k == 0 ? 0u : mo.so[k]);
     float M = kNegInf, L = 0.f;
     f32x4 O = {0.f, 0.f, 0.f, 0.f};
     merge_fold_n<kCnt>(o, pm, pl, 0, 0, lane, M, L, O);
     store_output(a, row0 + h, d0, O, M, L);
 }
-static __device__ __forceinline__ void merge_wide_one_batch(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
-                                                            __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo, int n,
-                                                            int h, int d0, int lane, int64_t row0) {
+static __device__ __forceinline__ void merge_wide_direct(const AttnLaunch &a, __amdgpu_buffer_rsrc_t ro,
+                                                         __amdgpu_buffer_rsrc_t rml, const MergeOffsets &mo, int n,
+                                                         int h, int d0, int lane, int64_t row0) {
+    static_assert(kMergeDirect == 16, "one case per count");
+    // two searches, so that the smaller counts take no more branches than
+    // one over 2 .. 8
+    if (n <= 8) {
+        switch (n) {
+        case 2: merge_wide_direct_n<2>(a, ro, rml, mo, h, d0, lane, row0); break;
+        case 3: merge_wide_direct_n<3>(a, ro, rml, mo, h, d0, lane, row0); break;
+        case 4: merge_wide_direct_n<4>(a, ro, rml, mo, h, d0, lane, row0); break;
+        case 5: merge_wide_direct_n<5>(a, ro, rml, mo, h, d0, lane, row0); break;
+        case 6: merge_wide_direct_n<6>(a, ro, rml, mo, h, d0, lane, row0); break;
+        case 7: merge_wide_direct_n<7>(a, ro, rml, mo, h, d0, lane, row0); break;
+        default: merge_wide_direct_n<8>(a, ro, rml, mo, h, d0, lane, row0); break;
+        }
+        return;
+    }
     switch (n) {
-    case 2: merge_wide_one_batch_n<2>(a, ro, rml, mo, h, d0, lane, row0); break;
-    case 3: merge_wide_one_batch_n<3>(a, ro, rml, mo, h, d0, lane, row0); break;
-    case 4: merge_wide_one_batch_n<4>(a, ro, rml, mo, h, d0, lane, row0); break;
-    case 5: merge_wide_one_batch_n<5>(a, ro, rml, mo, h, d0, lane, row0); break;
-    case 6: merge_wide_one_batch_n<6>(a, ro, rml, mo, h, d0, lane, row0); break;
-    case 7: merge_wide_one_batch_n<7>(a, ro, rml, mo, h, d0, lane, row0); break;
-    default: merge_wide_one_batch_n<8>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 9: merge_wide_direct_n<9>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 10: merge_wide_direct_n<10>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 11: merge_wide_direct_n<11>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 12: merge_wide_direct_n<12>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 13: merge_wide_direct_n<13>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 14: merge_wide_direct_n<14>(a, ro, rml, mo, h, d0, lane, row0); break;
+    case 15: merge_wide_direct_n<15>(a, ro, rml, mo, h, d0, lane, row0); break;
+    default: merge_wide_direct_n<16>(a, ro, rml, mo, h, d0, lane, row0); break;
     }
 }
 
@@ -1921,7 +1937,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (n == 1) return;
     MergeOffsets mo;
-    if (n <= (uint32_t)kMergeBatch) mo = merge_offsets((int)n, slot0, G, h, d0, lane);
+    if (n <= (uint32_t)kMergeDirect) mo = merge_offsets((int)n, slot0, G, h, d0, lane);
     // Ticket: one per workgroup, once every writer wavefront's partial stores
     // have completed (each waits for its own, then the barrier); the workgroup
     // that takes the group's n-th merges.  (A ticket per writer wavefront saves
@@ -1938,8 +1954,8 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     __syncthreads();
     if (!s_last) return;
     if (writer) {
-        if (n <= (uint32_t)kMergeBatch)
-            merge_wide_one_batch(a, ro, rml, mo, (int)n, h, d0, lane, row0);
+        if (n <= (uint32_t)kMergeDirect)
+            merge_wide_direct(a, ro, rml, mo, (int)n, h, d0, lane, row0);
         else
             merge_wide(a, ro, rml, (int)n, slot0, G, h, d0, lane, row0);
     }
