@@ -53,13 +53,15 @@ uint32_t magic16(uint32_t d) { return d <= 1 ? 0u : (uint32_t)((((uint64_t)1 << 
 // Estimated launch time (us) of a one-round split with at most len positions per
 // workgroup and at most n splits per group (the model behind the automatic choice,
 // with constants measured on MI355X): each compute unit streams its share at
-// kCuBytesPerUs, and more than one split adds the merge chain, the merging
-// workgroup's loads of n partials and a load round trip for every further two
-// batches of partials.
+// kCuBytesPerUs, in whole passes of kWaveTile rows (a wavefront issues a pass's
+// loads whether it holds 2 rows or 32), and more than one split adds the merge
+// chain, the merging workgroup's loads of n partials and a load round trip for
+// every further two batches of partials.
 double wide_cost(int64_t len, int64_t n, int64_t G) {
     const double part_bytes = (double)G * (kHeadDim + 2) * 4.0;
     const double trips = (double)((n - 1) / (2 * kMergeBatch)) * kMergeRoundTripUs;
-    return (double)len * 4.0 * kHeadDim / kCuBytesPerUs +
+    const int64_t rows = (len + kWaveTile - 1) / kWaveTile * kWaveTile;
+    return (double)rows * 4.0 * kHeadDim / kCuBytesPerUs +
            (n > 1 ? kMergeChainUs + n * part_bytes / kCuBytesPerUs + trips : 0.0);
 }
 

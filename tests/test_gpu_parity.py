@@ -468,6 +468,24 @@ def test_max_keep_far_above_the_counts():
         assert tickets_clear(db.ws, db.ws_bytes)
 
 
+def test_merge_every_partial_count():
+    """Every count of partials per group from 2 to 18 (the merge is specialised on the count up to 16 and
+    takes batches beyond): c1's 192 retained positions in splits of 96, 64 and 32 positions, with max_keep
+    raised so that the splits past the counts hold empty partials."""
+    wl = workload("c1")
+    s = wl.steps - 1
+    ref, ref_lse = oracle_step(wl, s)
+    cases = [(96, 192), (64, 192), (64, 256), (64, 320)] + [(32, 32 * n) for n in range(6, 19)]
+    for split_len, max_keep in cases:
+        n = -(-max_keep // split_len)
+        announce(f"attn c1 step {s}, split_len {split_len}, max_keep {max_keep}: {n} partials per group")
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[s], split_len=split_len, max_keep=max_keep)
+        assert db.split_len == split_len
+        y, l = run_gpu(db, 0)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL, (split_len, max_keep)
+        assert tickets_clear(db.ws, db.ws_bytes)
+
+
 # ---- murmur_decode_step: eviction and attention in one launch ------------------------------------
 
 def check_retained_outputs(db, wl, s, buf=0):
