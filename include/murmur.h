@@ -258,7 +258,9 @@ int murmur_paged_step(const murmur_seg *seg_dev, const murmur_policy *pol_dev, i
 /* Workspace bytes murmur_decode_attn needs for these sizes and split_len
  * (0 = the automatic choice, or positions per split).
  * The workspace holds ticket counters (one per (layer, sequence, kv-head)
- * group that is split) in a region at its start
+ * group that is split, and one per set of 8 splits of a group when the
+ * LDS-staged schedule merges its 17 to 128 splits in two levels) in a region
+ * at its start
  * whose size depends on ws_bytes alone (128 bytes per KiB, rounded up to 256),
  * and the split partials after that region.  It must be zero-filled once
  * before its first use (or reset with murmur_decode_attn_workspace_init);

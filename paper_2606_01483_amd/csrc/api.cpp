@@ -147,7 +147,11 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
         p.split_len = split_len;
         p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
         if (p.n_split > 1) {
-            p.tickets = groups;
+            // a counter per group, and for a two-level merge one per set of
+            // kSubSplits splits after them
+            const int64_t n_sub = (p.n_split + kSubSplits - 1) / kSubSplits;
+            const bool two_level = p.n_split > 2 * kMergeBatch && p.n_split <= kTwoLevelMax;
+            p.tickets = groups * (two_level ? 1 + n_sub : 1);
             p.ml_bytes = round_up((size_t)groups * p.n_split * G * 2 * sizeof(float), 256);
             p.o_bytes = round_up((size_t)groups * p.n_split * G * kHeadDim * sizeof(float), 256);
         }

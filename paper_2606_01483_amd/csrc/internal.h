@@ -21,6 +21,11 @@ constexpr int kRoundWorkgroups = 256;     // one workgroup per compute unit
 constexpr int kMaxMergeSplits = 240;
 constexpr int kMaxKeep = 1 << 28;  // retained positions per sequence the attention accepts
 constexpr int kMergeBatch = 8;  // splits whose partials one merging thread loads at once
+// The LDS-staged schedule merges groups of more than 2 * kMergeBatch and at
+// most kTwoLevelMax splits in two levels, sets of kSubSplits splits first (so
+// that the second level folds at most 16 partials too).
+constexpr int kSubSplits = 8;
+constexpr int kTwoLevelMax = 128;
 // Split-choice model (measured on MI355X): one compute unit streams about 40 GB/s from HBM however many
 // wavefronts it runs, and the split-K merge chain (partial stores, ticket, loading the partials) costs
 // about 2.3 us on top of the data phase.
@@ -84,7 +89,8 @@ struct AttnLaunch {
     const int32_t *idx;
     void *out;
     float *lse;
-    int32_t *ticket;   // [groups][kTicketStride]: one counter per split (layer, sequence, KV head)
+    int32_t *ticket;   // [groups][kTicketStride]: one counter per group (layer, sequence, KV head), then
+                       // for a two-level merge one per set of kSubSplits splits, [groups][n_sub]
     float *part_ml;    // [groups][n_split][G][2]  (running max in log2 units, sum)
     float *part_o;     // [groups][n_split][G][128]
     uint32_t part_ml_bytes, part_o_bytes;  // extents of the two partial arrays (< 2^31)

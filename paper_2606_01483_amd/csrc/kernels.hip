@@ -1170,72 +1170,17 @@ static __device__ __forceinline__ void write_result(const AttnLaunch &a, const f
 // Takes a ticket for group `grp` after this workgroup's partial stores have
 // completed; true in the workgroup that draws the last of `n` tickets (which
 // also resets the counter for the next call).  Block-wide.
-static __device__ __forceinline__ bool take_ticket(const AttnLaunch &a, int grp, int n, int tid, int &s_last) {
+static __device__ __forceinline__ bool take_ticket(const AttnLaunch &a, int counter, int n, int tid, int &s_last) {
     wait_vmem();
     __syncthreads();
     if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&a.ticket[grp * kTicketStride], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        int *t = &a.ticket[(int64_t)counter * kTicketStride];
+        const int prev = __hip_atomic_fetch_add(t, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = prev == n - 1;
-        if (s_last) __hip_atomic_store(&a.ticket[grp * kTicketStride], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (s_last) __hip_atomic_store(t, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
     return s_last != 0;
-}
-
-// Cross-split log-sum-exp merge of the n partials of one group; slot_of(i)
-// gives the slot of the i-th.  Each thread owns four consecutive head dims of
-// one head and folds the partials in batches whose loads are all in flight
-// together.  Block-wide.
-// Many partials (more than 2 * kMergeBatch): the (max, sum) pairs of every
-// partial and head are staged in LDS first (one load per pair, shared by the
-// threads of a head), so the overall max is known before any O value arrives;
-// the O values then stream through two register batches, the next batch's
-// loads in flight while the current one is accumulated (loads past the last
-// partial re-read it with a zero weight, so every load is unconditional).
-// s_ml: LDS scratch of n * G * 2 floats, free by the time the merge runs.
-template <int kThreads, typename SlotOf>
-static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
-                                               int64_t row0, float *s_ml) {
-    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
-    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
-    for (int e = tid; e < n * G; e += kThreads) {
-        const int i = e / G, h = e - i * G;
-        const uint32_t prow = slot_of(i) * G + h;
-        s_ml[2 * e] = load_coherent1(rml, prow * 8);
-        s_ml[2 * e + 1] = load_coherent1(rml, prow * 8 + 4);
-    }
-    __syncthreads();
-    for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
-        const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        float M = kNegInf;
-        for (int i = 0; i < n; ++i) M = fmaxf(M, s_ml[2 * (i * G + h)]);
-        float L = 0.f;
-        f32x4 O = {0.f, 0.f, 0.f, 0.f};
-        auto load_batch = [&](int base, f32x4 (&o)[kMergeBatch]) {
-#pragma unroll
-            for (int k = 0; k < kMergeBatch; ++k)
-                o[k] = load_coherent4(ro, ((slot_of(min(base + k, n - 1)) * G + h) * kHeadDim + d0) * 4);
-        };
-        auto add_batch = [&](int base, const f32x4 (&o)[kMergeBatch]) {
-#pragma unroll
-            for (int k = 0; k < kMergeBatch; ++k) {
-                const int i = base + k;
-                const float m = s_ml[2 * (min(i, n - 1) * G + h)], l = s_ml[2 * (min(i, n - 1) * G + h) + 1];
-                const float f = (i >= n || m == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m - M);
-                L += l * f;
-                O += o[k] * f;
-            }
-        };
-        f32x4 ba[kMergeBatch], bb[kMergeBatch];
-        load_batch(0, ba);
-        for (int base = 0; base < n; base += 2 * kMergeBatch) {
-            load_batch(base + kMergeBatch, bb);
-            add_batch(base, ba);
-            load_batch(base + 2 * kMergeBatch, ba);
-            add_batch(base + kMergeBatch, bb);
-        }
-        store_output(a, row0 + h, d0, O, M, L);
-    }
 }
 
 // Where a load past the last partial must stay unconditional (a branch around a
@@ -1244,12 +1189,109 @@ static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, Sl
 // and no memory access; a select or a zero weight drops it.
 constexpr uint32_t kNoPartial = 0x80000000u;  // a byte offset past both partial arrays (each < 2^31 bytes)
 
+// Cross-split log-sum-exp merges of the n partials of one group.  Each thread
+// owns four consecutive head dims of one head and folds the partials in
+// batches whose loads are all in flight together.  Block-wide.
+// Many partials (more than 2 * kMergeBatch), slots slot0 .. slot0+n-1.  Three
+// steps, none of them a chain of dependent round trips:
+// * the (max, sum) pairs of every partial and head are staged in LDS, each
+//   thread's loads (up to kManyPairLoads) in flight together;
+// * per head, its 32 threads take the slots t, t + 32, ... each: their max, a
+//   lane-shuffle max over the 32, each slot's weight exp2(m - M) (which
+//   replaces the max in LDS) and its weighted sum, and a shuffle sum: no thread
+//   walks all n slots;
+// * the O values stream through two register batches of kManyBatch slots, the
+//   next batch's loads in flight while the current one is accumulated with the
+//   staged weights (a slot past the last takes an out-of-range offset and
+//   weight 0).
+// A head's 32 threads are one half of a wavefront, whose LDS accesses complete
+// in order, so the weights need no barrier.  The sums run in slot order and in
+// a fixed shuffle tree: the result does not depend on which split merges.
+// s_ml: LDS scratch of n * G * 2 floats, free by the time the merge runs.
+constexpr int kManyBatch = 16;
+constexpr int kManyPairLoads = 4;
+template <int kThreads>
+static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, uint32_t slot0, int G, int tid,
+                                               int64_t row0, float *s_ml) {
+    const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+    const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+    // The pairs of the group lie in consecutive slots: entry e = i * G + h is
+    // pair slot0 * G + e.
+    const int total = n * G;
+    const uint32_t ml0 = slot0 * (uint32_t)G * 8;
+    for (int e0 = tid; e0 < total; e0 += kManyPairLoads * kThreads) {
+        float pm[kManyPairLoads], pl[kManyPairLoads];
+#pragma unroll
+        for (int j = 0; j < kManyPairLoads; ++j) {
+            const int e = e0 + j * kThreads;
+            const uint32_t off = e < total ? ml0 + (uint32_t)e * 8 : kNoPartial;
+            pm[j] = load_coherent1(rml, off);
+            pl[j] = load_coherent1(rml, off + 4);
+        }
+#pragma unroll
+        for (int j = 0; j < kManyPairLoads; ++j) {
+            const int e = e0 + j * kThreads;
+            if (e < total) {
+                s_ml[2 * e] = pm[j];
+                s_ml[2 * e + 1] = pl[j];
+            }
+        }
+    }
+    __syncthreads();
+    const uint32_t so = (uint32_t)G * kHeadDim * 4;  // bytes from one slot's O rows to the next
+    for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
+        const int h = c / (kHeadDim / 4), t = c % (kHeadDim / 4), d0 = t * 4;
+        float M = kNegInf;
+        for (int i = t; i < n; i += 32) M = fmaxf(M, s_ml[2 * (i * G + h)]);
+#pragma unroll
+        for (int x = 16; x >= 1; x /= 2) M = fmaxf(M, __shfl_xor(M, x, 32));
+        float L = 0.f;
+        for (int i = t; i < n; i += 32) {
+            const float m = s_ml[2 * (i * G + h)];
+            const float f = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - M);
+            L += s_ml[2 * (i * G + h) + 1] * f;
+            s_ml[2 * (i * G + h)] = f;
+        }
+#pragma unroll
+        for (int x = 16; x >= 1; x /= 2) L += __shfl_xor(L, x, 32);
+        asm volatile("" ::: "memory");  // the weights' stores stay ahead of their loads below
+        const uint32_t vo = ((slot0 * (uint32_t)G + (uint32_t)h) * kHeadDim + d0) * 4;
+        f32x4 O = {0.f, 0.f, 0.f, 0.f};
+        auto load_batch = [&](int base, f32x4 (&o)[kManyBatch]) {
+#pragma unroll
+            for (int k = 0; k < kManyBatch; ++k) {
+                const bool in = base + k < n;
+                o[k] = load_coherent4_s(ro, in ? vo : kNoPartial, in ? (uint32_t)(base + k) * so : 0u);
+            }
+        };
+        auto add_batch = [&](int base, const f32x4 (&o)[kManyBatch]) {
+#pragma unroll
+            for (int k = 0; k < kManyBatch; ++k) {
+                const int i = base + k;
+                const float f = i < n ? s_ml[2 * (i * G + h)] : 0.f;
+                O += o[k] * f;
+            }
+        };
+        f32x4 ba[kManyBatch], bb[kManyBatch];
+        load_batch(0, ba);
+        for (int base = 0;; base += 2 * kManyBatch) {
+            if (base + kManyBatch < n) load_batch(base + kManyBatch, bb);
+            add_batch(base, ba);
+            if (base + kManyBatch >= n) break;
+            if (base + 2 * kManyBatch < n) load_batch(base + 2 * kManyBatch, ba);
+            add_batch(base + kManyBatch, bb);
+            if (base + 2 * kManyBatch >= n) break;
+        }
+        store_output(a, row0 + h, d0, O, M, L);
+    }
+}
+
 // Up to kMergeBatch partials (every group of the 12 x 300 s workloads): one
 // batch, all loads of a thread in flight at once.
 
-template <int kThreads, int kCnt, typename SlotOf>
+template <int kThreads, int kCnt, typename SlotOf, typename Emit>
 static __device__ __forceinline__ void merge_one_batch_n(const AttnLaunch &a, SlotOf slot_of, int G, int tid,
-                                                         int64_t row0) {
+                                                         Emit emit) {
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
     for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
@@ -1274,38 +1316,42 @@ static __device__ __forceinline__ void merge_one_batch_n(const AttnLaunch &a, Sl
             L += ll[k] * f;
             O += oo[k] * f;
         }
-        store_output(a, row0 + h, d0, O, M, L);
+        emit(h, d0, O, M, L);
     }
 }
 
 // Up to kMergeBatch partials in one batch of loads, specialised on the count:
 // exactly n loads of each kind (a load past the last partial, even one the
 // hardware answers with zeros, still passes through the address unit).
-template <int kThreads, typename SlotOf>
+template <int kThreads, typename SlotOf, typename Emit>
 static __device__ __forceinline__ void merge_one_batch(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
-                                                       int64_t row0) {
+                                                       Emit emit) {
     static_assert(kMergeBatch == 8, "one case per batch size");
     switch (n) {
-    case 1: merge_one_batch_n<kThreads, 1>(a, slot_of, G, tid, row0); break;
-    case 2: merge_one_batch_n<kThreads, 2>(a, slot_of, G, tid, row0); break;
-    case 3: merge_one_batch_n<kThreads, 3>(a, slot_of, G, tid, row0); break;
-    case 4: merge_one_batch_n<kThreads, 4>(a, slot_of, G, tid, row0); break;
-    case 5: merge_one_batch_n<kThreads, 5>(a, slot_of, G, tid, row0); break;
-    case 6: merge_one_batch_n<kThreads, 6>(a, slot_of, G, tid, row0); break;
-    case 7: merge_one_batch_n<kThreads, 7>(a, slot_of, G, tid, row0); break;
-    default: merge_one_batch_n<kThreads, 8>(a, slot_of, G, tid, row0); break;
+    case 1: merge_one_batch_n<kThreads, 1>(a, slot_of, G, tid, emit); break;
+    case 2: merge_one_batch_n<kThreads, 2>(a, slot_of, G, tid, emit); break;
+    case 3: merge_one_batch_n<kThreads, 3>(a, slot_of, G, tid, emit); break;
+    case 4: merge_one_batch_n<kThreads, 4>(a, slot_of, G, tid, emit); break;
+    case 5: merge_one_batch_n<kThreads, 5>(a, slot_of, G, tid, emit); break;
+    case 6: merge_one_batch_n<kThreads, 6>(a, slot_of, G, tid, emit); break;
+    case 7: merge_one_batch_n<kThreads, 7>(a, slot_of, G, tid, emit); break;
+    default: merge_one_batch_n<kThreads, 8>(a, slot_of, G, tid, emit); break;
     }
 }
 
-template <int kThreads, typename SlotOf>
-static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n, SlotOf slot_of, int G, int tid,
-                                                      int64_t row0, float *s_ml) {
+// The n partials lie in the slots slot0 + i * stride; emit(h, d0, O, M, L)
+// takes each thread's merged state.  More than 2 * kMergeBatch partials only
+// in consecutive slots (stride 1) and into the output.
+template <int kThreads, typename Emit>
+static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n, uint32_t slot0, uint32_t stride,
+                                                      int G, int tid, int64_t row0, float *s_ml, Emit emit) {
     if (n > 2 * kMergeBatch) {
-        merge_many<kThreads>(a, n, slot_of, G, tid, row0, s_ml);
+        merge_many<kThreads>(a, n, slot0, G, tid, row0, s_ml);
         return;
     }
+    const auto slot_of = [slot0, stride](int i) { return slot0 + (uint32_t)i * stride; };
     if (n <= kMergeBatch) {
-        merge_one_batch<kThreads>(a, n, slot_of, G, tid, row0);
+        merge_one_batch<kThreads>(a, n, slot_of, G, tid, emit);
         return;
     }
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
@@ -1339,7 +1385,7 @@ static __device__ __forceinline__ void merge_partials(const AttnLaunch &a, int n
             }
             M = bm;
         }
-        store_output(a, row0 + h, d0, O, M, L);
+        emit(h, d0, O, M, L);
     }
 }
 
@@ -1500,10 +1546,48 @@ __global__ __launch_bounds__(256) void decode_attn_lds_kernel(const int32_t *__r
     if (bad && tid == 0)
         raise_device_error((wg_bad_pos ? MURMUR_DEVERR_POSITION : 0) | (bad_count ? MURMUR_DEVERR_COUNT : 0));
     if (a.n_split == 1) return;
-    if (!take_ticket(a, grp, a.n_split, tid, s_last)) return;
-    const uint32_t pbase = (uint32_t)grp * a.n_split;
-    merge_partials<kWavesPerWg * 64>(a, a.n_split, [pbase](int i) { return pbase + (uint32_t)i; }, G, tid, row0,
-                   reinterpret_cast<float *>(&stages[0][0][0]));
+    constexpr int kThreads = kWavesPerWg * 64;
+    const int n = a.n_split;
+    const uint32_t pbase = (uint32_t)grp * n;
+    float *s_ml = reinterpret_cast<float *>(&stages[0][0][0]);
+    const auto to_output = [&a, row0](int h, int d0, f32x4 O, float M, float L) {
+        store_output(a, row0 + h, d0, O, M, L);
+    };
+    if (n > 2 * kMergeBatch && n <= kTwoLevelMax) {
+        // Two levels: the last split of every kSubSplits folds their partials
+        // into the first one's slot (one ticket per such set, after the group
+        // tickets), and the last of those sets folds theirs into the output.
+        // Each merging workgroup then reads at most max(kSubSplits, n_sub)
+        // partials instead of n: the merge of many partials is bound by one
+        // compute unit's read rate.
+        const int n_sub = (n + kSubSplits - 1) / kSubSplits;
+        const int sub = (int)split / kSubSplits;
+        const int sub_n = min(kSubSplits, n - sub * kSubSplits);
+        const uint32_t sub0 = pbase + (uint32_t)(sub * kSubSplits);
+        if (sub_n > 1) {
+            const int groups = a.NL * a.B * a.Hkv;
+            if (!take_ticket(a, groups + grp * n_sub + sub, sub_n, tid, s_last)) return;
+            const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
+            const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+            // Each thread reads the set's (h, d0) values and its head's pairs
+            // before its own stores: a head's 32 threads are one half of a
+            // wavefront, whose stores follow its loads.
+            const auto to_slot = [ro, rml, sub0, G](int h, int d0, f32x4 O, float M, float L) {
+                const uint32_t prow = sub0 * (uint32_t)G + (uint32_t)h;
+                store_coherent4(ro, (prow * kHeadDim + d0) * 4, O);
+                if (d0 == 0) {
+                    store_coherent1(rml, prow * 8, M);
+                    store_coherent1(rml, prow * 8 + 4, L);
+                }
+            };
+            merge_partials<kThreads>(a, sub_n, sub0, 1, G, tid, row0, s_ml, to_slot);
+        }
+        if (!take_ticket(a, grp, n_sub, tid, s_last)) return;
+        merge_partials<kThreads>(a, n_sub, pbase, kSubSplits, G, tid, row0, s_ml, to_output);
+        return;
+    }
+    if (!take_ticket(a, grp, n, tid, s_last)) return;
+    merge_partials<kThreads>(a, n, pbase, 1, G, tid, row0, s_ml, to_output);
 }
 
 // ---------------------------------------------------------------------------

@@ -156,6 +156,12 @@ def split_partials(groups, n_split, G):
     return rnd(groups * n_split * G * 2 * 4) + rnd(groups * n_split * G * 128 * 4)
 
 
+def lds_tickets(groups, n_split):
+    """Ticket counters of the LDS-staged schedule: one per group, and one per set of 8 splits when it merges
+    17 to 128 splits in two levels."""
+    return groups * (1 + -(-n_split // 8)) if 16 < n_split <= 128 else groups
+
+
 def check_plan(ws, partials, tickets):
     """The workspace holds its ticket region and the partials, with room to spare, and so does any larger one."""
     for w in (ws, ws + 1, ws + 255, ws + 256, ws + 65536, ws + 65536 * 3 + 77, 2 * ws):
@@ -178,14 +184,14 @@ def test_workspace_sizing():
     assert M.murmur_decode_attn_workspace(1, 12, 28, 4, 850, 1024) == 256
     # an explicit split length on a long list
     ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160, 640)
-    check_plan(ws, split_partials(4, -(-35160 // 640), 7), 4)
+    check_plan(ws, split_partials(4, -(-35160 // 640), 7), lds_tickets(4, -(-35160 // 640)))
     # automatic split of 1100 units over 4 groups: 55 splits of 5 units
     ws = M.murmur_decode_attn_workspace(1, 1, 28, 4, 35160)
-    check_plan(ws, split_partials(4, 55, 7), 4)
+    check_plan(ws, split_partials(4, 55, 7), lds_tickets(4, 55))
     assert ws - ticket_region(ws) < split_partials(4, 56, 7)
     # one group of 300 units: too many one-pass splits to merge, so 60 splits of 5 units
     ws = M.murmur_decode_attn_workspace(1, 1, 7, 1, 300 * 128)
-    check_plan(ws, split_partials(1, 60, 7), 1)
+    check_plan(ws, split_partials(1, 60, 7), lds_tickets(1, 60))
     assert ws - ticket_region(ws) < split_partials(1, 61, 7)
     # many groups of two splits
     ws = M.murmur_decode_attn_workspace(28, 256, 4, 4, 512, 256)

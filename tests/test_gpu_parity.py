@@ -486,6 +486,27 @@ def test_merge_every_partial_count():
         assert tickets_clear(db.ws, db.ws_bytes)
 
 
+def test_two_level_merge_counts():
+    """The LDS-staged schedule's merges of 17 to 128 splits in two levels (sets of 8, the last set short or
+    whole) and beyond 128 in one: the one-hour dense list in splits of 2080 to 288 positions, the last with
+    max_keep raised to 130 splits (the ones past the count empty)."""
+    wl = workload("c4_dense")
+    s = wl.steps - 1
+    ref, ref_lse = oracle_step(wl, s)
+    seen = []
+    for split_len, max_keep in ((2080, None), (1472, None), (1408, None), (544, None), (288, None), (288, 288 * 130)):
+        db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[s], split_len=split_len, max_keep=max_keep)
+        n = -(-db.max_keep // split_len)
+        seen.append(n)
+        announce(f"attn c4_dense step {s}, split_len {split_len}: {n} partials per group")
+        y, l = run_gpu(db, 0)
+        assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL, (split_len, n)
+        assert tickets_clear(db.ws, db.ws_bytes)
+    # a short last set (n mod 8 == 1 and otherwise), a whole one, the largest two-level count's region, one level
+    assert any(16 < n <= 128 and n % 8 == 1 for n in seen) and any(16 < n <= 128 and n % 8 == 0 for n in seen)
+    assert any(16 < n <= 128 and n % 8 not in (0, 1) for n in seen) and any(n > 128 for n in seen)
+
+
 # ---- murmur_decode_step: eviction and attention in one launch ------------------------------------
 
 def check_retained_outputs(db, wl, s, buf=0):
