@@ -274,9 +274,9 @@ def test_index_mode_matches_range_mode_and_is_deterministic():
 
 def test_workspace_shared_across_shapes():
     """One workspace, zeroed once, serves calls of different shapes and kernels in turn (4, 48 and 384
-    (layer, sequence, KV head) groups; 2 to 21 splits per group; wide-schedule and LDS-staged splits), all
-    passing the same ws_bytes: a call with more groups than the one before never finds its tickets on
-    partials that call left behind."""
+    (layer, sequence, KV head) groups; 2 to 21 splits per group; wide-schedule and LDS-staged splits, and
+    the two-level merge of 17 splits with its per-set tickets), all passing the same ws_bytes: a call with
+    more groups than the one before never finds its tickets on partials that call left behind."""
     announce("attn workspace shared across shapes and schedules")
     rng = np.random.default_rng(404)
     B = 24
@@ -285,9 +285,9 @@ def test_workspace_shared_across_shapes():
     pol = np.stack([rng.integers(64, 300, B), rng.integers(0, 50, B), rng.integers(0, 8, B),
                     rng.integers(16, 128, B), rng.integers(0, 8, B)], axis=1).astype(np.int32)
     many = W.build("many", 41, 4, seg0, pol, steps=3, planted=False)
-    c3, c4 = workload("c3"), workload("c4_evict")
-    cases = [(c4, 128, 0), (many, 128, 0), (c3, 256, 1), (c4, 256, 1), (many, 0, 1), (c3, 512, 2), (c4, 512, 2),
-             (many, 256, 2), (c3, 128, 0), (many, 64, 1), (c4, 128, 2)]
+    c3, c4, c4d = workload("c3"), workload("c4_evict"), workload("c4_dense")
+    cases = [(c4, 128, 0), (many, 128, 0), (c3, 256, 1), (c4d, 2080, 0), (c4, 256, 1), (many, 0, 1), (c3, 512, 2),
+             (c4, 512, 2), (c4d, 2080, 1), (many, 256, 2), (c3, 128, 0), (many, 64, 1), (c4, 128, 2)]
     dbs = {}
     for wl, split_len, _ in cases:
         key = (wl.name, split_len)
@@ -363,13 +363,17 @@ def test_attn_strided_cache_layout():
     assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(db.lse.cpu().numpy(), ref_lse) <= LSE_TOL
 
 
-def test_attn_device_errors_give_nan():
+@pytest.mark.parametrize("split_len,max_keep", [(0, None), (96, None), (32, None), (288, 288 * 20), (288, 288 * 130)])
+def test_attn_device_errors_give_nan(split_len, max_keep):
     """A position outside the cache (index mode) and a count above max_keep are caught by the kernel's
     own bounds checks: nothing outside the cache is read, the sequence's outputs are NaN and the
-    device error word says why."""
-    announce("attn device errors")
+    device error word says why.  The NaN of the split that saw the position reaches the output through
+    every merge: one split, the wide schedule's merges of 2 and 6 partials, and the LDS-staged schedule's
+    two-level merge (20 partials) and one-level merge of many (130 partials)."""
+    announce(f"attn device errors, split_len {split_len}, max_keep {max_keep}")
     wl = workload("c1")
-    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[0], use_ranges=False)
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[0], use_ranges=False, split_len=split_len,
+                     max_keep=max_keep)
     db.evict(0)
     torch.cuda.synchronize()
     db.idx[0, 3] = wl.max_len + 5
@@ -381,8 +385,13 @@ def test_attn_device_errors_give_nan():
     db.count.fill_(db.max_keep + 1)
     db.attend(0)
     torch.cuda.synchronize()
-    assert M.murmur_device_error() == M.MURMUR_DEVERR_COUNT
+    err = M.murmur_device_error()
+    if max_keep is None:
+        assert err == M.MURMUR_DEVERR_COUNT
+    else:  # the ranks past the real count then hold -1, which the position check reports as well
+        assert err in (M.MURMUR_DEVERR_COUNT, M.MURMUR_DEVERR_COUNT | M.MURMUR_DEVERR_POSITION)
     assert torch.isnan(db.out).all().item()
+    assert tickets_clear(db.ws, db.ws_bytes)
 
 
 def test_graph_replays_match_eager_and_pipelined_schedule():
@@ -505,6 +514,15 @@ def test_two_level_merge_counts():
     # a short last set (n mod 8 == 1 and otherwise), a whole one, the largest two-level count's region, one level
     assert any(16 < n <= 128 and n % 8 == 1 for n in seen) and any(16 < n <= 128 and n % 8 == 0 for n in seen)
     assert any(16 < n <= 128 and n % 8 not in (0, 1) for n in seen) and any(n > 128 for n in seen)
+    # two levels in a grid of more than one dispatch round (the one-stage form): c3's 48 groups in 20 splits
+    # of 288 positions (the splits past each sequence's count empty), 960 workgroups
+    wl = workload("c3")
+    ref, ref_lse = oracle_step(wl, 0)
+    db = DecodeBatch(wl, out_dtype=M.MURMUR_DTYPE_F32, steps=[0], split_len=288, max_keep=288 * 20)
+    announce("attn c3 step 0, split_len 288, max_keep 5760: 20 partials per group, 960 workgroups")
+    y, l = run_gpu(db, 0)
+    assert rel_err_fp32(y, ref) <= REL_TOL and lse_err(l, ref_lse) <= LSE_TOL
+    assert tickets_clear(db.ws, db.ws_bytes)
 
 
 # ---- murmur_decode_step: eviction and attention in one launch ------------------------------------
