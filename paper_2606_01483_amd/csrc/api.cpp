@@ -77,55 +77,46 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     // The wide schedule (splits of at most kWideSplit positions, a wavefront per
     // pass) needs its work indices below 2^16.
     const bool wide_ok = groups < 65536 && Hkv < 65536 && B < 65536;
-    int64_t n_hi = 0, n_lo = 0, len_hi = 0, len_lo = 0, groups_hi = 0;
+    int64_t n_wide = 0, len_wide = 0;
     if (split_len == 0 && wide_ok && groups <= kRoundWorkgroups) {
-        // One dispatch round: n_lo splits per group, and one more for the first
-        // groups_hi groups when that fills the round; the candidate with the
-        // lowest estimate (fewer workgroups on a tie).
+        // One dispatch round: the number of splits per group with the lowest
+        // estimate (fewer workgroups on a tie).  Giving some groups one split
+        // more than the others never lowers it: the longest split stays and
+        // those groups merge one partial more.
         double best = 0.0;
         for (int64_t n = 1; n * groups <= kRoundWorkgroups; ++n) {
             const int64_t len = ((int64_t)max_keep + n - 1) / n;
             if (len > kWideSplit) continue;
-            for (int fill = 0; fill < 2; ++fill) {
-                const int64_t gh = fill ? std::min(groups, kRoundWorkgroups - n * groups) : 0;
-                if (fill && gh == 0) continue;
-                const int64_t lh = ((int64_t)max_keep + n) / (n + 1);
-                const double t = wide_cost(len, gh > 0 ? n + 1 : n, G);
-                if (n_lo == 0 || t < best - 1e-9) {
-                    best = t;
-                    n_lo = n;
-                    len_lo = len;
-                    groups_hi = gh;
-                    n_hi = gh > 0 ? n + 1 : 0;
-                    len_hi = gh > 0 ? lh : 0;
-                }
+            const double t = wide_cost(len, n, G);
+            if (n_wide == 0 || t < best - 1e-9) {
+                best = t;
+                n_wide = n;
+                len_wide = len;
             }
         }
     } else if (split_len > 0 && split_len <= kWideSplit && wide_ok) {
-        n_lo = ((int64_t)max_keep + split_len - 1) / split_len;
-        len_lo = split_len;
+        n_wide = ((int64_t)max_keep + split_len - 1) / split_len;
+        len_wide = split_len;
     }
-    if (split_len == 0 && n_lo > 0) {
+    if (split_len == 0 && n_wide > 0) {
         // The LDS-staged kernel's automatic split (below) when the model expects it to be faster.
         int64_t want = std::min<int64_t>(std::min<int64_t>(kRoundWorkgroups / groups, kMaxAutoSplits), units);
         if (want < 1) want = 1;
         const int64_t per = std::max<int64_t>((units + want - 1) / want, 2);
         const int64_t n_lds = ((int64_t)max_keep + per * kSplitUnit - 1) / (per * kSplitUnit);
-        const double t_wide = wide_cost(len_lo, groups_hi > 0 ? n_hi : n_lo, G);
-        if (wide_cost(std::min<int64_t>(per * kSplitUnit, max_keep), n_lds, G) < t_wide) n_lo = 0;
+        if (wide_cost(std::min<int64_t>(per * kSplitUnit, max_keep), n_lds, G) < wide_cost(len_wide, n_wide, G))
+            n_wide = 0;
     }
-    if (n_lo > 0 && n_lo < 65536 && groups * n_lo + groups_hi < 65536) {
-        p.wide_wg = (int32_t)(groups * n_lo + groups_hi);
-        p.sched.groups_hi = (uint32_t)groups_hi | (uint32_t)p.wide_wg << 16;
-        p.sched.n_split = (uint32_t)n_hi | (uint32_t)n_lo << 16;
-        p.sched.magic_hi = magic16((uint32_t)n_hi);
-        p.sched.magic_lo = magic16((uint32_t)n_lo);
-        p.sched.len = (uint32_t)len_hi | (uint32_t)len_lo << 9 | (uint32_t)G << 18;
+    if (n_wide > 0 && n_wide < 65536 && groups * n_wide < 65536) {
+        p.wide_wg = (int32_t)(groups * n_wide);
+        p.sched.wg_n = (uint32_t)p.wide_wg | (uint32_t)n_wide << 16;
+        p.sched.magic_n = magic16((uint32_t)n_wide);
+        p.sched.len = (uint32_t)len_wide | (uint32_t)G << 18;
         p.sched.hkv_b = (uint32_t)Hkv | (uint32_t)B << 16;
         p.sched.magic_hkv = magic16((uint32_t)Hkv);
         p.sched.magic_b = magic16((uint32_t)B);
-        p.n_split = (int32_t)(n_hi > n_lo ? n_hi : n_lo);
-        p.split_len = (int32_t)len_lo;
+        p.n_split = (int32_t)n_wide;
+        p.split_len = (int32_t)len_wide;
         if (p.n_split > 1) {
             p.tickets = groups;
             p.ml_bytes = round_up((size_t)p.wide_wg * G * 2 * sizeof(float), 256);

@@ -43,19 +43,16 @@ constexpr int kWideSplit = kWideWaves * kWaveTile;  // 256
 
 // Work of the wide schedule's workgroups, decoded on the device with exact
 // multiply-high divisions (values below 2^16, multipliers ceil(2^32 / d), 0
-// for d = 1): the
-// first groups_hi (layer, sequence, KV head) groups are cut into n_hi splits
-// of len_hi positions, the others into n_lo of len_lo; the w-th (group,
-// split) in that order goes to the workgroup that xcd_order maps to w and,
-// when its group has more than one split, leaves its partial in slot w.
+// for d = 1): every (layer, sequence, KV head) group is cut into n splits of
+// len positions; the w-th (group, split) in that order goes to the workgroup
+// that xcd_order maps to w and, when its group has more than one split,
+// leaves its partial in slot w.
 struct WideSched {
-    uint32_t groups_hi;  // groups_hi | W << 16, W the number of workgroups
-    uint32_t n_split;   // n_hi | n_lo << 16
-    uint32_t magic_hi;  // ceil(2^32 / n_hi)
-    uint32_t magic_lo;  // ceil(2^32 / n_lo)
-    uint32_t len;       // len_hi | len_lo << 9 | G << 18 (split lengths <= 256, G query heads per KV head);
-                        // the launch adds the policy mode (MURMUR_POL_* bits) << 23 and, at bit 25,
-                        // whether stride_pos < kRunRowLimit
+    uint32_t wg_n;      // W | n << 16, W the number of workgroups
+    uint32_t magic_n;   // ceil(2^32 / n)
+    uint32_t len;       // len | G << 18 (split lengths <= 256, G query heads per KV head); the launch
+                        // adds the policy mode (MURMUR_POL_* bits) << 23 and, at bit 25, whether
+                        // stride_pos < kRunRowLimit
     uint32_t hkv_b;     // Hkv | B << 16
     uint32_t magic_hkv;
     uint32_t magic_b;

@@ -1853,10 +1853,10 @@ static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) {
 // would be loaded from memory first).
 template <int kSrc>
 __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
-    const int32_t *__restrict__ src0, const int32_t *__restrict__ src1, uint32_t groups_hi, uint32_t n_split,
-    uint32_t magic_hi, uint32_t magic_lo, uint32_t len_hi_lo, uint32_t hkv_b, uint32_t magic_hkv, uint32_t magic_b,
+    const int32_t *__restrict__ src0, const int32_t *__restrict__ src1, uint32_t wg_n, uint32_t magic_n,
+    uint32_t len_g, uint32_t hkv_b, uint32_t magic_hkv, uint32_t magic_b,
     const int32_t *__restrict__ idx, const uint16_t *__restrict__ q, const AttnLaunch a) {
-    const WideSched ws{groups_hi, n_split, magic_hi, magic_lo, len_hi_lo, hkv_b, magic_hkv, magic_b};
+    const WideSched ws{wg_n, magic_n, len_g, hkv_b, magic_hkv, magic_b};
     // G and the policy mode from a preloaded argument: loading them from memory
     // put a second round trip in front of the first K/V loads
     const int G = (int)((ws.len >> 18) & 0x1fu);
@@ -1881,19 +1881,12 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
 
     // Which split of which group: scalar arithmetic on preloaded arguments,
     // so the retained-set description is the first memory access.
-    const uint32_t wg = xcd_order(blockIdx.x, ws.groups_hi >> 16);
-    const uint32_t gh = ws.groups_hi & 0xffffu;
-    const uint32_t n_hi = ws.n_split & 0xffffu, n_lo = ws.n_split >> 16;
-    const uint32_t hi_wg = gh * n_hi;
-    // selects, not branches: straight-line scalar code up to the first loads
-    const bool in_hi = wg < hi_wg;
-    const uint32_t w2 = in_hi ? wg : wg - hi_wg;
-    const uint32_t n = in_hi ? n_hi : n_lo;
-    const uint32_t gq = div16(w2, in_hi ? ws.magic_hi : ws.magic_lo);
-    const uint32_t grp = in_hi ? gq : gh + gq;
-    const uint32_t split = w2 - gq * n;
-    const uint32_t len = in_hi ? (ws.len & 0x1ffu) : ((ws.len >> 9) & 0x1ffu);
-    const uint32_t slot0 = (in_hi ? 0u : hi_wg) + gq * n;
+    const uint32_t wg = xcd_order(blockIdx.x, ws.wg_n & 0xffffu);
+    const uint32_t n = ws.wg_n >> 16;
+    const uint32_t grp = div16(wg, ws.magic_n);
+    const uint32_t split = wg - grp * n;
+    const uint32_t len = ws.len & 0x1ffu;
+    const uint32_t slot0 = grp * n;
     const int Hkv = (int)(ws.hkv_b & 0xffffu), B = (int)(ws.hkv_b >> 16);
     const uint32_t lb = div16(grp, ws.magic_hkv);
     const int g = (int)(grp - lb * (uint32_t)Hkv);
@@ -2112,7 +2105,7 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.wide_wg > 0) {
         const WideSched &w = a.sched;
         hipLaunchKernelGGL(decode_attn_wide_kernel<kSrc>, dim3((unsigned)a.wide_wg), dim3(kWideThreads), 0, stream,
-                           a.src0, a.src1, w.groups_hi, w.n_split, w.magic_hi, w.magic_lo,
+                           a.src0, a.src1, w.wg_n, w.magic_n,
                            w.len | (uint32_t)(a.pol_per_seq & 3) << 23 | (uint32_t)(a.s_pos < kRunRowLimit) << 25,
                            w.hkv_b, w.magic_hkv, w.magic_b, a.idx,
                            a.q, a);
