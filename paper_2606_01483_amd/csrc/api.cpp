@@ -107,11 +107,12 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
         if (wide_cost(std::min<int64_t>(per * kSplitUnit, max_keep), n_lds, G) < wide_cost(len_wide, n_wide, G))
             n_wide = 0;
     }
-    if (n_wide > 0 && n_wide < 65536 && groups * n_wide < 65536) {
+    if (n_wide > 0 && n_wide <= kMaxMergeSplits && groups * n_wide < 65536) {
         p.wide_wg = (int32_t)(groups * n_wide);
-        p.sched.wg_n = (uint32_t)p.wide_wg | (uint32_t)n_wide << 16;
+        const uint32_t per = ((uint32_t)p.wide_wg + 7) / 8;
+        p.sched.xcd = (per - 1) | ((uint32_t)p.wide_wg - 8 * (per - 1)) << 16;
         p.sched.magic_n = magic16((uint32_t)n_wide);
-        p.sched.len = (uint32_t)len_wide | (uint32_t)G << 18;
+        p.sched.len = (uint32_t)len_wide | (uint32_t)n_wide << 9 | (uint32_t)G << 18;
         p.sched.hkv_b = (uint32_t)Hkv | (uint32_t)B << 16;
         p.sched.magic_hkv = magic16((uint32_t)Hkv);
         p.sched.magic_b = magic16((uint32_t)B);

@@ -48,11 +48,12 @@ constexpr int kWideSplit = kWideWaves * kWaveTile;  // 256
 // that xcd_order maps to w and, when its group has more than one split,
 // leaves its partial in slot w.
 struct WideSched {
-    uint32_t wg_n;      // W | n << 16, W the number of workgroups
+    uint32_t xcd;       // (per - 1) | tall << 16 for W workgroups: per = ceil(W / 8) and tall = W - 8 (per - 1)
+                        // (see xcd_order)
     uint32_t magic_n;   // ceil(2^32 / n)
-    uint32_t len;       // len | G << 18 (split lengths <= 256, G query heads per KV head); the launch
-                        // adds the policy mode (MURMUR_POL_* bits) << 23 and, at bit 25, whether
-                        // stride_pos < kRunRowLimit
+    uint32_t len;       // len | n << 9 | G << 18 (split lengths <= 256, n <= kMaxMergeSplits, G query heads
+                        // per KV head); the launch adds the policy mode (MURMUR_POL_* bits) << 23 and, at
+                        // bit 25, whether stride_pos < kRunRowLimit
     uint32_t hkv_b;     // Hkv | B << 16
     uint32_t magic_hkv;
     uint32_t magic_b;

@@ -1833,13 +1833,13 @@ static __device__ __forceinline__ void merge_wide(const AttnLaunch &a, __amdgpu_
 // The hardware hands workgroup w of a launch to XCD w mod 8.  The work items
 // (in the order the schedule lists them) are dealt out XCD by XCD instead:
 // XCD x takes a contiguous run of them, so the splits of a group, which trade
-// partials, share one L2 where the counts allow.  A bijection of [0, W).
-static __device__ __forceinline__ uint32_t xcd_order(uint32_t wg, uint32_t W) {
-    const uint32_t per = (W + 7) >> 3;        // work items of the first XCDs
-    const uint32_t tall = W - 8 * (per - 1);  // XCDs that take `per` (the others per - 1)
+// partials, share one L2 where the counts allow.  Of W workgroups the first
+// `tall` XCDs take per = ceil(W / 8) items and the others per - 1, so XCD x's
+// run starts at x (per - 1) + min(x, tall); xcd = (per - 1) | tall << 16,
+// from the launch.  A bijection of [0, W).
+static __device__ __forceinline__ uint32_t xcd_order(uint32_t wg, uint32_t xcd) {
     const uint32_t x = wg & 7, local = wg >> 3;
-    const uint32_t first = x * per + local, rest = tall * per + (x - tall) * (per - 1) + local;
-    return x < tall ? first : rest;
+    return x * (xcd & 0xffffu) + min(x, xcd >> 16) + local;
 }
 
 // x / d for x < 2^16 from magic = ceil(2^32 / d); magic 0 stands for d = 1
@@ -1853,10 +1853,10 @@ static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) {
 // would be loaded from memory first).
 template <int kSrc>
 __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
-    const int32_t *__restrict__ src0, const int32_t *__restrict__ src1, uint32_t wg_n, uint32_t magic_n,
+    const int32_t *__restrict__ src0, const int32_t *__restrict__ src1, uint32_t xcd, uint32_t magic_n,
     uint32_t len_g, uint32_t hkv_b, uint32_t magic_hkv, uint32_t magic_b,
     const int32_t *__restrict__ idx, const uint16_t *__restrict__ q, const AttnLaunch a) {
-    const WideSched ws{wg_n, magic_n, len_g, hkv_b, magic_hkv, magic_b};
+    const WideSched ws{xcd, magic_n, len_g, hkv_b, magic_hkv, magic_b};
     // G and the policy mode from a preloaded argument: loading them from memory
     // put a second round trip in front of the first K/V loads
     const int G = (int)((ws.len >> 18) & 0x1fu);
@@ -1881,8 +1881,8 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
 
     // Which split of which group: scalar arithmetic on preloaded arguments,
     // so the retained-set description is the first memory access.
-    const uint32_t wg = xcd_order(blockIdx.x, ws.wg_n & 0xffffu);
-    const uint32_t n = ws.wg_n >> 16;
+    const uint32_t wg = xcd_order(blockIdx.x, ws.xcd);
+    const uint32_t n = (ws.len >> 9) & 0x1ffu;
     const uint32_t grp = div16(wg, ws.magic_n);
     const uint32_t split = wg - grp * n;
     const uint32_t len = ws.len & 0x1ffu;
@@ -2105,7 +2105,7 @@ static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.wide_wg > 0) {
         const WideSched &w = a.sched;
         hipLaunchKernelGGL(decode_attn_wide_kernel<kSrc>, dim3((unsigned)a.wide_wg), dim3(kWideThreads), 0, stream,
-                           a.src0, a.src1, w.wg_n, w.magic_n,
+                           a.src0, a.src1, w.xcd, w.magic_n,
                            w.len | (uint32_t)(a.pol_per_seq & 3) << 23 | (uint32_t)(a.s_pos < kRunRowLimit) << 25,
                            w.hkv_b, w.magic_hkv, w.magic_b, a.idx,
                            a.q, a);

@@ -208,6 +208,22 @@ def test_workspace_sizing():
     assert e.value.code == M.MURMUR_EINVAL
 
 
+def test_xcd_work_order_is_a_bijection():
+    """The wide schedule's workgroup-to-work mapping (the launch packs per - 1 and the number of XCDs that take
+    per = ceil(W / 8) items; the kernel maps workgroup w, which the hardware places on XCD w mod 8, to
+    x (per - 1) + min(x, tall) + w // 8): a bijection of [0, W) in which every XCD takes one contiguous run,
+    for every grid of up to 4096 workgroups."""
+    for W in range(1, 4097):
+        per = (W + 7) // 8
+        per_m1, tall = per - 1, W - 8 * (per - 1)
+        assert 1 <= tall <= 8
+        work = [(w & 7) * per_m1 + min(w & 7, tall) + (w >> 3) for w in range(W)]
+        assert sorted(work) == list(range(W)), W
+        for x in range(8):
+            run = [work[w] for w in range(x, W, 8)]
+            assert run == list(range(run[0], run[0] + len(run))) if run else True, (W, x)
+
+
 def test_decode_attn_accepts_any_larger_workspace():
     """Host validation (the workspace plan included) passes for the exact size and for larger ones; with no
     GPU the launch itself then fails with MURMUR_EHIP."""
