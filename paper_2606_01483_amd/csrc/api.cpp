@@ -45,10 +45,9 @@ size_t ticket_region(size_t ws_bytes) { return round_up(4 * kTicketStride * ((ws
 
 namespace {
 
-// ceil(2^32 / d): multiply-high by it divides values below 2^16 exactly.  0
-// for d = 1, whose value does not fit (the kernel then divides by one), and
-// for d = 0 (an unused divisor).
-uint32_t magic16(uint32_t d) { return d <= 1 ? 0u : (uint32_t)((((uint64_t)1 << 32) + d - 1) / d); }
+// ceil(2^32 / d) - 1: the kernel's x / d is the high word of (x + 1) times it,
+// exact for x < 2^16 and 1 <= d < 2^16.  0 for d = 0 (an unused divisor).
+uint32_t magic16(uint32_t d) { return d == 0 ? 0u : (uint32_t)((((uint64_t)1 << 32) + d - 1) / d - 1); }
 
 // Estimated launch time (us) of a one-round split with at most len positions per
 // workgroup and at most n splits per group (the model behind the automatic choice,

@@ -1842,11 +1842,12 @@ static __device__ __forceinline__ uint32_t xcd_order(uint32_t wg, uint32_t xcd) 
     return x * (xcd & 0xffffu) + min(x, xcd >> 16) + local;
 }
 
-// x / d for x < 2^16 from magic = ceil(2^32 / d); magic 0 stands for d = 1
-// (whose ceil(2^32 / d) does not fit in 32 bits).
-static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) {
-    return __umulhi(x, magic) + (x & (0u - (uint32_t)(magic == 0u)));  // no branch: umulhi(x, 0) = 0
-}
+// x / d for x < 2^16 and 1 <= d < 2^16 from magic = ceil(2^32 / d) - 1,
+// which fits in 32 bits for every such d: (x + 1) magic / 2^32 falls short of
+// (x + 1) / d by more than 0 and at most 2^-16, less than the distance from
+// x / d to the next integer unless x + 1 is a multiple of d, where it gives
+// exactly the floor of x / d.
+static __device__ __forceinline__ uint32_t div16(uint32_t x, uint32_t magic) { return __umulhi(x + 1u, magic); }
 
 // The WideSched fields are separate scalar arguments (with the pointers, the
 // first 16 dwords, which the build preloads into SGPRs; a struct argument

@@ -208,6 +208,25 @@ def test_workspace_sizing():
     assert e.value.code == M.MURMUR_EINVAL
 
 
+def test_work_decode_division_is_exact():
+    """The wide schedule's division x / d = high word of (x + 1)(ceil(2^32 / d) - 1), for x < 2^16 and
+    1 <= d < 2^16 (the launch computes the multiplier, the kernel the product): every x for d up to 1024, and
+    for every d the values around each multiple of d (x = kd - 1 and kd, where a short or long product
+    would first show) and the largest x."""
+    def magic(d):
+        return ((1 << 32) + d - 1) // d - 1
+
+    x = np.arange(1 << 16, dtype=np.uint64)
+    for d in range(1, 1025):
+        assert np.array_equal(((x + 1) * np.uint64(magic(d))) >> np.uint64(32), x // np.uint64(d)), d
+    for d in range(1025, 1 << 16):
+        k = np.arange(1, (1 << 16) // d + 1, dtype=np.uint64) * np.uint64(d)
+        xs = np.concatenate([k - np.uint64(1), k[k < (1 << 16)], np.array([(1 << 16) - 1, 0], dtype=np.uint64)])
+        assert magic(d) < (1 << 32)
+        assert np.array_equal(((xs + 1) * np.uint64(magic(d))) >> np.uint64(32), xs // np.uint64(d)), d
+    assert magic(1) == (1 << 32) - 1
+
+
 def test_xcd_work_order_is_a_bijection():
     """The wide schedule's workgroup-to-work mapping (the launch packs per - 1 and the number of XCDs that take
     per = ceil(W / 8) items; the kernel maps workgroup w, which the hardware places on XCD w mod 8, to
