@@ -52,8 +52,9 @@ struct WideSched {
                         // (see xcd_order)
     uint32_t magic_n;   // ceil(2^32 / n)
     uint32_t len;       // len | n << 9 | G << 18 (split lengths <= 256, n <= kMaxMergeSplits, G query heads
-                        // per KV head); the launch adds the policy mode (MURMUR_POL_* bits) << 23 and, at
-                        // bit 25, whether stride_pos < kRunRowLimit
+                        // per KV head); the launch adds the policy mode (MURMUR_POL_* bits) << 23, at
+                        // bit 25 whether stride_pos < kRunRowLimit and at bit 26 whether every group's
+                        // first K/V element lies below 2^31 elements
     uint32_t hkv_b;     // Hkv | B << 16
     uint32_t magic_hkv;
     uint32_t magic_b;

@@ -1917,7 +1917,16 @@ __global__ __launch_bounds__(kWideThreads) void decode_attn_wide_kernel(
     else irow = raw_buffer(idx + (int64_t)b * max_keep, (uint32_t)max_keep * 4u);  // ranks past the count are masked
 
     const int64_t row0 = (int64_t)lb * (Hkv * G) + g * G;  // first output row of the group
-    const int64_t kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
+    // The group's first K/V element: in 32-bit arithmetic when the launch found
+    // every group's offset below 2^31 elements (three 64-bit products cost
+    // about 30 scalar instructions between the description's arrival and the
+    // first K/V load).
+    int64_t kv_off;
+    if ((ws.len >> 26) & 1u)
+        kv_off = (int64_t)((uint32_t)layer * (uint32_t)a.s_layer + (uint32_t)b * (uint32_t)a.s_b +
+                           (uint32_t)g * (uint32_t)a.s_h);
+    else
+        kv_off = layer * a.s_layer + b * a.s_b + g * a.s_h;
     const uint16_t *kbase = a.k + kv_off;
     const uint16_t *vbase = a.v + kv_off;
     constexpr bool kRing = kSrc == kSrcRing;
@@ -2101,13 +2110,21 @@ int launch_evict_compact(const murmur_seg *seg, const murmur_policy *pol, int32_
     return (int)hipGetLastError();
 }
 
+// Whether every (layer, sequence, KV head) group's first K/V element lies
+// below 2^31 elements from the cache's base (the strides are non-negative).
+static bool small_group_offsets(const AttnLaunch &a) {
+    const __int128 last = (__int128)(a.NL - 1) * a.s_layer + (__int128)(a.B - 1) * a.s_b + (__int128)(a.Hkv - 1) * a.s_h;
+    return last < ((__int128)1 << 31);
+}
+
 template <int kSrc>
 static void launch_decode_attn_mode(const AttnLaunch &a, hipStream_t stream) {
     if (a.wide_wg > 0) {
         const WideSched &w = a.sched;
         hipLaunchKernelGGL(decode_attn_wide_kernel<kSrc>, dim3((unsigned)a.wide_wg), dim3(kWideThreads), 0, stream,
                            a.src0, a.src1, w.xcd, w.magic_n,
-                           w.len | (uint32_t)(a.pol_per_seq & 3) << 23 | (uint32_t)(a.s_pos < kRunRowLimit) << 25,
+                           w.len | (uint32_t)(a.pol_per_seq & 3) << 23 | (uint32_t)(a.s_pos < kRunRowLimit) << 25 |
+                               (uint32_t)small_group_offsets(a) << 26,
                            w.hkv_b, w.magic_hkv, w.magic_b, a.idx,
                            a.q, a);
         return;

@@ -152,3 +152,53 @@ def test_attn_long_row_strides(s_pos):
     for (out, lse), path in zip(outs, ("fused", "ranges")):
         assert rel_err_fp32(out, ref) <= REL_TOL, path
         assert lse_err(lse, ref_lse) <= LSE_TOL, path
+
+
+@pytest.mark.parametrize("s_h", [715827880, 1 << 30])
+def test_attn_group_offsets_near_and_past_2_31(s_h):
+    """KV heads s_h elements apart, rows contiguous within a head, so the last head's first element lies at
+    3 s_h: just below 2^31 elements (the launch lets the wide schedule compute each group's offset with 32-bit
+    products) and past it (64-bit products).  One sequence of 65 positions, eviction off, on the wide schedule
+    with the automatic split and with 32-position splits, through the fused step and the range-table attention,
+    against the fp64 oracle."""
+    L, hq, hkv, D = 65, W.HQ, W.HKV, W.HEAD_DIM
+    announce(f"KV heads {s_h} elements apart, {L} positions")
+    rng = np.random.default_rng(4400 + (s_h & 15))
+    k_bits = W.f32_to_bf16_bits(rng.standard_normal((1, 1, hkv, L, D), dtype=np.float32))
+    v_bits = W.f32_to_bf16_bits(rng.standard_normal((1, 1, hkv, L, D), dtype=np.float32))
+    q_bits = W.f32_to_bf16_bits(rng.standard_normal((1, 1, hq, D), dtype=np.float32))
+    scale = 1.0 / math.sqrt(D)
+    dev = torch.device("cuda")
+    span = (hkv - 1) * s_h + L * D  # elements from the first head's first row to the end of the last head's rows
+    kv_dev = []
+    for bits in (k_bits, v_bits):
+        buf = torch.empty(span, dtype=torch.bfloat16, device=dev)  # only the heads' rows are written and read
+        rows = torch.from_numpy(bits[0, 0].copy()).view(torch.bfloat16).to(dev)  # [hkv, L, D]
+        buf.as_strided((hkv, L, D), (s_h, D, 1)).copy_(rows)
+        kv_dev.append(buf)
+    kv = M.make_kv(kv_dev[0], kv_dev[1], 1, L, (0, 0, s_h, D))
+    seg_d = torch.tensor([[0, L - 1, 0, 1]], dtype=torch.int32, device=dev)  # speech 0..63, output token 64
+    pol_d = torch.tensor([OFF, 0, 0, OFF, 0], dtype=torch.int32, device=dev)
+    q = torch.from_numpy(q_bits).view(torch.bfloat16).to(dev)
+    count = torch.zeros(1, dtype=torch.int32, device=dev)
+    ranges = torch.zeros((1, M.N_PIECES, 2), dtype=torch.int32, device=dev)
+    ref, ref_lse = oracle.attend(q_bits, k_bits, v_bits, np.arange(L, dtype=np.int32)[None],
+                                 np.array([L], dtype=np.int32), scale=scale, n_threads=16)
+    for split_len in (0, 32):
+        ws_bytes = M.murmur_decode_attn_workspace(1, 1, hq, hkv, L, split_len)
+        ws = torch.zeros(ws_bytes // 4 + 64, dtype=torch.int32, device=dev)
+        for path in ("fused", "ranges"):
+            out = torch.full((1, 1, hq, D), float("nan"), dtype=torch.float32, device=dev)
+            lse = torch.zeros((1, 1, hq), dtype=torch.float32, device=dev)
+            if path == "fused":
+                M.murmur_decode_step(seg_d, pol_d, 0, q, kv, None, count, ranges, L, 1, hq, hkv, D, scale, split_len,
+                                     out, M.MURMUR_DTYPE_F32, lse, ws, ws_bytes)
+            else:
+                M.murmur_decode_attn(q, kv, None, ranges, count, L, 1, hq, hkv, D, scale, split_len, out,
+                                     M.MURMUR_DTYPE_F32, lse, ws, ws_bytes)
+            torch.cuda.synchronize()
+            assert M.murmur_device_error() == 0, (split_len, path)
+            assert int(count.item()) == L
+            assert rel_err_fp32(out.cpu().numpy(), ref) <= REL_TOL, (split_len, path)
+            assert lse_err(lse.cpu().numpy(), ref_lse) <= LSE_TOL, (split_len, path)
+    del kv_dev
