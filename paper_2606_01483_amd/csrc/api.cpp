@@ -64,12 +64,27 @@ double wide_cost(int64_t len, int64_t n, int64_t G) {
            (n > 1 ? kMergeChainUs + n * part_bytes / kCuBytesPerUs + trips : 0.0);
 }
 
+// The LDS-staged kernel's automatic split length: as many splits as keep one
+// dispatch round (fewer when there are more groups than that, at most
+// kMaxAutoSplits), counted in whole workgroup passes, then each split made as
+// short as that count allows in whole wavefront passes: a split's time is
+// bound by its compute unit's read rate, so rows past the longest sequence's
+// share only cost (12 x 300 s dense: 768 -> 704 positions, five splits either way).
+int64_t lds_auto_split(int64_t max_keep, int64_t groups) {
+    const int64_t units = (max_keep + kSplitUnit - 1) / kSplitUnit;
+    int64_t want = std::min<int64_t>(std::min<int64_t>(kRoundWorkgroups / groups, kMaxAutoSplits), units);
+    if (want < 1) want = 1;
+    const int64_t per = std::max<int64_t>((units + want - 1) / want, 2);
+    const int64_t n = (max_keep + per * kSplitUnit - 1) / (per * kSplitUnit);
+    const int64_t len = ((max_keep + n - 1) / n + kWaveTile - 1) / kWaveTile * kWaveTile;
+    return std::max<int64_t>(len, 2 * kSplitUnit);
+}
+
 }  // namespace
 
 WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hkv, int32_t max_keep,
                              int32_t split_len) {
     WorkspacePlan p{};
-    const int64_t units = ((int64_t)max_keep + kSplitUnit - 1) / kSplitUnit;
     const int64_t groups = (int64_t)n_layers * B * Hkv;
     const int64_t G = Hkv > 0 ? Hq / Hkv : 0;
     p.groups = groups;
@@ -99,12 +114,9 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
     }
     if (split_len == 0 && n_wide > 0) {
         // The LDS-staged kernel's automatic split (below) when the model expects it to be faster.
-        int64_t want = std::min<int64_t>(std::min<int64_t>(kRoundWorkgroups / groups, kMaxAutoSplits), units);
-        if (want < 1) want = 1;
-        const int64_t per = std::max<int64_t>((units + want - 1) / want, 2);
-        const int64_t n_lds = ((int64_t)max_keep + per * kSplitUnit - 1) / (per * kSplitUnit);
-        if (wide_cost(std::min<int64_t>(per * kSplitUnit, max_keep), n_lds, G) < wide_cost(len_wide, n_wide, G))
-            n_wide = 0;
+        const int64_t len_lds = lds_auto_split(max_keep, groups);
+        const int64_t n_lds = ((int64_t)max_keep + len_lds - 1) / len_lds;
+        if (wide_cost(std::min<int64_t>(len_lds, max_keep), n_lds, G) < wide_cost(len_wide, n_wide, G)) n_wide = 0;
     }
     if (n_wide > 0 && n_wide <= kMaxMergeSplits && groups * n_wide < 65536) {
         p.wide_wg = (int32_t)(groups * n_wide);
@@ -123,18 +135,7 @@ WorkspacePlan plan_workspace(int32_t n_layers, int32_t B, int32_t Hq, int32_t Hk
             p.o_bytes = round_up((size_t)p.wide_wg * G * kHeadDim * sizeof(float), 256);
         }
     } else {
-        if (split_len <= 0) {
-            // The LDS-staged kernel, which takes a whole compute unit: as many
-            // splits as keep one dispatch round, fewer when there are more groups
-            // than that, at most kMaxAutoSplits.
-            int64_t want = kRoundWorkgroups / groups;
-            if (want > kMaxAutoSplits) want = kMaxAutoSplits;
-            if (want > units) want = units;
-            if (want < 1) want = 1;
-            int64_t per = (units + want - 1) / want;
-            if (per < 2) per = 2;
-            split_len = (int32_t)(per * kSplitUnit);
-        }
+        if (split_len <= 0) split_len = (int32_t)lds_auto_split(max_keep, groups);  // a whole compute unit each
         p.split_len = split_len;
         p.n_split = (int32_t)(((int64_t)max_keep + split_len - 1) / split_len);
         if (p.n_split > 1) {
