@@ -1286,6 +1286,47 @@ static __device__ __forceinline__ void merge_many(const AttnLaunch &a, int n, ui
     }
 }
 
+// Folds the kCnt slots base .. base+kCnt-1 into (M, L, O); pair j of the
+// current chunk of pairs (pm, pl) sits in lane (lane & 32) + j, for
+// j = base - cb + k.
+template <int kCnt, int kLen>
+static __device__ __forceinline__ void merge_fold_n(const f32x4 (&o)[kLen], float pm, float pl, int cb, int base,
+                                                    int lane, float &M, float &L, f32x4 &O) {
+    static_assert(kCnt <= kLen && kCnt <= 32, "the slots lie in the array and in one chunk of pairs");
+    float m[kCnt], l[kCnt];
+#pragma unroll
+    for (int k = 0; k < kCnt; ++k) {
+        const int src = (lane & 32) + ((base - cb + k) & 31);
+        m[k] = __shfl(pm, src);
+        l[k] = __shfl(pl, src);
+    }
+    float mx = M;
+#pragma unroll
+    for (int k = 0; k < kCnt; ++k) mx = fmaxf(mx, m[k]);
+    // every factor first (independent exp2s), then sums in a tree
+    float lf[kCnt + 1];
+    f32x4 of[kCnt + 1];
+    const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - mx);
+#pragma unroll
+    for (int k = 0; k < kCnt; ++k) {
+        const float f = m[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[k] - mx);
+        lf[k] = l[k] * f;
+        of[k] = o[k] * f;
+    }
+    lf[kCnt] = L * sc;
+    of[kCnt] = O * sc;
+#pragma unroll
+    for (int w = 1; w < kCnt + 1; w *= 2)
+#pragma unroll
+        for (int k = 0; k + w < kCnt + 1; k += 2 * w) {
+            lf[k] += lf[k + w];
+            of[k] += of[k + w];
+        }
+    L = lf[0];
+    O = of[0];
+    M = mx;
+}
+
 // Up to kMergeBatch partials (every group of the 12 x 300 s workloads): one
 // batch, all loads of a thread in flight at once.
 
@@ -1294,28 +1335,21 @@ static __device__ __forceinline__ void merge_one_batch_n(const AttnLaunch &a, Sl
                                                          Emit emit) {
     const __amdgpu_buffer_rsrc_t ro = raw_buffer(a.part_o, a.part_o_bytes);
     const __amdgpu_buffer_rsrc_t rml = raw_buffer(a.part_ml, a.part_ml_bytes);
+    const int lane = tid & 63;
     for (int c = tid; c < G * (kHeadDim / 4); c += kThreads) {
         const int h = c / (kHeadDim / 4), d0 = (c % (kHeadDim / 4)) * 4;
-        float mm[kCnt], ll[kCnt];
+        // the (max, sum) pairs with one load: lane j of the head's half-wavefront
+        // takes slot j's, the fold shares them by lane shuffle
+        const int j = lane & 31;
+        const uint32_t vml = j < kCnt ? (slot_of(j) * G + h) * 8 : kNoPartial;
+        const float pm = load_coherent1(rml, vml);
+        const float pl = load_coherent1(rml, vml + 4);
         f32x4 oo[kCnt];
 #pragma unroll
-        for (int k = 0; k < kCnt; ++k) {
-            const uint32_t prow = slot_of(k) * G + h;
-            mm[k] = load_coherent1(rml, prow * 8);
-            ll[k] = load_coherent1(rml, prow * 8 + 4);
-            oo[k] = load_coherent4(ro, (prow * kHeadDim + d0) * 4);
-        }
-        float M = mm[0];
-#pragma unroll
-        for (int k = 1; k < kCnt; ++k) M = fmaxf(M, mm[k]);
-        float L = 0.f;
+        for (int k = 0; k < kCnt; ++k) oo[k] = load_coherent4(ro, ((slot_of(k) * G + h) * kHeadDim + d0) * 4);
+        float M = kNegInf, L = 0.f;
         f32x4 O = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int k = 0; k < kCnt; ++k) {
-            const float f = mm[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mm[k] - M);
-            L += ll[k] * f;
-            O += oo[k] * f;
-        }
+        merge_fold_n<kCnt>(oo, pm, pl, 0, 0, lane, M, L, O);
         emit(h, d0, O, M, L);
     }
 }
@@ -1665,47 +1699,6 @@ static __device__ __forceinline__ void merge_o_load(f32x4 (&o)[kMergeBatch], __a
         const bool in = base + k < n;
         o[k] = load_coherent4_s(ro, in ? vo : kNoPartial, in ? (uint32_t)(base + k) * so : 0u);
     }
-}
-
-// Folds the kCnt slots base .. base+kCnt-1 into (M, L, O); pair j of the
-// current chunk of pairs (pm, pl) sits in lane (lane & 32) + j, for
-// j = base - cb + k.
-template <int kCnt, int kLen>
-static __device__ __forceinline__ void merge_fold_n(const f32x4 (&o)[kLen], float pm, float pl, int cb, int base,
-                                                    int lane, float &M, float &L, f32x4 &O) {
-    static_assert(kCnt <= kLen && kCnt <= 32, "the slots lie in the array and in one chunk of pairs");
-    float m[kCnt], l[kCnt];
-#pragma unroll
-    for (int k = 0; k < kCnt; ++k) {
-        const int src = (lane & 32) + ((base - cb + k) & 31);
-        m[k] = __shfl(pm, src);
-        l[k] = __shfl(pl, src);
-    }
-    float mx = M;
-#pragma unroll
-    for (int k = 0; k < kCnt; ++k) mx = fmaxf(mx, m[k]);
-    // every factor first (independent exp2s), then sums in a tree
-    float lf[kCnt + 1];
-    f32x4 of[kCnt + 1];
-    const float sc = M == kNegInf ? 0.f : __builtin_amdgcn_exp2f(M - mx);
-#pragma unroll
-    for (int k = 0; k < kCnt; ++k) {
-        const float f = m[k] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[k] - mx);
-        lf[k] = l[k] * f;
-        of[k] = o[k] * f;
-    }
-    lf[kCnt] = L * sc;
-    of[kCnt] = O * sc;
-#pragma unroll
-    for (int w = 1; w < kCnt + 1; w *= 2)
-#pragma unroll
-        for (int k = 0; k + w < kCnt + 1; k += 2 * w) {
-            lf[k] += lf[k + w];
-            of[k] += of[k + w];
-        }
-    L = lf[0];
-    O = of[0];
-    M = mx;
 }
 
 // Folds the slots of the batch at `base` that exist (fewer than kMergeBatch
